@@ -1,0 +1,191 @@
+/*
+ * cagq.h -- C ABI of the MI355X (gfx950) Coverage-Aware Grid Query library.
+ *
+ * CAGQ is the data-structuring stage of Grid-GCN (Xu et al., arXiv
+ * 1912.02984, Sec. 3.2; Appendix D, "CAGQ general procedure"): voxelize a
+ * batch of point clouds, index the occupied voxels with at most n_v points
+ * each, choose M center voxels (Random Voxel Sampling or Coverage-Aware
+ * Sampling) and gather K node points per center from its (2r+1)^3 voxel
+ * neighbourhood (Cube Query or k-NN), then form each group's center
+ * (Appendix E, Eqs. 7-8).
+ *
+ * Conventions for every entry point:
+ *   - Pointers named "device" are HIP device pointers owned by the caller;
+ *     the library never allocates, frees or retains memory. Host pointers
+ *     are read before the call returns.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Work is enqueued asynchronously on it; results are valid once the
+ *     stream has reached the enqueued work. cagq_sample_centers with the
+ *     CAS mode synchronises `stream` (its round count is data dependent).
+ *   - Argument errors are detected on the host before anything is
+ *     enqueued and returned synchronously. Data-dependent errors
+ *     (non-finite coordinates, center voxels that are not occupied) are
+ *     recorded in the workspace and reported by cagq_get_device_status.
+ *   - Calls on one workspace are ordered by the stream; distinct
+ *     workspaces are independent (the library holds no global state).
+ *   - Array shapes are row-major; [B][N][3] means point n of cloud b has
+ *     x, y, z at ((b*N)+n)*3 + {0,1,2}.
+ */
+#ifndef CAGQ_H
+#define CAGQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define CAGQ_OK 0
+#define CAGQ_ERR_INVALID_ARG (-1)       /* a pointer, size or mode out of range */
+#define CAGQ_ERR_GRID_TOO_LARGE (-2)    /* D_x*D_y*D_z > 2^31-1 */
+#define CAGQ_ERR_WORKSPACE_TOO_SMALL (-3)
+#define CAGQ_ERR_NONFINITE_INPUT (-4)   /* device-side: a NaN/Inf coordinate */
+#define CAGQ_ERR_CAPACITY (-5)          /* device-side: an internal table overflowed */
+#define CAGQ_ERR_HIP (-6)               /* a HIP runtime call failed */
+#define CAGQ_ERR_CENTER_NOT_OCCUPIED (-7) /* device-side: a query center is not in O_v */
+
+#define CAGQ_SAMPLE_RVS 0   /* Random Voxel Sampling (Sec. 3.2) */
+#define CAGQ_SAMPLE_CAS 1   /* Coverage-Aware Sampling, greedy (Sec. 3.2, Eqs. 1-2) */
+#define CAGQ_QUERY_CUBE 0   /* Cube Query (Sec. 3.2) */
+#define CAGQ_QUERY_KNN 1    /* k-NN among the context points (Sec. 3.2) */
+
+/* Library limits (checked on the host). */
+#define CAGQ_MAX_K 64       /* node points per group */
+#define CAGQ_MAX_NV 64      /* points stored per voxel */
+#define CAGQ_MAX_RADIUS 3   /* neighbourhood half-width r */
+
+/*
+ * Voxel grid (Sec. 3.2: "voxelize the input space by setting up a voxel size
+ * (v_x, v_y, v_z)"). A point p maps, per axis a, to
+ *   g_a = clamp(floor((p_a - origin_a) / voxel_size_a), 0, dims_a - 1)
+ * (fp32 subtract then fp32 correctly rounded divide; points outside the
+ * grid are clamped onto its border voxels, never dropped), and to the
+ * linear id lin = g_x + D_x * (g_y + D_y * g_z).
+ * n_v: at most n_v points are stored per voxel (1..CAGQ_MAX_NV).
+ * radius: pi(v) is the (2r+1)^3 block of voxels around v (1..CAGQ_MAX_RADIUS).
+ */
+typedef struct cagq_grid_desc {
+    float origin[3];
+    float voxel_size[3];   /* > 0 and finite */
+    int32_t dims[3];       /* >= 1, product <= 2^31-1 */
+    int32_t n_v;
+    int32_t radius;
+} cagq_grid_desc;
+
+/*
+ * Byte offsets of the arrays a built grid exposes inside the caller's
+ * workspace (each 256-byte aligned), and the total size the workspace needs.
+ *   nvox      int32  [B]           |O_v| per cloud
+ *   vox_lin   uint32 [B][N]        lin of slot s; slots are ranks of lin, so
+ *                                  ascending; entries s < nvox[b] are valid
+ *   vox_count uint32 [B][N]        points falling in slot s
+ *   vox_off   uint32 [B][N+1]      exclusive prefix of min(count, n_v); entry
+ *                                  nvox[b] holds the stored total S_b
+ *   pt_list   uint32 [B][N]        stored point indices (0..N-1): slot s owns
+ *                                  [vox_off[s], vox_off[s+1]), the
+ *                                  min(count, n_v) lowest indices ascending
+ */
+typedef struct cagq_layout {
+    size_t total_bytes;
+    size_t nvox, vox_lin, vox_count, vox_off, pt_list;
+} cagq_layout;
+
+/*
+ * A built grid: a host-side record borrowing the caller's points and
+ * workspace. Filled by cagq_build_grid; valid while both stay alive and the
+ * workspace is not rebuilt.
+ */
+typedef struct cagq_grid {
+    int32_t B, N;
+    cagq_grid_desc desc;
+    const float* points;   /* device [B][N][3], borrowed */
+    void* workspace;       /* device, borrowed */
+    size_t workspace_bytes;
+} cagq_grid;
+
+/* Host only, no device work. Fills `out` for a batch of B clouds of N points
+ * on `desc`. Returns CAGQ_OK, CAGQ_ERR_INVALID_ARG or CAGQ_ERR_GRID_TOO_LARGE. */
+int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out);
+
+/*
+ * Voxelize and index a batch (Appendix D, general procedure, step 1: for each
+ * point, quantize it to its voxel, add the voxel to O_v on its first visit,
+ * and push the point index while the voxel stores fewer than n_v points).
+ * The stored points of a voxel are its n_v lowest point indices, the ones a
+ * sequential pass visits first.
+ *   points     device float [B][N][3]
+ *   workspace  device, >= cagq_workspace_layout(...).total_bytes bytes,
+ *              no alignment requirement beyond 256 bytes
+ *   out        host; receives the grid record
+ * 1 <= B, 1 <= N, B*N <= 2^31-1. A non-finite coordinate is clamped to voxel
+ * 0 on that axis and raises CAGQ_ERR_NONFINITE_INPUT in the device status.
+ */
+int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc,
+                    void* workspace, size_t workspace_bytes, void* stream, cagq_grid* out);
+
+/*
+ * Choose M center voxels per cloud (Sec. 3.2, "center voxels sampling";
+ * Appendix D step 2). m_valid[b] = min(M, nvox[b]) distinct voxels are chosen
+ * and written as linear ids in ascending order to center_lin[b][0..m_valid);
+ * slots j >= m_valid repeat center_lin[b][j mod m_valid].
+ *   mode CAGQ_SAMPLE_RVS: every occupied voxel equally likely. Slot s gets the
+ *     key (hi32(h(seed,1,b,s)) << 32) | s, h the splitmix64 chain
+ *     h(seed,t,a1..ak) = sm64(..sm64(sm64(seed ^ t) ^ a1).. ^ ak); the
+ *     m_valid smallest keys are chosen.
+ *   mode CAGQ_SAMPLE_CAS: coverage-aware greedy (Eqs. 1-2): repeatedly take
+ *     the unchosen voxel v maximising
+ *       2^16*lambda*#{V in pi(v): C_V = 0} - beta_q16 * sum_{V in pi(v)} C_V
+ *     (C_V = chosen voxels whose neighbourhood holds V, lambda = (2r+1)^3,
+ *     beta = beta_q16 / 2^16), ties to the lowest lin; the first m_valid
+ *     picks are the centers. Requires (2^16 + beta_q16) * lambda^2 < 2^31.
+ *     `seed` is unused. Synchronises `stream`.
+ *   center_lin  device int32 [B][M];  m_valid  device int32 [B]
+ */
+int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed,
+                        uint32_t beta_q16, int32_t* center_lin, int32_t* m_valid,
+                        void* stream);
+
+/*
+ * Gather K node points per center and form the group centers (Sec. 3.2 node
+ * points querying; Appendix D step 3; Appendix E). The context of center
+ * voxel v is the stored points of the occupied voxels of pi(v) (v included);
+ * c = their number. The n = min(K, c) context points of smallest 64-bit key
+ * are kept in ascending key order:
+ *   CAGQ_QUERY_CUBE: key = (hi32(h(seed,2,b,lin(v),i)) << 32) | i  (random subset)
+ *   CAGQ_QUERY_KNN:  key = (bits(d2) << 32) | i, d2 = (dx*dx + dy*dy) + dz*dz
+ *                    in fp32 from q_a = origin_a + ((float)g_a + 0.5f) * voxel_size_a
+ * Node slots k >= n repeat slot 0. Group center (Eqs. 7-8):
+ *   w_c = sum of the n node weights (uint32);
+ *   chi_c = S / (float)w_c per axis, S the fp32 pairwise sum of
+ *   (float)w_k * p_k over the n nodes: at stride h = 1, 2, 4, ..., entry k
+ *   (k a multiple of 2h) adds entry k + h when k + h < n.
+ *   weights     device uint32 [B][N] or NULL (all 1: raw points)
+ *   center_lin  device int32 [B][M], every entry an occupied voxel's lin
+ *   node_idx    device int32 [B][M][K]    point indices 0..N-1
+ *   node_xyz    device float [B][M][K][3] or NULL; bit copies of the points
+ *   n_valid     device int32 [B][M]
+ *   center_xyz  device float [B][M][3]
+ *   center_w    device uint32 [B][M]
+ *   ctx_count   device int32 [B][M] or NULL; c
+ * 1 <= K <= CAGQ_MAX_K. A center that is not occupied raises
+ * CAGQ_ERR_CENTER_NOT_OCCUPIED in the device status; its outputs are zero.
+ */
+int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_t* center_lin,
+                       int32_t M, int32_t K, int32_t mode, uint64_t seed,
+                       int32_t* node_idx, float* node_xyz, int32_t* n_valid,
+                       float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
+                       void* stream);
+
+/* Synchronises `stream` and returns the first device-side error recorded in
+ * g's workspace since it was last built (CAGQ_OK if none). */
+int cagq_get_device_status(const cagq_grid* g, void* stream);
+
+/* Static, human-readable name of a status code. */
+const char* cagq_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,455 @@
+"""The CPU oracle against what the paper and the mathematics fix.
+
+Each test pins one oracle function to something other than itself: published
+generator outputs, textbook routines (numpy unique / argsort / lexsort),
+brute force on small inputs, exhaustive optima, closed forms and statistics.
+"""
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1912_02984_amd import workloads as W
+from tests import pins
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _grid(origin=(0, 0, 0), size=(0.25, 0.25, 0.25), dims=(8, 8, 8), n_v=4, r=1):
+    return oracle.make_grid(origin, size, dims, n_v, r)
+
+
+# ---------------------------------------------------------------- splitmix64
+
+def test_splitmix64_published_outputs():
+    """The hash chain's primitive reproduces the generator's published outputs."""
+    rows = [l.split() for l in open(os.path.join(GOLDEN, "splitmix64.txt")) if l.strip() and l[0] != "#"]
+    assert len(rows) == 4
+    for seed, idx, out in rows:
+        state = int(seed)
+        # the idx-th output of a generator seeded with `state` is sm64(state + (idx-1)*gamma)
+        x = (state + (int(idx) - 1) * 0x9E3779B97F4A7C15) & pins.MASK64
+        assert oracle.splitmix64(x) == int(out, 16)
+        st, o = state, None
+        for _ in range(int(idx)):
+            st, o = pins.py_splitmix64_next(st)
+        assert o == int(out, 16)
+
+
+def test_splitmix64_matches_python_generator_on_random_inputs():
+    rng = np.random.default_rng(7)
+    for x in rng.integers(0, 2**63, size=200, dtype=np.int64):
+        x = int(x) * 2 + 1
+        assert oracle.splitmix64(x) == pins.py_sm64(x)
+
+
+# ---------------------------------------------------------------- voxelize
+
+def test_voxelize_hand_placed_points():
+    """Exact voxel faces, clamping outside the grid, x-fastest linear order."""
+    g = _grid(dims=(8, 4, 2))
+    P = np.array([
+        [0.0, 0.0, 0.0],        # corner -> voxel (0,0,0)
+        [0.25, 0.0, 0.0],       # exactly on the face x=1 -> g_x = 1
+        [0.2499999, 0.0, 0.0],  # just below the face -> 0
+        [1.999, 0.99, 0.49],    # last voxel (7,3,1)
+        [2.0, 1.0, 0.5],        # exactly dims*size -> clamped to (7,3,1)
+        [-5.0, -0.0, -1e-30],   # negative -> clamped to 0
+        [1e30, 0.5, 0.3],       # far outside -> clamped to D-1 on x
+        [0.75, 0.5, 0.25],      # (3,2,1)
+    ], np.float32)
+    lin = oracle.voxelize(P, g)
+    expect = [(0, 0, 0), (1, 0, 0), (0, 0, 0), (7, 3, 1), (7, 3, 1), (0, 0, 0), (7, 2, 1), (3, 2, 1)]
+    assert [int(l) for l in lin] == [x + 8 * (y + 4 * z) for x, y, z in expect]
+
+
+def test_voxelize_divide_is_correctly_rounded():
+    """(p - o) / s is one correctly rounded fp32 divide: with s = 0.1f and
+    p = 1.3f the exact quotient is 12.9999993..., so g = 12 (a reciprocal
+    multiply would round to 13)."""
+    g = oracle.make_grid((0, 0, 0), (0.1, 0.1, 0.1), (40, 40, 40), 4, 1)
+    xs = np.array([1.3, 2.1, 2.6], np.float32)
+    P = np.stack([xs, np.zeros(3, np.float32), np.zeros(3, np.float32)], 1)
+    exact = np.floor(xs.astype(np.float64) / np.float64(np.float32(0.1)))
+    assert list(exact) == [12, 20, 25]
+    assert list(oracle.voxelize(P, g)) == [12, 20, 25]
+
+
+def test_voxelize_nonfinite_is_an_error():
+    g = _grid()
+    with pytest.raises(oracle.OracleError, match="-4"):
+        oracle.voxelize(np.array([[0.1, np.nan, 0.1]], np.float32), g)
+    with pytest.raises(oracle.OracleError, match="-4"):
+        oracle.voxelize(np.array([[np.inf, 0.1, 0.1]], np.float32), g)
+
+
+def test_voxelize_agrees_with_fp64_floor_away_from_faces():
+    """Away from voxel faces the fp32 index equals the exact floor((p - o) / s)."""
+    w = W.get_workload("room")
+    P = w.points(B=1)[0]
+    gs = w.layers[0].grid
+    lin = oracle.voxelize(P, oracle.grid_from_spec(gs))
+    t = (P.astype(np.float64) - np.array(gs.origin)) / np.array(gs.voxel_size)
+    far = np.all(np.abs(t - np.round(t)) > 1e-4, axis=1)
+    assert far.mean() > 0.99
+    g = pins.grid_coords_f64(P, gs.origin, gs.voxel_size, gs.dims)
+    assert np.array_equal(lin[far], pins.lin_of(g, gs.dims)[far])
+
+
+# ---------------------------------------------------------------- table
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room"])
+def test_table_matches_numpy_unique_and_stable_argsort(name):
+    w = W.get_workload(name)
+    P = w.points()
+    gs = w.layers[0].grid
+    # a tighter cap than the workload's so that the cap binds somewhere
+    for n_v in (gs.n_v, 2):
+        grid = oracle.make_grid(gs.origin, gs.voxel_size, gs.dims, n_v, gs.radius)
+        t = oracle.Table(P, grid)
+        lin = oracle.voxelize(P, grid)
+        for b in range(min(t.B, 4)):
+            ref = pins.table_numpy(lin[b], n_v)
+            nv = t.nvox[b]
+            assert nv == len(ref["vox_lin"])
+            assert np.array_equal(t.vox_lin[b, :nv], ref["vox_lin"])
+            assert np.array_equal(t.vox_count[b, :nv], ref["vox_count"])
+            assert int(t.vox_count[b, :nv].sum()) == t.N          # every point in one voxel
+            assert np.array_equal(t.vox_off[b, :nv + 1], ref["vox_off"])
+            S = t.vox_off[b, nv]
+            assert np.array_equal(t.pt_list[b, :S], ref["pt_list"])
+
+
+def test_table_all_points_in_one_voxel():
+    P = np.full((1, 100, 3), 0.1, np.float32)
+    t = oracle.Table(P, _grid(n_v=5))
+    assert t.nvox[0] == 1 and t.vox_count[0, 0] == 100
+    assert list(t.pt_list[0, :5]) == [0, 1, 2, 3, 4]
+
+
+# ---------------------------------------------------------------- RVS
+
+def test_rvs_is_the_m_smallest_keys_in_slot_order():
+    w = W.get_workload("object")
+    P = w.points()[:3]
+    L = w.layers[0]
+    t = oracle.Table(P, oracle.grid_from_spec(L.grid))
+    for M, seed in ((128, 42), (5, 9), (10_000, 3)):
+        cl, mv = t.sample_rvs(M, seed)
+        for b in range(t.B):
+            nv = int(t.nvox[b])
+            keys = [((pins.py_chain(seed, 1, b, s) >> 32) << 32) | s for s in range(nv)]
+            m = min(M, nv)
+            assert mv[b] == m
+            chosen = sorted(k & 0xFFFFFFFF for k in sorted(keys)[:m])
+            expect = [int(t.vox_lin[b, s]) for s in chosen]
+            assert list(cl[b, :m]) == expect
+            assert all(cl[b, j] == cl[b, j % m] for j in range(m, M))
+
+
+def test_rvs_equal_inclusion_probability():
+    """Every occupied voxel is picked with the same probability (Sec. 3.2)."""
+    P = W.uniform_cube(1, 300, 5)
+    t = oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
+    nv = int(t.nvox[0])
+    M, trials = 16, 3000
+    hits = np.zeros(nv)
+    for seed in range(trials):
+        cl, _ = t.sample_rvs(M, seed)
+        hits[np.searchsorted(t.vox_lin[0, :nv], cl[0])] += 1
+    expect = trials * M / nv
+    chi2 = ((hits - expect) ** 2 / expect).sum()
+    # chi-square with nv-1 dof; 99.9th percentile is below dof + 4.5*sqrt(2 dof)
+    assert chi2 < (nv - 1) + 4.5 * math.sqrt(2 * (nv - 1)), chi2
+
+
+# ---------------------------------------------------------------- CAS
+
+def _small_table(seed, npts=60, dims=(6, 6, 3), n_v=4):
+    rng = np.random.default_rng(seed)
+    P = (rng.random((1, npts, 3)) * np.array(dims) * 0.25).astype(np.float32)
+    return oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, dims, n_v, 1))
+
+
+@pytest.mark.parametrize("beta_q16", [0, 65536 // 4, 3 * 65536])
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_cas_every_step_is_the_bruteforce_argmax(seed, beta_q16):
+    t = _small_table(seed)
+    nv = int(t.nvox[0])
+    vl = [int(x) for x in t.vox_lin[0, :nv]]
+    nbr = pins.neighbourhood_sets(vl, t.grid.dims, 1)
+    M = min(25, nv)
+    cl, mv, pick_lin, pick_score = t.sample_cas(M, beta_q16)
+    C = np.zeros(nv, np.int64)
+    picked = set()
+    for step in range(M):
+        scores = pins.cas_scores_bruteforce(nbr, C, 27, beta_q16)
+        cand = [v for v in range(nv) if v not in picked]
+        best = max(scores[v] for v in cand)
+        v = min(v for v in cand if scores[v] == best)          # ties -> lowest lin
+        assert pick_lin[0, step] == vl[v]
+        assert pick_score[0, step] == best
+        picked.add(v)
+        for V in nbr[v]:
+            C[V] += 1
+    assert list(cl[0, :M]) == sorted(pick_lin[0, :M])
+
+
+def test_cas_monotone_scores_and_exact_coverage_gain():
+    """beta = 0: pick scores never rise and each pick covers exactly U(pick) new voxels."""
+    w = W.get_workload("object")
+    t = oracle.Table(w.points()[:2], oracle.grid_from_spec(w.layers[0].grid))
+    M = 300
+    cl, mv, pick_lin, pick_score = t.sample_cas(M)
+    for b in range(t.B):
+        nv = int(t.nvox[b])
+        vl = [int(x) for x in t.vox_lin[b, :nv]]
+        index = {l: i for i, l in enumerate(vl)}
+        nbr = pins.neighbourhood_sets(vl, t.grid.dims, 1)
+        covered = set()
+        prev = None
+        for j in range(M):
+            s = int(pick_score[b, j])
+            if prev is not None:
+                assert s <= prev
+            prev = s
+            new = set(nbr[index[int(pick_lin[b, j])]]) - covered
+            assert s == 65536 * 27 * len(new)
+            covered |= new
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_cas_against_exhaustive_optimum(seed):
+    """Greedy max-coverage: equal to OPT at M = 1 and >= (1-(1-1/M)^M) OPT
+    (Nemhauser, Wolsey, Fisher 1978) on <= 64 occupied voxels."""
+    t = _small_table(100 + seed, npts=18, dims=(5, 5, 2))
+    nv = int(t.nvox[0])
+    assert nv <= 64
+    vl = [int(x) for x in t.vox_lin[0, :nv]]
+    index = {l: i for i, l in enumerate(vl)}
+    nbr = pins.neighbourhood_sets(vl, t.grid.dims, 1)
+    for M in (1, 2, 3):
+        cl, mv, _, _ = t.sample_cas(M)
+        got = pins.coverage(nbr, [index[int(l)] for l in cl[0, :M]])
+        opt = pins.exhaustive_best_coverage(nbr, M)
+        if M == 1:
+            assert got == opt
+        assert got >= (1 - (1 - 1 / M) ** M) * opt - 1e-9
+        assert got <= opt
+
+
+def test_cas_disjoint_neighbourhoods_pick_lowest_lin():
+    """All neighbourhoods disjoint and equal: every score ties, so CAS returns
+    the M lowest linear ids."""
+    pts = []
+    for x in range(0, 12, 3):
+        for y in range(0, 12, 3):
+            pts.append([(x + 0.5) * 0.25, (y + 0.5) * 0.25, 0.1])
+    P = np.array([pts], np.float32)
+    t = oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (12, 12, 1), 4, 1))
+    cl, mv, _, ps = t.sample_cas(5)
+    assert list(cl[0]) == sorted(t.vox_lin[0, :t.nvox[0]])[:5]
+    assert np.all(ps[0] == 65536 * 27 * 1)
+
+
+def test_cas_takes_everything_when_m_exceeds_occupancy():
+    t = _small_table(3, npts=10)
+    nv = int(t.nvox[0])
+    cl, mv, _, _ = t.sample_cas(nv + 7)
+    assert mv[0] == nv
+    assert list(cl[0, :nv]) == list(t.vox_lin[0, :nv])
+    assert all(cl[0, j] == cl[0, j % nv] for j in range(nv, nv + 7))
+
+
+# ---------------------------------------------------------------- query
+
+def _context_bruteforce(P, lin, tb, center_lin, dims, r):
+    """Stored points of every occupied voxel within Chebyshev distance r."""
+    gc = np.array(pins.decode(center_lin, dims))
+    stored = tb["pt_list"]
+    g = np.stack([lin % dims[0], (lin // dims[0]) % dims[1], lin // (dims[0] * dims[1])], -1)
+    near = np.abs(g - gc).max(axis=1) <= r
+    keep = np.zeros(len(lin), bool)
+    keep[stored] = True
+    return np.nonzero(near & keep)[0]
+
+
+@pytest.mark.parametrize("n_v", [32, 3])
+def test_knn_matches_bruteforce_over_the_context(n_v):
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.make_grid(gs.origin, gs.voxel_size, gs.dims, n_v, 1)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(200, 11)
+    K = 16
+    q = t.query(cl, mv, K, "knn", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, n_v)
+    o, s, dims = np.float32(gs.origin), np.float32(gs.voxel_size), gs.dims
+    for j in range(200):
+        ctx = _context_bruteforce(P[0], lin, tb, int(cl[0, j]), dims, 1)
+        assert q["ctx_count"][0, j] == len(ctx)
+        g = np.array(pins.decode(int(cl[0, j]), dims), np.float32)
+        c = o + (g + np.float32(0.5)) * s                   # voxel center, fp32
+        d = P[0, ctx] - c
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        order = np.lexsort((ctx, d2.view(np.uint32)))
+        n = min(K, len(ctx))
+        assert q["n_valid"][0, j] == n
+        assert list(q["node_idx"][0, j, :n]) == list(ctx[order[:n]])
+        assert np.all(q["node_idx"][0, j, n:] == q["node_idx"][0, j, 0])
+        assert np.array_equal(q["node_xyz"][0, j].view(np.uint32), P[0, q["node_idx"][0, j]].view(np.uint32))
+
+
+def test_knn_bruteforce_on_a_non_cubic_grid():
+    """Unequal dims and voxel sizes per axis exercise the x-fastest decode."""
+    P = W.uniform_cube(1, 600, 31) * np.array([0.7, 0.5, 0.8], np.float32)
+    dims, size = (7, 5, 4), (0.1, 0.1, 0.2)
+    grid = oracle.make_grid((0, 0, 0), size, dims, 6, 1)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(60, 2)
+    K = 12
+    q = t.query(cl, mv, K, "knn", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, 6)
+    for j in range(60):
+        ctx = _context_bruteforce(P[0], lin, tb, int(cl[0, j]), dims, 1)
+        g = np.array(pins.decode(int(cl[0, j]), dims), np.float32)
+        c = np.zeros(3, np.float32) + (g + np.float32(0.5)) * np.array(size, np.float32)
+        d = P[0, ctx] - c
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        order = np.lexsort((ctx, d2.view(np.uint32)))
+        n = min(K, len(ctx))
+        assert list(q["node_idx"][0, j, :n]) == list(ctx[order[:n]])
+
+
+def test_knn_equals_global_knn_when_the_neighbourhood_suffices():
+    """No cap binding and the K-th distance well inside the (2r+1)^3 block:
+    CAGQ k-NN is the ordinary k-NN over all N points (textbook brute force)."""
+    P = W.uniform_cube(1, 4000, 21)
+    size = 0.1
+    grid = oracle.make_grid((0, 0, 0), (size,) * 3, (10, 10, 10), 64, 1)
+    t = oracle.Table(P, grid)
+    assert t.vox_count.max() <= 64
+    cl, mv = t.sample_rvs(300, 4)
+    K = 8
+    q = t.query(cl, mv, K, "knn", 0)
+    checked = 0
+    for j in range(300):
+        g = np.array(pins.decode(int(cl[0, j]), (10, 10, 10)))
+        c = (g + 0.5) * size
+        d = np.sqrt(((P[0].astype(np.float64) - c) ** 2).sum(1))
+        order = np.argsort(d, kind="stable")
+        if d[order[K - 1]] < 1.5 * size - 1e-3 and d[order[K]] - d[order[K - 1]] > 1e-5:
+            assert set(q["node_idx"][0, j]) == set(order[:K])
+            checked += 1
+    assert checked > 100
+
+
+def test_cube_query_is_a_random_subset_of_the_context():
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.grid_from_spec(gs)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(300, 5)
+    K = 8
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, gs.n_v)
+    q = t.query(cl, mv, K, "cube", 77)
+    for j in range(300):
+        ctx = set(_context_bruteforce(P[0], lin, tb, int(cl[0, j]), gs.dims, 1))
+        n = min(K, len(ctx))
+        got = list(q["node_idx"][0, j, :n])
+        assert q["n_valid"][0, j] == n and len(set(got)) == n and set(got) <= ctx
+        if len(ctx) <= K:
+            assert set(got) == ctx
+        key = [pins.py_chain(77, 2, 0, int(cl[0, j]), i) >> 32 for i in got]
+        assert key == sorted(key)
+
+
+def test_cube_query_inclusion_frequency():
+    """Each context point is kept with probability K / c (uniform subset)."""
+    P = W.uniform_cube(1, 400, 8)
+    grid = oracle.make_grid((0, 0, 0), (0.5,) * 3, (2, 2, 2), 64, 1)
+    t = oracle.Table(P, grid)
+    cl = np.array([[int(t.vox_lin[0, 0])]], np.int32)
+    K, trials = 10, 2000
+    hits = np.zeros(400)
+    c = None
+    for seed in range(trials):
+        q = t.query(cl, np.array([1], np.int32), K, "cube", seed)
+        c = int(q["ctx_count"][0, 0])
+        hits[q["node_idx"][0, 0]] += 1
+    ctx = hits > 0
+    assert ctx.sum() == c
+    p = K / c
+    expect = trials * p
+    z = (hits[ctx] - expect) / math.sqrt(trials * p * (1 - p))
+    assert np.abs(z).max() < 5.0
+
+
+def test_center_closed_forms():
+    grid = oracle.make_grid((0, 0, 0), (4.0,) * 3, (1, 1, 1), 8, 1)
+    # one node, weight 1: the center is that point
+    P = np.array([[[1.25, 2.5, 3.75]]], np.float32)
+    t = oracle.Table(P, grid)
+    cl = np.array([[0]], np.int32)
+    q = t.query(cl, np.array([1], np.int32), 4, "knn", 0)
+    assert np.array_equal(q["center_xyz"][0, 0], P[0, 0]) and q["center_w"][0, 0] == 1
+    # two nodes: the correctly rounded midpoint
+    P = np.array([[[1.0, 0.1, 3.0], [1.0000001, 0.3, 2.9]]], np.float32)
+    t = oracle.Table(P, grid)
+    q = t.query(cl, np.array([1], np.int32), 4, "knn", 0)
+    mid = ((P[0, 0].astype(np.float64) + P[0, 1]) / 2).astype(np.float32)
+    assert np.array_equal(q["center_xyz"][0, 0], mid)
+    # weights: w_c is the integer sum, the center the weighted mean
+    w = np.array([[3, 5]], np.uint32)
+    q = t.query(cl, np.array([1], np.int32), 4, "knn", 0, weights=w)
+    assert q["center_w"][0, 0] == 8
+    ref = (3 * P[0, 0].astype(np.float64) + 5 * P[0, 1]) / 8
+    assert np.allclose(q["center_xyz"][0, 0], ref, rtol=2e-7, atol=0)
+
+
+def test_center_follows_the_pairwise_order():
+    """x = [1, 2^-24, 2^-24, 2^-24] (in node order): pairwise gives
+    (1 + 2^-24) + (2^-24 + 2^-24) = 1 + 2^-23, a left-to-right sum gives 1."""
+    e = 2.0 ** -24
+    # node order is the k-NN order; y places the points at increasing distance
+    # from the voxel center (2, 2, 2) while x carries the test values
+    P = np.array([[[1.0, 2.0, 2.0], [e, 2.0, 2.0], [e, 2.2, 2.0], [e, 2.4, 2.0]]], np.float32)
+    grid = oracle.make_grid((0, 0, 0), (4.0,) * 3, (1, 1, 1), 8, 1)
+    t = oracle.Table(P, grid)
+    q = t.query(np.array([[0]], np.int32), np.array([1], np.int32), 4, "knn", 0)
+    assert list(q["node_idx"][0, 0]) == [0, 1, 2, 3]
+    assert q["center_xyz"][0, 0, 0] == np.float32((1 + 2 * e) / 4)
+
+
+def test_center_error_bound_on_a_workload():
+    """|chi_c - exact weighted mean| <= (ceil(log2 n) + 1) * 2^-24 * max|p| (pairwise sum + divide)."""
+    w = W.get_workload("room")
+    P = w.points(B=2)
+    L = w.layers[0]
+    t, cl, mv, q = oracle.run_layer(P, L)
+    for b in range(2):
+        idx = q["node_idx"][b]
+        n = q["n_valid"][b]
+        for j in range(0, L.M, 7):
+            pts = P[b, idx[j, :n[j]]].astype(np.float64)
+            exact = pts.mean(0)
+            bound = (math.ceil(math.log2(max(n[j], 2))) + 1) * 2.0 ** -24 * np.abs(pts).max()
+            assert np.all(np.abs(q["center_xyz"][b, j] - exact) <= bound)
+            lo, hi = pts.min(0), pts.max(0)
+            assert np.all(q["center_xyz"][b, j] >= np.nextafter(lo.astype(np.float32), -np.inf))
+            assert np.all(q["center_xyz"][b, j] <= np.nextafter(hi.astype(np.float32), np.inf))
+
+
+def test_query_rejects_unoccupied_center():
+    t = _small_table(0)
+    occupied = set(int(x) for x in t.vox_lin[0, :t.nvox[0]])
+    empty = next(l for l in range(6 * 6 * 3) if l not in occupied)
+    with pytest.raises(oracle.OracleError, match="-7"):
+        t.query(np.array([[empty]], np.int32), np.array([1], np.int32), 4, "cube", 0)
