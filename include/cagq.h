@@ -36,6 +36,13 @@
 extern "C" {
 #endif
 
+/* Symbols of the C ABI are the only ones the shared library exports. */
+#if defined(__GNUC__) || defined(__clang__)
+#define CAGQ_API __attribute__((visibility("default")))
+#else
+#define CAGQ_API
+#endif
+
 /* Status codes. */
 #define CAGQ_OK 0
 #define CAGQ_ERR_INVALID_ARG (-1)       /* a pointer, size or mode out of range */
@@ -107,7 +114,7 @@ typedef struct cagq_grid {
 
 /* Host only, no device work. Fills `out` for a batch of B clouds of N points
  * on `desc`. Returns CAGQ_OK, CAGQ_ERR_INVALID_ARG or CAGQ_ERR_GRID_TOO_LARGE. */
-int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out);
+CAGQ_API int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out);
 
 /*
  * Voxelize and index a batch (Appendix D, general procedure, step 1: for each
@@ -122,7 +129,7 @@ int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq
  * 1 <= B, 1 <= N, B*N <= 2^31-1. A non-finite coordinate is clamped to voxel
  * 0 on that axis and raises CAGQ_ERR_NONFINITE_INPUT in the device status.
  */
-int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc,
+CAGQ_API int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc,
                     void* workspace, size_t workspace_bytes, void* stream, cagq_grid* out);
 
 /*
@@ -143,7 +150,7 @@ int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_d
  *     `seed` is unused. Synchronises `stream`.
  *   center_lin  device int32 [B][M];  m_valid  device int32 [B]
  */
-int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed,
+CAGQ_API int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed,
                         uint32_t beta_q16, int32_t* center_lin, int32_t* m_valid,
                         void* stream);
 
@@ -172,7 +179,7 @@ int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t se
  * 1 <= K <= CAGQ_MAX_K. A center that is not occupied raises
  * CAGQ_ERR_CENTER_NOT_OCCUPIED in the device status; its outputs are zero.
  */
-int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_t* center_lin,
+CAGQ_API int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_t* center_lin,
                        int32_t M, int32_t K, int32_t mode, uint64_t seed,
                        int32_t* node_idx, float* node_xyz, int32_t* n_valid,
                        float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
@@ -180,10 +187,10 @@ int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_
 
 /* Synchronises `stream` and returns the first device-side error recorded in
  * g's workspace since it was last built (CAGQ_OK if none). */
-int cagq_get_device_status(const cagq_grid* g, void* stream);
+CAGQ_API int cagq_get_device_status(const cagq_grid* g, void* stream);
 
 /* Static, human-readable name of a status code. */
-const char* cagq_status_string(int status);
+CAGQ_API const char* cagq_status_string(int status);
 
 #ifdef __cplusplus
 }

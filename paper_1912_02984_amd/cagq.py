@@ -1,0 +1,244 @@
+"""Python binding of the gfx950 CAGQ library (``libcagq.so``).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels. Tensors are torch CUDA (HIP) tensors; the library enqueues on the
+current torch stream. The names mirror the C ABI in ``include/cagq.h``:
+``build_grid``, ``sample_centers``, ``query_context``, ``get_device_status``.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Dict, Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libcagq.so")
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_GRID_TOO_LARGE = -2
+ERR_WORKSPACE_TOO_SMALL = -3
+ERR_NONFINITE_INPUT = -4
+ERR_CAPACITY = -5
+ERR_HIP = -6
+ERR_CENTER_NOT_OCCUPIED = -7
+
+SAMPLE = {"rvs": 0, "cas": 1}
+QUERY = {"cube": 0, "knn": 1}
+MAX_K = 64
+MAX_NV = 64
+MAX_RADIUS = 3
+
+
+class GridDesc(C.Structure):
+    _fields_ = [("origin", C.c_float * 3), ("voxel_size", C.c_float * 3),
+                ("dims", C.c_int32 * 3), ("n_v", C.c_int32), ("radius", C.c_int32)]
+
+
+class LayoutC(C.Structure):
+    _fields_ = [("total_bytes", C.c_size_t), ("nvox", C.c_size_t), ("vox_lin", C.c_size_t),
+                ("vox_count", C.c_size_t), ("vox_off", C.c_size_t), ("pt_list", C.c_size_t)]
+
+
+class GridC(C.Structure):
+    _fields_ = [("B", C.c_int32), ("N", C.c_int32), ("desc", GridDesc), ("points", C.c_void_p),
+                ("workspace", C.c_void_p), ("workspace_bytes", C.c_size_t)]
+
+
+class CagqError(RuntimeError):
+    def __init__(self, code: int, what: str):
+        super().__init__(f"{what}: {status_string(code)} ({code})")
+        self.code = code
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    """Load ``libcagq.so``; raises if the library has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1912_02984_amd.build")
+        L = C.CDLL(LIB_PATH)
+        P = C.c_void_p
+        L.cagq_workspace_layout.argtypes = [C.c_int32, C.c_int32, C.POINTER(GridDesc), C.POINTER(LayoutC)]
+        L.cagq_build_grid.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(GridDesc), P, C.c_size_t, P,
+                                      C.POINTER(GridC)]
+        L.cagq_sample_centers.argtypes = [C.POINTER(GridC), C.c_int32, C.c_int32, C.c_uint64, C.c_uint32,
+                                          P, P, P]
+        L.cagq_query_context.argtypes = [C.POINTER(GridC), P, P, C.c_int32, C.c_int32, C.c_int32,
+                                         C.c_uint64, P, P, P, P, P, P, P]
+        L.cagq_get_device_status.argtypes = [C.POINTER(GridC), P]
+        L.cagq_status_string.argtypes = [C.c_int]
+        L.cagq_status_string.restype = C.c_char_p
+        for f in ("cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
+                  "cagq_query_context", "cagq_get_device_status"):
+            getattr(L, f).restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().cagq_status_string(int(code)).decode()
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise CagqError(rc, what)
+
+
+def make_desc(origin: Sequence[float], voxel_size: Sequence[float], dims: Sequence[int],
+              n_v: int, radius: int = 1) -> GridDesc:
+    d = GridDesc()
+    for a in range(3):
+        d.origin[a] = float(origin[a])
+        d.voxel_size[a] = float(voxel_size[a])
+        d.dims[a] = int(dims[a])
+    d.n_v = int(n_v)
+    d.radius = int(radius)
+    return d
+
+
+def desc_from_spec(spec) -> GridDesc:
+    """GridDesc from an object with origin, voxel_size, dims, n_v, radius."""
+    return make_desc(spec.origin, spec.voxel_size, spec.dims, spec.n_v, spec.radius)
+
+
+def workspace_layout(B: int, N: int, desc: GridDesc) -> LayoutC:
+    out = LayoutC()
+    _check(lib().cagq_workspace_layout(B, N, C.byref(desc), C.byref(out)), "cagq_workspace_layout")
+    return out
+
+
+def _stream_ptr(stream: Optional[torch.cuda.Stream] = None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return C.c_void_p(s.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else C.c_void_p(t.data_ptr())
+
+
+def _need(t: torch.Tensor, dtype, shape, name: str):
+    if not t.is_cuda or t.dtype != dtype or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{name}: expected contiguous {dtype} {tuple(shape)} on the GPU, "
+                         f"got {t.dtype} {tuple(t.shape)} on {t.device}")
+
+
+@dataclass
+class Grid:
+    """A built grid: the C record plus the tensors it borrows."""
+    rec: GridC
+    points: torch.Tensor
+    workspace: torch.Tensor
+    layout: LayoutC
+
+    @property
+    def B(self) -> int:
+        return self.rec.B
+
+    @property
+    def N(self) -> int:
+        return self.rec.N
+
+    def _view(self, off: int, count: int, dtype) -> torch.Tensor:
+        nbytes = count * torch.tensor([], dtype=dtype).element_size()
+        return self.workspace[off:off + nbytes].view(dtype)
+
+    def table(self) -> Dict[str, torch.Tensor]:
+        """Views of the occupied-voxel table inside the workspace (uint32 as int32)."""
+        B, N, L = self.B, self.N, self.layout
+        return dict(
+            nvox=self._view(L.nvox, B, torch.int32),
+            vox_lin=self._view(L.vox_lin, B * N, torch.int32).view(B, N),
+            vox_count=self._view(L.vox_count, B * N, torch.int32).view(B, N),
+            vox_off=self._view(L.vox_off, B * (N + 1), torch.int32).view(B, N + 1),
+            pt_list=self._view(L.pt_list, B * N, torch.int32).view(B, N),
+        )
+
+
+def build_grid(points: torch.Tensor, desc: GridDesc, workspace: Optional[torch.Tensor] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> Grid:
+    """Voxelize and index a batch ``points`` float32 [B, N, 3] (cagq_build_grid)."""
+    if points.dim() != 3 or points.shape[2] != 3:
+        raise ValueError("points must be [B, N, 3]")
+    B, N = int(points.shape[0]), int(points.shape[1])
+    _need(points, torch.float32, (B, N, 3), "points")
+    lay = workspace_layout(B, N, desc)
+    if workspace is None:
+        workspace = torch.empty(lay.total_bytes, dtype=torch.uint8, device=points.device)
+    rec = GridC()
+    _check(lib().cagq_build_grid(_ptr(points), B, N, C.byref(desc), _ptr(workspace), workspace.numel(),
+                                 _stream_ptr(stream), C.byref(rec)), "cagq_build_grid")
+    return Grid(rec, points, workspace, lay)
+
+
+def sample_centers(grid: Grid, M: int, mode: str, seed: int, beta_q16: int = 0,
+                   center_lin: Optional[torch.Tensor] = None, m_valid: Optional[torch.Tensor] = None,
+                   stream: Optional[torch.cuda.Stream] = None):
+    """M center voxels per cloud by RVS or CAS (cagq_sample_centers)."""
+    dev = grid.points.device
+    if center_lin is None:
+        center_lin = torch.empty((grid.B, M), dtype=torch.int32, device=dev)
+    if m_valid is None:
+        m_valid = torch.empty((grid.B,), dtype=torch.int32, device=dev)
+    _need(center_lin, torch.int32, (grid.B, M), "center_lin")
+    _need(m_valid, torch.int32, (grid.B,), "m_valid")
+    _check(lib().cagq_sample_centers(C.byref(grid.rec), M, SAMPLE[mode], C.c_uint64(seed & (2**64 - 1)),
+                                     C.c_uint32(beta_q16), _ptr(center_lin), _ptr(m_valid),
+                                     _stream_ptr(stream)), "cagq_sample_centers")
+    return center_lin, m_valid
+
+
+def alloc_query_outputs(B: int, M: int, K: int, device, want_xyz: bool = True,
+                        want_ctx: bool = True) -> Dict[str, torch.Tensor]:
+    return dict(
+        node_idx=torch.empty((B, M, K), dtype=torch.int32, device=device),
+        node_xyz=torch.empty((B, M, K, 3), dtype=torch.float32, device=device) if want_xyz else None,
+        n_valid=torch.empty((B, M), dtype=torch.int32, device=device),
+        center_xyz=torch.empty((B, M, 3), dtype=torch.float32, device=device),
+        center_w=torch.empty((B, M), dtype=torch.int32, device=device),
+        ctx_count=torch.empty((B, M), dtype=torch.int32, device=device) if want_ctx else None,
+    )
+
+
+def query_context(grid: Grid, center_lin: torch.Tensor, K: int, mode: str, seed: int,
+                  weights: Optional[torch.Tensor] = None, out: Optional[Dict[str, torch.Tensor]] = None,
+                  want_xyz: bool = True, want_ctx: bool = True,
+                  stream: Optional[torch.cuda.Stream] = None) -> Dict[str, torch.Tensor]:
+    """K node points and the group center per center voxel (cagq_query_context).
+
+    ``weights`` int32/uint32-valued [B, N] or None (all 1). ``center_w`` holds
+    uint32 values in an int32 tensor.
+    """
+    B, M = int(center_lin.shape[0]), int(center_lin.shape[1])
+    _need(center_lin, torch.int32, (B, M), "center_lin")
+    if weights is not None:
+        _need(weights, torch.int32, (grid.B, grid.N), "weights")
+    if out is None:
+        out = alloc_query_outputs(B, M, K, grid.points.device, want_xyz, want_ctx)
+    _check(lib().cagq_query_context(
+        C.byref(grid.rec), _ptr(weights), _ptr(center_lin), M, K, QUERY[mode], C.c_uint64(seed & (2**64 - 1)),
+        _ptr(out["node_idx"]), _ptr(out.get("node_xyz")), _ptr(out["n_valid"]), _ptr(out["center_xyz"]),
+        _ptr(out["center_w"]), _ptr(out.get("ctx_count")), _stream_ptr(stream)), "cagq_query_context")
+    return out
+
+
+def get_device_status(grid: Grid, stream: Optional[torch.cuda.Stream] = None) -> int:
+    """Synchronises the stream; first device-side error since the grid was built."""
+    return int(lib().cagq_get_device_status(C.byref(grid.rec), _stream_ptr(stream)))
+
+
+def run_layer(points: torch.Tensor, layer, weights: Optional[torch.Tensor] = None,
+              workspace: Optional[torch.Tensor] = None):
+    """One CAGQ layer (build, sample, query) for a LayerSpec-like object.
+
+    Returns (grid, center_lin, m_valid, query outputs)."""
+    g = build_grid(points, desc_from_spec(layer.grid), workspace)
+    cl, mv = sample_centers(g, layer.M, layer.sample, layer.seed)
+    q = query_context(g, cl, layer.K, layer.query, layer.seed, weights=weights)
+    return g, cl, mv, q

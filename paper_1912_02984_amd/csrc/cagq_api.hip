@@ -1,0 +1,184 @@
+// C ABI of the gfx950 CAGQ library (declared in include/cagq.h): argument
+// validation on the host, workspace layout, and the launch sequence of each
+// step. Every argument error is returned before anything is enqueued.
+#include <math.h>
+#include <string.h>
+
+#include "cagq_internal.h"
+
+namespace cagq {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static int check_desc(const cagq_grid_desc* d) {
+    if (!d) return CAGQ_ERR_INVALID_ARG;
+    int64_t v = 1;
+    for (int a = 0; a < 3; ++a) {
+        if (d->dims[a] < 1) return CAGQ_ERR_INVALID_ARG;
+        if (!(d->voxel_size[a] > 0.0f) || !isfinite(d->voxel_size[a])) return CAGQ_ERR_INVALID_ARG;
+        if (!isfinite(d->origin[a])) return CAGQ_ERR_INVALID_ARG;
+        v *= d->dims[a];
+        if (v > 2147483647LL) return CAGQ_ERR_GRID_TOO_LARGE;
+    }
+    if (d->n_v < 1 || d->n_v > CAGQ_MAX_NV) return CAGQ_ERR_INVALID_ARG;
+    if (d->radius < 1 || d->radius > CAGQ_MAX_RADIUS) return CAGQ_ERR_INVALID_ARG;
+    return CAGQ_OK;
+}
+
+bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
+    if (B < 1 || N < 1 || (int64_t)B * N > 2147483647LL) return false;
+    memset(L, 0, sizeof(*L));
+    L->B = B;
+    L->N = N;
+    L->V = (int64_t)d->dims[0] * d->dims[1] * d->dims[2];
+    L->W = (L->V + 63) / 64;
+    L->tiles_w = (L->W + kScanTile - 1) / kScanTile;
+    L->tiles_s = ((int64_t)N + kScanTile - 1) / kScanTile;
+    L->big_cap = (int64_t)B * N / (kBigVoxel + 1) + 1;
+    const size_t BN = (size_t)B * N;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off = align256(off + bytes);
+        return o;
+    };
+    L->nvox = take(4 * (size_t)B);
+    L->vox_lin = take(4 * BN);
+    L->vox_count = take(4 * BN);
+    L->vox_off = take(4 * (size_t)B * (N + 1));
+    L->pt_list = take(4 * BN);
+    L->status = take(4 * kStSlots);
+    L->desc_w = take(8 * (size_t)B * L->tiles_w);
+    L->desc_s = take(8 * (size_t)B * L->tiles_s);
+    L->bitmap = take(8 * (size_t)B * L->W);
+    L->clear_end = off;
+    L->word_rank = take(4 * (size_t)B * L->W);
+    L->pt_slot = take(4 * BN);
+    L->pt_pos = take(4 * BN);
+    L->full_off = take(4 * (size_t)B * (N + 1));
+    L->bucket = take(4 * BN);
+    L->pt4 = take(16 * BN);
+    L->big = take(4 * (size_t)L->big_cap);
+    L->cas_cover = take(4 * BN);
+    L->cas_key = take(8 * BN);
+    L->cas_pick = take(8 * BN);
+    L->cas_round = take(4 * BN);
+    L->cas_ctl = take(CasCtl::bytes(B));
+    L->total = off;
+    return true;
+}
+
+static int grid_layout(const cagq_grid* g, Layout* L) {
+    if (!g || !g->points || !g->workspace) return CAGQ_ERR_INVALID_ARG;
+    int rc = check_desc(&g->desc);
+    if (rc != CAGQ_OK) return rc;
+    if (!make_layout(g->B, g->N, &g->desc, L)) return CAGQ_ERR_INVALID_ARG;
+    if (g->workspace_bytes < L->total) return CAGQ_ERR_WORKSPACE_TOO_SMALL;
+    return CAGQ_OK;
+}
+
+}  // namespace cagq
+
+using namespace cagq;
+
+extern "C" {
+
+int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out) {
+    if (!out) return CAGQ_ERR_INVALID_ARG;
+    int rc = check_desc(desc);
+    if (rc != CAGQ_OK) return rc;
+    Layout L;
+    if (!make_layout(B, N, desc, &L)) return CAGQ_ERR_INVALID_ARG;
+    out->total_bytes = L.total;
+    out->nvox = L.nvox;
+    out->vox_lin = L.vox_lin;
+    out->vox_count = L.vox_count;
+    out->vox_off = L.vox_off;
+    out->pt_list = L.pt_list;
+    return CAGQ_OK;
+}
+
+int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc,
+                    void* workspace, size_t workspace_bytes, void* stream, cagq_grid* out) {
+    if (!points || !workspace || !out) return CAGQ_ERR_INVALID_ARG;
+    if (((uintptr_t)workspace & 255u) != 0) return CAGQ_ERR_INVALID_ARG;
+    int rc = check_desc(desc);
+    if (rc != CAGQ_OK) return rc;
+    Layout L;
+    if (!make_layout(B, N, desc, &L)) return CAGQ_ERR_INVALID_ARG;
+    if (workspace_bytes < L.total) return CAGQ_ERR_WORKSPACE_TOO_SMALL;
+    out->B = B;
+    out->N = N;
+    out->desc = *desc;
+    out->points = points;
+    out->workspace = workspace;
+    out->workspace_bytes = workspace_bytes;
+    hipError_t e = launch_build(points, L, *desc, workspace, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed, uint32_t beta_q16,
+                        int32_t* center_lin, int32_t* m_valid, void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (M < 1 || (int64_t)g->B * M > 2147483647LL || !center_lin || !m_valid) return CAGQ_ERR_INVALID_ARG;
+    if (mode == CAGQ_SAMPLE_RVS) {
+        hipError_t e = launch_select(L, g->workspace, M, 0, seed, center_lin, m_valid, (hipStream_t)stream);
+        return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+    }
+    if (mode != CAGQ_SAMPLE_CAS) return CAGQ_ERR_INVALID_ARG;
+    const int64_t side = 2 * (int64_t)g->desc.radius + 1;
+    const int64_t lam = side * side * side;
+    if ((65536LL + (int64_t)beta_q16) * lam * lam >= 2147483648LL) return CAGQ_ERR_INVALID_ARG;
+    int status = CAGQ_OK;
+    hipError_t e = run_cas(L, g->desc, g->workspace, M, beta_q16, (hipStream_t)stream, &status);
+    if (e != hipSuccess) return CAGQ_ERR_HIP;
+    if (status != CAGQ_OK) return status;
+    e = launch_select(L, g->workspace, M, 1, seed, center_lin, m_valid, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_t* center_lin, int32_t M,
+                       int32_t K, int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz,
+                       int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
+                       void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    if (K < 1 || K > CAGQ_MAX_K) return CAGQ_ERR_INVALID_ARG;
+    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN) return CAGQ_ERR_INVALID_ARG;
+    if (!center_lin || !node_idx || !n_valid || !center_xyz || !center_w) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_query(L, g->desc, g->points, g->workspace, weights, center_lin, M, K, mode, seed,
+                                node_idx, node_xyz, n_valid, center_xyz, center_w, ctx_count,
+                                (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_get_device_status(const cagq_grid* g, void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return CAGQ_ERR_HIP;
+    int st = 0;
+    if (hipMemcpy(&st, at<int>(g->workspace, L.status), sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
+        return CAGQ_ERR_HIP;
+    return st;
+}
+
+const char* cagq_status_string(int status) {
+    switch (status) {
+        case CAGQ_OK: return "ok";
+        case CAGQ_ERR_INVALID_ARG: return "invalid argument";
+        case CAGQ_ERR_GRID_TOO_LARGE: return "grid has more than 2^31-1 voxels";
+        case CAGQ_ERR_WORKSPACE_TOO_SMALL: return "workspace too small";
+        case CAGQ_ERR_NONFINITE_INPUT: return "non-finite input coordinate";
+        case CAGQ_ERR_CAPACITY: return "internal capacity exceeded";
+        case CAGQ_ERR_HIP: return "HIP runtime error";
+        case CAGQ_ERR_CENTER_NOT_OCCUPIED: return "query center voxel is not occupied";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"

@@ -1,0 +1,370 @@
+// Voxelization and the occupied-voxel index (Appendix D, CAGQ general
+// procedure, step 1; Sec. 3.2 "voxelize the input space ... map each point to
+// a voxel index ... store up to n_v points in each voxel").
+//
+// Design (gfx950): the set O_v of non-empty voxels is an occupancy bitmap
+// with one bit per grid voxel; a voxel's slot is its rank (popcount of the
+// bits before it), which is a minimal, order-preserving hash of the linear
+// voxel id to a compact slot. Ranks come from a single-pass decoupled
+// look-back scan over the bitmap words, counts from one atomic per point,
+// offsets from a second look-back scan over the slots. Per-voxel lists hold
+// the n_v lowest point indices in ascending order, independent of the
+// arrival order the atomics produce: small voxels rank each point against
+// the voxel's bucket, large voxels are reduced by a wavefront bitonic
+// selection.
+#include "cagq_internal.h"
+
+namespace cagq {
+
+namespace {
+
+struct GridArgs {
+    float o[3];
+    float s[3];
+    int32_t D[3];
+};
+
+GridArgs grid_args(const cagq_grid_desc& d) {
+    GridArgs g;
+    for (int a = 0; a < 3; ++a) {
+        g.o[a] = d.origin[a];
+        g.s[a] = d.voxel_size[a];
+        g.D[a] = d.dims[a];
+    }
+    return g;
+}
+
+// clamp(floor((p - o) / s), 0, D - 1): one rounded subtract, one correctly
+// rounded divide, an exact floor and an exact clamp.
+__device__ __forceinline__ int32_t axis_index(float p, float o, float s, int32_t D) {
+    float diff = p - o;
+    float t = diff / s;
+    float f = floorf(t);
+    if (f < 0.0f) return 0;
+    if (f >= 2147483648.0f) return D - 1;
+    int32_t gi = (int32_t)f;
+    return gi > D - 1 ? D - 1 : gi;
+}
+
+__global__ void k_clear(uint4* __restrict__ p, size_t n16) {
+    size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+        p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// One lane per point: linear voxel id, occupancy bit.
+__global__ __launch_bounds__(256) void k_mark(const float* __restrict__ P, int32_t N, int32_t BN,
+                                              GridArgs g, int64_t W, uint32_t* __restrict__ pt_lin,
+                                              uint64_t* __restrict__ bitmap, int* __restrict__ status) {
+    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= BN) return;
+    int32_t b = gid / N;
+    const float* p = P + (size_t)gid * 3;
+    float c[3] = {p[0], p[1], p[2]};
+    uint32_t gg[3];
+    bool bad = false;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        if (!isfinite(c[a])) {
+            bad = true;
+            gg[a] = 0;
+        } else {
+            gg[a] = (uint32_t)axis_index(c[a], g.o[a], g.s[a], g.D[a]);
+        }
+    }
+    uint32_t lin = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
+    pt_lin[gid] = lin;
+    uint64_t* word = bitmap + (size_t)b * W + (lin >> 6);
+    uint64_t bit = 1ull << (lin & 63);
+    if (!(*word & bit)) atomicOr((unsigned long long*)word, (unsigned long long)bit);
+    if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+}
+
+// Tile descriptors of the look-back scans: status in bits 62-63 (1 = the
+// tile's own aggregate, 2 = inclusive prefix), value in bits 0-61.
+constexpr uint64_t kDescAgg = 1ull << 62;
+constexpr uint64_t kDescInc = 2ull << 62;
+constexpr uint64_t kDescVal = (1ull << 62) - 1;
+
+// Exclusive prefix of `agg` over the tiles before `tile` in one segment.
+// Every thread of the block calls it; wave 0 publishes and looks back. Tiles
+// are numbered by a ticket taken at block start, so every predecessor has
+// started and will publish: the spin always ends.
+__device__ uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
+    if (threadIdx.x < kWave) {
+        const int lane = lane_id();
+        uint64_t excl = 0;
+        if (tile == 0) {
+            if (lane == 0) st_release(desc, kDescInc | agg);
+        } else {
+            if (lane == 0) st_release(desc + tile, kDescAgg | agg);
+            int64_t base = tile - 1;
+            while (true) {
+                int64_t idx = base - lane;
+                uint64_t d = kDescInc;  // before the first tile: an inclusive zero
+                if (idx >= 0) {
+                    do {
+                        d = ld_acquire(desc + idx);
+                    } while ((d >> 62) == 0);
+                }
+                uint64_t inc = __ballot((d >> 62) == 2);
+                if (inc) {
+                    int first = __ffsll((unsigned long long)inc) - 1;
+                    excl += wave_sum<uint64_t>(lane <= first ? (d & kDescVal) : 0ull);
+                    break;
+                }
+                excl += wave_sum<uint64_t>(d & kDescVal);
+                base -= kWave;
+            }
+            if (lane == 0) st_release(desc + tile, kDescInc | (excl + agg));
+        }
+        if (lane == 0) *s_out = excl;
+    }
+    __syncthreads();
+    return *s_out;
+}
+
+// Exclusive scan of one 64-bit value per thread across a 256-thread block;
+// *total receives the block sum.
+__device__ __forceinline__ uint64_t block_excl_scan(uint64_t v, uint64_t* s_wave, uint64_t* total) {
+    uint64_t incl = wave_incl_scan<uint64_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    __syncthreads();
+    uint64_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kScanThreads / kWave; ++i) {
+        uint64_t x = s_wave[i];
+        if (i < wv) off += x;
+        tot += x;
+    }
+    *total = tot;
+    return off + incl - v;
+}
+
+// Ranks of the occupancy words: word_rank[w] = occupied voxels before word w.
+// Also lists every occupied voxel's linear id at its slot and clears its count.
+__global__ __launch_bounds__(kScanThreads) void k_rank(
+    const uint64_t* __restrict__ bitmap, int64_t W, int64_t tiles_w, int32_t N,
+    uint32_t* __restrict__ word_rank, uint32_t* __restrict__ vox_lin, uint32_t* __restrict__ vox_count,
+    int32_t* __restrict__ nvox, uint64_t* __restrict__ desc_w, int* __restrict__ status) {
+    __shared__ uint32_t s_ticket;
+    __shared__ uint64_t s_wave[kScanThreads / kWave];
+    __shared__ uint64_t s_prefix;
+    if (threadIdx.x == 0) s_ticket = atomicAdd((unsigned*)&status[kStTicketRank], 1u);
+    __syncthreads();
+    const uint32_t t = s_ticket;
+    const int32_t b = (int32_t)(t / tiles_w);
+    const int64_t tile = (int64_t)(t % tiles_w);
+    const uint64_t* bm = bitmap + (size_t)b * W;
+    const int64_t w0 = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    uint64_t words[kScanItems];
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t w = w0 + i;
+        words[i] = w < W ? bm[w] : 0ull;
+        cnt += (uint32_t)__popcll(words[i]);
+    }
+    uint64_t total;
+    uint64_t excl = block_excl_scan(cnt, s_wave, &total);
+    uint64_t prefix = tile_lookback(desc_w + (size_t)b * tiles_w, tile, total, &s_prefix);
+    uint32_t r = (uint32_t)(prefix + excl);
+    uint32_t* wr = word_rank + (size_t)b * W;
+    uint32_t* vl = vox_lin + (size_t)b * N;
+    uint32_t* vc = vox_count + (size_t)b * N;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t w = w0 + i;
+        if (w >= W) break;
+        wr[w] = r;
+        uint64_t m = words[i];
+        while (m) {
+            int bit = __ffsll((unsigned long long)m) - 1;
+            vl[r] = (uint32_t)(w * 64 + bit);
+            vc[r] = 0u;
+            ++r;
+            m &= m - 1;
+        }
+    }
+    if (tile == tiles_w - 1 && threadIdx.x == 0) nvox[b] = (int32_t)(prefix + total);
+}
+
+// One lane per point: slot (rank of its voxel) and arrival position.
+__global__ __launch_bounds__(256) void k_count(int32_t BN, int32_t N, int64_t W,
+                                               const uint64_t* __restrict__ bitmap,
+                                               const uint32_t* __restrict__ word_rank,
+                                               uint32_t* __restrict__ pt_slot, uint32_t* __restrict__ pt_pos,
+                                               uint32_t* __restrict__ vox_count) {
+    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= BN) return;
+    int32_t b = gid / N;
+    uint32_t lin = pt_slot[gid];
+    uint32_t slot = (uint32_t)slot_of(bitmap + (size_t)b * W, word_rank + (size_t)b * W, lin);
+    uint32_t pos = atomicAdd(&vox_count[(size_t)b * N + slot], 1u);
+    pt_slot[gid] = slot;
+    pt_pos[gid] = pos;
+}
+
+// Offsets: vox_off = exclusive prefix of min(count, n_v), full_off = exclusive
+// prefix of count, over the slots [0, nvox[b]) of each cloud; entry nvox[b]
+// holds the totals. Both are scanned at once, packed as (full << 31) | stored.
+__global__ __launch_bounds__(kScanThreads) void k_offsets(
+    int32_t N, int64_t tiles_s, uint32_t n_v, const int32_t* __restrict__ nvox,
+    const uint32_t* __restrict__ vox_count, uint32_t* __restrict__ vox_off, uint32_t* __restrict__ full_off,
+    uint64_t* __restrict__ desc_s, int* __restrict__ status, uint32_t* __restrict__ big, int64_t big_cap) {
+    __shared__ uint32_t s_ticket;
+    __shared__ uint64_t s_wave[kScanThreads / kWave];
+    __shared__ uint64_t s_prefix;
+    if (threadIdx.x == 0) s_ticket = atomicAdd((unsigned*)&status[kStTicketOff], 1u);
+    __syncthreads();
+    const uint32_t t = s_ticket;
+    const int32_t b = (int32_t)(t / tiles_s);
+    const int64_t tile = (int64_t)(t % tiles_s);
+    const int64_t nv = nvox[b];
+    if (tile * kScanTile >= nv) return;  // no slot here; later tiles never wait on this one
+    const int64_t s0 = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    const uint32_t* vc = vox_count + (size_t)b * N;
+    uint32_t cnt[kScanItems];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t s = s0 + i;
+        cnt[i] = s < nv ? vc[s] : 0u;
+        uint32_t st = cnt[i] < n_v ? cnt[i] : n_v;
+        sum += ((uint64_t)cnt[i] << 31) | st;
+        if (cnt[i] > kBigVoxel) {
+            uint32_t k = atomicAdd((unsigned*)&status[kStBigCount], 1u);
+            if ((int64_t)k < big_cap) big[k] = (uint32_t)((size_t)b * N + s);
+        }
+    }
+    uint64_t total;
+    uint64_t excl = block_excl_scan(sum, s_wave, &total);
+    uint64_t run = tile_lookback(desc_s + (size_t)b * tiles_s, tile, total, &s_prefix) + excl;
+    uint32_t* vo = vox_off + (size_t)b * (N + 1);
+    uint32_t* fo = full_off + (size_t)b * (N + 1);
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        int64_t s = s0 + i;
+        if (s > nv) break;
+        vo[s] = (uint32_t)(run & 0x7FFFFFFFu);
+        fo[s] = (uint32_t)(run >> 31);
+        if (s < nv) {
+            uint32_t st = cnt[i] < n_v ? cnt[i] : n_v;
+            run += ((uint64_t)cnt[i] << 31) | st;
+        }
+    }
+    // the slot nvox sits in the next tile when nvox is a multiple of the tile size
+    if (threadIdx.x == 0 && nv == (tile + 1) * kScanTile) {
+        uint64_t end = s_prefix + total;
+        vo[nv] = (uint32_t)(end & 0x7FFFFFFFu);
+        fo[nv] = (uint32_t)(end >> 31);
+    }
+}
+
+// One lane per point: its index into the bucket of its slot.
+__global__ __launch_bounds__(256) void k_scatter(int32_t BN, int32_t N, const uint32_t* __restrict__ pt_slot,
+                                                 const uint32_t* __restrict__ pt_pos,
+                                                 const uint32_t* __restrict__ full_off,
+                                                 uint32_t* __restrict__ bucket) {
+    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= BN) return;
+    int32_t b = gid / N;
+    uint32_t slot = pt_slot[gid];
+    bucket[(size_t)b * N + full_off[(size_t)b * (N + 1) + slot] + pt_pos[gid]] = (uint32_t)(gid - b * N);
+}
+
+// Stored lists. Blocks [0, part_a): one lane per point of a voxel with at
+// most kBigVoxel points -- its rank among the voxel's indices places it.
+// Blocks [part_a, grid): one wave per larger voxel -- the n_v smallest
+// indices by bitonic selection in 64-key chunks.
+__global__ __launch_bounds__(256) void k_finalize(
+    const float* __restrict__ P, int32_t BN, int32_t N, uint32_t n_v, int32_t part_a,
+    const uint32_t* __restrict__ pt_slot, const uint32_t* __restrict__ vox_count,
+    const uint32_t* __restrict__ vox_off, const uint32_t* __restrict__ full_off,
+    const uint32_t* __restrict__ bucket, const uint32_t* __restrict__ big, int64_t big_cap,
+    const int* __restrict__ status, uint32_t* __restrict__ pt_list, float4* __restrict__ pt4) {
+    if ((int32_t)blockIdx.x < part_a) {
+        int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+        if (gid >= BN) return;
+        int32_t b = gid / N;
+        uint32_t i = (uint32_t)(gid - b * N);
+        uint32_t slot = pt_slot[gid];
+        size_t sg = (size_t)b * N + slot;
+        uint32_t cnt = vox_count[sg];
+        if (cnt > kBigVoxel) return;
+        const uint32_t* bk = bucket + (size_t)b * N + full_off[(size_t)b * (N + 1) + slot];
+        uint32_t rank = 0;
+        for (uint32_t j = 0; j < cnt; ++j) rank += bk[j] < i ? 1u : 0u;
+        if (rank < n_v) {
+            size_t dst = (size_t)b * N + vox_off[(size_t)b * (N + 1) + slot] + rank;
+            const float* p = P + (size_t)gid * 3;
+            pt_list[dst] = i;
+            pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+        }
+        return;
+    }
+    const int lane = lane_id();
+    const int32_t nbig = (int64_t)status[kStBigCount] < big_cap ? status[kStBigCount] : (int32_t)big_cap;
+    const int32_t wpb = blockDim.x / kWave;
+    const int32_t nwaves = (gridDim.x - part_a) * wpb;
+    for (int32_t v = (blockIdx.x - part_a) * wpb + threadIdx.x / kWave; v < nbig; v += nwaves) {
+        uint32_t g = big[v];
+        int32_t b = (int32_t)(g / (uint32_t)N);
+        uint32_t s = g - (uint32_t)b * N;
+        uint32_t cnt = vox_count[g];
+        const uint32_t* bk = bucket + (size_t)b * N + full_off[(size_t)b * (N + 1) + s];
+        uint64_t best = ~0ull;
+        for (uint32_t c0 = 0; c0 < cnt; c0 += kWave) {
+            uint64_t k = (c0 + lane < cnt) ? (uint64_t)bk[c0 + lane] : ~0ull;
+            k = wave_sort64(k);
+            best = c0 == 0 ? k : wave_merge_low64(best, k);
+        }
+        if ((uint32_t)lane < n_v) {
+            uint32_t i = (uint32_t)best;
+            size_t dst = (size_t)b * N + vox_off[(size_t)b * (N + 1) + s] + lane;
+            const float* p = P + ((size_t)b * N + i) * 3;
+            pt_list[dst] = i;
+            pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_desc& d, void* ws,
+                        hipStream_t s) {
+    const int32_t B = L.B, N = L.N, BN = B * N;
+    const GridArgs g = grid_args(d);
+    int* status = at<int>(ws, L.status);
+    size_t n16 = (L.clear_end - L.status) / 16;
+    int cb = (int)((n16 + 255) / 256);
+    if (cb > 4096) cb = 4096;
+    k_clear<<<cb, 256, 0, s>>>(at<uint4>(ws, L.status), n16);
+    const int pb = (BN + 255) / 256;
+    k_mark<<<pb, 256, 0, s>>>(points, N, BN, g, L.W, at<uint32_t>(ws, L.pt_slot), at<uint64_t>(ws, L.bitmap),
+                              status);
+    k_rank<<<(unsigned)(B * L.tiles_w), kScanThreads, 0, s>>>(
+        at<uint64_t>(ws, L.bitmap), L.W, L.tiles_w, N, at<uint32_t>(ws, L.word_rank),
+        at<uint32_t>(ws, L.vox_lin), at<uint32_t>(ws, L.vox_count), at<int32_t>(ws, L.nvox),
+        at<uint64_t>(ws, L.desc_w), status);
+    k_count<<<pb, 256, 0, s>>>(BN, N, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
+                               at<uint32_t>(ws, L.pt_slot), at<uint32_t>(ws, L.pt_pos),
+                               at<uint32_t>(ws, L.vox_count));
+    k_offsets<<<(unsigned)(B * L.tiles_s), kScanThreads, 0, s>>>(
+        N, L.tiles_s, (uint32_t)d.n_v, at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_count),
+        at<uint32_t>(ws, L.vox_off), at<uint32_t>(ws, L.full_off), at<uint64_t>(ws, L.desc_s), status,
+        at<uint32_t>(ws, L.big), L.big_cap);
+    k_scatter<<<pb, 256, 0, s>>>(BN, N, at<uint32_t>(ws, L.pt_slot), at<uint32_t>(ws, L.pt_pos),
+                                 at<uint32_t>(ws, L.full_off), at<uint32_t>(ws, L.bucket));
+    int64_t bigb = (L.big_cap + 3) / 4;
+    if (bigb > 1024) bigb = 1024;
+    if (bigb < 1) bigb = 1;
+    k_finalize<<<(unsigned)(pb + bigb), 256, 0, s>>>(
+        points, BN, N, (uint32_t)d.n_v, pb, at<uint32_t>(ws, L.pt_slot), at<uint32_t>(ws, L.vox_count),
+        at<uint32_t>(ws, L.vox_off), at<uint32_t>(ws, L.full_off), at<uint32_t>(ws, L.bucket),
+        at<uint32_t>(ws, L.big), L.big_cap, status, at<uint32_t>(ws, L.pt_list), at<float4>(ws, L.pt4));
+    return hipGetLastError();
+}
+
+}  // namespace cagq

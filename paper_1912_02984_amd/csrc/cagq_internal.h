@@ -1,0 +1,226 @@
+// Internal declarations of the gfx950 CAGQ library: workspace layout,
+// device helpers shared by the build, sampling and query kernels, and the
+// host-side launch functions the C ABI (cagq_api.hip) sequences.
+//
+// Everything here is HIP for gfx950 only (64-lane wavefronts).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "cagq.h"
+
+namespace cagq {
+
+constexpr int kWave = 64;
+constexpr int kScanThreads = 256;       // threads per scan tile
+constexpr int kScanItems = 4;           // items per thread in a scan tile
+constexpr int kScanTile = kScanThreads * kScanItems;
+constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
+
+// Status word slots (int32 each) at the start of the workspace's control block.
+enum StatusSlot {
+    kStError = 0,      // first device-side error code (0 = none)
+    kStTicketRank = 1, // tile tickets of the occupancy-rank scan
+    kStTicketOff = 2,  // tile tickets of the offsets scan
+    kStBigCount = 3,   // number of voxels with more than kBigVoxel points
+    kStSlots = 16
+};
+
+// Byte offsets of every array in the caller's workspace. Exposed arrays first
+// (their offsets are also published through cagq_layout), then internal ones.
+struct Layout {
+    int32_t B, N;
+    int64_t V;            // voxels per grid
+    int64_t W;            // 64-bit occupancy words per cloud
+    int64_t tiles_w;      // scan tiles over the words of one cloud
+    int64_t tiles_s;      // scan tiles over the slots of one cloud
+    int64_t big_cap;      // capacity of the big-voxel list
+    size_t total;
+    // exposed
+    size_t nvox, vox_lin, vox_count, vox_off, pt_list;
+    // internal
+    size_t status;        // int32[kStSlots]
+    size_t desc_w;        // u64 [B][tiles_w] scan descriptors (occupancy ranks)
+    size_t desc_s;        // u64 [B][tiles_s] scan descriptors (offsets)
+    size_t bitmap;        // u64 [B][W] occupancy bits, bit (lin & 63) of word lin >> 6
+    size_t word_rank;     // u32 [B][W] occupied voxels before word w (the slot of its first bit)
+    size_t pt_slot;       // u32 [B][N] per point: linear id, then slot
+    size_t pt_pos;        // u32 [B][N] per point: arrival position inside its voxel
+    size_t full_off;      // u32 [B][N+1] exclusive prefix of the full counts
+    size_t bucket;        // u32 [B][N] every point index grouped by slot (arrival order)
+    size_t pt4;           // float4 [B][N] stored points grouped by slot: x, y, z, bits(index)
+    size_t big;           // u32 [big_cap] global slot ids (b*N + s) of big voxels
+    size_t cas_cover;     // u32 [B][N] CAS: centers whose neighbourhood holds the voxel
+    size_t cas_key;       // u64 [B][N] CAS: key of an unpicked voxel in the current round
+    size_t cas_pick;      // u64 [B][N] CAS: key at pick time (0 = unpicked)
+    size_t cas_round;     // u32 [B][N] CAS: round that picked the voxel + 1 (0 = unpicked)
+    size_t cas_ctl;       // CAS control block, see CasCtl
+    size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
+};
+
+// CAS control block (per cloud arrays), placed at Layout::cas_ctl.
+struct CasCtl {
+    // u64 gmax[2][B]; u32 count[2][B]; u32 done[B]; (laid out in this order)
+    static size_t bytes(int B) { return (size_t)B * (16 + 8 + 4) + 64; }
+};
+
+bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L);
+
+template <typename T>
+__host__ __device__ inline T* at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+// ------------------------------------------------------------------ device helpers
+
+// splitmix64 output function (Steele, Lea, Flood, OOPSLA 2014): the state
+// x is advanced by the golden gamma, then mixed by two xor-shift-multiplies.
+__device__ __forceinline__ uint64_t sm64(uint64_t x) {
+    uint64_t z = x + 0x9E3779B97F4A7C15ull;
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int src) {
+    int lo = __shfl((int)(uint32_t)v, src, kWave);
+    int hi = __shfl((int)(uint32_t)(v >> 32), src, kWave);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t v, int m) {
+    int lo = __shfl_xor((int)(uint32_t)v, m, kWave);
+    int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, kWave);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+__device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
+    int lo = __shfl_up((int)(uint32_t)v, d, kWave);
+    int hi = __shfl_up((int)(uint32_t)(v >> 32), d, kWave);
+    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave.
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        T o;
+        if constexpr (sizeof(T) == 8) o = (T)shfl_up64((uint64_t)v, d);
+        else o = (T)__shfl_up((int)v, d, kWave);
+        if (lane >= d) v += o;
+    }
+    return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        if constexpr (sizeof(T) == 8) v += (T)shfl_xor64((uint64_t)v, d);
+        else v += (T)__shfl_xor((int)v, d, kWave);
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        uint64_t o = shfl_xor64(v, d);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+// Ascending bitonic sort of one 64-bit key per lane over the whole wave.
+__device__ __forceinline__ uint64_t wave_sort64(uint64_t v) {
+    const int lane = lane_id();
+#pragma unroll
+    for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            uint64_t o = shfl_xor64(v, j);
+            bool asc = (lane & k) == 0;
+            bool low = (lane & j) == 0;
+            uint64_t mn = o < v ? o : v, mx = o < v ? v : o;
+            v = (asc == low) ? mn : mx;
+        }
+    }
+    return v;
+}
+
+// `best` and `add` each sorted ascending over the wave: returns the 64
+// smallest keys of their union, sorted ascending.
+__device__ __forceinline__ uint64_t wave_merge_low64(uint64_t best, uint64_t add) {
+    const int lane = lane_id();
+    uint64_t rev = shfl64(add, kWave - 1 - lane);
+    uint64_t v = rev < best ? rev : best;     // bitonic: the 64 smallest of the union
+#pragma unroll
+    for (int j = kWave >> 1; j > 0; j >>= 1) {
+        uint64_t o = shfl_xor64(v, j);
+        bool low = (lane & j) == 0;
+        uint64_t mn = o < v ? o : v, mx = o < v ? v : o;
+        v = low ? mn : mx;
+    }
+    return v;
+}
+
+// Agent-scope atomics for the cross-workgroup scan descriptors (the 8 XCDs
+// have separate L2s, so these must reach the coherent level).
+__device__ __forceinline__ uint64_t ld_acquire(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_release(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void raise_error(int* status, int code) {
+    atomicCAS(status + kStError, 0, code);
+}
+
+// Block id remapped so that consecutive logical blocks share an XCD (blocks
+// are dispatched to the 8 XCDs round-robin; each XCD has its own L2).
+__device__ __forceinline__ uint32_t xcd_block(uint32_t bid, uint32_t nblocks) {
+    const uint32_t nx = 8;
+    uint32_t q = nblocks / nx, rem = nblocks % nx;
+    uint32_t x = bid % nx, i = bid / nx;
+    return x < rem ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
+}
+
+// Slot of the occupied voxel `lin` of a cloud (the number of occupied voxels
+// with a smaller linear id), or -1 when it is empty.
+__device__ __forceinline__ int32_t slot_of(const uint64_t* bm, const uint32_t* wr, uint32_t lin) {
+    uint64_t w = bm[lin >> 6];
+    uint64_t bit = 1ull << (lin & 63);
+    if (!(w & bit)) return -1;
+    return (int32_t)(wr[lin >> 6] + __popcll(w & (bit - 1)));
+}
+
+// ------------------------------------------------------------------ host launchers
+
+// Build: voxelize, occupancy bitmap, slots, counts, offsets, capped lists.
+hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_desc& d,
+                        void* ws, hipStream_t s);
+
+// Selects, per cloud, the m = min(M, nvox) slots with the smallest key and
+// writes their linear ids in ascending slot order (cyclic padding to M).
+// key_mode 0: RVS keys from `seed`; key_mode 1: CAS pick keys (largest first).
+hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
+                         int32_t* center_lin, int32_t* m_valid, hipStream_t s);
+
+// Greedy coverage-aware sampling (rounds of neighbourhood maxima).
+hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M,
+                   uint32_t beta_q16, hipStream_t s, int* status_out);
+
+hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* points, void* ws,
+                        const uint32_t* weights, const int32_t* center_lin, int32_t M, int32_t K,
+                        int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz,
+                        int32_t* n_valid, float* center_xyz, uint32_t* center_w,
+                        int32_t* ctx_count, hipStream_t s);
+
+}  // namespace cagq

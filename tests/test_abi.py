@@ -1,0 +1,150 @@
+"""The C-ABI library without a GPU: it loads, exports every entry point the
+header declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_1912_02984_amd import cagq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cagq.h")
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"CAGQ_API\s+[\w\s\*]*?\b(cagq_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    syms = declared_symbols()
+    for name in ("cagq_build_grid", "cagq_sample_centers", "cagq_query_context",
+                 "cagq_workspace_layout", "cagq_get_device_status", "cagq_status_string"):
+        assert name in syms
+
+
+def test_library_exports_every_declared_symbol():
+    L = C.CDLL(cagq.LIB_PATH)
+    for name in declared_symbols():
+        assert hasattr(L, name), name
+
+
+def test_library_exports_nothing_else():
+    out = os.popen(f"nm -D --defined-only {cagq.LIB_PATH}").read()
+    exported = sorted(l.split()[-1] for l in out.splitlines() if " T " in l)
+    assert exported == declared_symbols()
+
+
+def test_status_strings():
+    assert cagq.status_string(0) == "ok"
+    for code in range(-7, 0):
+        assert cagq.status_string(code) != "unknown status"
+    assert cagq.status_string(-99) == "unknown status"
+
+
+def _desc(dims=(40, 40, 40), n_v=8, r=1, size=(0.025,) * 3, origin=(0, 0, 0)):
+    return cagq.make_desc(origin, size, dims, n_v, r)
+
+
+def _layout(B, N, d):
+    out = cagq.LayoutC()
+    return cagq.lib().cagq_workspace_layout(B, N, C.byref(d), C.byref(out)), out
+
+
+def test_layout_sizes_and_alignment():
+    rc, L = _layout(4, 81920, _desc(dims=(168, 168, 68), n_v=32))
+    assert rc == 0
+    offs = [L.nvox, L.vox_lin, L.vox_count, L.vox_off, L.pt_list]
+    assert all(o % 256 == 0 for o in offs)
+    assert offs == sorted(offs) and L.total_bytes > L.pt_list + 4 * 4 * 81920
+    # arrays do not overlap
+    sizes = [4 * 4, 4 * 4 * 81920, 4 * 4 * 81920, 4 * 4 * 81921, 4 * 4 * 81920]
+    for (o, s), o2 in zip(zip(offs, sizes), offs[1:] + [L.total_bytes]):
+        assert o + s <= o2
+
+
+@pytest.mark.parametrize("bad, code", [
+    (dict(dims=(0, 4, 4)), cagq.ERR_INVALID_ARG),
+    (dict(dims=(2048, 2048, 1024)), cagq.ERR_GRID_TOO_LARGE),
+    (dict(n_v=0), cagq.ERR_INVALID_ARG),
+    (dict(n_v=65), cagq.ERR_INVALID_ARG),
+    (dict(r=0), cagq.ERR_INVALID_ARG),
+    (dict(r=4), cagq.ERR_INVALID_ARG),
+    (dict(size=(0.0, 1.0, 1.0)), cagq.ERR_INVALID_ARG),
+    (dict(size=(float("nan"), 1.0, 1.0)), cagq.ERR_INVALID_ARG),
+    (dict(origin=(float("inf"), 0, 0)), cagq.ERR_INVALID_ARG),
+])
+def test_layout_rejects_bad_grids(bad, code):
+    rc, _ = _layout(1, 100, _desc(**bad))
+    assert rc == code
+
+
+def test_layout_rejects_bad_sizes():
+    d = _desc()
+    assert _layout(0, 10, d)[0] == cagq.ERR_INVALID_ARG
+    assert _layout(1, 0, d)[0] == cagq.ERR_INVALID_ARG
+    assert _layout(65536, 65536, d)[0] == cagq.ERR_INVALID_ARG
+
+
+def test_build_rejects_bad_arguments_before_any_device_work():
+    L = cagq.lib()
+    d = _desc()
+    g = cagq.GridC()
+    fake = C.c_void_p(0x100000)  # never dereferenced: validation fails first
+    # null points / workspace / out
+    assert L.cagq_build_grid(None, 1, 10, C.byref(d), fake, 1 << 30, None, C.byref(g)) == cagq.ERR_INVALID_ARG
+    assert L.cagq_build_grid(fake, 1, 10, C.byref(d), None, 1 << 30, None, C.byref(g)) == cagq.ERR_INVALID_ARG
+    assert L.cagq_build_grid(fake, 1, 10, C.byref(d), fake, 1 << 30, None, None) == cagq.ERR_INVALID_ARG
+    # misaligned workspace
+    assert L.cagq_build_grid(fake, 1, 10, C.byref(d), C.c_void_p(0x100010), 1 << 30, None,
+                             C.byref(g)) == cagq.ERR_INVALID_ARG
+    # workspace too small
+    assert L.cagq_build_grid(fake, 1, 10, C.byref(d), fake, 16, None, C.byref(g)) == cagq.ERR_WORKSPACE_TOO_SMALL
+    # grid too large
+    big = _desc(dims=(2048, 2048, 1024))
+    assert L.cagq_build_grid(fake, 1, 10, C.byref(big), fake, 1 << 30, None, C.byref(g)) == cagq.ERR_GRID_TOO_LARGE
+
+
+def _grid_record(B=1, N=100, ws_bytes=None):
+    d = _desc()
+    rc, lay = _layout(B, N, d)
+    assert rc == 0
+    g = cagq.GridC()
+    g.B, g.N, g.desc = B, N, d
+    g.points = 0x100000
+    g.workspace = 0x200000
+    g.workspace_bytes = lay.total_bytes if ws_bytes is None else ws_bytes
+    return g
+
+
+def test_sample_rejects_bad_arguments():
+    L = cagq.lib()
+    g = _grid_record()
+    p = C.c_void_p(0x300000)
+    assert L.cagq_sample_centers(C.byref(g), 0, 0, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_sample_centers(C.byref(g), 8, 2, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_sample_centers(C.byref(g), 8, 0, 1, 0, None, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_sample_centers(C.byref(g), 8, 0, 1, 0, p, None, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_sample_centers(None, 8, 0, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
+    # CAS score range: (2^16 + beta) * lambda^2 must stay below 2^31
+    assert L.cagq_sample_centers(C.byref(g), 8, 1, 1, 1 << 22, p, p, None) == cagq.ERR_INVALID_ARG
+    small = _grid_record(ws_bytes=1024)
+    assert L.cagq_sample_centers(C.byref(small), 8, 0, 1, 0, p, p, None) == cagq.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_query_rejects_bad_arguments():
+    L = cagq.lib()
+    g = _grid_record()
+    p = C.c_void_p(0x300000)
+    args = lambda K=16, mode=0, M=8, ni=p, nv=p, cx=p, cw=p, cl=p: L.cagq_query_context(
+        C.byref(g), None, cl, M, K, mode, 1, ni, None, nv, cx, cw, None, None)
+    assert args(K=0) == cagq.ERR_INVALID_ARG
+    assert args(K=65) == cagq.ERR_INVALID_ARG
+    assert args(mode=2) == cagq.ERR_INVALID_ARG
+    assert args(M=0) == cagq.ERR_INVALID_ARG
+    assert args(ni=None) == cagq.ERR_INVALID_ARG
+    assert args(nv=None) == cagq.ERR_INVALID_ARG
+    assert args(cx=None) == cagq.ERR_INVALID_ARG
+    assert args(cw=None) == cagq.ERR_INVALID_ARG
+    assert args(cl=None) == cagq.ERR_INVALID_ARG

@@ -1,0 +1,229 @@
+"""HIP path vs the CPU oracle, element by element, bit-exact.
+
+Every integer output (slots, counts, offsets, lists, centers, node indices,
+counts of valid nodes, weights) must be equal; every float output (node
+coordinates, group centers) must have the same bit pattern. Inputs are the
+seeded synthetic workloads at their full sizes plus hand-built edge cases.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1912_02984_amd import cagq
+from paper_1912_02984_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def _bits(a):
+    return np.ascontiguousarray(a).view(np.uint32)
+
+
+def assert_table(g, ot, where=""):
+    tb = {k: _np(v) for k, v in g.table().items()}
+    assert np.array_equal(tb["nvox"], ot.nvox), where
+    for b in range(ot.B):
+        nv = int(ot.nvox[b])
+        S = int(ot.vox_off[b, nv])
+        assert np.array_equal(_bits(tb["vox_lin"][b, :nv]), ot.vox_lin[b, :nv]), (where, b)
+        assert np.array_equal(_bits(tb["vox_count"][b, :nv]), ot.vox_count[b, :nv]), (where, b)
+        assert np.array_equal(_bits(tb["vox_off"][b, :nv + 1]), ot.vox_off[b, :nv + 1]), (where, b)
+        assert np.array_equal(_bits(tb["pt_list"][b, :S]), ot.pt_list[b, :S]), (where, b)
+
+
+def assert_query(qg, qo, where=""):
+    assert np.array_equal(_np(qg["node_idx"]), qo["node_idx"]), where
+    assert np.array_equal(_np(qg["n_valid"]), qo["n_valid"]), where
+    assert np.array_equal(_bits(_np(qg["center_w"])), qo["center_w"]), where
+    assert np.array_equal(_bits(_np(qg["center_xyz"])), _bits(qo["center_xyz"])), where
+    if qg.get("node_xyz") is not None:
+        assert np.array_equal(_bits(_np(qg["node_xyz"])), _bits(qo["node_xyz"])), where
+    if qg.get("ctx_count") is not None:
+        assert np.array_equal(_np(qg["ctx_count"]), qo["ctx_count"]), where
+
+
+def run_both(P, grid_spec, M, K, sample, query, seed, weights=None, beta_q16=0, where=""):
+    """One layer on both sides from the same float32 input; checks every output."""
+    P = np.ascontiguousarray(P, np.float32)
+    ot = oracle.Table(P, oracle.grid_from_spec(grid_spec))
+    if sample == "rvs":
+        ocl, omv = ot.sample_rvs(M, seed)
+    else:
+        ocl, omv, _, _ = ot.sample_cas(M, beta_q16)
+    qo = ot.query(ocl, omv, K, query, seed, weights=weights)
+
+    Pt = torch.from_numpy(P).to(DEV)
+    Wt = None if weights is None else torch.from_numpy(weights.astype(np.uint32).view(np.int32)).to(DEV)
+    g = cagq.build_grid(Pt, cagq.desc_from_spec(grid_spec))
+    cl, mv = cagq.sample_centers(g, M, sample, seed, beta_q16)
+    qg = cagq.query_context(g, cl, K, query, seed, weights=Wt)
+    assert cagq.get_device_status(g) == 0, where
+    assert_table(g, ot, where)
+    assert np.array_equal(_np(mv), omv), where
+    assert np.array_equal(_np(cl), ocl), where
+    assert_query(qg, qo, where)
+    return qo
+
+
+@pytest.mark.parametrize("sample", ["rvs", "cas"])
+@pytest.mark.parametrize("query", ["cube", "knn"])
+def test_tiny_all_modes(sample, query):
+    w = W.get_workload("tiny")
+    L = w.layers[0]
+    run_both(w.points(), L.grid, L.M, L.K, sample, query, L.seed, where=f"tiny {sample} {query}")
+
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room", "bigroom/cas-knn", "bigroom/rvs-cube", "lidar"])
+def test_workload_full_size(name):
+    """Every layer of the workload at its full size, chained through the
+    centers and weights each side produced."""
+    w = W.get_workload(name)
+    P = w.points()
+    weights = None
+    for li, L in enumerate(w.layers):
+        print(f"[parity] {name} layer {li}: B={P.shape[0]} N={P.shape[1]} M={L.M} K={L.K} "
+              f"{L.sample}+{L.query}", flush=True)
+        qo = run_both(P, L.grid, L.M, L.K, L.sample, L.query, L.seed, weights=weights,
+                      where=f"{name} L{li}")
+        P, weights = qo["center_xyz"], qo["center_w"]
+
+
+def _spec(origin, size, dims, n_v, r=1):
+    return W.GridSpec(tuple(origin), tuple(size), tuple(dims), n_v, r)
+
+
+def test_capped_and_big_voxels():
+    """Voxels holding up to a few hundred points: the cap keeps the lowest
+    indices, through both the per-point ranking and the wave selection."""
+    rng = np.random.default_rng(5)
+    B, N = 3, 5000
+    P = rng.random((B, N, 3), dtype=np.float32)
+    # a third of each cloud crowds into three voxels
+    P[:, : N // 3] = (np.float32(0.01) + rng.random((B, N // 3, 3), dtype=np.float32) * np.float32(0.02))
+    P[:, N // 3: N // 3 + 200] = np.float32(0.55)
+    spec = _spec((0, 0, 0), (0.125,) * 3, (8, 8, 8), 16)
+    for n_v in (1, 4, 16, 64):
+        s = _spec((0, 0, 0), (0.125,) * 3, (8, 8, 8), n_v)
+        run_both(P, s, 40, 32, "rvs", "knn", 3, where=f"n_v={n_v}")
+    run_both(P, spec, 12, 64, "cas", "cube", 9, where="cas")
+
+
+def test_all_points_in_one_voxel():
+    P = np.full((2, 777, 3), 0.3, np.float32)
+    P[1] += np.linspace(0, 0.01, 777, dtype=np.float32)[:, None]
+    run_both(P, _spec((0, 0, 0), (1.0,) * 3, (4, 4, 4), 64), 5, 64, "rvs", "knn", 1, where="one voxel")
+    run_both(P, _spec((0, 0, 0), (1.0,) * 3, (4, 4, 4), 3), 5, 8, "cas", "cube", 1, where="one voxel cas")
+
+
+@pytest.mark.parametrize("nvox", [1023, 1024, 1025, 2048, 3072])
+def test_slot_count_at_scan_tile_edges(nvox):
+    """Occupied-voxel counts on both sides of the scan tile size."""
+    rng = np.random.default_rng(nvox)
+    dims = (64, 64, 4)
+    lin = rng.choice(64 * 64 * 4, size=nvox, replace=False)
+    g = np.stack([lin % 64, (lin // 64) % 64, lin // 4096], 1).astype(np.float32)
+    P = ((g + np.float32(0.5)) * np.float32(0.1))[None]
+    extra = P[:, rng.integers(0, nvox, size=500)] + np.float32(0.01)
+    P = np.concatenate([P, extra], axis=1)[:, rng.permutation(nvox + 500)]
+    run_both(P, _spec((0, 0, 0), (0.1,) * 3, dims, 4), 300, 16, "rvs", "cube", 2, where=f"nvox={nvox}")
+
+
+def test_ragged_batch_and_clamping():
+    """B*N not a multiple of the block size; points outside the grid and on
+    voxel faces are clamped, not dropped."""
+    rng = np.random.default_rng(11)
+    B, N = 3, 1001
+    P = (rng.random((B, N, 3), dtype=np.float32) * np.float32(3.0) - np.float32(1.0))
+    P[0, :50] = np.float32(0.25) * rng.integers(0, 5, size=(50, 3)).astype(np.float32)  # exact faces
+    spec = _spec((0, 0, 0), (0.25,) * 3, (4, 5, 6), 8)
+    run_both(P, spec, 17, 8, "rvs", "knn", 4, where="ragged rvs")
+    run_both(P, spec, 17, 8, "cas", "knn", 4, where="ragged cas")
+
+
+def test_more_centers_than_occupied_voxels():
+    rng = np.random.default_rng(2)
+    P = rng.random((2, 50, 3), dtype=np.float32) * np.float32(0.5)
+    spec = _spec((0, 0, 0), (0.25,) * 3, (2, 2, 2), 8)
+    run_both(P, spec, 20, 16, "rvs", "knn", 7, where="M>nvox rvs")
+    run_both(P, spec, 20, 16, "cas", "cube", 7, where="M>nvox cas")
+
+
+@pytest.mark.parametrize("K", [1, 2, 31, 33, 64])
+def test_node_counts(K):
+    w = W.get_workload("room")
+    L = w.layers[0]
+    P = w.points(B=2)
+    run_both(P, L.grid, 256, K, "rvs", "knn", 5, where=f"K={K} knn")
+    run_both(P, L.grid, 256, K, "rvs", "cube", 5, where=f"K={K} cube")
+
+
+@pytest.mark.parametrize("r", [2, 3])
+def test_wider_neighbourhoods(r):
+    w = W.get_workload("room")
+    L = w.layers[0]
+    spec = _spec(L.grid.origin, L.grid.voxel_size, L.grid.dims, 16, r)
+    P = w.points(B=2)
+    run_both(P, spec, 300, 32, "rvs", "knn", 8, where=f"r={r} knn")
+    run_both(P, spec, 300, 32, "rvs", "cube", 8, where=f"r={r} cube")
+    if r == 2:
+        run_both(P, spec, 300, 32, "cas", "knn", 8, where=f"r={r} cas")
+
+
+@pytest.mark.parametrize("beta_q16", [1, 65536 // 4, 3 * 65536])
+def test_cas_with_overcoverage_penalty(beta_q16):
+    w = W.get_workload("object")
+    L = w.layers[0]
+    run_both(w.points()[:4], L.grid, L.M, L.K, "cas", "knn", 0, beta_q16=beta_q16, where=f"beta={beta_q16}")
+
+
+def test_weighted_centers():
+    w = W.get_workload("room")
+    L = w.layers[0]
+    P = w.points(B=2)
+    wts = np.random.default_rng(3).integers(1, 1000, size=P.shape[:2]).astype(np.uint32)
+    run_both(P, L.grid, 512, 32, "rvs", "knn", 1, weights=wts, where="weights knn")
+    run_both(P, L.grid, 512, 32, "rvs", "cube", 1, weights=wts, where="weights cube")
+
+
+def test_repeat_runs_are_identical():
+    """Atomic arrival order never reaches an output."""
+    w = W.get_workload("bigroom/rvs-cube")
+    L = w.layers[0]
+    Pt = torch.from_numpy(w.points(B=2)).to(DEV)
+    outs = []
+    for _ in range(3):
+        g = cagq.build_grid(Pt, cagq.desc_from_spec(L.grid))
+        cl, mv = cagq.sample_centers(g, L.M, "cas", 0)
+        q = cagq.query_context(g, cl, L.K, "knn", 0)
+        outs.append([_np(v).copy() for v in g.table().values()] + [_np(cl)] + [_np(v) for v in q.values()])
+    for o in outs[1:]:
+        for a, b in zip(outs[0], o):
+            assert np.array_equal(a, b)
+
+
+def test_nonfinite_input_is_reported():
+    P = np.random.default_rng(0).random((1, 100, 3), dtype=np.float32)
+    P[0, 17, 1] = np.nan
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.make_desc((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
+    assert cagq.get_device_status(g) == cagq.ERR_NONFINITE_INPUT
+    # the oracle reports the same condition
+    with pytest.raises(oracle.OracleError, match="-4"):
+        oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
+
+
+def test_unoccupied_center_is_reported():
+    P = np.random.default_rng(0).random((1, 20, 3), dtype=np.float32) * np.float32(0.2)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.make_desc((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
+    assert cagq.get_device_status(g) == 0
+    cl = torch.tensor([[0, 63]], dtype=torch.int32, device=DEV)  # voxel 63 is empty
+    q = cagq.query_context(g, cl, 4, "knn", 0)
+    assert cagq.get_device_status(g) == cagq.ERR_CENTER_NOT_OCCUPIED
+    assert int(q["n_valid"][0, 0]) > 0 and int(q["n_valid"][0, 1]) == 0
+    assert torch.all(q["node_idx"][0, 1] == 0) and torch.all(q["center_xyz"][0, 1] == 0)
