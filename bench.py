@@ -1,0 +1,201 @@
+"""CAGQ throughput on one MI355X.
+
+A step is one pass of the whole CAGQ hot path over one batch: B = 4 synthetic
+indoor scenes of 81920 points, four downsampling layers (voxel sizes 0.05 /
+0.1 / 0.2 / 0.4 m, M = 8192 / 2048 / 512 / 128, K = 32, n_v = 32), run once
+with Coverage-Aware Sampling + k-NN and once with Random Voxel Sampling +
+Cube Query. Each layer builds the grid, samples the centers and queries the
+nodes; layer l+1 consumes the centers and weights of layer l. Inputs are
+resident in HBM before timing starts; workspaces and outputs are allocated
+once, outside the timed region.
+
+Prints one JSON line: points/s over the step, ms per step, a roofline entry
+for the layer-1 query kernel (algorithmic bytes per launch over its HIP-event
+duration on the launch stream) and the CPU oracle timed on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+WORKLOAD = "bigroom"
+VARIANTS = ("bigroom/cas-knn", "bigroom/rvs-cube")
+METRIC = "CAGQ points/sec & ms/batch at 81920 pts; achieved HBM GB/s vs MI355X peak"
+
+
+def query_alg_bytes(M_total: int, K: int, ctx_total: int) -> int:
+    """Algorithmic bytes of one query launch: per center the center id (4 B)
+    and its outputs (node_idx 4K, node_xyz 12K, center_xyz 12, center_w 4,
+    n_valid 4, ctx_count 4); per context point its coordinates and index
+    (16 B)."""
+    return M_total * (16 * K + 28) + 16 * ctx_total
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--batch", type=int, default=4)
+    ap.add_argument("--variants", default="both", choices=["both", "cas-knn", "rvs-cube"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum oracle time to accumulate for the CPU baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              "(the CAGQ path here is single-GPU; see the sharding notes in the design document)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1912_02984_amd import cagq
+    from paper_1912_02984_amd import workloads as W
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    variants = VARIANTS if args.variants == "both" else (f"bigroom/{args.variants}",)
+    wls = [W.get_workload(v) for v in variants]
+    B = args.batch
+    N = wls[0].N
+    P_np = wls[0].points(B=B)
+    P = torch.from_numpy(P_np).to(dev)
+
+    # per variant, per layer: workspace and outputs, allocated once
+    plans = []
+    for w in wls:
+        layers = []
+        n = N
+        for L in w.layers:
+            desc = cagq.desc_from_spec(L.grid)
+            lay = cagq.workspace_layout(B, n, desc)
+            ws = torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev)
+            out = cagq.alloc_query_outputs(B, L.M, L.K, dev)
+            cl = torch.empty((B, L.M), dtype=torch.int32, device=dev)
+            mv = torch.empty((B,), dtype=torch.int32, device=dev)
+            layers.append((L, desc, ws, out, cl, mv))
+            n = L.M
+        plans.append((w, layers))
+
+    q_events = []  # (start, end) around every layer-1 query launch in the timed region
+
+    def step(which, record=False):
+        for w, layers in which:
+            pts, wts = P, None
+            for li, (L, desc, ws, out, cl, mv) in enumerate(layers):
+                g = cagq.build_grid(pts, desc, ws)
+                cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
+                if record and li == 0:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
+                if record and li == 0:
+                    e1.record()
+                    q_events.append((w.name, e0, e1))
+                pts, wts = out["center_xyz"], out["center_w"]
+
+    for _ in range(args.warmup):
+        step(plans)
+    torch.cuda.synchronize()
+    t_ev0 = torch.cuda.Event(enable_timing=True)
+    t_ev1 = torch.cuda.Event(enable_timing=True)
+    wall0 = time.perf_counter()
+    t_ev0.record()
+    for _ in range(args.steps):
+        step(plans, record=True)
+    t_ev1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms_step = t_ev0.elapsed_time(t_ev1) / args.steps
+    points_per_s = B * N / (ms_step / 1e3)
+
+    # per-variant step times (one extra untimed-in-the-metric pass each)
+    variant_ms = {}
+    for plan in plans:
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        reps = 5
+        for _ in range(reps):
+            step([plan])
+        e1.record()
+        torch.cuda.synchronize()
+        variant_ms[plan[0].name] = e0.elapsed_time(e1) / reps
+
+    # roofline of the layer-1 query kernel, per variant
+    roof = {}
+    for w, layers in plans:
+        L, desc, ws, out, cl, mv = layers[0]
+        durs = [a.elapsed_time(b) for name, a, b in q_events if name == w.name]
+        t_ms = float(np.mean(durs))
+        ctx_total = int(out["ctx_count"].sum().item())
+        alg = query_alg_bytes(B * L.M, L.K, ctx_total)
+        gbs = alg / (t_ms / 1e3) / 1e9
+        roof[w.name] = dict(kernel=f"k_query<{L.query}>", us=t_ms * 1e3, alg_bytes=alg, achieved_gbs=gbs,
+                            ctx_total=ctx_total)
+    dom = max(roof.values(), key=lambda r: r["us"])
+    roofline = {"bound": "hbm", "achieved": round(dom["achieved_gbs"], 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(dom["achieved_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": dom["kernel"], "launch_us": round(dom["us"], 2), "alg_bytes": dom["alg_bytes"],
+                "per_variant": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
+                                for k, v in roof.items()}}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        done = 0
+        while True:
+            for w in wls:
+                pts, wts = P_np[:1], None
+                for L in w.layers:
+                    _, _, _, q = oracle.run_layer(pts, L, weights=wts)
+                    pts, wts = q["center_xyz"], q["center_w"]
+            done += 1
+            if time.perf_counter() - t0 >= args.cpu_seconds or done >= 8:
+                break
+        dt = time.perf_counter() - t0
+        cpu = {"value": round(done * N / dt, 1), "unit": "points/s", "cores": 1, "kind": "oracle",
+               "sample": f"{done} pass(es) of the same hot path (all layers, "
+                         f"{'both variants' if len(wls) == 2 else variants[0]}) over 1 of the {B} scenes, "
+                         f"single-threaded C oracle, {dt:.1f} s"}
+
+    line = {
+        "metric": METRIC,
+        "value": round(points_per_s, 1),
+        "unit": "points/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"indoor scenes B={B} x {N} pts, 4 layers "
+                               f"(M=8192/2048/512/128, K=32, n_v=32), "
+                               + (" and ".join(v.split('/')[1] for v in variants)),
+                   "global_batch": B, "points_per_scene": N},
+        "variant_ms": {k: round(v, 4) for k, v in variant_ms.items()},
+        "wall_s": round(wall, 3),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -202,7 +202,14 @@ def test_repeat_runs_are_identical():
         g = cagq.build_grid(Pt, cagq.desc_from_spec(L.grid))
         cl, mv = cagq.sample_centers(g, L.M, "cas", 0)
         q = cagq.query_context(g, cl, L.K, "knn", 0)
-        outs.append([_np(v).copy() for v in g.table().values()] + [_np(cl)] + [_np(v) for v in q.values()])
+        tb = {k: _np(v) for k, v in g.table().items()}
+        valid = [tb["nvox"]]
+        for b in range(2):  # entries past nvox / the stored total are unspecified
+            nv = int(tb["nvox"][b])
+            S = int(tb["vox_off"][b, nv])
+            valid += [tb["vox_lin"][b, :nv], tb["vox_count"][b, :nv], tb["vox_off"][b, :nv + 1],
+                      tb["pt_list"][b, :S]]
+        outs.append(valid + [_np(cl)] + [_np(v) for v in q.values()])
     for o in outs[1:]:
         for a, b in zip(outs[0], o):
             assert np.array_equal(a, b)
