@@ -63,7 +63,10 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_key = take(8 * BN);
     L->cas_pick = take(8 * BN);
     L->cas_round = take(4 * BN);
+    L->cas_blocker = take(4 * BN);
+    L->cas_dirty = take(4 * BN);
     L->cas_ctl = take(CasCtl::bytes(B));
+    L->sel_thr = take(8 * (size_t)B);
     L->total = off;
     return true;
 }

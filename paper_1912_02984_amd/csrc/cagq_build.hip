@@ -56,7 +56,7 @@ __global__ void k_clear(uint4* __restrict__ p, size_t n16) {
 __global__ __launch_bounds__(256) void k_mark(const float* __restrict__ P, int32_t N, int32_t BN,
                                               GridArgs g, int64_t W, uint32_t* __restrict__ pt_lin,
                                               uint64_t* __restrict__ bitmap, int* __restrict__ status) {
-    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (gid >= BN) return;
     int32_t b = gid / N;
     const float* p = P + (size_t)gid * 3;
@@ -78,68 +78,6 @@ __global__ __launch_bounds__(256) void k_mark(const float* __restrict__ P, int32
     uint64_t bit = 1ull << (lin & 63);
     if (!(*word & bit)) atomicOr((unsigned long long*)word, (unsigned long long)bit);
     if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
-}
-
-// Tile descriptors of the look-back scans: status in bits 62-63 (1 = the
-// tile's own aggregate, 2 = inclusive prefix), value in bits 0-61.
-constexpr uint64_t kDescAgg = 1ull << 62;
-constexpr uint64_t kDescInc = 2ull << 62;
-constexpr uint64_t kDescVal = (1ull << 62) - 1;
-
-// Exclusive prefix of `agg` over the tiles before `tile` in one segment.
-// Every thread of the block calls it; wave 0 publishes and looks back. Tiles
-// are numbered by a ticket taken at block start, so every predecessor has
-// started and will publish: the spin always ends.
-__device__ uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
-    if (threadIdx.x < kWave) {
-        const int lane = lane_id();
-        uint64_t excl = 0;
-        if (tile == 0) {
-            if (lane == 0) st_release(desc, kDescInc | agg);
-        } else {
-            if (lane == 0) st_release(desc + tile, kDescAgg | agg);
-            int64_t base = tile - 1;
-            while (true) {
-                int64_t idx = base - lane;
-                uint64_t d = kDescInc;  // before the first tile: an inclusive zero
-                if (idx >= 0) {
-                    do {
-                        d = ld_acquire(desc + idx);
-                    } while ((d >> 62) == 0);
-                }
-                uint64_t inc = __ballot((d >> 62) == 2);
-                if (inc) {
-                    int first = __ffsll((unsigned long long)inc) - 1;
-                    excl += wave_sum<uint64_t>(lane <= first ? (d & kDescVal) : 0ull);
-                    break;
-                }
-                excl += wave_sum<uint64_t>(d & kDescVal);
-                base -= kWave;
-            }
-            if (lane == 0) st_release(desc + tile, kDescInc | (excl + agg));
-        }
-        if (lane == 0) *s_out = excl;
-    }
-    __syncthreads();
-    return *s_out;
-}
-
-// Exclusive scan of one 64-bit value per thread across a 256-thread block;
-// *total receives the block sum.
-__device__ __forceinline__ uint64_t block_excl_scan(uint64_t v, uint64_t* s_wave, uint64_t* total) {
-    uint64_t incl = wave_incl_scan<uint64_t>(v);
-    const int wv = threadIdx.x / kWave;
-    if (lane_id() == kWave - 1) s_wave[wv] = incl;
-    __syncthreads();
-    uint64_t off = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < kScanThreads / kWave; ++i) {
-        uint64_t x = s_wave[i];
-        if (i < wv) off += x;
-        tot += x;
-    }
-    *total = tot;
-    return off + incl - v;
 }
 
 // Ranks of the occupancy words: word_rank[w] = occupied voxels before word w.
@@ -196,7 +134,7 @@ __global__ __launch_bounds__(256) void k_count(int32_t BN, int32_t N, int64_t W,
                                                const uint32_t* __restrict__ word_rank,
                                                uint32_t* __restrict__ pt_slot, uint32_t* __restrict__ pt_pos,
                                                uint32_t* __restrict__ vox_count) {
-    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (gid >= BN) return;
     int32_t b = gid / N;
     uint32_t lin = pt_slot[gid];
@@ -267,7 +205,7 @@ __global__ __launch_bounds__(256) void k_scatter(int32_t BN, int32_t N, const ui
                                                  const uint32_t* __restrict__ pt_pos,
                                                  const uint32_t* __restrict__ full_off,
                                                  uint32_t* __restrict__ bucket) {
-    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (gid >= BN) return;
     int32_t b = gid / N;
     uint32_t slot = pt_slot[gid];
@@ -285,7 +223,7 @@ __global__ __launch_bounds__(256) void k_finalize(
     const uint32_t* __restrict__ bucket, const uint32_t* __restrict__ big, int64_t big_cap,
     const int* __restrict__ status, uint32_t* __restrict__ pt_list, float4* __restrict__ pt4) {
     if ((int32_t)blockIdx.x < part_a) {
-        int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+        int32_t gid = (int32_t)xcd_block(blockIdx.x, (uint32_t)part_a) * blockDim.x + threadIdx.x;
         if (gid >= BN) return;
         int32_t b = gid / N;
         uint32_t i = (uint32_t)(gid - b * N);

@@ -25,6 +25,7 @@ enum StatusSlot {
     kStTicketRank = 1, // tile tickets of the occupancy-rank scan
     kStTicketOff = 2,  // tile tickets of the offsets scan
     kStBigCount = 3,   // number of voxels with more than kBigVoxel points
+    kStTicketSel = 4,  // tile tickets of the center compaction scan
     kStSlots = 16
 };
 
@@ -56,14 +57,21 @@ struct Layout {
     size_t cas_key;       // u64 [B][N] CAS: key of an unpicked voxel in the current round
     size_t cas_pick;      // u64 [B][N] CAS: key at pick time (0 = unpicked)
     size_t cas_round;     // u32 [B][N] CAS: round that picked the voxel + 1 (0 = unpicked)
+    size_t cas_blocker;   // i32 [B][N] CAS: a neighbour whose key beat the voxel's (-1 = none)
+    size_t cas_dirty;     // u32 [B][N] CAS: round whose scoring must recompute the voxel
     size_t cas_ctl;       // CAS control block, see CasCtl
+    size_t sel_thr;       // u64 [B] selection threshold: keys <= it are chosen
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };
 
-// CAS control block (per cloud arrays), placed at Layout::cas_ctl.
+// CAS control block, placed at Layout::cas_ctl: per round parity and cloud,
+// kCasParts partial maxima / counts (spreading the atomics of one round over
+// several addresses), then per cloud a done flag, then the number of clouds
+// done:  u64 gpart[2][B][kCasParts]; u32 cpart[2][B][kCasParts]; u32 done[B];
+// u32 ndone.
+constexpr int kCasParts = 32;
 struct CasCtl {
-    // u64 gmax[2][B]; u32 count[2][B]; u32 done[B]; (laid out in this order)
-    static size_t bytes(int B) { return (size_t)B * (16 + 8 + 4) + 64; }
+    static size_t bytes(int B) { return (size_t)B * (2 * kCasParts * 12 + 4) + 64; }
 };
 
 bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L);
@@ -183,6 +191,68 @@ __device__ __forceinline__ void raise_error(int* status, int code) {
     atomicCAS(status + kStError, 0, code);
 }
 
+// Tile descriptors of the look-back scans: status in bits 62-63 (1 = the
+// tile's own aggregate, 2 = inclusive prefix), value in bits 0-61.
+constexpr uint64_t kDescAgg = 1ull << 62;
+constexpr uint64_t kDescInc = 2ull << 62;
+constexpr uint64_t kDescVal = (1ull << 62) - 1;
+
+// Exclusive prefix of `agg` over the tiles before `tile` in one segment.
+// Every thread of the block calls it; wave 0 publishes and looks back. Tiles
+// are numbered by a ticket taken at block start, so every predecessor has
+// started and will publish: the spin always ends.
+__device__ inline uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
+    if (threadIdx.x < kWave) {
+        const int lane = lane_id();
+        uint64_t excl = 0;
+        if (tile == 0) {
+            if (lane == 0) st_release(desc, kDescInc | agg);
+        } else {
+            if (lane == 0) st_release(desc + tile, kDescAgg | agg);
+            int64_t base = tile - 1;
+            while (true) {
+                int64_t idx = base - lane;
+                uint64_t d = kDescInc;  // before the first tile: an inclusive zero
+                if (idx >= 0) {
+                    do {
+                        d = ld_acquire(desc + idx);
+                    } while ((d >> 62) == 0);
+                }
+                uint64_t inc = __ballot((d >> 62) == 2);
+                if (inc) {
+                    int first = __ffsll((unsigned long long)inc) - 1;
+                    excl += wave_sum<uint64_t>(lane <= first ? (d & kDescVal) : 0ull);
+                    break;
+                }
+                excl += wave_sum<uint64_t>(d & kDescVal);
+                base -= kWave;
+            }
+            if (lane == 0) st_release(desc + tile, kDescInc | (excl + agg));
+        }
+        if (lane == 0) *s_out = excl;
+    }
+    __syncthreads();
+    return *s_out;
+}
+
+// Exclusive scan of one 64-bit value per thread across a kScanThreads block;
+// *total receives the block sum.
+__device__ inline uint64_t block_excl_scan(uint64_t v, uint64_t* s_wave, uint64_t* total) {
+    uint64_t incl = wave_incl_scan<uint64_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    __syncthreads();
+    uint64_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kScanThreads / kWave; ++i) {
+        uint64_t x = s_wave[i];
+        if (i < wv) off += x;
+        tot += x;
+    }
+    *total = tot;
+    return off + incl - v;
+}
+
 // Block id remapped so that consecutive logical blocks share an XCD (blocks
 // are dispatched to the 8 XCDs round-robin; each XCD has its own L2).
 __device__ __forceinline__ uint32_t xcd_block(uint32_t bid, uint32_t nblocks) {
@@ -199,6 +269,40 @@ __device__ __forceinline__ int32_t slot_of(const uint64_t* bm, const uint32_t* w
     uint64_t bit = 1ull << (lin & 63);
     if (!(w & bit)) return -1;
     return (int32_t)(wr[lin >> 6] + __popcll(w & (bit - 1)));
+}
+
+// Calls f(slot) for every occupied voxel within Chebyshev distance `rad` of
+// grid cell (x, y, z), in ascending linear id, one occupancy word per grid
+// row segment; stops early (returning false) when f returns false.
+template <typename F>
+__device__ __forceinline__ bool for_each_neighbour(const uint64_t* __restrict__ bm,
+                                                   const uint32_t* __restrict__ wr, const int32_t* D,
+                                                   int32_t x, int32_t y, int32_t z, int32_t rad, F f) {
+    const int32_t x0 = x - rad < 0 ? 0 : x - rad;
+    const int32_t x1 = x + rad > D[0] - 1 ? D[0] - 1 : x + rad;
+    const int32_t z0 = z - rad < 0 ? 0 : z - rad, z1 = z + rad > D[2] - 1 ? D[2] - 1 : z + rad;
+    const int32_t y0 = y - rad < 0 ? 0 : y - rad, y1 = y + rad > D[1] - 1 ? D[1] - 1 : y + rad;
+    for (int32_t zz = z0; zz <= z1; ++zz) {
+        for (int32_t yy = y0; yy <= y1; ++yy) {
+            const uint32_t base = (uint32_t)D[0] * ((uint32_t)yy + (uint32_t)D[1] * (uint32_t)zz);
+            const uint32_t l0 = base + (uint32_t)x0, l1 = base + (uint32_t)x1;
+            for (uint32_t w = l0 >> 6; w <= (l1 >> 6); ++w) {
+                const uint64_t bits = bm[w];
+                const uint32_t lo = w == (l0 >> 6) ? (l0 & 63) : 0u;
+                const uint32_t hi = w == (l1 >> 6) ? (l1 & 63) : 63u;
+                const uint64_t upto = hi == 63 ? ~0ull : ((1ull << (hi + 1)) - 1);
+                uint64_t m = bits & upto & ~((1ull << lo) - 1);
+                if (!m) continue;
+                const uint32_t rb = wr[w];
+                while (m) {
+                    const int bit = __ffsll((unsigned long long)m) - 1;
+                    if (!f(rb + (uint32_t)__popcll(bits & ((1ull << bit) - 1)))) return false;
+                    m &= m - 1;
+                }
+            }
+        }
+    }
+    return true;
 }
 
 // ------------------------------------------------------------------ host launchers

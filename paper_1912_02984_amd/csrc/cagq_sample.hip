@@ -4,8 +4,8 @@
 // RVS: every occupied voxel is equally likely. Slot s of cloud b gets the
 // key (hi32(h(seed, 1, b, s)) << 32) | s with h the splitmix64 chain; the
 // m = min(M, |O_v|) smallest keys win. One workgroup per cloud finds the m-th
-// smallest key by an 8-bit radix select in LDS and writes the winners in slot
-// (= ascending linear id) order.
+// smallest key by an 8-bit radix select in LDS; a look-back compaction over
+// the slots then writes the winners in slot (= ascending linear id) order.
 //
 // CAS (Eqs. 1-2, greedy reading): the sequential greedy repeatedly picks the
 // unpicked voxel of largest score 2^16*lambda*#{V in pi(v): C_V = 0} -
@@ -27,17 +27,20 @@ namespace {
 constexpr int kSelThreads = 1024;
 
 struct CasPtrs {
-    uint64_t* gmax;   // [2][B] best key among unpicked voxels, per round parity
-    uint32_t* count;  // [2][B] picks whose key beats that best, per round parity
+    uint64_t* gpart;  // [2][B][kCasParts] partial maxima of the unpicked keys, per round parity
+    uint32_t* cpart;  // [2][B][kCasParts] partial counts of picks above that maximum
     uint32_t* done;   // [B]
+    uint32_t* ndone;  // clouds done
 };
 
 CasPtrs cas_ptrs(const Layout& L, void* ws) {
     char* base = static_cast<char*>(ws) + L.cas_ctl;
+    const size_t parts = (size_t)2 * L.B * kCasParts;
     CasPtrs c;
-    c.gmax = reinterpret_cast<uint64_t*>(base);
-    c.count = reinterpret_cast<uint32_t*>(base + (size_t)16 * L.B);
-    c.done = reinterpret_cast<uint32_t*>(base + (size_t)24 * L.B);
+    c.gpart = reinterpret_cast<uint64_t*>(base);
+    c.cpart = reinterpret_cast<uint32_t*>(base + parts * 8);
+    c.done = reinterpret_cast<uint32_t*>(base + parts * 12);
+    c.ndone = c.done + L.B;
     return c;
 }
 
@@ -50,32 +53,58 @@ __device__ __forceinline__ uint64_t select_key(int key_mode, uint64_t hb, int32_
     return ~pick[s];  // largest pick key first; unpicked voxels (0) last
 }
 
-__global__ __launch_bounds__(kSelThreads) void k_select(int32_t N, const int32_t* __restrict__ nvox,
-                                                        const uint32_t* __restrict__ vox_lin, int32_t M,
-                                                        int key_mode, uint64_t seed,
-                                                        const uint64_t* __restrict__ cas_pick,
-                                                        int32_t* __restrict__ center_lin,
-                                                        int32_t* __restrict__ m_valid) {
+// One workgroup per cloud: the m-th smallest key T of the cloud (m =
+// min(M, |O_v|)) by an 8-bit radix select; every key <= T is chosen. Keys are
+// distinct (their low half is the slot or the linear id), unpicked CAS voxels
+// aside, which are never among the m smallest. Also clears the scan state of
+// the compaction that follows.
+__global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
+    int32_t N, int64_t tiles_s, const int32_t* __restrict__ nvox, int32_t M, int key_mode, uint64_t seed,
+    const uint64_t* __restrict__ cas_pick, uint64_t* __restrict__ thr, int32_t* __restrict__ m_valid,
+    uint64_t* __restrict__ desc_s, int* __restrict__ status) {
     __shared__ uint32_t hist[256];
     __shared__ uint32_t s_digit, s_below, s_cnt;
-    __shared__ uint32_t s_wave[kSelThreads / kWave];
+    constexpr int U = 4;  // keys per thread per sweep, loaded together
     const int32_t b = blockIdx.x;
     const int32_t nv = nvox[b];
     const int32_t m = M < nv ? M : nv;
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
     const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
     const int tid = threadIdx.x;
+    const int lane = lane_id();
+    for (int64_t t = tid; t < tiles_s; t += kSelThreads) desc_s[(size_t)b * tiles_s + t] = 0;
+    if (b == 0 && tid == 0) status[kStTicketSel] = 0;
 
-    // radix select of the m-th smallest key T
     uint64_t prefix = 0, mask = 0, T = 0;
     uint32_t need = (uint32_t)m;
     bool exact = true;
     for (int shift = 56; shift >= 0; shift -= 8) {
         if (tid < 256) hist[tid] = 0;
         __syncthreads();
-        for (int32_t s = tid; s < nv; s += kSelThreads) {
-            uint64_t k = select_key(key_mode, hb, s, pick);
-            if ((k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255], 1u);
+        for (int32_t s0 = 0; s0 < nv; s0 += kSelThreads * U) {
+            uint64_t k[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t s = s0 + u * kSelThreads + tid;
+                k[u] = s < nv ? select_key(key_mode, hb, s, pick) : 0;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int32_t s = s0 + u * kSelThreads + tid;
+                const bool act = s < nv && (k[u] & mask) == prefix;
+                const uint32_t d = (uint32_t)(k[u] >> shift) & 255u;
+                // one atomic for the wave when all its counted keys share a digit
+                const uint64_t am = __ballot(act);
+                if (am) {
+                    const int leader = __ffsll((unsigned long long)am) - 1;
+                    const uint32_t d0 = (uint32_t)__shfl((int)d, leader, kWave);
+                    if (__ballot(act && d == d0) == am) {
+                        if (lane == leader) atomicAdd(&hist[d0], (uint32_t)__popcll(am));
+                    } else if (act) {
+                        atomicAdd(&hist[d], 1u);
+                    }
+                }
+            }
         }
         __syncthreads();
         if (tid < kWave) {
@@ -86,7 +115,7 @@ __global__ __launch_bounds__(kSelThreads) void k_select(int32_t N, const int32_t
                 h4[j] = hist[tid * 4 + j];
                 sum += h4[j];
             }
-            uint32_t incl = wave_incl_scan<uint32_t>(sum);
+            const uint32_t incl = wave_incl_scan<uint32_t>(sum);
             uint32_t run = incl - sum;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
@@ -111,26 +140,58 @@ __global__ __launch_bounds__(kSelThreads) void k_select(int32_t N, const int32_t
         }
     }
     if (exact) T = prefix;
+    if (tid == 0) {
+        thr[b] = T;
+        m_valid[b] = m;
+    }
+}
 
-    // ordered compaction of {s : key(s) <= T}
-    const int32_t chunk = (nv + kSelThreads - 1) / kSelThreads;
-    const int32_t s_begin = tid * chunk;
-    const int32_t s_end = min(nv, s_begin + chunk);
-    uint32_t mine = 0;
-    for (int32_t s = s_begin; s < s_end; ++s) mine += select_key(key_mode, hb, s, pick) <= T ? 1u : 0u;
-    uint32_t incl = wave_incl_scan<uint32_t>(mine);
-    const int wv = tid / kWave;
-    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+// Ordered compaction of the chosen slots: tile of kScanTile slots per block,
+// look-back scan for the output position. Slot s chosen at position p < m
+// writes its linear id to every j = p, p + m, p + 2m, ... < M (the cyclic
+// padding).
+__global__ __launch_bounds__(kScanThreads) void k_sel_emit(
+    int32_t N, int64_t tiles_s, const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin,
+    int32_t M, int key_mode, uint64_t seed, const uint64_t* __restrict__ cas_pick,
+    const uint64_t* __restrict__ thr, int32_t* __restrict__ center_lin, uint64_t* __restrict__ desc_s,
+    int* __restrict__ status) {
+    __shared__ uint32_t s_ticket;
+    __shared__ uint64_t s_wave[kScanThreads / kWave];
+    __shared__ uint64_t s_prefix;
+    if (threadIdx.x == 0) s_ticket = atomicAdd((unsigned*)&status[kStTicketSel], 1u);
     __syncthreads();
-    uint32_t pos = incl - mine;
-    for (int i = 0; i < wv; ++i) pos += s_wave[i];
+    const uint32_t t = s_ticket;
+    const int32_t b = (int32_t)(t / tiles_s);
+    const int64_t tile = (int64_t)(t % tiles_s);
+    const int32_t nv = nvox[b];
+    if (tile * kScanTile >= nv) return;  // later tiles never wait on this one
+    const int32_t m = M < nv ? M : nv;
+    const uint64_t T = thr[b];
+    const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
+    const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
+    const int32_t s0 = (int32_t)(tile * kScanTile) + (int32_t)threadIdx.x * kScanItems;
+    bool chosen[kScanItems];
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        const int32_t s = s0 + i;
+        chosen[i] = s < nv && select_key(key_mode, hb, s, pick) <= T;
+        cnt += chosen[i] ? 1u : 0u;
+    }
+    uint64_t total;
+    const uint64_t excl = block_excl_scan(cnt, s_wave, &total);
+    uint64_t pos = tile_lookback(desc_s + (size_t)b * tiles_s, tile, total, &s_prefix) + excl;
     int32_t* out = center_lin + (size_t)b * M;
     const uint32_t* vl = vox_lin + (size_t)b * N;
-    for (int32_t s = s_begin; s < s_end; ++s)
-        if (select_key(key_mode, hb, s, pick) <= T && pos < (uint32_t)m) out[pos++] = (int32_t)vl[s];
-    __syncthreads();
-    for (int32_t j = m + tid; j < M; j += kSelThreads) out[j] = out[j % m];
-    if (tid == 0) m_valid[b] = m;
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        if (!chosen[i]) continue;
+        if (pos < (uint64_t)m) {
+            const int32_t l = (int32_t)vl[s0 + i];
+            for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
+        }
+        ++pos;
+    }
 }
 
 struct GridDims {
@@ -143,176 +204,319 @@ __device__ __forceinline__ void decode(uint32_t lin, const GridDims& g, int32_t*
     *z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
 }
 
-__global__ void k_cas_init(int32_t BN, int32_t B, uint32_t* __restrict__ cover, uint64_t* __restrict__ pick,
-                           uint32_t* __restrict__ round, CasPtrs ctl) {
-    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid < BN) {
-        cover[gid] = 0;
-        pick[gid] = 0;
-        round[gid] = 0;
-    }
-    if (gid < B) {
-        ctl.gmax[gid] = 0;
-        ctl.gmax[B + gid] = 0;
-        ctl.count[gid] = 0;
-        ctl.count[B + gid] = 0;
-        ctl.done[gid] = 0;
-    }
+// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz): bit j of
+// `mask` stands for x' = x - h + j (0 outside the grid); `first` is the slot
+// of the first occupied voxel at or after the segment's start, so bit j's
+// slot is first + popcount(mask below bit j). Branch-free: rows outside the
+// grid are clamped into it for the loads and get an empty mask, so the loads
+// of all rows of a window are issued together.
+struct RowDesc {
+    uint32_t first;
+    uint32_t mask;
+};
+
+__device__ __forceinline__ RowDesc row_desc(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
+                                            const GridDims& g, int32_t x, int32_t yy, int32_t zz, int32_t h) {
+    const bool inside = yy >= 0 && yy < g.D[1] && zz >= 0 && zz < g.D[2];
+    const int32_t yc = yy < 0 ? 0 : (yy >= g.D[1] ? g.D[1] - 1 : yy);
+    const int32_t zc = zz < 0 ? 0 : (zz >= g.D[2] ? g.D[2] - 1 : zz);
+    const int32_t xs = x - h;
+    const int32_t lo_x = xs < 0 ? 0 : xs;
+    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
+    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
+    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
+    const uint32_t w0 = lo >> 6, w1 = hi >> 6, o = lo & 63;
+    const uint64_t a = bm[w0];
+    const uint64_t c = bm[w1];  // the same word unless the segment crosses a word boundary (then o > 0)
+    const uint64_t bits = (a >> o) | (w1 != w0 ? c << (64 - o) : 0ull);
+    const uint32_t width = hi - lo + 1;
+    RowDesc r;
+    r.mask = inside ? (uint32_t)(bits & ((1ull << width) - 1)) << (lo_x - xs) : 0u;
+    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
+    return r;
 }
 
-// Round R, phase 1: key of every unpicked voxel and their maximum per cloud.
+// Slot of bit j of a row, or `self` when bit j is clear (a harmless address).
+__device__ __forceinline__ uint32_t row_slot_or(const RowDesc& r, int j, uint32_t self) {
+    return ((r.mask >> j) & 1u) ? r.first + (uint32_t)__popc(r.mask & ((1u << j) - 1)) : self;
+}
+
+__device__ __forceinline__ uint32_t row_slot(const RowDesc& r, int j) {
+    return r.first + (uint32_t)__popc(r.mask & ((1u << j) - 1));
+}
+
+// Reduction of the kCasParts partials of the cloud `b` of each lane. Every
+// lane of the wave must call it.
+__device__ __forceinline__ uint64_t parts_max(const uint64_t* __restrict__ part, int32_t b) {
+    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
+    if (b0 == b1) {
+        uint64_t v = part[(size_t)b0 * kCasParts + (lane_id() & (kCasParts - 1))];
+#pragma unroll
+        for (int d = 1; d < kCasParts; d <<= 1) {
+            uint64_t o = shfl_xor64(v, d);
+            v = o > v ? o : v;
+        }
+        return v;
+    }
+    uint64_t v = 0;
+    for (int i = 0; i < kCasParts; ++i) {
+        uint64_t o = part[(size_t)b * kCasParts + i];
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint32_t parts_sum(const uint32_t* __restrict__ part, int32_t b) {
+    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
+    if (b0 == b1) {
+        uint32_t v = part[(size_t)b0 * kCasParts + (lane_id() & (kCasParts - 1))];
+#pragma unroll
+        for (int d = 1; d < kCasParts; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
+        return v;
+    }
+    uint32_t v = 0;
+    for (int i = 0; i < kCasParts; ++i) v += part[(size_t)b * kCasParts + i];
+    return v;
+}
+
+// Partial slot a wave accumulates into.
+__device__ __forceinline__ int part_slot() {
+    return (int)((blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave) & (kCasParts - 1));
+}
+
+struct CasState {
+    uint32_t* cover;    // centers whose neighbourhood holds the voxel (C_V)
+    uint64_t* key;      // current key of an unpicked voxel
+    uint64_t* pick;     // key at pick time, 0 = unpicked
+    uint32_t* round;    // round that picked the voxel + 1, 0 = unpicked
+    int32_t* blocker;   // a neighbour whose key beat the voxel's last time, -1 = none
+    uint32_t* dirty;    // round whose scoring must recompute the voxel's key
+};
+
+__global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
+    int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid < BN) {
+        st.cover[gid] = 0;
+        st.pick[gid] = 0;
+        st.round[gid] = 0;
+        st.blocker[gid] = -1;
+        st.dirty[gid] = 0;
+    }
+    if (gid < 2 * B * kCasParts) {
+        ctl.gpart[gid] = 0;
+        ctl.cpart[gid] = 0;
+    }
+    if (gid < B) ctl.done[gid] = 0;
+    if (gid == 0) *ctl.ndone = 0;
+}
+
+// Round R, phase 1: the key of every unpicked voxel (recomputed in round 0
+// and wherever a pick of round R-1 came within distance 2r) and their
+// maximum per cloud. Also retires a cloud once round R-1 found enough picks
+// above the best unpicked key.
+template <int RAD>
 __global__ __launch_bounds__(256) void k_cas_score(
-    int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, int32_t rad, int64_t lam, uint32_t beta_q16,
-    int32_t M, const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin,
-    const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
-    const uint32_t* __restrict__ cover, const uint64_t* __restrict__ pick, uint64_t* __restrict__ key,
-    CasPtrs ctl) {
-    // no early exit: every lane takes part in the wave reduction at the end
-    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, int64_t lam, uint32_t beta_q16, int32_t M,
+    const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
+    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
+    // no early exit: every lane takes part in the wave reductions
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
     bool active = in_range && ctl.done[b] == 0;
     const int32_t nv = nvox[b];
-    if (active && R > 0) {
-        const uint32_t m = (uint32_t)(M < nv ? M : nv);
-        if (ctl.count[((R - 1) & 1) * B + b] >= m) {
-            if (s == 0) ctl.done[b] = 1;
-            active = false;
+    const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) & 1) * B * kCasParts, b) : 0u;
+    if (active && R > 0 && prev >= (uint32_t)(M < nv ? M : nv)) {
+        if (s == 0) {
+            ctl.done[b] = 1;
+            atomicAdd(ctl.ndone, 1u);
         }
+        active = false;
     }
-    if (active && s == 0) ctl.count[(R & 1) * B + b] = 0;
+    if (active)  // this round's pick counts start from zero
+        for (int32_t i = s; i < kCasParts; i += N) ctl.cpart[((size_t)(R & 1) * B + b) * kCasParts + i] = 0;
     uint64_t k = 0;
-    if (active && s < nv && pick[gid] == 0) {
-        const uint64_t* bm = bitmap + (size_t)b * W;
-        const uint32_t* wr = word_rank + (size_t)b * W;
-        const uint32_t* cv = cover + (size_t)b * N;
-        const uint32_t lin = vox_lin[gid];
-        int32_t x, y, z;
-        decode(lin, g, &x, &y, &z);
-        int64_t U = 0, cs = 0;
-        for (int32_t dz = -rad; dz <= rad; ++dz) {
-            int32_t zz = z + dz;
-            if (zz < 0 || zz >= g.D[2]) continue;
-            for (int32_t dy = -rad; dy <= rad; ++dy) {
-                int32_t yy = y + dy;
-                if (yy < 0 || yy >= g.D[1]) continue;
-                for (int32_t dx = -rad; dx <= rad; ++dx) {
-                    int32_t xx = x + dx;
-                    if (xx < 0 || xx >= g.D[0]) continue;
-                    uint32_t nl = (uint32_t)xx + (uint32_t)g.D[0] * ((uint32_t)yy + (uint32_t)g.D[1] * (uint32_t)zz);
-                    int32_t sl = slot_of(bm, wr, nl);
-                    if (sl < 0) continue;
-                    uint32_t c = cv[sl];
-                    U += c == 0 ? 1 : 0;
-                    cs += c;
-                }
-            }
-        }
-        int64_t score = 65536ll * lam * U - (int64_t)beta_q16 * cs;
-        k = ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
-        key[gid] = k;
-    }
-    // per-cloud maximum: reduce over the lanes of this wave that share the cloud
-    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
-    if (b0 == b1) {
-        uint64_t mx = wave_max64(k);
-        if (lane_id() == 0 && mx) atomicMax((unsigned long long*)&ctl.gmax[(R & 1) * B + b], mx);
-    } else if (k) {
-        atomicMax((unsigned long long*)&ctl.gmax[(R & 1) * B + b], k);
-    }
-}
-
-// Round R, phase 2: voxels whose key beats every voxel unpicked at the round's
-// start within distance 2r are picked; coverage counts of their neighbourhoods
-// rise by one. Also counts earlier picks whose key beats this round's best.
-__global__ __launch_bounds__(256) void k_cas_pick(
-    int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, int32_t rad, const int32_t* __restrict__ nvox,
-    const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
-    const uint32_t* __restrict__ word_rank, uint32_t* __restrict__ cover, uint64_t* __restrict__ pick,
-    uint32_t* __restrict__ round, const uint64_t* __restrict__ key, CasPtrs ctl) {
-    // no early exit: every lane takes part in the wave reduction at the end
-    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
-    const bool in_range = gid < B * N;
-    const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
-    const bool active = in_range && ctl.done[b] == 0;
-    if (active && s == 0) ctl.gmax[((R + 1) & 1) * B + b] = 0;
-    const int32_t nv = nvox[b];
-    uint32_t above = 0;
-    if (active && s < nv) {
-        const uint64_t G = ctl.gmax[(R & 1) * B + b];
-        const uint64_t pk = pick[gid];
-        if (pk != 0) {
-            above = pk > G ? 1u : 0u;
-        } else {
+    const uint32_t rnd = active && s < nv ? st.round[gid] : 0u;
+    // a voxel picked in the previous round stops competing: its key becomes 0
+    if (active && s < nv && rnd != 0 && rnd == (uint32_t)R) st.key[gid] = 0;
+    if (active && s < nv && rnd == 0) {
+        if (R == 0 || st.dirty[gid] == (uint32_t)R) {
             const uint64_t* bm = bitmap + (size_t)b * W;
             const uint32_t* wr = word_rank + (size_t)b * W;
-            const uint64_t* ky = key + (size_t)b * N;
-            const uint32_t* rd = round + (size_t)b * N;
-            const uint64_t my = key[gid];
+            const uint32_t* cv = st.cover + (size_t)b * N;
             const uint32_t lin = vox_lin[gid];
             int32_t x, y, z;
             decode(lin, g, &x, &y, &z);
-            const int32_t r2 = 2 * rad;
-            bool best = true;
-            for (int32_t dz = -r2; dz <= r2 && best; ++dz) {
-                int32_t zz = z + dz;
-                if (zz < 0 || zz >= g.D[2]) continue;
-                for (int32_t dy = -r2; dy <= r2 && best; ++dy) {
-                    int32_t yy = y + dy;
-                    if (yy < 0 || yy >= g.D[1]) continue;
-                    for (int32_t dx = -r2; dx <= r2; ++dx) {
-                        int32_t xx = x + dx;
-                        if (xx < 0 || xx >= g.D[0] || (dx == 0 && dy == 0 && dz == 0)) continue;
-                        uint32_t nl = (uint32_t)xx + (uint32_t)g.D[0] * ((uint32_t)yy + (uint32_t)g.D[1] * (uint32_t)zz);
-                        int32_t sl = slot_of(bm, wr, nl);
-                        if (sl < 0) continue;
-                        uint32_t rr = rd[sl];
-                        // unpicked at the round's start: never picked, or picked in this round
-                        if ((rr == 0 || rr == (uint32_t)R + 1) && ky[sl] > my) {
-                            best = false;
-                            break;
-                        }
-                    }
+            constexpr int S = 2 * RAD + 1;
+            RowDesc rows[S * S];
+#pragma unroll
+            for (int j = 0; j < S * S; ++j) rows[j] = row_desc(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
+            // every coverage count of the window loaded at once, then masked
+            uint32_t c[S * S * S];
+#pragma unroll
+            for (int j = 0; j < S * S; ++j)
+#pragma unroll
+                for (int q = 0; q < S; ++q) c[j * S + q] = cv[row_slot_or(rows[j], q, (uint32_t)s)];
+            int64_t U = 0, cs = 0;
+#pragma unroll
+            for (int j = 0; j < S * S; ++j)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    const bool occ = (rows[j].mask >> q) & 1u;
+                    const uint32_t cc = occ ? c[j * S + q] : 0u;
+                    U += (occ && cc == 0) ? 1 : 0;
+                    cs += cc;
                 }
-            }
-            if (best) {
-                round[gid] = (uint32_t)R + 1;
-                pick[gid] = my;
-                uint32_t* cv = cover + (size_t)b * N;
-                for (int32_t dz = -rad; dz <= rad; ++dz) {
-                    int32_t zz = z + dz;
-                    if (zz < 0 || zz >= g.D[2]) continue;
-                    for (int32_t dy = -rad; dy <= rad; ++dy) {
-                        int32_t yy = y + dy;
-                        if (yy < 0 || yy >= g.D[1]) continue;
-                        for (int32_t dx = -rad; dx <= rad; ++dx) {
-                            int32_t xx = x + dx;
-                            if (xx < 0 || xx >= g.D[0]) continue;
-                            uint32_t nl = (uint32_t)xx + (uint32_t)g.D[0] * ((uint32_t)yy + (uint32_t)g.D[1] * (uint32_t)zz);
-                            int32_t sl = slot_of(bm, wr, nl);
-                            if (sl >= 0) atomicAdd(&cv[sl], 1u);
-                        }
-                    }
+            const int64_t score = 65536ll * lam * U - (int64_t)beta_q16 * cs;
+            k = ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
+            st.key[gid] = k;
+        } else {
+            k = st.key[gid];
+        }
+    }
+    // per-cloud maximum into one of the partial slots
+    uint64_t* gp = ctl.gpart + (size_t)(R & 1) * B * kCasParts;
+    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
+    if (b0 == b1) {
+        const uint64_t mx = wave_max64(k);
+        if (lane_id() == 0 && mx) atomicMax((unsigned long long*)&gp[(size_t)b * kCasParts + part_slot()], mx);
+    } else if (k) {
+        atomicMax((unsigned long long*)&gp[(size_t)b * kCasParts + part_slot()], k);
+    }
+}
+
+// Round R, phase 2: a voxel whose key beats that of every voxel unpicked at
+// the round's start within distance 2r is picked: the coverage counts of its
+// neighbourhood rise by one and the voxels within 2r are marked for
+// rescoring. A voxel first re-checks the neighbour that beat it last time
+// and scans its 2r-neighbourhood, one z-plane at a time, only when that one
+// no longer does. Also counts earlier picks whose key beats this round's
+// best unpicked key.
+template <int RAD>
+__global__ __launch_bounds__(256) void k_cas_pick(
+    int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, const int32_t* __restrict__ nvox,
+    const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
+    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
+    constexpr int H = 2 * RAD;      // half-width of the competition window
+    constexpr int S2 = 2 * H + 1;
+    // no early exit: every lane takes part in the wave-wide steps
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    const bool in_range = gid < B * N;
+    const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
+    const bool active = in_range && ctl.done[b] == 0;
+    const uint64_t G = parts_max(ctl.gpart + (size_t)(R & 1) * B * kCasParts, b);
+    if (active)  // next round's maxima start from zero
+        for (int32_t i = s; i < kCasParts; i += N) ctl.gpart[((size_t)((R + 1) & 1) * B + b) * kCasParts + i] = 0;
+    const int32_t nv = nvox[b];
+    const uint32_t cur = (uint32_t)R + 1;
+    const size_t cb = (size_t)b * N;
+    const uint64_t* bm = bitmap + (size_t)b * W;
+    const uint32_t* wr = word_rank + (size_t)b * W;
+    uint32_t above = 0;
+    bool winner = false;
+    int32_t x = 0, y = 0, z = 0;
+    if (active && s < nv) {
+        const uint64_t pk = st.pick[gid];
+        if (pk != 0) {
+            above = pk > G ? 1u : 0u;
+        } else {
+            // competitors are the voxels unpicked at the round's start: earlier
+            // picks have key 0 (set by this round's scoring), this round's keep theirs
+            const uint64_t* ky = st.key + cb;
+            const uint64_t my = st.key[gid];
+            const int32_t bl = st.blocker[gid];
+            const bool beaten = bl >= 0 && ky[bl] > my;
+            if (!beaten) {
+                decode(vox_lin[gid], g, &x, &y, &z);
+                int32_t found = -1;
+                // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
+                // row descriptors, then all keys are loaded before comparing (a
+                // clear bit loads the voxel's own key, which never beats it)
+                for (int p = 0; p < S2 && found < 0; ++p) {
+                    const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
+                    RowDesc rows[S2];
+#pragma unroll
+                    for (int j = 0; j < S2; ++j) rows[j] = row_desc(bm, wr, g, x, y + j - H, z + dz, H);
+                    uint32_t sl[S2 * S2];
+                    uint64_t kk[S2 * S2];
+#pragma unroll
+                    for (int i = 0; i < S2 * S2; ++i) sl[i] = row_slot_or(rows[i / S2], i % S2, (uint32_t)s);
+#pragma unroll
+                    for (int i = 0; i < S2 * S2; ++i) kk[i] = ky[sl[i]];
+#pragma unroll
+                    for (int i = 0; i < S2 * S2; ++i)
+                        if (found < 0 && kk[i] > my) found = (int32_t)sl[i];
+                }
+                if (found >= 0) {
+                    st.blocker[gid] = found;
+                } else {
+                    winner = true;
+                    st.round[gid] = cur;
+                    st.pick[gid] = my;
                 }
             }
         }
     }
+    // the whole wave marks each winner's window, one grid row per lane:
+    // rescoring flags within 2r, coverage counts within r
+    uint64_t wins = __ballot(winner);
+    while (wins) {
+        const int wl = __ffsll((unsigned long long)wins) - 1;
+        wins &= wins - 1;
+        const int32_t wx = __shfl(x, wl, kWave), wy = __shfl(y, wl, kWave), wz = __shfl(z, wl, kWave);
+        const int32_t wb = __shfl(b, wl, kWave);
+        const uint64_t* wbm = bitmap + (size_t)wb * W;
+        const uint32_t* wwr = word_rank + (size_t)wb * W;
+        uint32_t* cv = st.cover + (size_t)wb * N;
+        uint32_t* dt = st.dirty + (size_t)wb * N;
+        for (int j = lane_id(); j < S2 * S2; j += kWave) {
+            const int dy = j % S2 - H, dz = j / S2 - H;
+            const RowDesc r = row_desc(wbm, wwr, g, wx, wy + dy, wz + dz, H);
+            const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
+#pragma unroll
+            for (int q = 0; q < S2; ++q) {
+                if ((r.mask >> q) & 1u) {
+                    const uint32_t sl = row_slot(r, q);
+                    dt[sl] = cur;
+                    if (inner && q - H >= -RAD && q - H <= RAD) atomicAdd(&cv[sl], 1u);
+                }
+            }
+        }
+    }
+    uint32_t* cp = ctl.cpart + (size_t)(R & 1) * B * kCasParts;
     const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
     if (b0 == b1) {
-        uint32_t tot = wave_sum<uint32_t>(above);
-        if (lane_id() == 0 && tot) atomicAdd(&ctl.count[(R & 1) * B + b], tot);
+        const uint32_t tot = wave_sum<uint32_t>(above);
+        if (lane_id() == 0 && tot) atomicAdd(&cp[(size_t)b * kCasParts + part_slot()], tot);
     } else if (above) {
-        atomicAdd(&ctl.count[(R & 1) * B + b], above);
+        atomicAdd(&cp[(size_t)b * kCasParts + part_slot()], above);
     }
+}
+
+// A small pinned host buffer per calling thread for polling the number of
+// clouds done without stalling the stream. Allocated on first use, kept for
+// the life of the process.
+uint32_t* poll_buffer() {
+    thread_local uint32_t* buf = nullptr;
+    if (!buf) {
+        void* p = nullptr;
+        if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
+        buf = static_cast<uint32_t*>(p);
+    }
+    return buf;
 }
 
 }  // namespace
 
 hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
                          int32_t* center_lin, int32_t* m_valid, hipStream_t s) {
-    k_select<<<L.B, kSelThreads, 0, s>>>(L.N, at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_lin), M, key_mode,
-                                         seed, key_mode ? at<uint64_t>(ws, L.cas_pick) : nullptr, center_lin,
-                                         m_valid);
+    const uint64_t* pick = key_mode ? at<uint64_t>(ws, L.cas_pick) : nullptr;
+    k_sel_threshold<<<L.B, kSelThreads, 0, s>>>(L.N, L.tiles_s, at<int32_t>(ws, L.nvox), M, key_mode, seed, pick,
+                                                at<uint64_t>(ws, L.sel_thr), m_valid, at<uint64_t>(ws, L.desc_s),
+                                                at<int>(ws, L.status));
+    k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(
+        L.N, L.tiles_s, at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_lin), M, key_mode, seed, pick,
+        at<uint64_t>(ws, L.sel_thr), center_lin, at<uint64_t>(ws, L.desc_s), at<int>(ws, L.status));
     return hipGetLastError();
 }
 
@@ -322,52 +526,95 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     const int32_t B = L.B, N = L.N, BN = B * N;
     const int pb = (BN + 255) / 256;
     CasPtrs ctl = cas_ptrs(L, ws);
+    CasState st;
+    st.cover = at<uint32_t>(ws, L.cas_cover);
+    st.key = at<uint64_t>(ws, L.cas_key);
+    st.pick = at<uint64_t>(ws, L.cas_pick);
+    st.round = at<uint32_t>(ws, L.cas_round);
+    st.blocker = at<int32_t>(ws, L.cas_blocker);
+    st.dirty = at<uint32_t>(ws, L.cas_dirty);
     GridDims g;
     for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
     const int32_t rad = d.radius;
+    if (rad != 1 && rad != 2) {
+        *status_out = CAGQ_ERR_INVALID_ARG;
+        return hipSuccess;
+    }
     const int64_t side = 2 * rad + 1;
     const int64_t lam = side * side * side;
-    k_cas_init<<<pb, 256, 0, s>>>(BN, B, at<uint32_t>(ws, L.cas_cover), at<uint64_t>(ws, L.cas_pick),
-                                  at<uint32_t>(ws, L.cas_round), ctl);
+    const int32_t init_n = BN > 2 * B * kCasParts ? BN : 2 * B * kCasParts;
+    k_cas_init<<<(init_n + 255) / 256, 256, 0, s>>>(BN, B, st, ctl);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+
+    const int32_t* nvox = at<int32_t>(ws, L.nvox);
+    const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
+    const uint64_t* bitmap = at<uint64_t>(ws, L.bitmap);
+    const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
+    int64_t R = 0;
+    auto launch_batch = [&](int rounds) {
+        for (int i = 0; i < rounds; ++i, ++R) {
+            if (rad == 1) {
+                k_cas_score<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
+                                                  bitmap, word_rank, st, ctl);
+                k_cas_pick<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap, word_rank,
+                                                 st, ctl);
+            } else {
+                k_cas_score<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
+                                                  bitmap, word_rank, st, ctl);
+                k_cas_pick<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap, word_rank,
+                                                 st, ctl);
+            }
+        }
+        return hipGetLastError();
+    };
     // every round picks at least the best unpicked voxel, so min(M, N) + 2
     // rounds always suffice (the last one only records that the cloud is done)
     const int64_t max_rounds = (int64_t)(M < N ? M : N) + 2;
-    uint32_t done_h[64];
-    const int check_every = 8;
-    int64_t R = 0;
-    bool all_done = false;
-    while (!all_done) {
-        for (int i = 0; i < check_every; ++i, ++R) {
-            k_cas_score<<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, rad, lam, beta_q16, M,
-                                           at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_lin),
-                                           at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
-                                           at<uint32_t>(ws, L.cas_cover), at<uint64_t>(ws, L.cas_pick),
-                                           at<uint64_t>(ws, L.cas_key), ctl);
-            k_cas_pick<<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, rad, at<int32_t>(ws, L.nvox),
-                                          at<uint32_t>(ws, L.vox_lin), at<uint64_t>(ws, L.bitmap),
-                                          at<uint32_t>(ws, L.word_rank), at<uint32_t>(ws, L.cas_cover),
-                                          at<uint64_t>(ws, L.cas_pick), at<uint32_t>(ws, L.cas_round),
-                                          at<uint64_t>(ws, L.cas_key), ctl);
+    const int batch = 4;
+    uint32_t* poll = poll_buffer();
+    if (!poll) {
+        // synchronous polling
+        while (true) {
+            if ((e = launch_batch(batch)) != hipSuccess) return e;
+            uint32_t nd = 0;
+            if ((e = hipMemcpyAsync(&nd, ctl.ndone, sizeof nd, hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
+            if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
+            if (nd == (uint32_t)B) return hipSuccess;
+            if (R > max_rounds + 2 * batch) break;
         }
-        e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        all_done = true;
-        for (int32_t b0 = 0; b0 < B && all_done; b0 += 64) {
-            int32_t nb = B - b0 < 64 ? B - b0 : 64;
-            e = hipMemcpyAsync(done_h, ctl.done + b0, sizeof(uint32_t) * nb, hipMemcpyDeviceToHost, s);
-            if (e != hipSuccess) return e;
-            e = hipStreamSynchronize(s);
-            if (e != hipSuccess) return e;
-            for (int32_t i = 0; i < nb; ++i) all_done = all_done && done_h[i] != 0;
-        }
-        if (!all_done && R > max_rounds) {
-            *status_out = CAGQ_ERR_CAPACITY;
-            return hipSuccess;
-        }
+        *status_out = CAGQ_ERR_CAPACITY;
+        return hipSuccess;
     }
-    return hipSuccess;
+    // two batches in flight: the host reads batch k's count while batch k+1 runs
+    hipEvent_t ev[2];
+    if ((e = hipEventCreateWithFlags(&ev[0], hipEventDisableTiming)) != hipSuccess) return e;
+    if ((e = hipEventCreateWithFlags(&ev[1], hipEventDisableTiming)) != hipSuccess) {
+        (void)hipEventDestroy(ev[0]);
+        return e;
+    }
+    auto issue = [&](int slot) {
+        hipError_t r = launch_batch(batch);
+        if (r == hipSuccess)
+            r = hipMemcpyAsync(&poll[slot], ctl.ndone, sizeof(uint32_t), hipMemcpyDeviceToHost, s);
+        if (r == hipSuccess) r = hipEventRecord(ev[slot], s);
+        return r;
+    };
+    e = issue(0);
+    if (e == hipSuccess) e = issue(1);
+    for (int k = 0; e == hipSuccess; ++k) {
+        const int slot = k & 1;
+        if ((e = hipEventSynchronize(ev[slot])) != hipSuccess) break;
+        if (poll[slot] == (uint32_t)B) break;
+        if (R > max_rounds + 2 * batch) {
+            *status_out = CAGQ_ERR_CAPACITY;
+            break;
+        }
+        e = issue(slot);
+    }
+    (void)hipEventDestroy(ev[0]);
+    (void)hipEventDestroy(ev[1]);
+    return e;
 }
 
 }  // namespace cagq
