@@ -67,6 +67,7 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_dirty = take(4 * BN);
     L->cas_ctl = take(CasCtl::bytes(B));
     L->sel_thr = take(8 * (size_t)B);
+    L->sel_hist = take(4 * (size_t)kSelPasses * B * kSelBins);
     L->total = off;
     return true;
 }

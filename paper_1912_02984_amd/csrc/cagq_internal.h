@@ -18,6 +18,8 @@ constexpr int kScanThreads = 256;       // threads per scan tile
 constexpr int kScanItems = 4;           // items per thread in a scan tile
 constexpr int kScanTile = kScanThreads * kScanItems;
 constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
+constexpr int kSelPasses = 6;           // 11-bit digits of a 64-bit key (the last one 9 bits)
+constexpr int kSelBins = 2048;
 
 // Status word slots (int32 each) at the start of the workspace's control block.
 enum StatusSlot {
@@ -61,6 +63,7 @@ struct Layout {
     size_t cas_dirty;     // u32 [B][N] CAS: round whose scoring must recompute the voxel
     size_t cas_ctl;       // CAS control block, see CasCtl
     size_t sel_thr;       // u64 [B] selection threshold: keys <= it are chosen
+    size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };
 

@@ -25,6 +25,7 @@ namespace cagq {
 namespace {
 
 constexpr int kSelThreads = 1024;
+constexpr int32_t kSelManyBlockMin = 16384;  // clouds of this many points use the many-block select
 
 struct CasPtrs {
     uint64_t* gpart;  // [2][B][kCasParts] partial maxima of the unpicked keys, per round parity
@@ -192,6 +193,138 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
         }
         ++pos;
     }
+}
+
+// ---- many-block selection (large clouds): one histogram kernel per digit.
+// Digit q covers key bits [lo(q), hi(q)): 11-bit digits from the top.
+__device__ __forceinline__ int sel_lo(int q) { return q == kSelPasses - 1 ? 0 : 64 - 11 * (q + 1); }
+__device__ __forceinline__ int sel_hi(int q) { return 64 - 11 * q; }
+
+struct SelState {
+    uint64_t prefix, mask, T;
+    uint32_t need;
+    bool done;  // T is known
+};
+
+// Re-derives, from the histograms of digits 0..passes-1 of cloud b, the digits
+// chosen so far (each the digit whose cumulative count first reaches the
+// remaining rank). Called by every thread of a kScanThreads block.
+__device__ SelState sel_derive(const uint32_t* __restrict__ hist, int32_t B, int32_t b, uint32_t m, int passes) {
+    __shared__ uint64_t s_wave[kScanThreads / kWave];
+    __shared__ uint32_t s_digit, s_below, s_cnt;
+    SelState st{0ull, 0ull, 0ull, m, false};
+    const int tid = threadIdx.x;
+    for (int q = 0; q < passes && !st.done; ++q) {
+        const int lo = sel_lo(q), width = sel_hi(q) - lo;
+        const int bins = 1 << width;
+        const int per = bins / kScanThreads;  // 8, or 2 for the last digit
+        const uint32_t* h = hist + ((size_t)q * B + b) * kSelBins;
+        uint32_t v[8], sum = 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            v[i] = i < per ? h[tid * per + i] : 0u;
+            sum += v[i];
+        }
+        uint64_t total;
+        uint32_t run = (uint32_t)block_excl_scan(sum, s_wave, &total);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            if (i < per && run < st.need && run + v[i] >= st.need) {
+                s_digit = (uint32_t)(tid * per + i);
+                s_below = run;
+                s_cnt = v[i];
+            }
+            run += v[i];
+        }
+        __syncthreads();
+        const uint32_t digit = s_digit, below = s_below, cnt = s_cnt;
+        __syncthreads();
+        st.prefix |= (uint64_t)digit << lo;
+        st.mask |= (uint64_t)(bins - 1) << lo;
+        st.need -= below;
+        if (cnt == st.need) {  // every key under this prefix is among the m smallest
+            st.T = st.prefix | ~st.mask;
+            st.done = true;
+        }
+    }
+    if (!st.done && passes == kSelPasses) {
+        st.T = st.prefix;
+        st.done = true;
+    }
+    return st;
+}
+
+__global__ void k_sel_mb_clear(int32_t B, int64_t tiles_s, uint32_t* __restrict__ hist,
+                               uint64_t* __restrict__ desc_s, int* __restrict__ status, int32_t M,
+                               const int32_t* __restrict__ nvox, int32_t* __restrict__ m_valid) {
+    const size_t n = (size_t)kSelPasses * B * kSelBins;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) hist[i] = 0;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < (size_t)B * tiles_s; i += stride) desc_s[i] = 0;
+    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid == 0) status[kStTicketSel] = 0;
+    if (gid < B) m_valid[gid] = M < nvox[gid] ? M : nvox[gid];
+}
+
+// Digit q: blocks (j, b) count the keys of their share of cloud b's slots that
+// match the digits chosen so far.
+constexpr int kSelItems = 16;  // slots per thread of a histogram block
+
+__global__ __launch_bounds__(kScanThreads) void k_sel_mb_hist(
+    int q, int32_t B, int32_t N, const int32_t* __restrict__ nvox, int32_t M, int key_mode, uint64_t seed,
+    const uint64_t* __restrict__ cas_pick, uint32_t* __restrict__ hist) {
+    __shared__ uint32_t lh[kSelBins];
+    const int32_t b = blockIdx.y;
+    const int32_t nv = nvox[b];
+    const uint32_t m = (uint32_t)(M < nv ? M : nv);
+    const SelState st = sel_derive(hist, B, b, m, q);
+    if (st.done) return;  // the whole block
+    const int lo = sel_lo(q), width = sel_hi(q) - lo;
+    const uint32_t dmask = (1u << width) - 1;
+    for (int i = threadIdx.x; i < kSelBins; i += kScanThreads) lh[i] = 0;
+    __syncthreads();
+    const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
+    const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
+    const int lane = lane_id();
+    const int32_t s0 = (int32_t)blockIdx.x * kScanThreads * kSelItems;
+    uint64_t k[kSelItems];
+#pragma unroll
+    for (int u = 0; u < kSelItems; ++u) {
+        const int32_t s = s0 + u * kScanThreads + (int32_t)threadIdx.x;
+        k[u] = s < nv ? select_key(key_mode, hb, s, pick) : ~0ull;
+    }
+#pragma unroll
+    for (int u = 0; u < kSelItems; ++u) {
+        const int32_t s = s0 + u * kScanThreads + (int32_t)threadIdx.x;
+        // an unpicked CAS voxel (key ~0) is never chosen: it is not counted
+        const bool act = s < nv && (k[u] & st.mask) == st.prefix && (key_mode == 0 || k[u] != ~0ull);
+        const uint32_t d = (uint32_t)(k[u] >> lo) & dmask;
+        // one LDS atomic per distinct digit of the wave for the first few
+        // digits (pick keys share their leading digits), then one per lane
+        uint64_t am = __ballot(act);
+        for (int r = 0; r < 4 && am; ++r) {
+            const int leader = __ffsll((unsigned long long)am) - 1;
+            const uint32_t d0 = (uint32_t)__shfl((int)d, leader, kWave);
+            const uint64_t same = __ballot(act && d == d0) & am;
+            if (lane == leader) atomicAdd(&lh[d0], (uint32_t)__popcll(same));
+            am &= ~same;
+        }
+        if ((am >> lane) & 1ull) atomicAdd(&lh[d], 1u);
+    }
+    __syncthreads();
+    uint32_t* gh = hist + ((size_t)q * B + b) * kSelBins;
+    for (int i = threadIdx.x; i < (int)(dmask + 1); i += kScanThreads)
+        if (lh[i]) atomicAdd(&gh[i], lh[i]);
+}
+
+// The threshold of each cloud from its six histograms.
+__global__ __launch_bounds__(kScanThreads) void k_sel_mb_final(int32_t B, const int32_t* __restrict__ nvox,
+                                                               int32_t M, const uint32_t* __restrict__ hist,
+                                                               uint64_t* __restrict__ thr) {
+    const int32_t b = blockIdx.x;
+    const int32_t nv = nvox[b];
+    const SelState st = sel_derive(hist, B, b, (uint32_t)(M < nv ? M : nv), kSelPasses);
+    if (threadIdx.x == 0) thr[b] = st.T;
 }
 
 struct GridDims {
@@ -458,7 +591,9 @@ __global__ __launch_bounds__(256) void k_cas_pick(
         }
     }
     // the whole wave marks each winner's window, one grid row per lane:
-    // rescoring flags within 2r, coverage counts within r
+    // rescoring flags within 2r, coverage counts within r. Winners of a round
+    // are more than 2r apart, so their r-neighbourhoods are disjoint and no
+    // count is raised twice in a round: plain read-modify-write is exact.
     uint64_t wins = __ballot(winner);
     while (wins) {
         const int wl = __ffsll((unsigned long long)wins) - 1;
@@ -478,7 +613,7 @@ __global__ __launch_bounds__(256) void k_cas_pick(
                 if ((r.mask >> q) & 1u) {
                     const uint32_t sl = row_slot(r, q);
                     dt[sl] = cur;
-                    if (inner && q - H >= -RAD && q - H <= RAD) atomicAdd(&cv[sl], 1u);
+                    if (inner && q - H >= -RAD && q - H <= RAD) cv[sl] = cv[sl] + 1u;
                 }
             }
         }
@@ -511,12 +646,27 @@ uint32_t* poll_buffer() {
 hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
                          int32_t* center_lin, int32_t* m_valid, hipStream_t s) {
     const uint64_t* pick = key_mode ? at<uint64_t>(ws, L.cas_pick) : nullptr;
-    k_sel_threshold<<<L.B, kSelThreads, 0, s>>>(L.N, L.tiles_s, at<int32_t>(ws, L.nvox), M, key_mode, seed, pick,
-                                                at<uint64_t>(ws, L.sel_thr), m_valid, at<uint64_t>(ws, L.desc_s),
-                                                at<int>(ws, L.status));
-    k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(
-        L.N, L.tiles_s, at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_lin), M, key_mode, seed, pick,
-        at<uint64_t>(ws, L.sel_thr), center_lin, at<uint64_t>(ws, L.desc_s), at<int>(ws, L.status));
+    const int32_t* nvox = at<int32_t>(ws, L.nvox);
+    uint64_t* thr = at<uint64_t>(ws, L.sel_thr);
+    uint64_t* desc_s = at<uint64_t>(ws, L.desc_s);
+    int* status = at<int>(ws, L.status);
+    if (L.N >= kSelManyBlockMin) {
+        // large clouds: one histogram kernel per 11-bit digit over many blocks
+        uint32_t* hist = at<uint32_t>(ws, L.sel_hist);
+        const size_t nclear = (size_t)kSelPasses * L.B * kSelBins;
+        k_sel_mb_clear<<<(unsigned)((nclear + 255) / 256), 256, 0, s>>>(L.B, L.tiles_s, hist, desc_s, status, M, nvox,
+                                                                        m_valid);
+        const dim3 grid((unsigned)((L.N + kScanThreads * kSelItems - 1) / (kScanThreads * kSelItems)), (unsigned)L.B);
+        for (int q = 0; q < kSelPasses; ++q)
+            k_sel_mb_hist<<<grid, kScanThreads, 0, s>>>(q, L.B, L.N, nvox, M, key_mode, seed, pick, hist);
+        k_sel_mb_final<<<L.B, kScanThreads, 0, s>>>(L.B, nvox, M, hist, thr);
+    } else {
+        k_sel_threshold<<<L.B, kSelThreads, 0, s>>>(L.N, L.tiles_s, nvox, M, key_mode, seed, pick, thr, m_valid,
+                                                    desc_s, status);
+    }
+    k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(L.N, L.tiles_s, nvox,
+                                                                   at<uint32_t>(ws, L.vox_lin), M, key_mode, seed,
+                                                                   pick, thr, center_lin, desc_s, status);
     return hipGetLastError();
 }
 
@@ -571,7 +721,9 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     // every round picks at least the best unpicked voxel, so min(M, N) + 2
     // rounds always suffice (the last one only records that the cloud is done)
     const int64_t max_rounds = (int64_t)(M < N ? M : N) + 2;
-    const int batch = 4;
+    // every cloud needs several rounds: the first batches are long, later ones
+    // short so that few rounds run after the last cloud is done
+    const int first_batch = 6, batch = 2;
     uint32_t* poll = poll_buffer();
     if (!poll) {
         // synchronous polling
@@ -593,15 +745,15 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
         (void)hipEventDestroy(ev[0]);
         return e;
     }
-    auto issue = [&](int slot) {
-        hipError_t r = launch_batch(batch);
+    auto issue = [&](int slot, int rounds) {
+        hipError_t r = launch_batch(rounds);
         if (r == hipSuccess)
             r = hipMemcpyAsync(&poll[slot], ctl.ndone, sizeof(uint32_t), hipMemcpyDeviceToHost, s);
         if (r == hipSuccess) r = hipEventRecord(ev[slot], s);
         return r;
     };
-    e = issue(0);
-    if (e == hipSuccess) e = issue(1);
+    e = issue(0, first_batch);
+    if (e == hipSuccess) e = issue(1, batch);
     for (int k = 0; e == hipSuccess; ++k) {
         const int slot = k & 1;
         if ((e = hipEventSynchronize(ev[slot])) != hipSuccess) break;
@@ -610,7 +762,7 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
             *status_out = CAGQ_ERR_CAPACITY;
             break;
         }
-        e = issue(slot);
+        e = issue(slot, batch);
     }
     (void)hipEventDestroy(ev[0]);
     (void)hipEventDestroy(ev[1]);
