@@ -66,6 +66,8 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_blocker = take(4 * BN);
     L->cas_dirty = take(4 * BN);
     L->cas_ctl = take(CasCtl::bytes(B));
+    const bool lists = N <= kCasLdsMaxN && d->radius <= 2;
+    L->cas_nbr = take(lists ? 2 * BN * (size_t)nbr_stride(d->radius) : 0);
     L->sel_thr = take(8 * (size_t)B);
     L->sel_hist = take(4 * (size_t)kSelPasses * B * kSelBins);
     L->total = off;
@@ -135,6 +137,10 @@ int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t se
     const int64_t side = 2 * (int64_t)g->desc.radius + 1;
     const int64_t lam = side * side * side;
     if ((65536LL + (int64_t)beta_q16) * lam * lam >= 2147483648LL) return CAGQ_ERR_INVALID_ARG;
+    if (cas_lds_fits(L, g->desc, beta_q16)) {
+        hipError_t e = launch_cas_lds(L, g->desc, g->workspace, M, center_lin, m_valid, (hipStream_t)stream);
+        return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+    }
     int status = CAGQ_OK;
     hipError_t e = run_cas(L, g->desc, g->workspace, M, beta_q16, (hipStream_t)stream, &status);
     if (e != hipSuccess) return CAGQ_ERR_HIP;

@@ -1,0 +1,443 @@
+// Coverage-Aware Sampling (Sec. 3.2, Eqs. 1-2, greedy reading) for small
+// clouds: one 1024-thread workgroup per cloud runs every round with all of
+// its state in LDS, then selects and emits the centers, in one launch.
+//
+// The greedy, its exact round formulation and its tie-break are those of the
+// many-kernel path in cagq_sample.hip; only the storage and the scheduling
+// differ. With beta = 0 a score is 2^16 * lambda * U with U the number of
+// uncovered voxels of the neighbourhood, so the key (score, -lin) orders
+// exactly as the 32-bit key (U << 25) | (2^25 - 1 - slot): slots are ranks of
+// lin, and an unpicked voxel's key is never 0.
+//
+// Every round walks, for some voxels, the occupied voxels within distance r
+// (scoring) or 2r (picking, marking). A first kernel, one thread per voxel
+// over the whole batch, writes these as neighbour lists once; the rounds
+// then need no geometry at all.
+//
+// Per round, each thread first looks at the slots it owns (slot tid + k*1024)
+// and puts those that need real work into an LDS queue: voxels to rescore,
+// then voxels that their cached blocker no longer beats. The workgroup then
+// drains the queue, one voxel per thread, packed into as few waves as
+// possible. A voxel picked in round R keeps its key as a competitor for the
+// rest of round R; from round R+1 on its key is 0 (it competes no more) and
+// its pick key is kept in the two 16-bit words that an unpicked voxel uses
+// for its blocker and its rescoring round.
+#include "cagq_internal.h"
+
+namespace cagq {
+
+namespace {
+
+constexpr int kT = 1024;                   // threads of the workgroup
+constexpr int kNW = kT / kWave;            // waves of the workgroup
+constexpr int kKS = kCasLdsMaxN / kT;      // owned slots per thread
+constexpr int kKeyShift = 25;              // key = (U << 25) | (2^25 - 1 - slot)
+constexpr uint32_t kSlotMask = (1u << kKeyShift) - 1;
+constexpr uint16_t kNone = 0xFFFF;
+constexpr int kNbrThreads = 256;
+
+struct Dims {
+    int32_t D[3];
+};
+
+// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz): bit j of
+// `mask` is x' = x - h + j (0 outside the grid); the set bits, in ascending
+// order, have the slots first, first + 1, ...
+__device__ __forceinline__ void grid_row(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
+                                         const Dims& g, int32_t x, int32_t yy, int32_t zz, int32_t h,
+                                         uint32_t& first, uint32_t& mask) {
+    first = 0;
+    mask = 0;
+    if (yy < 0 || yy >= g.D[1] || zz < 0 || zz >= g.D[2]) return;
+    const int32_t xs = x - h;
+    const int32_t lo_x = xs < 0 ? 0 : xs;
+    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
+    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yy + (uint32_t)g.D[1] * (uint32_t)zz);
+    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
+    const uint32_t w0 = lo >> 6, o = lo & 63;
+    const uint64_t a = bm[w0];
+    uint64_t bits = a >> o;
+    if ((hi >> 6) != w0) bits |= bm[w0 + 1] << (64 - o);  // o > 0 here
+    mask = (uint32_t)(bits & ((1ull << (hi - lo + 1)) - 1)) << (lo_x - xs);
+    first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
+}
+
+// Neighbour lists: for every occupied voxel, the slots of the occupied voxels
+// within Chebyshev distance r (itself included), then those at distance
+// r+1..2r, each group in ascending (dz, dy, dx) order.
+template <int RAD>
+__global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, int64_t W, Dims g,
+                                                         const int32_t* __restrict__ nvox,
+                                                         const uint32_t* __restrict__ vox_lin,
+                                                         const uint64_t* __restrict__ bitmap,
+                                                         const uint32_t* __restrict__ word_rank,
+                                                         uint16_t* __restrict__ nbr) {
+    constexpr int H = 2 * RAD;
+    constexpr int ST = nbr_stride(RAD);
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    if (gid >= B * N) return;
+    const int32_t b = gid / N, s = gid - b * N;
+    if (s >= nvox[b]) return;
+    const uint32_t lin = vox_lin[gid];
+    const int32_t x = (int32_t)(lin % (uint32_t)g.D[0]);
+    const int32_t y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
+    const int32_t z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
+    const uint64_t* bm = bitmap + (size_t)b * W;
+    const uint32_t* wr = word_rank + (size_t)b * W;
+    uint16_t* out = nbr + (size_t)gid * ST;
+    uint32_t n = 8;
+    for (int dz = -RAD; dz <= RAD; ++dz)
+        for (int dy = -RAD; dy <= RAD; ++dy) {
+            uint32_t first, mask;
+            grid_row(bm, wr, g, x, y + dy, z + dz, RAD, first, mask);
+            for (uint32_t sl = first; mask; mask &= mask - 1, ++sl) out[n++] = (uint16_t)sl;
+        }
+    const uint32_t n_r = n - 8;
+    for (int dz = -H; dz <= H; ++dz)
+        for (int dy = -H; dy <= H; ++dy) {
+            uint32_t first, mask;
+            grid_row(bm, wr, g, x, y + dy, z + dz, H, first, mask);
+            const bool inner = dz >= -RAD && dz <= RAD && dy >= -RAD && dy <= RAD;
+            for (uint32_t sl = first; mask; mask &= mask - 1, ++sl) {
+                const int q = __ffs(mask) - 1;  // dx = q - H
+                if (!(inner && q >= H - RAD && q <= H + RAD)) out[n++] = (uint16_t)sl;
+            }
+        }
+    out[0] = (uint16_t)n_r;
+    out[1] = (uint16_t)(n - 8);
+}
+
+__device__ __forceinline__ uint32_t wmax32(uint32_t v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint32_t o = (uint32_t)__shfl_xor((int)v, d, kWave);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+__device__ __forceinline__ uint32_t wsum32(uint32_t v) {
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
+    return v;
+}
+
+// Appends the slots s = tid + k*kT with bit k of `want` set to the queue.
+// One LDS atomic per wave. Every thread of the workgroup must call it.
+__device__ __forceinline__ void enqueue(uint32_t want, uint16_t* q, uint32_t* s_qn) {
+    const int lane = lane_id();
+    const uint64_t below = (1ull << lane) - 1;
+    uint64_t bal[kKS];
+    uint32_t tot = 0;
+#pragma unroll
+    for (int k = 0; k < kKS; ++k) {
+        bal[k] = __ballot((want >> k) & 1u);
+        tot += (uint32_t)__popcll(bal[k]);
+    }
+    uint32_t base = 0;
+    if (lane == 0 && tot) base = atomicAdd(s_qn, tot);
+    base = (uint32_t)__shfl((int)base, 0, kWave);
+#pragma unroll
+    for (int k = 0; k < kKS; ++k) {
+        if ((want >> k) & 1u) q[base + (uint32_t)__popcll(bal[k] & below)] = (uint16_t)(threadIdx.x + k * kT);
+        base += (uint32_t)__popcll(bal[k]);
+    }
+}
+
+// Entry j (0..7) of a 16-byte group of list entries.
+__device__ __forceinline__ uint32_t entry(const uint4& v, int j) {
+    const uint32_t w = j < 2 ? v.x : j < 4 ? v.y : j < 6 ? v.z : v.w;
+    return (j & 1) ? w >> 16 : w & 0xFFFFu;
+}
+
+// Number of entries base..base+7 of a list (of n entries) whose voxel is
+// not covered.
+__device__ __forceinline__ uint32_t uncovered(const uint4& v, uint32_t base, uint32_t n, const uint8_t* cov) {
+    uint32_t cv[8], u = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) cv[j] = base + j < n ? cov[entry(v, j)] : 1u;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) u += cv[j] == 0 ? 1u : 0u;
+    return u;
+}
+
+// A winner's marks on entries base..base+7 of its list: rescoring for the
+// unpicked ones (the winner itself and earlier picks keep their pick key in
+// dty), coverage for the first n_r (those within distance r).
+__device__ __forceinline__ void mark(const uint4& v, uint32_t base, uint32_t n_r, uint32_t n2, uint32_t self,
+                                     uint16_t cur, const uint16_t* rnd, uint16_t* dty, uint8_t* cov) {
+    uint32_t sl[8];
+    uint16_t rr[8];
+    uint8_t cc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) sl[j] = base + j < n2 ? entry(v, j) : self;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        rr[j] = rnd[sl[j]];
+        cc[j] = cov[sl[j]];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (base + j < n2) {
+            if (rr[j] == 0) dty[sl[j]] = cur;
+            if (base + j < n_r) cov[sl[j]] = (uint8_t)(cc[j] + 1);
+        }
+    }
+}
+
+template <int RAD>
+__global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t cap,
+                                                const int32_t* __restrict__ nvox,
+                                                const uint32_t* __restrict__ vox_lin,
+                                                const uint16_t* __restrict__ nbr,
+                                                int32_t* __restrict__ center_lin, int32_t* __restrict__ m_valid,
+                                                int* __restrict__ status) {
+    constexpr int ST = nbr_stride(RAD);
+    extern __shared__ __align__(16) unsigned char lds[];
+    uint32_t* key = reinterpret_cast<uint32_t*>(lds);           // competitor key, 0 once out
+    uint16_t* rnd = reinterpret_cast<uint16_t*>(key + cap);     // round that picked it + 1, 0 = unpicked
+    uint16_t* blk = rnd + cap;   // unpicked: a neighbour that beat it; picked: pick key >> 16
+    uint16_t* dty = blk + cap;   // unpicked: round that must rescore it; picked: pick key & 0xFFFF
+    uint16_t* que = dty + cap;   // work queue of slots
+    uint8_t* cov = reinterpret_cast<uint8_t*>(que + cap);       // centers covering the voxel
+    __shared__ uint32_t s_max, s_cnt, s_qn;
+    __shared__ uint32_t s_hist[128];
+    __shared__ uint32_t s_digit, s_below;
+    __shared__ uint32_t s_wsum[kNW];
+
+    const int32_t b = blockIdx.x;
+    const int tid = threadIdx.x, lane = lane_id(), wv = tid / kWave;
+    const int32_t nv = nvox[b];
+    const int32_t m = M < nv ? M : nv;
+    if (m <= 0) {  // no occupied voxel (the build has raised an error): nothing to choose
+        if (tid == 0) m_valid[b] = 0;
+        return;
+    }
+    const uint32_t* vl = vox_lin + (size_t)b * N;
+    const uint16_t* nb = nbr + (size_t)b * N * ST;
+    for (int32_t s = tid; s < nv; s += kT) {
+        rnd[s] = 0;
+        blk[s] = kNone;
+        dty[s] = 0;
+        cov[s] = 0;
+    }
+
+    bool done = false;
+    const int32_t max_r = m + 2;
+    for (int32_t R = 0; R < max_r; ++R) {
+        const uint16_t cur = (uint16_t)(R + 1);
+        __syncthreads();
+        if (tid == 0) {
+            s_max = 0;
+            s_cnt = 0;
+            s_qn = 0;
+        }
+        __syncthreads();
+        // -- scoring. Owned slots: last round's picks leave the competition,
+        // clean unpicked keys count towards the maximum, the rest is queued.
+        uint32_t lmax = 0, want = 0;
+#pragma unroll
+        for (int k = 0; k < kKS; ++k) {
+            const int32_t s = tid + k * kT;
+            if (s < nv) {
+                const uint16_t r = rnd[s];
+                if (R > 0 && r == (uint16_t)R) key[s] = 0;
+                const bool dirty = r == 0 && (R == 0 || dty[s] == (uint16_t)R);
+                if (r == 0 && !dirty) {
+                    const uint32_t kv = key[s];
+                    lmax = kv > lmax ? kv : lmax;
+                }
+                want |= dirty ? 1u << k : 0u;
+            }
+        }
+        enqueue(want, que, &s_qn);
+        __syncthreads();
+        const uint32_t qa = s_qn;
+        for (uint32_t i = tid; i < qa; i += kT) {
+            const uint32_t s = que[i];
+            const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
+            const uint32_t n_r = e[0].x & 0xFFFFu;
+            uint32_t U = 0;
+            for (uint32_t c = 0; c * 8 < n_r; ++c) U += uncovered(e[1 + c], c * 8, n_r, cov);
+            const uint32_t kv = (U << kKeyShift) | (kSlotMask - s);
+            key[s] = kv;
+            lmax = kv > lmax ? kv : lmax;
+        }
+        lmax = wmax32(lmax);
+        if (lane == 0 && lmax) atomicMax(&s_max, lmax);
+        __syncthreads();
+        const uint32_t G = s_max;
+        if (tid == 0) s_qn = 0;
+        __syncthreads();
+        // -- picking. Owned slots: earlier picks above the best unpicked key
+        // are counted; an unpicked voxel still beaten by its cached blocker
+        // stays out; the rest is queued for a pass over its list.
+        uint32_t above = 0;
+        want = 0;
+#pragma unroll
+        for (int k = 0; k < kKS; ++k) {
+            const int32_t s = tid + k * kT;
+            if (s < nv) {
+                const uint16_t r = rnd[s], bl = blk[s];
+                if (r != 0) {
+                    const uint32_t pk = ((uint32_t)bl << 16) | dty[s];
+                    above += pk > G ? 1u : 0u;
+                } else {
+                    const bool beaten = bl != kNone && key[bl] > key[s];
+                    want |= beaten ? 0u : 1u << k;
+                }
+            }
+        }
+        above = wsum32(above);
+        if (lane == 0 && above) atomicAdd(&s_cnt, above);
+        enqueue(want, que, &s_qn);
+        __syncthreads();
+        // the picks above the best unpicked key are the sequential greedy's
+        // first ones; the voxels this round would pick all have keys <= G
+        if (s_cnt >= (uint32_t)m) {
+            done = true;
+            break;
+        }
+        const uint32_t qb = s_qn;
+        for (uint32_t i = tid; i < qb; i += kT) {
+            const uint32_t s = que[i];
+            const uint32_t my = key[s];
+            const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
+            const uint4 h = e[0];
+            const uint32_t n_r = h.x & 0xFFFFu, n2 = h.x >> 16;
+            int32_t found = -1;
+            for (uint32_t c = 0; c * 8 < n2 && found < 0; ++c) {
+                const uint4 v = e[1 + c];
+                uint32_t sl[8], kk[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(v, j) : s;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (found < 0 && kk[j] > my) found = (int32_t)sl[j];
+            }
+            if (found >= 0) {
+                blk[s] = (uint16_t)found;
+                continue;
+            }
+            // a winner: rescoring within 2r, coverage within r. A round's
+            // winners are more than 2r apart, so no other winner is on the
+            // list and their r-neighbourhoods are disjoint: plain updates
+            // are exact.
+            rnd[s] = cur;
+            blk[s] = (uint16_t)(my >> 16);
+            dty[s] = (uint16_t)(my & 0xFFFFu);
+            for (uint32_t c = 0; c * 8 < n2; ++c) mark(e[1 + c], c * 8, n_r, n2, s, cur, rnd, dty, cov);
+        }
+    }
+    if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
+    __syncthreads();
+
+    // The m largest pick keys. A pick key is (U << 25) | (2^25 - 1 - slot):
+    // with U* the largest U for which at least m picks have U >= U*, the
+    // chosen picks are those with U > U* and, of those with U = U*, the
+    // `need` lowest slots.
+    uint32_t pk[kKS];
+    for (int32_t i = tid; i < 128; i += kT) s_hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < kKS; ++k) {
+        const int32_t s = tid + k * kT;
+        pk[k] = 0;
+        if (s < nv && rnd[s] != 0) pk[k] = ((uint32_t)blk[s] << 16) | dty[s];
+        const bool act = pk[k] != 0;
+        const uint32_t u = pk[k] >> kKeyShift;
+        uint64_t am = __ballot(act);
+        // one LDS atomic per distinct U for the first few values of the wave
+        for (int rr = 0; rr < 4 && am; ++rr) {
+            const int leader = __ffsll((unsigned long long)am) - 1;
+            const uint32_t u0 = (uint32_t)__shfl((int)u, leader, kWave);
+            const uint64_t same = __ballot(act && u == u0) & am;
+            if (lane == leader) atomicAdd(&s_hist[u0], (uint32_t)__popcll(same));
+            am &= ~same;
+        }
+        if ((am >> lane) & 1ull) atomicAdd(&s_hist[u], 1u);
+    }
+    __syncthreads();
+    if (tid < kWave) {
+        // lane l holds U = 127 - 2l and 126 - 2l: the scan counts from the top
+        const uint32_t h0 = s_hist[127 - 2 * tid], h1 = s_hist[126 - 2 * tid];
+        const uint32_t incl = wave_incl_scan<uint32_t>(h0 + h1);
+        const uint32_t run0 = incl - h0 - h1, run1 = run0 + h0;
+        if (run0 < (uint32_t)m && run0 + h0 >= (uint32_t)m) {
+            s_digit = (uint32_t)(127 - 2 * tid);
+            s_below = (uint32_t)m - run0;
+        }
+        if (run1 < (uint32_t)m && run1 + h1 >= (uint32_t)m) {
+            s_digit = (uint32_t)(126 - 2 * tid);
+            s_below = (uint32_t)m - run1;
+        }
+    }
+    __syncthreads();
+    const uint32_t ustar = s_digit, need = s_below;
+
+    // chosen slots in ascending slot (= lin) order; position p < m also
+    // fills p + m, p + 2m, ... < M (cyclic padding)
+    int32_t* out = center_lin + (size_t)b * M;
+    const uint64_t below = (1ull << lane) - 1;
+    uint32_t base_h = 0, base_t = 0;
+#pragma unroll
+    for (int k = 0; k < kKS; ++k) {
+        const int32_t s = k * kT + tid;
+        const uint32_t u = pk[k] >> kKeyShift;
+        const bool hi = pk[k] != 0 && u > ustar, tie = pk[k] != 0 && u == ustar;
+        const uint64_t bh = __ballot(hi), bt = __ballot(tie);
+        if (lane == 0) s_wsum[wv] = (uint32_t)__popcll(bh) | ((uint32_t)__popcll(bt) << 16);
+        __syncthreads();
+        uint32_t off = 0, tot = 0;
+        for (int w = 0; w < kNW; ++w) {
+            const uint32_t c = s_wsum[w];
+            if (w < wv) off += c;
+            tot += c;
+        }
+        const uint32_t hb = base_h + (off & 0xFFFFu) + (uint32_t)__popcll(bh & below);
+        const uint32_t tb = base_t + (off >> 16) + (uint32_t)__popcll(bt & below);
+        if (hi || (tie && tb < need)) {
+            const uint32_t pos = hb + (tb < need ? tb : need);
+            const int32_t lin = (int32_t)vl[s];
+            for (int32_t j = (int32_t)pos; j < M; j += m) out[j] = lin;
+        }
+        base_h += tot & 0xFFFFu;
+        base_t += tot >> 16;
+        __syncthreads();
+    }
+    if (tid == 0) m_valid[b] = m;
+}
+
+int32_t lds_cap(int32_t N) { return (N + 3) & ~3; }
+size_t lds_bytes(int32_t cap) { return (size_t)13 * cap + 16; }
+
+}  // namespace
+
+bool cas_lds_fits(const Layout& L, const cagq_grid_desc& d, uint32_t beta_q16) {
+    return beta_q16 == 0 && (d.radius == 1 || d.radius == 2) && L.N <= kCasLdsMaxN;
+}
+
+hipError_t launch_cas_lds(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, int32_t* center_lin,
+                          int32_t* m_valid, hipStream_t s) {
+    Dims g;
+    for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
+    const int32_t cap = lds_cap(L.N);
+    const size_t bytes = lds_bytes(cap);
+    const int32_t* nvox = at<int32_t>(ws, L.nvox);
+    const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
+    uint16_t* nbr = at<uint16_t>(ws, L.cas_nbr);
+    const unsigned nb_blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
+    auto go = [&](auto nbr_kern, auto kern) {
+        nbr_kern<<<nb_blocks, kNbrThreads, 0, s>>>(L.B, L.N, L.W, g, nvox, vox_lin, at<uint64_t>(ws, L.bitmap),
+                                                   at<uint32_t>(ws, L.word_rank), nbr);
+        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (e != hipSuccess) return e;
+        kern<<<L.B, kT, bytes, s>>>(L.N, M, cap, nvox, vox_lin, nbr, center_lin, m_valid, at<int>(ws, L.status));
+        return hipGetLastError();
+    };
+    return d.radius == 1 ? go(k_cas_nbr<1>, k_cas_lds<1>) : go(k_cas_nbr<2>, k_cas_lds<2>);
+}
+
+}  // namespace cagq

@@ -62,6 +62,7 @@ struct Layout {
     size_t cas_blocker;   // i32 [B][N] CAS: a neighbour whose key beat the voxel's (-1 = none)
     size_t cas_dirty;     // u32 [B][N] CAS: round whose scoring must recompute the voxel
     size_t cas_ctl;       // CAS control block, see CasCtl
+    size_t cas_nbr;       // u16 [B][N][nbr_stride(r)] CAS neighbour lists of small clouds (see below)
     size_t sel_thr;       // u64 [B] selection threshold: keys <= it are chosen
     size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
@@ -76,6 +77,15 @@ constexpr int kCasParts = 32;
 struct CasCtl {
     static size_t bytes(int B) { return (size_t)B * (2 * kCasParts * 12 + 4) + 64; }
 };
+
+// Neighbour lists of the single-workgroup CAS (clouds of at most kCasLdsMaxN
+// points, r <= 2): per slot a header of 8 u16 (entries within Chebyshev r,
+// entries within 2r, 6 unused) and then the slots of the occupied voxels
+// within distance 2r, those within r (the slot itself included) first.
+constexpr int32_t kCasLdsMaxN = 8192;
+__host__ __device__ constexpr int nbr_stride(int r) {
+    return 8 + (((4 * r + 1) * (4 * r + 1) * (4 * r + 1) + 7) & ~7);
+}
 
 bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L);
 
@@ -323,6 +333,12 @@ hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uin
 // Greedy coverage-aware sampling (rounds of neighbourhood maxima).
 hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M,
                    uint32_t beta_q16, hipStream_t s, int* status_out);
+
+// The same greedy for small clouds with beta = 0: one workgroup per cloud
+// holds every round's state in LDS and also selects and emits the centers.
+bool cas_lds_fits(const Layout& L, const cagq_grid_desc& d, uint32_t beta_q16);
+hipError_t launch_cas_lds(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, int32_t* center_lin,
+                          int32_t* m_valid, hipStream_t s);
 
 hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* points, void* ws,
                         const uint32_t* weights, const int32_t* center_lin, int32_t M, int32_t K,
