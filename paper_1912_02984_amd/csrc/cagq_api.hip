@@ -66,8 +66,10 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_blocker = take(4 * BN);
     L->cas_dirty = take(4 * BN);
     L->cas_ctl = take(CasCtl::bytes(B));
-    const bool lists = N <= kCasLdsMaxN && d->radius <= 2;
-    L->cas_nbr = take(lists ? 2 * BN * (size_t)nbr_stride(d->radius) : 0);
+    L->has_nbr16 = N <= kCasLdsMaxN && d->radius <= 2;
+    L->has_nbr32 = N > kCasLdsMaxN && d->radius == 1;
+    L->cas_nbr = take(L->has_nbr16 ? 2 * BN * (size_t)nbr_stride(d->radius) : 0);
+    L->cas_nbr32 = take(L->has_nbr32 ? 4 * BN * (size_t)kNbr32Stride : 0);
     L->sel_thr = take(8 * (size_t)B);
     L->sel_hist = take(4 * (size_t)kSelPasses * B * kSelBins);
     L->total = off;

@@ -10,9 +10,9 @@
 // lin, and an unpicked voxel's key is never 0.
 //
 // Every round walks, for some voxels, the occupied voxels within distance r
-// (scoring) or 2r (picking, marking). A first kernel, one thread per voxel
-// over the whole batch, writes these as neighbour lists once; the rounds
-// then need no geometry at all.
+// (scoring) or 2r (picking, marking): the neighbour lists of
+// cagq_cas_nbr.hip, written once before the rounds, so that the rounds need
+// no geometry at all.
 //
 // Per round, each thread first looks at the slots it owns (slot tid + k*1024)
 // and puts those that need real work into an LDS queue: voxels to rescore,
@@ -34,78 +34,6 @@ constexpr int kKS = kCasLdsMaxN / kT;      // owned slots per thread
 constexpr int kKeyShift = 25;              // key = (U << 25) | (2^25 - 1 - slot)
 constexpr uint32_t kSlotMask = (1u << kKeyShift) - 1;
 constexpr uint16_t kNone = 0xFFFF;
-constexpr int kNbrThreads = 256;
-
-struct Dims {
-    int32_t D[3];
-};
-
-// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz): bit j of
-// `mask` is x' = x - h + j (0 outside the grid); the set bits, in ascending
-// order, have the slots first, first + 1, ...
-__device__ __forceinline__ void grid_row(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
-                                         const Dims& g, int32_t x, int32_t yy, int32_t zz, int32_t h,
-                                         uint32_t& first, uint32_t& mask) {
-    first = 0;
-    mask = 0;
-    if (yy < 0 || yy >= g.D[1] || zz < 0 || zz >= g.D[2]) return;
-    const int32_t xs = x - h;
-    const int32_t lo_x = xs < 0 ? 0 : xs;
-    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
-    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yy + (uint32_t)g.D[1] * (uint32_t)zz);
-    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
-    const uint32_t w0 = lo >> 6, o = lo & 63;
-    const uint64_t a = bm[w0];
-    uint64_t bits = a >> o;
-    if ((hi >> 6) != w0) bits |= bm[w0 + 1] << (64 - o);  // o > 0 here
-    mask = (uint32_t)(bits & ((1ull << (hi - lo + 1)) - 1)) << (lo_x - xs);
-    first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
-}
-
-// Neighbour lists: for every occupied voxel, the slots of the occupied voxels
-// within Chebyshev distance r (itself included), then those at distance
-// r+1..2r, each group in ascending (dz, dy, dx) order.
-template <int RAD>
-__global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, int64_t W, Dims g,
-                                                         const int32_t* __restrict__ nvox,
-                                                         const uint32_t* __restrict__ vox_lin,
-                                                         const uint64_t* __restrict__ bitmap,
-                                                         const uint32_t* __restrict__ word_rank,
-                                                         uint16_t* __restrict__ nbr) {
-    constexpr int H = 2 * RAD;
-    constexpr int ST = nbr_stride(RAD);
-    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
-    if (gid >= B * N) return;
-    const int32_t b = gid / N, s = gid - b * N;
-    if (s >= nvox[b]) return;
-    const uint32_t lin = vox_lin[gid];
-    const int32_t x = (int32_t)(lin % (uint32_t)g.D[0]);
-    const int32_t y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
-    const int32_t z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
-    const uint64_t* bm = bitmap + (size_t)b * W;
-    const uint32_t* wr = word_rank + (size_t)b * W;
-    uint16_t* out = nbr + (size_t)gid * ST;
-    uint32_t n = 8;
-    for (int dz = -RAD; dz <= RAD; ++dz)
-        for (int dy = -RAD; dy <= RAD; ++dy) {
-            uint32_t first, mask;
-            grid_row(bm, wr, g, x, y + dy, z + dz, RAD, first, mask);
-            for (uint32_t sl = first; mask; mask &= mask - 1, ++sl) out[n++] = (uint16_t)sl;
-        }
-    const uint32_t n_r = n - 8;
-    for (int dz = -H; dz <= H; ++dz)
-        for (int dy = -H; dy <= H; ++dy) {
-            uint32_t first, mask;
-            grid_row(bm, wr, g, x, y + dy, z + dz, H, first, mask);
-            const bool inner = dz >= -RAD && dz <= RAD && dy >= -RAD && dy <= RAD;
-            for (uint32_t sl = first; mask; mask &= mask - 1, ++sl) {
-                const int q = __ffs(mask) - 1;  // dx = q - H
-                if (!(inner && q >= H - RAD && q <= H + RAD)) out[n++] = (uint16_t)sl;
-            }
-        }
-    out[0] = (uint16_t)n_r;
-    out[1] = (uint16_t)(n - 8);
-}
 
 __device__ __forceinline__ uint32_t wmax32(uint32_t v) {
 #pragma unroll
@@ -416,28 +344,25 @@ size_t lds_bytes(int32_t cap) { return (size_t)13 * cap + 16; }
 }  // namespace
 
 bool cas_lds_fits(const Layout& L, const cagq_grid_desc& d, uint32_t beta_q16) {
-    return beta_q16 == 0 && (d.radius == 1 || d.radius == 2) && L.N <= kCasLdsMaxN;
+    return beta_q16 == 0 && (d.radius == 1 || d.radius == 2) && L.N <= kCasLdsMaxN && L.has_nbr16;
 }
 
 hipError_t launch_cas_lds(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, int32_t* center_lin,
                           int32_t* m_valid, hipStream_t s) {
-    Dims g;
-    for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
+    hipError_t e = launch_cas_nbr(L, d, ws, s);
+    if (e != hipSuccess) return e;
     const int32_t cap = lds_cap(L.N);
     const size_t bytes = lds_bytes(cap);
     const int32_t* nvox = at<int32_t>(ws, L.nvox);
     const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
-    uint16_t* nbr = at<uint16_t>(ws, L.cas_nbr);
-    const unsigned nb_blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
-    auto go = [&](auto nbr_kern, auto kern) {
-        nbr_kern<<<nb_blocks, kNbrThreads, 0, s>>>(L.B, L.N, L.W, g, nvox, vox_lin, at<uint64_t>(ws, L.bitmap),
-                                                   at<uint32_t>(ws, L.word_rank), nbr);
-        hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
-        if (e != hipSuccess) return e;
+    const uint16_t* nbr = at<uint16_t>(ws, L.cas_nbr);
+    auto go = [&](auto kern) {
+        hipError_t r = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes);
+        if (r != hipSuccess) return r;
         kern<<<L.B, kT, bytes, s>>>(L.N, M, cap, nvox, vox_lin, nbr, center_lin, m_valid, at<int>(ws, L.status));
         return hipGetLastError();
     };
-    return d.radius == 1 ? go(k_cas_nbr<1>, k_cas_lds<1>) : go(k_cas_nbr<2>, k_cas_lds<2>);
+    return d.radius == 1 ? go(k_cas_lds<1>) : go(k_cas_lds<2>);
 }
 
 }  // namespace cagq

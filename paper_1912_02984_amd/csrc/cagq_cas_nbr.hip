@@ -1,0 +1,159 @@
+// Neighbour lists for Coverage-Aware Sampling (Sec. 3.2, Eqs. 1-2): every
+// round of the greedy walks, for some voxels, the occupied voxels within
+// Chebyshev distance r (the coverage term of a score) or 2r (the voxels a
+// pick competes with and the voxels whose score it changes). One thread per
+// occupied voxel writes these slots once per grid, so that the rounds need
+// no geometry: first those within r (the voxel itself included), then those
+// at distance r+1..2r, each group in ascending (dz, dy, dx) order.
+//
+// Two formats: u16 entries behind an 8-entry header for clouds of at most
+// kCasLdsMaxN points (r <= 2), u32 entries behind a 4-entry header for
+// larger clouds with r = 1. Header entry 0 is the number within r, entry 1
+// the number within 2r.
+#include "cagq_internal.h"
+
+namespace cagq {
+
+namespace {
+
+constexpr int kNbrThreads = 256;
+
+struct Dims {
+    int32_t D[3];
+};
+
+struct Row {
+    uint32_t first;  // slot of the first occupied voxel at or after the segment's start
+    uint32_t mask;   // bit j: voxel x - h + j occupied (0 outside the grid)
+};
+
+// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz).
+// Branch-free: rows outside the grid are clamped into it for the loads and
+// get an empty mask, and the second word is always loaded (the same word
+// unless the segment crosses a word boundary), so the loads of many rows are
+// in flight together.
+__device__ __forceinline__ Row load_row(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
+                                        const Dims& g, int32_t x, int32_t yy, int32_t zz, int32_t h) {
+    const bool inside = yy >= 0 && yy < g.D[1] && zz >= 0 && zz < g.D[2];
+    const int32_t yc = yy < 0 ? 0 : (yy >= g.D[1] ? g.D[1] - 1 : yy);
+    const int32_t zc = zz < 0 ? 0 : (zz >= g.D[2] ? g.D[2] - 1 : zz);
+    const int32_t xs = x - h;
+    const int32_t lo_x = xs < 0 ? 0 : xs;
+    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
+    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
+    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
+    const uint32_t w0 = lo >> 6, o = lo & 63;
+    const uint64_t a = bm[w0];
+    const uint64_t c = bm[hi >> 6];
+    // when both ends share a word, the bits shifted in from c lie above the segment
+    const uint64_t bits = (a >> o) | (o ? c << (64 - o) : 0ull);
+    Row r;
+    r.mask = inside ? (uint32_t)(bits & ((1ull << (hi_x - lo_x + 1)) - 1)) << (lo_x - xs) : 0u;
+    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
+    return r;
+}
+
+// E: entry type, ST: entries per voxel (header included), HDR: header entries.
+template <int RAD, typename E, int ST, int HDR>
+__global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, int64_t W, Dims g,
+                                                         const int32_t* __restrict__ nvox,
+                                                         const uint32_t* __restrict__ vox_lin,
+                                                         const uint64_t* __restrict__ bitmap,
+                                                         const uint32_t* __restrict__ word_rank, E* __restrict__ nbr) {
+    constexpr int H = 2 * RAD, S2 = 2 * H + 1;
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    if (gid >= B * N) return;
+    const int32_t b = gid / N, s = gid - b * N;
+    if (s >= nvox[b]) return;
+    const uint32_t lin = vox_lin[gid];
+    const int32_t x = (int32_t)(lin % (uint32_t)g.D[0]);
+    const int32_t y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
+    const int32_t z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
+    const uint64_t* bm = bitmap + (size_t)b * W;
+    const uint32_t* wr = word_rank + (size_t)b * W;
+    E* out = nbr + (size_t)gid * ST;
+    uint32_t n = HDR;
+    // bits H-RAD..H+RAD of a row of half-width H are the voxels within r in x
+    constexpr uint32_t kInner = ((1u << (2 * RAD + 1)) - 1) << (H - RAD);
+    if constexpr (RAD == 1) {
+        // all 25 rows of the window at once
+        Row rows[S2 * S2];
+#pragma unroll
+        for (int j = 0; j < S2 * S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j % S2 - H, z + j / S2 - H, H);
+#pragma unroll
+        for (int j = 0; j < S2 * S2; ++j) {
+            const int dy = j % S2 - H, dz = j / S2 - H;
+            if (dy < -RAD || dy > RAD || dz < -RAD || dz > RAD) continue;
+            for (uint32_t m = rows[j].mask & kInner; m; m &= m - 1) {
+                const uint32_t q = (uint32_t)__ffs(m) - 1;
+                out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+            }
+        }
+        const uint32_t n_r = n - HDR;
+#pragma unroll
+        for (int j = 0; j < S2 * S2; ++j) {
+            const int dy = j % S2 - H, dz = j / S2 - H;
+            const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
+            for (uint32_t m = rows[j].mask & (inner ? ~kInner : ~0u); m; m &= m - 1) {
+                const uint32_t q = (uint32_t)__ffs(m) - 1;
+                out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+            }
+        }
+        out[0] = (E)n_r;
+        out[1] = (E)(n - HDR);
+    } else {
+        // one plane of rows at a time, the window within r first
+        for (int dz = -RAD; dz <= RAD; ++dz) {
+            Row rows[2 * RAD + 1];
+#pragma unroll
+            for (int j = 0; j < 2 * RAD + 1; ++j) rows[j] = load_row(bm, wr, g, x, y + j - RAD, z + dz, RAD);
+#pragma unroll
+            for (int j = 0; j < 2 * RAD + 1; ++j)
+                for (uint32_t sl = rows[j].first, m = rows[j].mask; m; m &= m - 1, ++sl) out[n++] = (E)sl;
+        }
+        const uint32_t n_r = n - HDR;
+        for (int dz = -H; dz <= H; ++dz) {
+            Row rows[S2];
+#pragma unroll
+            for (int j = 0; j < S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j - H, z + dz, H);
+#pragma unroll
+            for (int j = 0; j < S2; ++j) {
+                const int dy = j - H;
+                const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
+                for (uint32_t m = rows[j].mask & (inner ? ~kInner : ~0u); m; m &= m - 1) {
+                    const uint32_t q = (uint32_t)__ffs(m) - 1;
+                    out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                }
+            }
+        }
+        out[0] = (E)n_r;
+        out[1] = (E)(n - HDR);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s) {
+    Dims g;
+    for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
+    const unsigned blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
+    const int32_t* nvox = at<int32_t>(ws, L.nvox);
+    const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
+    const uint64_t* bitmap = at<uint64_t>(ws, L.bitmap);
+    const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
+    if (L.has_nbr32 && d.radius == 1) {
+        k_cas_nbr<1, uint32_t, kNbr32Stride, 4><<<blocks, kNbrThreads, 0, s>>>(
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint32_t>(ws, L.cas_nbr32));
+    } else if (L.has_nbr16 && d.radius == 1) {
+        k_cas_nbr<1, uint16_t, nbr_stride(1), 8><<<blocks, kNbrThreads, 0, s>>>(
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr));
+    } else if (L.has_nbr16 && d.radius == 2) {
+        k_cas_nbr<2, uint16_t, nbr_stride(2), 8><<<blocks, kNbrThreads, 0, s>>>(
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr));
+    } else {
+        return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace cagq

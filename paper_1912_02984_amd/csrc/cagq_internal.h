@@ -63,6 +63,8 @@ struct Layout {
     size_t cas_dirty;     // u32 [B][N] CAS: round whose scoring must recompute the voxel
     size_t cas_ctl;       // CAS control block, see CasCtl
     size_t cas_nbr;       // u16 [B][N][nbr_stride(r)] CAS neighbour lists of small clouds (see below)
+    size_t cas_nbr32;     // u32 [B][N][kNbr32Stride] CAS neighbour lists of larger clouds, r = 1
+    bool has_nbr16, has_nbr32;
     size_t sel_thr;       // u64 [B] selection threshold: keys <= it are chosen
     size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
@@ -86,6 +88,10 @@ constexpr int32_t kCasLdsMaxN = 8192;
 __host__ __device__ constexpr int nbr_stride(int r) {
     return 8 + (((4 * r + 1) * (4 * r + 1) * (4 * r + 1) + 7) & ~7);
 }
+
+// The same lists with u32 entries behind a 4-entry header, for clouds of
+// more than kCasLdsMaxN points with r = 1 (at most 125 entries).
+constexpr int kNbr32Stride = 4 + 128;
 
 bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L);
 
@@ -329,6 +335,10 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
 // key_mode 0: RVS keys from `seed`; key_mode 1: CAS pick keys (largest first).
 hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
                          int32_t* center_lin, int32_t* m_valid, hipStream_t s);
+
+// Writes the CAS neighbour lists of the grid in whichever format the layout
+// holds (has_nbr16 or has_nbr32).
+hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s);
 
 // Greedy coverage-aware sampling (rounds of neighbourhood maxima).
 hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M,

@@ -378,6 +378,11 @@ __device__ __forceinline__ uint32_t row_slot(const RowDesc& r, int j) {
     return r.first + (uint32_t)__popc(r.mask & ((1u << j) - 1));
 }
 
+// Component j (0..3) of a 16-byte group of u32 list entries.
+__device__ __forceinline__ uint32_t u4(const uint4& v, int j) {
+    return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+
 // Reduction of the kCasParts partials of the cloud `b` of each lane. Every
 // lane of the wave must call it.
 __device__ __forceinline__ uint64_t parts_max(const uint64_t* __restrict__ part, int32_t b) {
@@ -447,11 +452,11 @@ __global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
 // and wherever a pick of round R-1 came within distance 2r) and their
 // maximum per cloud. Also retires a cloud once round R-1 found enough picks
 // above the best unpicked key.
-template <int RAD>
+template <int RAD, bool LIST>
 __global__ __launch_bounds__(256) void k_cas_score(
     int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, int64_t lam, uint32_t beta_q16, int32_t M,
     const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
-    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
+    const uint32_t* __restrict__ word_rank, const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
     // no early exit: every lane takes part in the wave reductions
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
@@ -474,32 +479,52 @@ __global__ __launch_bounds__(256) void k_cas_score(
     if (active && s < nv && rnd != 0 && rnd == (uint32_t)R) st.key[gid] = 0;
     if (active && s < nv && rnd == 0) {
         if (R == 0 || st.dirty[gid] == (uint32_t)R) {
-            const uint64_t* bm = bitmap + (size_t)b * W;
-            const uint32_t* wr = word_rank + (size_t)b * W;
             const uint32_t* cv = st.cover + (size_t)b * N;
             const uint32_t lin = vox_lin[gid];
-            int32_t x, y, z;
-            decode(lin, g, &x, &y, &z);
-            constexpr int S = 2 * RAD + 1;
-            RowDesc rows[S * S];
-#pragma unroll
-            for (int j = 0; j < S * S; ++j) rows[j] = row_desc(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
-            // every coverage count of the window loaded at once, then masked
-            uint32_t c[S * S * S];
-#pragma unroll
-            for (int j = 0; j < S * S; ++j)
-#pragma unroll
-                for (int q = 0; q < S; ++q) c[j * S + q] = cv[row_slot_or(rows[j], q, (uint32_t)s)];
             int64_t U = 0, cs = 0;
+            if constexpr (LIST) {
+                // the voxels within r head the list: at most 27 of them
+                static_assert(RAD == 1, "lists of the many-kernel path are for r = 1");
+                const uint4* e = reinterpret_cast<const uint4*>(nbr + (size_t)gid * kNbr32Stride);
+                uint4 q[8];
 #pragma unroll
-            for (int j = 0; j < S * S; ++j)
+                for (int j = 0; j < 8; ++j) q[j] = e[j];
+                const uint32_t n_r = q[0].x;
+                uint32_t c[28];
 #pragma unroll
-                for (int q = 0; q < S; ++q) {
-                    const bool occ = (rows[j].mask >> q) & 1u;
-                    const uint32_t cc = occ ? c[j * S + q] : 0u;
-                    U += (occ && cc == 0) ? 1 : 0;
-                    cs += cc;
+                for (int j = 0; j < 28; ++j) c[j] = cv[(uint32_t)j < n_r ? u4(q[1 + j / 4], j % 4) : (uint32_t)s];
+#pragma unroll
+                for (int j = 0; j < 28; ++j) {
+                    const bool occ = (uint32_t)j < n_r;
+                    U += (occ && c[j] == 0) ? 1 : 0;
+                    cs += occ ? c[j] : 0u;
                 }
+            } else {
+                const uint64_t* bm = bitmap + (size_t)b * W;
+                const uint32_t* wr = word_rank + (size_t)b * W;
+                int32_t x, y, z;
+                decode(lin, g, &x, &y, &z);
+                constexpr int S = 2 * RAD + 1;
+                RowDesc rows[S * S];
+#pragma unroll
+                for (int j = 0; j < S * S; ++j)
+                    rows[j] = row_desc(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
+                // every coverage count of the window loaded at once, then masked
+                uint32_t c[S * S * S];
+#pragma unroll
+                for (int j = 0; j < S * S; ++j)
+#pragma unroll
+                    for (int q = 0; q < S; ++q) c[j * S + q] = cv[row_slot_or(rows[j], q, (uint32_t)s)];
+#pragma unroll
+                for (int j = 0; j < S * S; ++j)
+#pragma unroll
+                    for (int q = 0; q < S; ++q) {
+                        const bool occ = (rows[j].mask >> q) & 1u;
+                        const uint32_t cc = occ ? c[j * S + q] : 0u;
+                        U += (occ && cc == 0) ? 1 : 0;
+                        cs += cc;
+                    }
+            }
             const int64_t score = 65536ll * lam * U - (int64_t)beta_q16 * cs;
             k = ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
             st.key[gid] = k;
@@ -525,11 +550,11 @@ __global__ __launch_bounds__(256) void k_cas_score(
 // and scans its 2r-neighbourhood, one z-plane at a time, only when that one
 // no longer does. Also counts earlier picks whose key beats this round's
 // best unpicked key.
-template <int RAD>
+template <int RAD, bool LIST>
 __global__ __launch_bounds__(256) void k_cas_pick(
     int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, const int32_t* __restrict__ nvox,
     const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
-    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
+    const uint32_t* __restrict__ word_rank, const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
     constexpr int H = 2 * RAD;      // half-width of the competition window
     constexpr int S2 = 2 * H + 1;
     // no early exit: every lane takes part in the wave-wide steps
@@ -560,25 +585,43 @@ __global__ __launch_bounds__(256) void k_cas_pick(
             const int32_t bl = st.blocker[gid];
             const bool beaten = bl >= 0 && ky[bl] > my;
             if (!beaten) {
-                decode(vox_lin[gid], g, &x, &y, &z);
                 int32_t found = -1;
-                // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
-                // row descriptors, then all keys are loaded before comparing (a
-                // clear bit loads the voxel's own key, which never beats it)
-                for (int p = 0; p < S2 && found < 0; ++p) {
-                    const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
-                    RowDesc rows[S2];
+                if constexpr (LIST) {
+                    // 16 entries of the list at a time (a voxel's own key
+                    // stands in past its end: it never beats itself)
+                    const uint4* e = reinterpret_cast<const uint4*>(nbr + (size_t)gid * kNbr32Stride);
+                    const uint32_t n2 = e[0].y;
+                    for (uint32_t c0 = 0; c0 < n2 && found < 0; c0 += 16) {
+                        uint4 q[4];
 #pragma unroll
-                    for (int j = 0; j < S2; ++j) rows[j] = row_desc(bm, wr, g, x, y + j - H, z + dz, H);
-                    uint32_t sl[S2 * S2];
-                    uint64_t kk[S2 * S2];
+                        for (int j = 0; j < 4; ++j) q[j] = e[1 + c0 / 4 + j];
+                        uint64_t kk[16];
 #pragma unroll
-                    for (int i = 0; i < S2 * S2; ++i) sl[i] = row_slot_or(rows[i / S2], i % S2, (uint32_t)s);
+                        for (int j = 0; j < 16; ++j) kk[j] = ky[c0 + j < n2 ? u4(q[j / 4], j % 4) : (uint32_t)s];
 #pragma unroll
-                    for (int i = 0; i < S2 * S2; ++i) kk[i] = ky[sl[i]];
+                        for (int j = 0; j < 16; ++j)
+                            if (found < 0 && kk[j] > my) found = (int32_t)u4(q[j / 4], j % 4);
+                    }
+                } else {
+                    decode(vox_lin[gid], g, &x, &y, &z);
+                    // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
+                    // row descriptors, then all keys are loaded before comparing (a
+                    // clear bit loads the voxel's own key, which never beats it)
+                    for (int p = 0; p < S2 && found < 0; ++p) {
+                        const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
+                        RowDesc rows[S2];
 #pragma unroll
-                    for (int i = 0; i < S2 * S2; ++i)
-                        if (found < 0 && kk[i] > my) found = (int32_t)sl[i];
+                        for (int j = 0; j < S2; ++j) rows[j] = row_desc(bm, wr, g, x, y + j - H, z + dz, H);
+                        uint32_t sl[S2 * S2];
+                        uint64_t kk[S2 * S2];
+#pragma unroll
+                        for (int i = 0; i < S2 * S2; ++i) sl[i] = row_slot_or(rows[i / S2], i % S2, (uint32_t)s);
+#pragma unroll
+                        for (int i = 0; i < S2 * S2; ++i) kk[i] = ky[sl[i]];
+#pragma unroll
+                        for (int i = 0; i < S2 * S2; ++i)
+                            if (found < 0 && kk[i] > my) found = (int32_t)sl[i];
+                    }
                 }
                 if (found >= 0) {
                     st.blocker[gid] = found;
@@ -590,30 +633,41 @@ __global__ __launch_bounds__(256) void k_cas_pick(
             }
         }
     }
-    // the whole wave marks each winner's window, one grid row per lane:
-    // rescoring flags within 2r, coverage counts within r. Winners of a round
-    // are more than 2r apart, so their r-neighbourhoods are disjoint and no
-    // count is raised twice in a round: plain read-modify-write is exact.
+    // the whole wave marks each winner's window, one grid row (or one list
+    // entry) per lane: rescoring flags within 2r, coverage counts within r.
+    // Winners of a round are more than 2r apart, so their r-neighbourhoods
+    // are disjoint and no count is raised twice in a round: plain
+    // read-modify-write is exact.
     uint64_t wins = __ballot(winner);
     while (wins) {
         const int wl = __ffsll((unsigned long long)wins) - 1;
         wins &= wins - 1;
-        const int32_t wx = __shfl(x, wl, kWave), wy = __shfl(y, wl, kWave), wz = __shfl(z, wl, kWave);
         const int32_t wb = __shfl(b, wl, kWave);
-        const uint64_t* wbm = bitmap + (size_t)wb * W;
-        const uint32_t* wwr = word_rank + (size_t)wb * W;
         uint32_t* cv = st.cover + (size_t)wb * N;
         uint32_t* dt = st.dirty + (size_t)wb * N;
-        for (int j = lane_id(); j < S2 * S2; j += kWave) {
-            const int dy = j % S2 - H, dz = j / S2 - H;
-            const RowDesc r = row_desc(wbm, wwr, g, wx, wy + dy, wz + dz, H);
-            const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
+        if constexpr (LIST) {
+            const uint32_t* lst = nbr + (size_t)__shfl(gid, wl, kWave) * kNbr32Stride;
+            const uint32_t n_r = lst[0], n2 = lst[1];
+            for (uint32_t j = (uint32_t)lane_id(); j < n2; j += kWave) {
+                const uint32_t sl = lst[4 + j];
+                dt[sl] = cur;
+                if (j < n_r) cv[sl] = cv[sl] + 1u;
+            }
+        } else {
+            const int32_t wx = __shfl(x, wl, kWave), wy = __shfl(y, wl, kWave), wz = __shfl(z, wl, kWave);
+            const uint64_t* wbm = bitmap + (size_t)wb * W;
+            const uint32_t* wwr = word_rank + (size_t)wb * W;
+            for (int j = lane_id(); j < S2 * S2; j += kWave) {
+                const int dy = j % S2 - H, dz = j / S2 - H;
+                const RowDesc r = row_desc(wbm, wwr, g, wx, wy + dy, wz + dz, H);
+                const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
 #pragma unroll
-            for (int q = 0; q < S2; ++q) {
-                if ((r.mask >> q) & 1u) {
-                    const uint32_t sl = row_slot(r, q);
-                    dt[sl] = cur;
-                    if (inner && q - H >= -RAD && q - H <= RAD) cv[sl] = cv[sl] + 1u;
+                for (int q = 0; q < S2; ++q) {
+                    if ((r.mask >> q) & 1u) {
+                        const uint32_t sl = row_slot(r, q);
+                        dt[sl] = cur;
+                        if (inner && q - H >= -RAD && q - H <= RAD) cv[sl] = cv[sl] + 1u;
+                    }
                 }
             }
         }
@@ -702,18 +756,27 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     const uint64_t* bitmap = at<uint64_t>(ws, L.bitmap);
     const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
     int64_t R = 0;
+    // neighbour lists replace the row scans where the layout holds them
+    const bool lists = L.has_nbr32 && rad == 1;
+    if (lists && (e = launch_cas_nbr(L, d, ws, s)) != hipSuccess) return e;
+    const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
     auto launch_batch = [&](int rounds) {
         for (int i = 0; i < rounds; ++i, ++R) {
-            if (rad == 1) {
-                k_cas_score<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
-                                                  bitmap, word_rank, st, ctl);
-                k_cas_pick<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap, word_rank,
-                                                 st, ctl);
+            if (lists) {
+                k_cas_score<1, true><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
+                                                        bitmap, word_rank, nbr, st, ctl);
+                k_cas_pick<1, true><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
+                                                       word_rank, nbr, st, ctl);
+            } else if (rad == 1) {
+                k_cas_score<1, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
+                                                         vox_lin, bitmap, word_rank, nullptr, st, ctl);
+                k_cas_pick<1, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
+                                                        word_rank, nullptr, st, ctl);
             } else {
-                k_cas_score<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
-                                                  bitmap, word_rank, st, ctl);
-                k_cas_pick<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap, word_rank,
-                                                 st, ctl);
+                k_cas_score<2, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
+                                                         vox_lin, bitmap, word_rank, nullptr, st, ctl);
+                k_cas_pick<2, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
+                                                        word_rank, nullptr, st, ctl);
             }
         }
         return hipGetLastError();
