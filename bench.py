@@ -17,8 +17,11 @@ duration on the launch stream) and the CPU oracle timed on a bounded sample.
 from __future__ import annotations
 
 import argparse
+import csv
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -29,6 +32,10 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+COPY_PROBE_BYTES = 1 << 30  # the calibration copy reads and writes this many bytes
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_query_bigroom_b4_traffic.md")
+QUERY_SOURCES = ("paper_1912_02984_amd/csrc/cagq_query.hip", "paper_1912_02984_amd/csrc/cagq_internal.h")
+QUERY_NAMES = {"0": "k_query<cube>", "1": "k_query<knn>"}
 WORKLOAD = "bigroom"
 VARIANTS = ("bigroom/cas-knn", "bigroom/rvs-cube")
 METRIC = "CAGQ points/sec & ms/batch at 81920 pts; achieved HBM GB/s vs MI355X peak"
@@ -42,6 +49,77 @@ def query_alg_bytes(M_total: int, K: int, ctx_total: int) -> int:
     return M_total * (16 * K + 28) + 16 * ctx_total
 
 
+def query_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in QUERY_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic() -> dict:
+    """Per-launch HBM bytes of the layer-1 query kernels from the committed
+    counter summary; empty unless it was taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            txt = f.read()
+    except OSError:
+        return {}
+    m = re.search(r"kernel source sha256\[:16\]: `([0-9a-f]+)`", txt)
+    if not m or m.group(1) != query_source_hash():
+        return {}
+    return {k: int(v) for k, v in re.findall(r"^\| `(k_query<\w+>)` \|(?:[^|]*\|){3} (\d+) \|", txt, re.M)}
+
+
+def _short(name: str) -> str:
+    m = re.search(r"(k_\w+)<(\d)(?:, \d+)?>", name)
+    if m and m.group(1) == "k_query":
+        return QUERY_NAMES[m.group(2)]
+    m = re.search(r"(k_\w+(?:<[^>(]*>)?)\(", name)
+    return m.group(1) if m else name[:40]
+
+
+def summarize_stats(stats_csv: str, command: str) -> str:
+    """Markdown table of a rocprofv3 --stats kernel summary."""
+    rows = list(csv.DictReader(open(stats_csv)))
+    out = ["| Kernel | Calls | Total (us) | Avg (us) | Min (us) | Max (us) | % |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e3:.1f} | "
+                   f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
+                   f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    return "\n".join([f"Command: `{command}`", ""] + out) + "\n"
+
+
+def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
+    """HBM bytes per launch of the layer-1 query kernels from a FETCH_SIZE
+    and a WRITE_SIZE pass, each scaled by what the same counter reads for
+    the calibration copy (COPY_PROBE_BYTES read and written)."""
+    def load(path, counter):
+        return [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+    fr, wr = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+
+    def copy_kib(rows):  # the largest torch kernel of the run is the calibration copy
+        return max(float(r["Counter_Value"]) for r in rows if "at::native" in r["Kernel_Name"])
+    cf, cw = copy_kib(fr), copy_kib(wr)
+    sf, sw = COPY_PROBE_BYTES / (cf * 1024), COPY_PROBE_BYTES / (cw * 1024)
+
+    def layer1(rows, mode):
+        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+>", r["Kernel_Name"])]
+        g = max(int(r["Grid_Size"]) for r in q)
+        return [float(r["Counter_Value"]) for r in q if int(r["Grid_Size"]) == g]
+    lines = [f"Calibration: a {COPY_PROBE_BYTES >> 20} MiB fp32 copy kernel reads FETCH_SIZE {cf:.0f} KiB "
+             f"(scale {sf:.4f}) and WRITE_SIZE {cw:.0f} KiB (scale {sw:.4f}).", "",
+             "| Kernel | Dispatches | FETCH_SIZE (KiB) | WRITE_SIZE (KiB) | HBM bytes per launch |",
+             "|---|---|---|---|---|"]
+    for mode, name in QUERY_NAMES.items():
+        f, w = layer1(fr, mode), layer1(wr, mode)
+        fk, wk = float(np.mean(f)), float(np.mean(w))
+        lines.append(f"| `{name}` | {len(f)} | {fk:.1f} | {wk:.1f} | {int(round(fk * 1024 * sf + wk * 1024 * sw))} |")
+    lines += ["", f"kernel source sha256[:16]: `{query_source_hash()}` "
+                  f"({' + '.join(QUERY_SOURCES)})"]
+    return "\n".join(lines) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -52,7 +130,19 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time to accumulate for the CPU baseline")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="run one fp32 copy kernel of known size first (counter calibration)")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "COMMAND"),
+                    help="print a markdown table of a rocprofv3 kernel summary and exit")
+    ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="print the query kernels' HBM bytes from two counter passes and exit")
     args = ap.parse_args()
+    if args.summarize_stats:
+        print(summarize_stats(*args.summarize_stats), end="")
+        return
+    if args.summarize_traffic:
+        print(summarize_traffic(*args.summarize_traffic), end="")
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               "(the CAGQ path here is single-GPU; see the sharding notes in the design document)",
@@ -123,6 +213,13 @@ def main():
         for st in streams:
             main.wait_stream(st)
 
+    if args.copy_probe:
+        src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -166,8 +263,9 @@ def main():
         roof[w.name] = dict(kernel=f"k_query<{L.query}>", us=t_ms * 1e3, alg_bytes=alg, achieved_gbs=gbs,
                             ctx_total=ctx_total)
     dom = max(roof.values(), key=lambda r: r["us"])
+    traffic = load_traffic().get(dom["kernel"])
     roofline = {"bound": "hbm", "achieved": round(dom["achieved_gbs"], 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(dom["achieved_gbs"] / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(dom["achieved_gbs"] / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": dom["kernel"], "launch_us": round(dom["us"], 2), "alg_bytes": dom["alg_bytes"],
                 "per_variant": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                                 for k, v in roof.items()}}
@@ -184,7 +282,7 @@ def main():
                     _, _, _, q = oracle.run_layer(pts, L, weights=wts)
                     pts, wts = q["center_xyz"], q["center_w"]
             done += 1
-            if time.perf_counter() - t0 >= args.cpu_seconds or done >= 8:
+            if time.perf_counter() - t0 >= args.cpu_seconds or done >= 32:
                 break
         dt = time.perf_counter() - t0
         cpu = {"value": round(done * N / dt, 1), "unit": "points/s", "cores": 1, "kind": "oracle",
