@@ -26,10 +26,30 @@ namespace {
 
 constexpr int kQueryThreads = 256;
 
+// Division by a divisor d that is the same for the whole launch, for
+// dividends below 2^31: floor(n / d) = (n * m) >> (31 + l) with
+// l = ceil(log2 d) and m = ceil(2^(31+l) / d) < 2^32 (Granlund and
+// Montgomery, "Division by invariant integers using multiplication", 1994).
+struct Magic {
+    uint32_t m, sh;
+};
+
+Magic make_magic(uint32_t d) {
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    const uint64_t p = 1ull << (31 + l);
+    return Magic{(uint32_t)((p + d - 1) / d), 31 + l};
+}
+
+__device__ __forceinline__ uint32_t udiv(uint32_t n, const Magic& g) {
+    return (uint32_t)(((uint64_t)n * g.m) >> g.sh);
+}
+
 struct QGrid {
     float o[3];
     float s[3];
     int32_t D[3];
+    Magic d0, d01, mm;  // division by D_x, by D_x * D_y and by M
 };
 
 __device__ __forceinline__ void wave_lds_sync() {
@@ -38,17 +58,48 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Value of lane `lane ^ j` (j a power of two below 64, known at compile time
+// once unrolled): DPP moves within rows of 16 lanes for j <= 8 (quad
+// permutes for 1 and 2, both row shifts for 4, a row rotate for 8), a
+// swizzle for 16 and a permute for 32. None of them touches LDS memory.
+__device__ __forceinline__ uint32_t xlane(uint32_t v, int j) {
+    switch (j) {
+        case 1: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true);  // quad_perm 1,0,3,2
+        case 2: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true);  // quad_perm 2,3,0,1
+        case 4: {
+            const uint32_t up = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x104, 0xF, 0xF, true);  // row_shl:4
+            const uint32_t dn = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+            return (threadIdx.x & 4) ? dn : up;
+        }
+        case 8: return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, true);  // row_ror:8
+        case 16: return (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F);  // xor 16 within 32 lanes
+        default: return (uint32_t)__shfl_xor((int)v, j, kWave);
+    }
+}
+
+__device__ __forceinline__ float xlanef(float v, int j) { return __uint_as_float(xlane(__float_as_uint(v), j)); }
+
+__device__ __forceinline__ uint64_t xlane64(uint64_t v, int j) {
+    return ((uint64_t)xlane((uint32_t)(v >> 32), j) << 32) | xlane((uint32_t)v, j);
+}
+
+// Value of lane `first` (0 or G-1) of this lane's group of G, by lane reads.
+template <int G>
+__device__ __forceinline__ uint32_t gbcast(uint32_t v, int first) {
+    const int lane = lane_id();
+    uint32_t r = 0;
+#pragma unroll
+    for (int g0 = 0; g0 < kWave; g0 += G) {
+        const uint32_t x = (uint32_t)__builtin_amdgcn_readlane((int)v, g0 + first);
+        r = (lane >= g0 && lane < g0 + G) ? x : r;
+    }
+    return r;
+}
+
 template <int G>
 __device__ __forceinline__ uint64_t gshfl64(uint64_t v, int src) {
     int lo = __shfl((int)(uint32_t)v, src, G);
     int hi = __shfl((int)(uint32_t)(v >> 32), src, G);
-    return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-
-template <int G>
-__device__ __forceinline__ uint64_t gxor64(uint64_t v, int m) {
-    int lo = __shfl_xor((int)(uint32_t)v, m, G);
-    int hi = __shfl_xor((int)(uint32_t)(v >> 32), m, G);
     return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
@@ -65,33 +116,37 @@ __device__ __forceinline__ uint32_t gscan_incl(uint32_t v, int lg) {
 template <int G>
 __device__ __forceinline__ uint32_t gsum(uint32_t v) {
 #pragma unroll
-    for (int d = 1; d < G; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, G);
+    for (int d = 1; d < G; d <<= 1) v += xlane(v, d);
     return v;
 }
 
 // Compare-exchange of (key, payload) with the partner lane lg ^ j: this lane
 // keeps the smaller key when keep_min, else the larger.
-template <int G>
 __device__ __forceinline__ void gcx(uint64_t& k, uint32_t& p, int j, bool keep_min) {
-    const uint64_t ok = gxor64<G>(k, j);
-    const uint32_t op = (uint32_t)__shfl_xor((int)p, j, G);
-    const bool take = keep_min ? (ok < k) : (ok > k);
+    const uint64_t ok = xlane64(k, j);
+    const uint32_t op = xlane(p, j);
+    // keys are distinct but for the ~0 fillers, which may trade places freely
+    const bool take = (ok < k) == keep_min;
     if (take) {
         k = ok;
         p = op;
     }
 }
 
-// Ascending bitonic sort of one (key, payload) per lane across the group.
+// Ascending bitonic sort of one (key, payload) per lane across the group,
+// given that only lanes below `top` (a power of two, the same for the whole
+// wave) hold keys other than ~0: the merge levels above `top` change nothing
+// and are skipped.
 template <int G>
-__device__ __forceinline__ void gsort(uint64_t& k, uint32_t& p, int lg) {
+__device__ __forceinline__ void gsort(uint64_t& k, uint32_t& p, int lg, uint32_t top) {
 #pragma unroll
     for (int s = 2; s <= G; s <<= 1) {
+        if ((uint32_t)s > top && s > 2) break;
 #pragma unroll
         for (int j = s >> 1; j > 0; j >>= 1) {
             const bool asc = (lg & s) == 0;
             const bool low = (lg & j) == 0;
-            gcx<G>(k, p, j, asc == low);
+            gcx(k, p, j, asc == low);
         }
     }
 }
@@ -107,12 +162,12 @@ __device__ __forceinline__ void gmerge_low(uint64_t& bk, uint32_t& bp, uint64_t 
         bp = rp;
     }
 #pragma unroll
-    for (int j = G >> 1; j > 0; j >>= 1) gcx<G>(bk, bp, j, (lg & j) == 0);
+    for (int j = G >> 1; j > 0; j >>= 1) gcx(bk, bp, j, (lg & j) == 0);
 }
 
-template <int MODE, int G>
+template <int MODE, int G, int RAD>
 __global__ __launch_bounds__(kQueryThreads) void k_query(
-    const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g, int32_t rad,
+    const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
     int64_t W, const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
     const uint32_t* __restrict__ vox_off, const float4* __restrict__ pt4, const int32_t* __restrict__ center_lin,
     uint64_t seed, int32_t* __restrict__ node_idx, float* __restrict__ node_xyz, int32_t* __restrict__ n_valid,
@@ -120,8 +175,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     int* __restrict__ status) {
     extern __shared__ uint32_t smem[];
     constexpr int GPB = kQueryThreads / G;  // groups per block
-    const int side = 2 * rad + 1;
-    const int nnb = side * side * side;
+    constexpr int rad = RAD, side = 2 * RAD + 1, nnb = side * side * side;
     const int lane = lane_id();
     const int lg = lane & (G - 1);
     const int gb = threadIdx.x / G;  // group within the block
@@ -133,7 +187,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     // lanes); a group past the end works on center 0 and writes nothing
     const bool live = cid < total;
     const int32_t c_id = live ? cid : 0;
-    const int32_t b = c_id / M;
+    const int32_t b = (int32_t)udiv((uint32_t)c_id, g.mm);
     const size_t cK = (size_t)c_id * K;
     const int32_t lin_s = center_lin[c_id];
     const int64_t V = (int64_t)g.D[0] * g.D[1] * g.D[2];
@@ -141,23 +195,25 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     const uint32_t* wr = word_rank + (size_t)b * W;
     const uint32_t* vo = vox_off + (size_t)b * (N + 1);
     const float4* p4 = pt4 + (size_t)b * N;
-    // an unoccupied center has an empty context and gets zeros
-    const bool occupied = lin_s >= 0 && (int64_t)lin_s < V && slot_of(bm, wr, (uint32_t)lin_s) >= 0;
-    if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
-    const uint32_t lin = occupied ? (uint32_t)lin_s : 0u;
-    const int32_t gx = (int32_t)(lin % (uint32_t)g.D[0]);
-    const int32_t gy = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
-    const int32_t gz = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
+    const bool in_grid = lin_s >= 0 && (int64_t)lin_s < V;
+    const uint32_t lin = in_grid ? (uint32_t)lin_s : 0u;
+    const uint32_t zq = udiv(lin, g.d01);
+    const uint32_t rem = lin - zq * (uint32_t)g.D[0] * (uint32_t)g.D[1];
+    const uint32_t yq = udiv(rem, g.d0);
+    const int32_t gx = (int32_t)(rem - yq * (uint32_t)g.D[0]), gy = (int32_t)yq, gz = (int32_t)zq;
 
-    // 1. occupied voxels of pi(v), compacted in ascending linear id
+    // 1. occupied voxels of pi(v), compacted in ascending linear id; the
+    // center voxel is one of them (q = nnb / 2), so its own check costs
+    // nothing extra
     uint32_t nocc = 0, c = 0;
+    bool occupied = false;
     const int gshift = lane & ~(G - 1);
     const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
     for (int q0 = 0; q0 < nnb; q0 += G) {
         const int q = q0 + lg;
         bool occ = false;
         uint32_t st = 0, cnt = 0;
-        if (occupied && q < nnb) {
+        if (in_grid && q < nnb) {
             const int32_t x = gx + q % side - rad;
             const int32_t y = gy + (q / side) % side - rad;
             const int32_t z = gz + q / (side * side) - rad;
@@ -172,14 +228,21 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             }
         }
         const uint64_t mask = (__ballot(occ) >> gshift) & gmask;
+        if (nnb / 2 >= q0 && nnb / 2 < q0 + G) occupied = (mask >> (nnb / 2 - q0)) & 1ull;
         const uint32_t pos = nocc + (uint32_t)__popcll(mask & ((1ull << lg) - 1));
         const uint32_t incl = gscan_incl<G>(cnt, lg);
         if (occ) {
             s_st[pos] = st;
             s_pre[pos] = c + incl - cnt;
         }
-        c += (uint32_t)__shfl((int)incl, G - 1, G);
+        c += gbcast<G>(incl, G - 1);
         nocc += (uint32_t)__popcll(mask);
+    }
+    // an unoccupied center has an empty context and gets zeros
+    if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
+    if (!occupied) {
+        nocc = 0;
+        c = 0;
     }
     if (lg == 0) s_pre[nocc] = c;
     wave_lds_sync();
@@ -200,9 +263,18 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     uint32_t cmax = c;
 #pragma unroll
     for (int d = G; d < kWave; d <<= 1) {
-        const uint32_t o = (uint32_t)__shfl_xor((int)cmax, d, kWave);
+        const uint32_t o = xlane(cmax, d);
         cmax = o > cmax ? o : cmax;
     }
+    // a context of at most G points is one chunk: its points and weights stay
+    // in the lanes that loaded them, and the sort carries the lane (entry)
+    // instead of the position in the copy
+    const bool one = c <= (uint32_t)G;
+    // the sort levels that matter: up to the smallest power of two >= cmax
+    uint32_t top = 2;
+    while (top < cmax && top < (uint32_t)G) top <<= 1;
+    float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f);
+    uint32_t w0 = 1u;
     for (uint32_t e0 = 0; e0 < cmax; e0 += G) {
         const uint32_t e = e0 + lg;
         uint64_t key = ~0ull;
@@ -217,6 +289,11 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             pos = s_st[lo] + (e - s_pre[lo]);
             const float4 v = p4[pos];
             const uint32_t i = __float_as_uint(v.w);
+            if (one) {
+                v0 = v;
+                if (Wt) w0 = Wt[(size_t)b * N + i];
+                pos = e;
+            }
             if (MODE == CAGQ_QUERY_CUBE) {
                 key = (sm64(hc ^ (uint64_t)i) & 0xFFFFFFFF00000000ull) | i;
             } else {
@@ -227,7 +304,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
                 key = ((uint64_t)__float_as_uint(d2) << 32) | i;
             }
         }
-        gsort<G>(key, pos, lg);
+        gsort<G>(key, pos, lg, top);
         if (e0 == 0) {
             bk = key;
             bp = pos;
@@ -238,12 +315,28 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
 
     // 4. outputs (an empty context gives n = 0 and zeros)
     const uint32_t n = c < (uint32_t)K ? c : (uint32_t)K;
-    const int src = (uint32_t)lg < n ? lg : 0;
-    const uint64_t mine = gshfl64<G>(bk, src);
-    const uint32_t mpos = (uint32_t)__shfl((int)bp, src, G);
+    // slots k >= n repeat slot 0
+    const bool own = (uint32_t)lg < n;
+    const uint64_t k0 = ((uint64_t)gbcast<G>((uint32_t)(bk >> 32), 0) << 32) | gbcast<G>((uint32_t)bk, 0);
+    const uint64_t mine = own ? bk : k0;
+    const uint32_t mpos = own ? bp : gbcast<G>(bp, 0);
     const uint32_t idx = n ? (uint32_t)mine : 0u;
-    const float4 pv = n ? p4[mpos] : make_float4(0.f, 0.f, 0.f, 0.f);
-    const float x = pv.x, y = pv.y, z = pv.z;
+    // a one-chunk context reads node point and weight from the lane holding
+    // them; a longer one reads them again
+    const int from = one ? (int)mpos : 0;
+    float x = __shfl(v0.x, from, G), y = __shfl(v0.y, from, G), z = __shfl(v0.z, from, G);
+    uint32_t w = (uint32_t)__shfl((int)w0, from, G);
+    if (!one) {
+        const float4 pv = p4[mpos];
+        x = pv.x;
+        y = pv.y;
+        z = pv.z;
+        w = Wt ? Wt[(size_t)b * N + idx] : 1u;
+    }
+    if (!n) {
+        x = y = z = 0.0f;
+        w = 1u;
+    }
     if (live && lg < K) {
         node_idx[cK + lg] = (int32_t)idx;
         if (node_xyz) {
@@ -253,15 +346,15 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         }
     }
     const bool valid = (uint32_t)lg < n;
-    const uint32_t w = (Wt && n) ? Wt[(size_t)b * N + idx] : 1u;
     const uint32_t wc = gsum<G>(valid ? w : 0u);
     const float wf = (float)w;
     float tx = wf * x, ty = wf * y, tz = wf * z;
 #pragma unroll
     for (int h = 1; h < G; h <<= 1) {
-        const float ox = __shfl_down(tx, h, G);
-        const float oy = __shfl_down(ty, h, G);
-        const float oz = __shfl_down(tz, h, G);
+        // the lanes that add (multiples of 2h) read lane + h = lane ^ h
+        const float ox = xlanef(tx, h);
+        const float oy = xlanef(ty, h);
+        const float oz = xlanef(tz, h);
         if ((lg & (2 * h - 1)) == 0 && (uint32_t)(lg + h) < n) {
             tx = tx + ox;
             ty = ty + oy;
@@ -279,19 +372,34 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     }
 }
 
-template <int MODE, int G>
-void launch_g(const Layout& L, const QGrid& g, int32_t rad, void* ws, const uint32_t* weights,
+template <int MODE, int G, int RAD>
+void launch_g(const Layout& L, const QGrid& g, void* ws, const uint32_t* weights,
               const int32_t* center_lin, int32_t M, int32_t K, uint64_t seed, int32_t* node_idx, float* node_xyz,
               int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count, hipStream_t s) {
     constexpr int GPB = kQueryThreads / G;
     const int32_t total = L.B * M;
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
-    const int side = 2 * rad + 1;
+    constexpr int side = 2 * RAD + 1;
     const size_t lds = (size_t)GPB * (2 * side * side * side + 1) * sizeof(uint32_t);
-    k_query<MODE, G><<<blocks, kQueryThreads, lds, s>>>(
-        weights, L.N, M, K, total, g, rad, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
+    k_query<MODE, G, RAD><<<blocks, kQueryThreads, lds, s>>>(
+        weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), center_lin, seed, node_idx, node_xyz, n_valid,
         center_xyz, center_w, ctx_count, at<int>(ws, L.status));
+}
+
+template <int MODE, int G>
+void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const uint32_t* weights,
+              const int32_t* center_lin, int32_t M, int32_t K, uint64_t seed, int32_t* node_idx, float* node_xyz,
+              int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count, hipStream_t s) {
+    if (rad == 1)
+        launch_g<MODE, G, 1>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
+                             center_w, ctx_count, s);
+    else if (rad == 2)
+        launch_g<MODE, G, 2>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
+                             center_w, ctx_count, s);
+    else
+        launch_g<MODE, G, 3>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
+                             center_w, ctx_count, s);
 }
 
 template <int MODE>
@@ -300,13 +408,13 @@ void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const u
                  float* node_xyz, int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
                  hipStream_t s) {
     if (K <= 16)
-        launch_g<MODE, 16>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
+        launch_r<MODE, 16>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
                            center_xyz, center_w, ctx_count, s);
     else if (K <= 32)
-        launch_g<MODE, 32>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
+        launch_r<MODE, 32>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
                            center_xyz, center_w, ctx_count, s);
     else
-        launch_g<MODE, 64>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
+        launch_r<MODE, 64>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
                            center_xyz, center_w, ctx_count, s);
 }
 
@@ -324,6 +432,9 @@ hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* p
         g.s[a] = d.voxel_size[a];
         g.D[a] = d.dims[a];
     }
+    g.d0 = make_magic((uint32_t)d.dims[0]);
+    g.d01 = make_magic((uint32_t)d.dims[0] * (uint32_t)d.dims[1]);
+    g.mm = make_magic((uint32_t)M);
     if (mode == CAGQ_QUERY_CUBE)
         launch_mode<CAGQ_QUERY_CUBE>(L, g, d.radius, ws, weights, center_lin, M, K, seed, node_idx, node_xyz,
                                      n_valid, center_xyz, center_w, ctx_count, s);
