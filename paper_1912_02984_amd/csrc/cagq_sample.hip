@@ -32,6 +32,8 @@ struct CasPtrs {
     uint32_t* cpart;  // [2][B][kCasParts] partial counts of picks above that maximum
     uint32_t* done;   // [B]
     uint32_t* ndone;  // clouds done
+    uint32_t* host;       // pinned host words (or null): [0] = 1 once every cloud is done,
+                          // [1] = the round being scored (all earlier rounds have finished)
 };
 
 CasPtrs cas_ptrs(const Layout& L, void* ws) {
@@ -42,6 +44,7 @@ CasPtrs cas_ptrs(const Layout& L, void* ws) {
     c.cpart = reinterpret_cast<uint32_t*>(base + parts * 8);
     c.done = reinterpret_cast<uint32_t*>(base + parts * 12);
     c.ndone = c.done + L.B;
+    c.host = nullptr;
     return c;
 }
 
@@ -462,12 +465,16 @@ __global__ __launch_bounds__(256) void k_cas_score(
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
     bool active = in_range && ctl.done[b] == 0;
+    if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
+        __hip_atomic_store(ctl.host + 1, (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int32_t nv = nvox[b];
     const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) & 1) * B * kCasParts, b) : 0u;
     if (active && R > 0 && prev >= (uint32_t)(M < nv ? M : nv)) {
         if (s == 0) {
             ctl.done[b] = 1;
-            atomicAdd(ctl.ndone, 1u);
+            // the last cloud to finish tells the host, without a copy on the stream
+            if (atomicAdd(ctl.ndone, 1u) + 1 == (uint32_t)B && ctl.host)
+                __hip_atomic_store(ctl.host, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
         active = false;
     }
@@ -801,35 +808,33 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
         *status_out = CAGQ_ERR_CAPACITY;
         return hipSuccess;
     }
-    // two batches in flight: the host reads batch k's count while batch k+1 runs
-    hipEvent_t ev[2];
-    if ((e = hipEventCreateWithFlags(&ev[0], hipEventDisableTiming)) != hipSuccess) return e;
-    if ((e = hipEventCreateWithFlags(&ev[1], hipEventDisableTiming)) != hipSuccess) {
-        (void)hipEventDestroy(ev[0]);
-        return e;
-    }
-    auto issue = [&](int slot, int rounds) {
-        hipError_t r = launch_batch(rounds);
-        if (r == hipSuccess)
-            r = hipMemcpyAsync(&poll[slot], ctl.ndone, sizeof(uint32_t), hipMemcpyDeviceToHost, s);
-        if (r == hipSuccess) r = hipEventRecord(ev[slot], s);
-        return r;
-    };
-    e = issue(0, first_batch);
-    if (e == hipSuccess) e = issue(1, batch);
-    for (int k = 0; e == hipSuccess; ++k) {
-        const int slot = k & 1;
-        if ((e = hipEventSynchronize(ev[slot])) != hipSuccess) break;
-        if (poll[slot] == (uint32_t)B) break;
-        if (R > max_rounds + 2 * batch) {
-            *status_out = CAGQ_ERR_CAPACITY;
-            break;
+    const int ahead = 3;
+    // The scoring kernel publishes its round and, once every cloud is done,
+    // a done flag in pinned host memory. The host keeps at least `ahead`
+    // rounds queued until it sees the flag: no copies and no events on the
+    // stream, so the GPU does not idle between rounds.
+    void* dev_words = nullptr;
+    if ((e = hipHostGetDevicePointer(&dev_words, poll, 0)) != hipSuccess) return e;
+    volatile uint32_t* words = poll;
+    words[0] = 0;
+    words[1] = 0;
+    ctl.host = static_cast<uint32_t*>(dev_words);
+    if ((e = launch_batch(first_batch)) != hipSuccess) return e;
+    for (uint64_t spins = 1;; ++spins) {
+        if (words[0] == 1u) return hipSuccess;
+        if ((int64_t)words[1] + ahead >= R) {  // fewer than `ahead` rounds still queued
+            if (R > max_rounds + 2 * batch) {
+                *status_out = CAGQ_ERR_CAPACITY;
+                return hipSuccess;
+            }
+            if ((e = launch_batch(batch)) != hipSuccess) return e;
+            continue;
         }
-        e = issue(slot, batch);
+        if (spins % 1024 == 0) {  // a failed stream ends the wait
+            const hipError_t q = hipStreamQuery(s);
+            if (q != hipSuccess && q != hipErrorNotReady) return q;
+        }
     }
-    (void)hipEventDestroy(ev[0]);
-    (void)hipEventDestroy(ev[1]);
-    return e;
 }
 
 }  // namespace cagq
