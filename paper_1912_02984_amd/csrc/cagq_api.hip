@@ -50,8 +50,9 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->status = take(4 * kStSlots);
     L->desc_w = take(8 * (size_t)B * L->tiles_w);
     L->desc_s = take(8 * (size_t)B * L->tiles_s);
-    L->bitmap = take(8 * (size_t)B * L->W);
+    L->bytemap = take(64 * (size_t)B * L->W);
     L->clear_end = off;
+    L->bitmap = take(8 * (size_t)B * L->W);
     L->word_rank = take(4 * (size_t)B * L->W);
     L->pt_slot = take(4 * BN);
     L->pt_pos = take(4 * BN);

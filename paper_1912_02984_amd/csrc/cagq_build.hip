@@ -5,8 +5,9 @@
 // Design (gfx950): the set O_v of non-empty voxels is an occupancy bitmap
 // with one bit per grid voxel; a voxel's slot is its rank (popcount of the
 // bits before it), which is a minimal, order-preserving hash of the linear
-// voxel id to a compact slot. Ranks come from a single-pass decoupled
-// look-back scan over the bitmap words, counts from one atomic per point,
+// voxel id to a compact slot. Points mark a byte per voxel with plain stores
+// (no atomics); a single-pass decoupled look-back scan packs the bytes into
+// bitmap words and ranks them; counts come from one atomic per point,
 // offsets from a second look-back scan over the slots. Per-voxel lists hold
 // the n_v lowest point indices in ascending order, independent of the
 // arrival order the atomics produce: small voxels rank each point against
@@ -52,10 +53,10 @@ __global__ void k_clear(uint4* __restrict__ p, size_t n16) {
         p[i] = make_uint4(0u, 0u, 0u, 0u);
 }
 
-// One lane per point: linear voxel id, occupancy bit.
+// One lane per point: linear voxel id, occupancy byte.
 __global__ __launch_bounds__(256) void k_mark(const float* __restrict__ P, int32_t N, int32_t BN,
                                               GridArgs g, int64_t W, uint32_t* __restrict__ pt_lin,
-                                              uint64_t* __restrict__ bitmap, int* __restrict__ status) {
+                                              uint8_t* __restrict__ bytemap, int* __restrict__ status) {
     int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (gid >= BN) return;
     int32_t b = gid / N;
@@ -74,16 +75,31 @@ __global__ __launch_bounds__(256) void k_mark(const float* __restrict__ P, int32
     }
     uint32_t lin = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
     pt_lin[gid] = lin;
-    uint64_t* word = bitmap + (size_t)b * W + (lin >> 6);
-    uint64_t bit = 1ull << (lin & 63);
-    if (!(*word & bit)) atomicOr((unsigned long long*)word, (unsigned long long)bit);
+    // every point of a voxel stores the same byte: no atomic is needed
+    bytemap[(size_t)b * W * 64 + lin] = 1;
     if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
 }
 
-// Ranks of the occupancy words: word_rank[w] = occupied voxels before word w.
-// Also lists every occupied voxel's linear id at its slot and clears its count.
+// 64 occupancy bytes (each 0 or 1) to one occupancy word: byte j -> bit j.
+// Multiplying 4 such bytes by 0x01020408 moves byte k to bit 24 + k with no
+// other term reaching bits 24..31.
+__device__ __forceinline__ uint64_t pack_bytes(const uint4* __restrict__ p) {
+    uint64_t r = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const uint4 v = p[q];
+        const uint32_t a[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+        for (int k = 0; k < 4; ++k) r |= (uint64_t)((a[k] * 0x01020408u) >> 24) << (16 * q + 4 * k);
+    }
+    return r;
+}
+
+// Occupancy words from the bytes, and their ranks: word_rank[w] = occupied
+// voxels before word w. Also lists every occupied voxel's linear id at its
+// slot and clears its count.
 __global__ __launch_bounds__(kScanThreads) void k_rank(
-    const uint64_t* __restrict__ bitmap, int64_t W, int64_t tiles_w, int32_t N,
+    const uint8_t* __restrict__ bytemap, uint64_t* __restrict__ bitmap, int64_t W, int64_t tiles_w, int32_t N,
     uint32_t* __restrict__ word_rank, uint32_t* __restrict__ vox_lin, uint32_t* __restrict__ vox_count,
     int32_t* __restrict__ nvox, uint64_t* __restrict__ desc_w, int* __restrict__ status) {
     __shared__ uint32_t s_ticket;
@@ -94,14 +110,16 @@ __global__ __launch_bounds__(kScanThreads) void k_rank(
     const uint32_t t = s_ticket;
     const int32_t b = (int32_t)(t / tiles_w);
     const int64_t tile = (int64_t)(t % tiles_w);
-    const uint64_t* bm = bitmap + (size_t)b * W;
+    const uint4* bytes = reinterpret_cast<const uint4*>(bytemap + (size_t)b * W * 64);
+    uint64_t* bm = bitmap + (size_t)b * W;
     const int64_t w0 = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
     uint64_t words[kScanItems];
     uint32_t cnt = 0;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         int64_t w = w0 + i;
-        words[i] = w < W ? bm[w] : 0ull;
+        words[i] = w < W ? pack_bytes(bytes + (size_t)w * 4) : 0ull;
+        if (w < W) bm[w] = words[i];
         cnt += (uint32_t)__popcll(words[i]);
     }
     uint64_t total;
@@ -280,10 +298,10 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
     if (cb > 4096) cb = 4096;
     k_clear<<<cb, 256, 0, s>>>(at<uint4>(ws, L.status), n16);
     const int pb = (BN + 255) / 256;
-    k_mark<<<pb, 256, 0, s>>>(points, N, BN, g, L.W, at<uint32_t>(ws, L.pt_slot), at<uint64_t>(ws, L.bitmap),
+    k_mark<<<pb, 256, 0, s>>>(points, N, BN, g, L.W, at<uint32_t>(ws, L.pt_slot), at<uint8_t>(ws, L.bytemap),
                               status);
     k_rank<<<(unsigned)(B * L.tiles_w), kScanThreads, 0, s>>>(
-        at<uint64_t>(ws, L.bitmap), L.W, L.tiles_w, N, at<uint32_t>(ws, L.word_rank),
+        at<uint8_t>(ws, L.bytemap), at<uint64_t>(ws, L.bitmap), L.W, L.tiles_w, N, at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_lin), at<uint32_t>(ws, L.vox_count), at<int32_t>(ws, L.nvox),
         at<uint64_t>(ws, L.desc_w), status);
     k_count<<<pb, 256, 0, s>>>(BN, N, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),

@@ -47,6 +47,7 @@ struct Layout {
     size_t status;        // int32[kStSlots]
     size_t desc_w;        // u64 [B][tiles_w] scan descriptors (occupancy ranks)
     size_t desc_s;        // u64 [B][tiles_s] scan descriptors (offsets)
+    size_t bytemap;       // u8  [B][64 W] one byte per voxel, 1 when a point lies in it
     size_t bitmap;        // u64 [B][W] occupancy bits, bit (lin & 63) of word lin >> 6
     size_t word_rank;     // u32 [B][W] occupied voxels before word w (the slot of its first bit)
     size_t pt_slot;       // u32 [B][N] per point: linear id, then slot
