@@ -18,7 +18,7 @@ constexpr int kScanThreads = 256;       // threads per scan tile
 constexpr int kScanItems = 4;           // items per thread in a scan tile
 constexpr int kScanTile = kScanThreads * kScanItems;
 constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
-constexpr int kSelPasses = 6;           // 11-bit digits of a 64-bit key (the last one 9 bits)
+constexpr int kSelPasses = 3;           // digits of a key's top 32 bits: 11, 11 and 10 bits
 constexpr int kSelBins = 2048;
 
 // Status word slots (int32 each) at the start of the workspace's control block.
@@ -66,7 +66,7 @@ struct Layout {
     size_t cas_nbr;       // u16 [B][N][nbr_stride(r)] CAS neighbour lists of small clouds (see below)
     size_t cas_nbr32;     // u32 [B][N][kNbr32Stride] CAS neighbour lists of larger clouds, r = 1
     bool has_nbr16, has_nbr32;
-    size_t sel_thr;       // u64 [B] selection threshold: keys <= it are chosen
+    size_t sel_thr;       // u64 [B] selection threshold, see sel_pack
     size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };

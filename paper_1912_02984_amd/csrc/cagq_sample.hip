@@ -3,9 +3,14 @@
 //
 // RVS: every occupied voxel is equally likely. Slot s of cloud b gets the
 // key (hi32(h(seed, 1, b, s)) << 32) | s with h the splitmix64 chain; the
-// m = min(M, |O_v|) smallest keys win. One workgroup per cloud finds the m-th
-// smallest key by an 8-bit radix select in LDS; a look-back compaction over
-// the slots then writes the winners in slot (= ascending linear id) order.
+// m = min(M, |O_v|) smallest keys win. The low half of every select key (the
+// slot, or the linear id for CAS) rises with the slot, so the m smallest
+// keys are those whose top half is below a bound T, plus the first `need`
+// slots whose top half equals T. A radix select over the top halves finds T
+// and `need` (one workgroup per cloud in LDS, or one histogram kernel per
+// digit for large clouds); a look-back compaction over the slots, counting
+// keys below T and keys equal to T, then writes the winners in slot (=
+// ascending linear id) order.
 //
 // CAS (Eqs. 1-2, greedy reading): the sequential greedy repeatedly picks the
 // unpicked voxel of largest score 2^16*lambda*#{V in pi(v): C_V = 0} -
@@ -57,11 +62,16 @@ __device__ __forceinline__ uint64_t select_key(int key_mode, uint64_t hb, int32_
     return ~pick[s];  // largest pick key first; unpicked voxels (0) last
 }
 
-// One workgroup per cloud: the m-th smallest key T of the cloud (m =
-// min(M, |O_v|)) by an 8-bit radix select; every key <= T is chosen. Keys are
-// distinct (their low half is the slot or the linear id), unpicked CAS voxels
-// aside, which are never among the m smallest. Also clears the scan state of
-// the compaction that follows.
+// Per-cloud selection result: top halves below `bound` (<= 2^32) are
+// chosen, and of those equal to `bound` the first `need` in slot order.
+__device__ __forceinline__ uint64_t sel_pack(uint64_t bound, uint32_t need) {
+    return ((uint64_t)need << 33) | bound;
+}
+
+// One workgroup per cloud: the bound and tie count of the m = min(M, |O_v|)
+// smallest keys by an 8-bit radix select over their top halves. Unpicked CAS
+// voxels (key ~0) are never among the m smallest and are not counted. Also
+// clears the scan state of the compaction that follows.
 __global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
     int32_t N, int64_t tiles_s, const int32_t* __restrict__ nvox, int32_t M, int key_mode, uint64_t seed,
     const uint64_t* __restrict__ cas_pick, uint64_t* __restrict__ thr, int32_t* __restrict__ m_valid,
@@ -79,10 +89,10 @@ __global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
     for (int64_t t = tid; t < tiles_s; t += kSelThreads) desc_s[(size_t)b * tiles_s + t] = 0;
     if (b == 0 && tid == 0) status[kStTicketSel] = 0;
 
-    uint64_t prefix = 0, mask = 0, T = 0;
+    uint64_t prefix = 0, mask = 0, bound = 0;
     uint32_t need = (uint32_t)m;
     bool exact = true;
-    for (int shift = 56; shift >= 0; shift -= 8) {
+    for (int shift = 56; shift >= 32; shift -= 8) {
         if (tid < 256) hist[tid] = 0;
         __syncthreads();
         for (int32_t s0 = 0; s0 < nv; s0 += kSelThreads * U) {
@@ -95,7 +105,7 @@ __global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int32_t s = s0 + u * kSelThreads + tid;
-                const bool act = s < nv && (k[u] & mask) == prefix;
+                const bool act = s < nv && (k[u] & mask) == prefix && (key_mode == 0 || k[u] != ~0ull);
                 const uint32_t d = (uint32_t)(k[u] >> shift) & 255u;
                 // one atomic for the wave when all its counted keys share a digit
                 const uint64_t am = __ballot(act);
@@ -138,22 +148,23 @@ __global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
         mask |= 255ull << shift;
         need -= below;
         if (cnt == need) {  // every key under this prefix is among the m smallest
-            T = prefix | ~mask;
+            bound = ((prefix | ~mask) >> 32) + 1;
+            need = 0;
             exact = false;
             break;
         }
     }
-    if (exact) T = prefix;
+    if (exact) bound = prefix >> 32;
     if (tid == 0) {
-        thr[b] = T;
+        thr[b] = sel_pack(bound, need);
         m_valid[b] = m;
     }
 }
 
 // Ordered compaction of the chosen slots: tile of kScanTile slots per block,
-// look-back scan for the output position. Slot s chosen at position p < m
-// writes its linear id to every j = p, p + m, p + 2m, ... < M (the cyclic
-// padding).
+// look-back scan over the packed pair (keys below the bound << 31 | keys at
+// the bound). Slot s chosen at position p < m writes its linear id to every
+// j = p, p + m, p + 2m, ... < M (the cyclic padding).
 __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     int32_t N, int64_t tiles_s, const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin,
     int32_t M, int key_mode, uint64_t seed, const uint64_t* __restrict__ cas_pick,
@@ -170,43 +181,52 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     const int32_t nv = nvox[b];
     if (tile * kScanTile >= nv) return;  // later tiles never wait on this one
     const int32_t m = M < nv ? M : nv;
-    const uint64_t T = thr[b];
+    const uint64_t packed = thr[b];
+    const uint64_t bound = packed & ((1ull << 33) - 1);
+    const uint32_t need = (uint32_t)(packed >> 33);
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
     const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
     const int32_t s0 = (int32_t)(tile * kScanTile) + (int32_t)threadIdx.x * kScanItems;
-    bool chosen[kScanItems];
-    uint32_t cnt = 0;
+    bool lt[kScanItems], eq[kScanItems];
+    uint64_t cnt = 0;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         const int32_t s = s0 + i;
-        chosen[i] = s < nv && select_key(key_mode, hb, s, pick) <= T;
-        cnt += chosen[i] ? 1u : 0u;
+        const uint64_t k = s < nv ? select_key(key_mode, hb, s, pick) : ~0ull;
+        const uint64_t top = k >> 32;
+        const bool counted = s < nv && (key_mode == 0 || k != ~0ull);
+        lt[i] = counted && top < bound;
+        eq[i] = counted && top == bound;
+        cnt += lt[i] ? (1ull << 31) : (eq[i] ? 1ull : 0ull);
     }
     uint64_t total;
     const uint64_t excl = block_excl_scan(cnt, s_wave, &total);
-    uint64_t pos = tile_lookback(desc_s + (size_t)b * tiles_s, tile, total, &s_prefix) + excl;
+    uint64_t before = tile_lookback(desc_s + (size_t)b * tiles_s, tile, total, &s_prefix) + excl;
     int32_t* out = center_lin + (size_t)b * M;
     const uint32_t* vl = vox_lin + (size_t)b * N;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
-        if (!chosen[i]) continue;
-        if (pos < (uint64_t)m) {
-            const int32_t l = (int32_t)vl[s0 + i];
-            for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
+        const uint32_t nlt = (uint32_t)(before >> 31), neq = (uint32_t)(before & 0x7FFFFFFFull);
+        if (lt[i] || (eq[i] && neq < need)) {
+            const uint32_t pos = nlt + (neq < need ? neq : need);
+            if (pos < (uint32_t)m) {
+                const int32_t l = (int32_t)vl[s0 + i];
+                for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
+            }
         }
-        ++pos;
+        before += lt[i] ? (1ull << 31) : (eq[i] ? 1ull : 0ull);
     }
 }
 
 // ---- many-block selection (large clouds): one histogram kernel per digit.
-// Digit q covers key bits [lo(q), hi(q)): 11-bit digits from the top.
-__device__ __forceinline__ int sel_lo(int q) { return q == kSelPasses - 1 ? 0 : 64 - 11 * (q + 1); }
+// Digit q covers key bits [lo(q), hi(q)): bits 53..63, 42..52 and 32..41.
+__device__ __forceinline__ int sel_lo(int q) { return q == kSelPasses - 1 ? 32 : 64 - 11 * (q + 1); }
 __device__ __forceinline__ int sel_hi(int q) { return 64 - 11 * q; }
 
 struct SelState {
-    uint64_t prefix, mask, T;
+    uint64_t prefix, mask, bound;
     uint32_t need;
-    bool done;  // T is known
+    bool done;  // bound and need are known
 };
 
 // Re-derives, from the histograms of digits 0..passes-1 of cloud b, the digits
@@ -220,7 +240,7 @@ __device__ SelState sel_derive(const uint32_t* __restrict__ hist, int32_t B, int
     for (int q = 0; q < passes && !st.done; ++q) {
         const int lo = sel_lo(q), width = sel_hi(q) - lo;
         const int bins = 1 << width;
-        const int per = bins / kScanThreads;  // 8, or 2 for the last digit
+        const int per = bins / kScanThreads;  // 8, or 4 for the last digit
         const uint32_t* h = hist + ((size_t)q * B + b) * kSelBins;
         uint32_t v[8], sum = 0;
 #pragma unroll
@@ -246,12 +266,13 @@ __device__ SelState sel_derive(const uint32_t* __restrict__ hist, int32_t B, int
         st.mask |= (uint64_t)(bins - 1) << lo;
         st.need -= below;
         if (cnt == st.need) {  // every key under this prefix is among the m smallest
-            st.T = st.prefix | ~st.mask;
+            st.bound = ((st.prefix | ~st.mask) >> 32) + 1;
+            st.need = 0;
             st.done = true;
         }
     }
     if (!st.done && passes == kSelPasses) {
-        st.T = st.prefix;
+        st.bound = st.prefix >> 32;
         st.done = true;
     }
     return st;
@@ -320,14 +341,14 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_mb_hist(
         if (lh[i]) atomicAdd(&gh[i], lh[i]);
 }
 
-// The threshold of each cloud from its six histograms.
+// The bound and tie count of each cloud from its three histograms.
 __global__ __launch_bounds__(kScanThreads) void k_sel_mb_final(int32_t B, const int32_t* __restrict__ nvox,
                                                                int32_t M, const uint32_t* __restrict__ hist,
                                                                uint64_t* __restrict__ thr) {
     const int32_t b = blockIdx.x;
     const int32_t nv = nvox[b];
     const SelState st = sel_derive(hist, B, b, (uint32_t)(M < nv ? M : nv), kSelPasses);
-    if (threadIdx.x == 0) thr[b] = st.T;
+    if (threadIdx.x == 0) thr[b] = sel_pack(st.bound, st.need);
 }
 
 struct GridDims {
