@@ -485,6 +485,12 @@ __global__ __launch_bounds__(256) void k_cas_score(
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
+    // the voxel's own state is loaded up front, together with the cloud's,
+    // so that the chain of dependent loads stays short
+    const uint32_t rnd0 = in_range ? st.round[gid] : 0u;
+    const uint32_t dty0 = in_range ? st.dirty[gid] : 0u;
+    const uint64_t key0 = in_range ? st.key[gid] : 0ull;
+    const uint32_t lin0 = in_range ? vox_lin[gid] : 0u;
     bool active = in_range && ctl.done[b] == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
         __hip_atomic_store(ctl.host + 1, (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -502,13 +508,13 @@ __global__ __launch_bounds__(256) void k_cas_score(
     if (active)  // this round's pick counts start from zero
         for (int32_t i = s; i < kCasParts; i += N) ctl.cpart[((size_t)(R & 1) * B + b) * kCasParts + i] = 0;
     uint64_t k = 0;
-    const uint32_t rnd = active && s < nv ? st.round[gid] : 0u;
+    const uint32_t rnd = active && s < nv ? rnd0 : 0u;
     // a voxel picked in the previous round stops competing: its key becomes 0
     if (active && s < nv && rnd != 0 && rnd == (uint32_t)R) st.key[gid] = 0;
     if (active && s < nv && rnd == 0) {
-        if (R == 0 || st.dirty[gid] == (uint32_t)R) {
+        if (R == 0 || dty0 == (uint32_t)R) {
             const uint32_t* cv = st.cover + (size_t)b * N;
-            const uint32_t lin = vox_lin[gid];
+            const uint32_t lin = lin0;
             int64_t U = 0, cs = 0;
             if constexpr (LIST) {
                 // the voxels within r head the list: at most 27 of them
@@ -557,7 +563,7 @@ __global__ __launch_bounds__(256) void k_cas_score(
             k = ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
             st.key[gid] = k;
         } else {
-            k = st.key[gid];
+            k = key0;
         }
     }
     // per-cloud maximum into one of the partial slots
@@ -589,6 +595,10 @@ __global__ __launch_bounds__(256) void k_cas_pick(
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
+    // the voxel's own state is loaded up front, together with the cloud's
+    const uint64_t pk0 = in_range ? st.pick[gid] : 0ull;
+    const uint64_t my0 = in_range ? st.key[gid] : 0ull;
+    const int32_t bl0 = in_range ? st.blocker[gid] : -1;
     const bool active = in_range && ctl.done[b] == 0;
     const uint64_t G = parts_max(ctl.gpart + (size_t)(R & 1) * B * kCasParts, b);
     if (active)  // next round's maxima start from zero
@@ -602,15 +612,15 @@ __global__ __launch_bounds__(256) void k_cas_pick(
     bool winner = false;
     int32_t x = 0, y = 0, z = 0;
     if (active && s < nv) {
-        const uint64_t pk = st.pick[gid];
+        const uint64_t pk = pk0;
         if (pk != 0) {
             above = pk > G ? 1u : 0u;
         } else {
             // competitors are the voxels unpicked at the round's start: earlier
             // picks have key 0 (set by this round's scoring), this round's keep theirs
             const uint64_t* ky = st.key + cb;
-            const uint64_t my = st.key[gid];
-            const int32_t bl = st.blocker[gid];
+            const uint64_t my = my0;
+            const int32_t bl = bl0;
             const bool beaten = bl >= 0 && ky[bl] > my;
             if (!beaten) {
                 int32_t found = -1;
