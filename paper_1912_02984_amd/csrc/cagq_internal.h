@@ -76,7 +76,7 @@ struct Layout {
 // several addresses), then per cloud a done flag, then the number of clouds
 // done:  u64 gpart[2][B][kCasParts]; u32 cpart[2][B][kCasParts]; u32 done[B];
 // u32 ndone.
-constexpr int kCasParts = 32;
+constexpr int kCasParts = 128;
 struct CasCtl {
     static size_t bytes(int B) { return (size_t)B * (2 * kCasParts * 12 + 4) + 64; }
 };

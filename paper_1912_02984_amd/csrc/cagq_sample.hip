@@ -410,11 +410,17 @@ __device__ __forceinline__ uint32_t u4(const uint4& v, int j) {
 // Reduction of the kCasParts partials of the cloud `b` of each lane. Every
 // lane of the wave must call it.
 __device__ __forceinline__ uint64_t parts_max(const uint64_t* __restrict__ part, int32_t b) {
+    static_assert(kCasParts % kWave == 0, "partials per lane");
     const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
     if (b0 == b1) {
-        uint64_t v = part[(size_t)b0 * kCasParts + (lane_id() & (kCasParts - 1))];
+        uint64_t v = 0;
 #pragma unroll
-        for (int d = 1; d < kCasParts; d <<= 1) {
+        for (int i = 0; i < kCasParts / kWave; ++i) {
+            const uint64_t o = part[(size_t)b0 * kCasParts + i * kWave + lane_id()];
+            v = o > v ? o : v;
+        }
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) {
             uint64_t o = shfl_xor64(v, d);
             v = o > v ? o : v;
         }
@@ -431,9 +437,11 @@ __device__ __forceinline__ uint64_t parts_max(const uint64_t* __restrict__ part,
 __device__ __forceinline__ uint32_t parts_sum(const uint32_t* __restrict__ part, int32_t b) {
     const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
     if (b0 == b1) {
-        uint32_t v = part[(size_t)b0 * kCasParts + (lane_id() & (kCasParts - 1))];
+        uint32_t v = 0;
 #pragma unroll
-        for (int d = 1; d < kCasParts; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
+        for (int i = 0; i < kCasParts / kWave; ++i) v += part[(size_t)b0 * kCasParts + i * kWave + lane_id()];
+#pragma unroll
+        for (int d = 1; d < kWave; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
         return v;
     }
     uint32_t v = 0;
