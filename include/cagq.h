@@ -16,7 +16,7 @@
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Work is enqueued asynchronously on it; results are valid once the
  *     stream has reached the enqueued work. cagq_sample_centers with the
- *     CAS mode may synchronise `stream` (see there).
+ *     CAS mode may wait for its rounds (see there).
  *   - Argument errors are detected on the host before anything is
  *     enqueued and returned synchronously. Data-dependent errors
  *     (non-finite coordinates, center voxels that are not occupied) are
@@ -147,10 +147,10 @@ CAGQ_API int cagq_build_grid(const float* points, int32_t B, int32_t N, const ca
  *     (C_V = chosen voxels whose neighbourhood holds V, lambda = (2r+1)^3,
  *     beta = beta_q16 / 2^16), ties to the lowest lin; the first m_valid
  *     picks are the centers. Requires (2^16 + beta_q16) * lambda^2 < 2^31.
- *     `seed` is unused. With beta_q16 = 0, r <= 2 and N <= 8192 (one
+ *     `seed` is unused. With beta_q16 = 0, r <= 2 and N <= 4096 (one
  *     workgroup per cloud holds the whole state) the call is asynchronous;
- *     otherwise its round count is data dependent and it synchronises
- *     `stream`.
+ *     otherwise its round count is data dependent and it waits on the host
+ *     for the rounds to finish (without synchronising `stream` as a whole).
  *   center_lin  device int32 [B][M];  m_valid  device int32 [B]
  */
 CAGQ_API int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed,

@@ -85,7 +85,7 @@ struct CasCtl {
 // points, r <= 2): per slot a header of 8 u16 (entries within Chebyshev r,
 // entries within 2r, 6 unused) and then the slots of the occupied voxels
 // within distance 2r, those within r (the slot itself included) first.
-constexpr int32_t kCasLdsMaxN = 8192;
+constexpr int32_t kCasLdsMaxN = 4096;
 __host__ __device__ constexpr int nbr_stride(int r) {
     return 8 + (((4 * r + 1) * (4 * r + 1) * (4 * r + 1) + 7) & ~7);
 }
