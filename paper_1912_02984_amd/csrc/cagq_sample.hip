@@ -679,27 +679,52 @@ __global__ __launch_bounds__(256) void k_cas_pick(
             }
         }
     }
-    // the whole wave marks each winner's window, one grid row (or one list
-    // entry) per lane: rescoring flags within 2r, coverage counts within r.
-    // Winners of a round are more than 2r apart, so their r-neighbourhoods
-    // are disjoint and no count is raised twice in a round: plain
-    // read-modify-write is exact.
-    uint64_t wins = __ballot(winner);
+    // Marks of the winners: rescoring flags within 2r, coverage counts
+    // within r. Winners of a round are more than 2r apart, so their
+    // r-neighbourhoods are disjoint and no count is raised twice in a round:
+    // plain read-modify-write is exact. Without lists the whole wave marks
+    // each winner's window, one grid row per lane.
+    if constexpr (LIST) {
+        // the wave marks all (winner, list entry) pairs of its winners, 64
+        // at a time: the entries of one list are contiguous, so a winner's
+        // marks are coalesced, and the wave waits for two dependent loads
+        // per 64 pairs, not per winner
+        const uint32_t n2w = winner ? nbr[(size_t)gid * kNbr32Stride + 1] : 0u;
+        const uint32_t n_rw = winner ? nbr[(size_t)gid * kNbr32Stride] : 0u;
+        const uint32_t incl = wave_incl_scan<uint32_t>(n2w);
+        const uint32_t total = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+        for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
+            const uint32_t p = p0 + (uint32_t)lane_id();
+            // owner: the first lane whose inclusive count exceeds p
+            int lo = 0;
+#pragma unroll
+            for (int step = kWave / 2; step > 0; step >>= 1) {
+                const uint32_t v = (uint32_t)__shfl((int)incl, lo + step - 1, kWave);
+                if (v <= p) lo += step;
+            }
+            const int owner = lo < kWave ? lo : kWave - 1;
+            const uint32_t o_incl = (uint32_t)__shfl((int)incl, owner, kWave);
+            const uint32_t o_n2 = (uint32_t)__shfl((int)n2w, owner, kWave);
+            const uint32_t o_nr = (uint32_t)__shfl((int)n_rw, owner, kWave);
+            const int32_t o_gid = __shfl(gid, owner, kWave);
+            const int32_t o_b = __shfl(b, owner, kWave);
+            if (p < total) {
+                const uint32_t j = p - (o_incl - o_n2);
+                const uint32_t sl = nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
+                uint32_t* cv = st.cover + (size_t)o_b * N;
+                st.dirty[(size_t)o_b * N + sl] = cur;
+                if (j < o_nr) cv[sl] = cv[sl] + 1u;
+            }
+        }
+    }
+    uint64_t wins = LIST ? 0ull : __ballot(winner);
     while (wins) {
         const int wl = __ffsll((unsigned long long)wins) - 1;
         wins &= wins - 1;
         const int32_t wb = __shfl(b, wl, kWave);
         uint32_t* cv = st.cover + (size_t)wb * N;
         uint32_t* dt = st.dirty + (size_t)wb * N;
-        if constexpr (LIST) {
-            const uint32_t* lst = nbr + (size_t)__shfl(gid, wl, kWave) * kNbr32Stride;
-            const uint32_t n_r = lst[0], n2 = lst[1];
-            for (uint32_t j = (uint32_t)lane_id(); j < n2; j += kWave) {
-                const uint32_t sl = lst[4 + j];
-                dt[sl] = cur;
-                if (j < n_r) cv[sl] = cv[sl] + 1u;
-            }
-        } else {
+        {
             const int32_t wx = __shfl(x, wl, kWave), wy = __shfl(y, wl, kWave), wz = __shfl(z, wl, kWave);
             const uint64_t* wbm = bitmap + (size_t)wb * W;
             const uint32_t* wwr = word_rank + (size_t)wb * W;
