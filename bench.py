@@ -72,7 +72,7 @@ def load_traffic() -> dict:
 
 
 def _short(name: str) -> str:
-    m = re.search(r"(k_\w+)<(\d)(?:, \d+)?>", name)
+    m = re.search(r"(k_\w+)<(\d)(?:, \d+)*>", name)
     if m and m.group(1) == "k_query":
         return QUERY_NAMES[m.group(2)]
     m = re.search(r"(k_\w+(?:<[^>(]*>)?)\(", name)
@@ -104,7 +104,7 @@ def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
     sf, sw = COPY_PROBE_BYTES / (cf * 1024), COPY_PROBE_BYTES / (cw * 1024)
 
     def layer1(rows, mode):
-        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+>", r["Kernel_Name"])]
+        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+(?:, \d+)?>", r["Kernel_Name"])]
         g = max(int(r["Grid_Size"]) for r in q)
         return [float(r["Counter_Value"]) for r in q if int(r["Grid_Size"]) == g]
     lines = [f"Calibration: a {COPY_PROBE_BYTES >> 20} MiB fp32 copy kernel reads FETCH_SIZE {cf:.0f} KiB "
