@@ -58,9 +58,11 @@ def lib():
         L.orc_build_table.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(Grid), P, P, P, P, P]
         L.orc_sample_rvs.argtypes = [C.POINTER(_Table), C.c_int32, C.c_uint64, P, P]
         L.orc_sample_cas.argtypes = [C.POINTER(_Table), C.c_int32, C.c_uint32, P, P, P, P]
+        L.orc_sample_cas_swap.argtypes = [C.POINTER(_Table), C.c_int32, C.c_uint64, C.c_uint32, P, P, P, P]
         L.orc_query.argtypes = [C.POINTER(_Table), P, P, P, P, C.c_int32, C.c_int32,
                                 C.c_int32, C.c_uint64, P, P, P, P, P, P]
-        for f in ("orc_voxelize", "orc_build_table", "orc_sample_rvs", "orc_sample_cas", "orc_query"):
+        for f in ("orc_voxelize", "orc_build_table", "orc_sample_rvs", "orc_sample_cas", "orc_sample_cas_swap",
+                  "orc_query"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -141,9 +143,25 @@ class Table:
                                     _ptr(pl), _ptr(ps)), "orc_sample_cas")
         return cl, mv, pl, ps
 
+    def sample_cas_swap(self, M: int, seed: int, beta_q16: int = 0):
+        """The paper's challenger / incumbent CAS from the RVS choice.
+        Returns (center_lin ascending, m_valid, decision [B][N], n_swaps [B]);
+        decision[b, t] is the slot challenge t went to, >= 0 when accepted,
+        -(slot + 1) when refused; entries past the last challenge are 0."""
+        cl = np.zeros((self.B, M), np.int32)
+        mv = np.zeros(self.B, np.int32)
+        dec = np.zeros((self.B, self.N), np.int32)
+        ns = np.zeros(self.B, np.int32)
+        _check(lib().orc_sample_cas_swap(C.byref(self._t), M, C.c_uint64(seed), C.c_uint32(beta_q16),
+                                         _ptr(cl), _ptr(mv), _ptr(dec), _ptr(ns)), "orc_sample_cas_swap")
+        return cl, mv, dec, ns
+
     def sample(self, M: int, mode: str, seed: int, beta_q16: int = 0):
         if mode == "rvs":
             return self.sample_rvs(M, seed)
+        if mode == "cas_swap":
+            cl, mv, _, _ = self.sample_cas_swap(M, seed, beta_q16)
+            return cl, mv
         cl, mv, _, _ = self.sample_cas(M, beta_q16)
         return cl, mv
 

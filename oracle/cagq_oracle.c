@@ -28,6 +28,16 @@
  *             H_add exactly), ties to the lowest lin; lambda = (2r+1)^3.
  *             The chosen set is emitted in ascending lin (as for RVS); the
  *             pick order and pick-time scores are returned separately.
+ *   CAS-P     Sec. 3.2, Eqs. 2-3, the paper's own procedure: M random
+ *             incumbents; every other occupied voxel challenges a random
+ *             incumbent and replaces it when H_add > H_rmv, with
+ *             H_rmv = #{V in pi(I): C_V = 1}. Reading: the incumbents are
+ *             the RVS choice with the same seed, held in slots 0..m-1 in
+ *             ascending lin; the challengers are the other occupied voxels
+ *             in ascending lin, each challenging once (a replaced incumbent
+ *             does not challenge again); challenge t goes to slot
+ *             hi32(h(seed, 3, b, t)) mod m; both heuristics are compared
+ *             scaled by 2^16 * lambda, as integers. Output in ascending lin.
  *   pi(v)     Sec. 3.2 and the notation table: the occupied voxels of the
  *             (2r+1)^3 cube around v, v included, clipped to the grid.
  *   query     Sec. 3.2: Cube Query picks K context points at random, k-NN
@@ -41,14 +51,17 @@
  *             in node order (stride 1, 2, 4, ...), then one fp32 divide.
  *   h         splitmix64 chain: h(seed, tag, a1..ak) =
  *             sm64(...sm64(sm64(seed ^ tag) ^ a1)... ^ ak), tags RVS=1,
- *             CUBE=2 (splitmix64: Steele, Lea, Flood, OOPSLA 2014).
+ *             CUBE=2, CAS-P=3 (splitmix64: Steele, Lea, Flood, OOPSLA 2014).
  *
  * Pins (tests marked "not gpu"): splitmix64 published outputs; voxelize vs
  * a numpy fp32 re-derivation and hand-placed boundary points; the table vs
  * numpy unique/argsort; RVS vs an explicit lexsort and a chi-square test of
  * equal inclusion probability; CAS vs brute-force recomputation at every
  * step, exhaustive optimum on <= 64 voxels (1 - 1/e bound, equality at
- * M = 1), disjoint-neighbourhood closed form; k-NN vs brute force and vs
+ * M = 1), disjoint-neighbourhood closed form; CAS-P: covered space strictly
+ * grows with every accepted swap at beta = 0 (recomputed from the replayed
+ * incumbent sets), slot draws vs an independent hash, no swap among
+ * isolated voxels, hand-worked examples; k-NN vs brute force and vs
  * global k-NN when the cap never binds; cube subset / frequency checks;
  * centers vs closed forms and an fp64 error bound.
  */
@@ -316,6 +329,79 @@ int orc_sample_cas(const orc_table* t, int32_t M, uint32_t beta_q16,
         free(C);
         free(picked);
         free(score);
+    }
+    return rc;
+}
+
+/* CAS-P: the paper's challenger / incumbent procedure (Sec. 3.2, Eqs. 2-3).
+ * decision [B][N] (may be NULL): for challenge t, the incumbent slot it
+ * challenged if the swap was accepted, -(slot + 1) if it was refused;
+ * n_swaps [B] (may be NULL): accepted swaps. */
+int orc_sample_cas_swap(const orc_table* t, int32_t M, uint64_t seed, uint32_t beta_q16,
+                        int32_t* center_lin, int32_t* m_valid, int32_t* decision, int32_t* n_swaps) {
+    if (!table_ok(t) || M < 1 || !center_lin || !m_valid) return ORC_EINVAL;
+    int rc = orc_sample_rvs(t, M, seed, center_lin, m_valid);
+    if (rc != 0) return rc;
+    int32_t rad = t->g.radius;
+    int32_t side = 2 * rad + 1;
+    int64_t lambda = (int64_t)side * side * side;
+    for (int32_t b = 0; b < t->B && rc == 0; ++b) {
+        int32_t nv = t->nvox[b];
+        int32_t m = m_valid[b];
+        const uint32_t* vl = t->vox_lin + (size_t)b * t->N;
+        int32_t* c = center_lin + (size_t)b * M;
+        int32_t* inc = (int32_t*)malloc(sizeof(int32_t) * (size_t)m);        /* slot -> voxel (its slot in O_v) */
+        unsigned char* initial = (unsigned char*)calloc((size_t)nv, 1);      /* in the RVS choice */
+        uint32_t* C = (uint32_t*)calloc((size_t)nv, sizeof(uint32_t));       /* incumbents covering V */
+        int32_t* pc = (int32_t*)malloc(sizeof(int32_t) * (size_t)lambda);
+        int32_t* pi = (int32_t*)malloc(sizeof(int32_t) * (size_t)lambda);
+        if (!inc || !initial || !C || !pc || !pi) {
+            rc = ORC_EINVAL;
+        } else {
+            for (int32_t j = 0; j < m; ++j) {
+                inc[j] = find_slot(t, b, (uint32_t)c[j]);
+                initial[inc[j]] = 1;
+                int32_t n = neighbours(t, b, (uint32_t)c[j], rad, pc);
+                for (int32_t k = 0; k < n; ++k) C[pc[k]] += 1;
+            }
+            uint64_t hb = orc_splitmix64(orc_splitmix64(seed ^ 3ull) ^ (uint64_t)b);
+            int32_t tch = 0, swaps = 0;
+            for (int32_t v = 0; v < nv; ++v) {
+                if (initial[v]) continue;
+                int32_t j = (int32_t)((orc_splitmix64(hb ^ (uint64_t)tch) >> 32) % (uint64_t)m);
+                int32_t I = inc[j];
+                int32_t nc = neighbours(t, b, vl[v], rad, pc);
+                int32_t ni = neighbours(t, b, vl[I], rad, pi);
+                /* Eq. 2 and Eq. 3, both scaled by 2^16 * lambda */
+                int64_t uncovered = 0, covsum = 0, single = 0;
+                for (int32_t k = 0; k < nc; ++k) {
+                    if (C[pc[k]] == 0) uncovered += 1;
+                    covsum += C[pc[k]];
+                }
+                for (int32_t k = 0; k < ni; ++k)
+                    if (C[pi[k]] == 1) single += 1;
+                int64_t h_add = 65536LL * lambda * uncovered - (int64_t)beta_q16 * covsum;
+                int64_t h_rmv = 65536LL * lambda * single;
+                int accept = h_add > h_rmv;
+                if (accept) {
+                    for (int32_t k = 0; k < ni; ++k) C[pi[k]] -= 1;
+                    for (int32_t k = 0; k < nc; ++k) C[pc[k]] += 1;
+                    inc[j] = v;
+                    ++swaps;
+                }
+                if (decision) decision[(size_t)b * t->N + tch] = accept ? j : -(j + 1);
+                ++tch;
+            }
+            for (int32_t j = 0; j < m; ++j) c[j] = (int32_t)vl[inc[j]];
+            qsort(c, (size_t)m, sizeof(int32_t), cmp_i32);
+            pad_cyclic(c, m, M);
+            if (n_swaps) n_swaps[b] = swaps;
+        }
+        free(inc);
+        free(initial);
+        free(C);
+        free(pc);
+        free(pi);
     }
     return rc;
 }

@@ -64,6 +64,14 @@ int orc_sample_cas(const orc_table* t, int32_t M, uint32_t beta_q16,
                    int32_t* center_lin, int32_t* m_valid,
                    int32_t* pick_lin, int64_t* pick_score);
 
+/* Coverage-Aware Sampling, the paper's challenger / incumbent procedure
+ * (Sec. 3.2, Eqs. 2-3), starting from the RVS choice: center_lin [B][M] in
+ * ascending lin, m_valid [B]; decision [B][N] (may be NULL) per challenge t
+ * the slot challenged, >= 0 if the swap was accepted, -(slot + 1) if not;
+ * n_swaps [B] (may be NULL) the accepted swaps. */
+int orc_sample_cas_swap(const orc_table* t, int32_t M, uint64_t seed, uint32_t beta_q16,
+                        int32_t* center_lin, int32_t* m_valid, int32_t* decision, int32_t* n_swaps);
+
 /* Node query (Sec. 3.2: Cube Query when mode == 0, k-NN when mode == 1) and
  * group centers (Appendix E). weights [B][N] may be NULL (all 1). */
 int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,

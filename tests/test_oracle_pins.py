@@ -263,6 +263,107 @@ def test_cas_takes_everything_when_m_exceeds_occupancy():
     assert all(cl[0, j] == cl[0, j % nv] for j in range(nv, nv + 7))
 
 
+# ---------------------------------------------------------------- CAS, the paper's swap procedure
+
+def _replay_swaps(t, b, M, seed, dec):
+    """Incumbent slots after every challenge, replaying the oracle's
+    decisions from its RVS choice: a list of (accepted, incumbent voxel
+    indices) per challenge."""
+    nv = int(t.nvox[b])
+    vl = [int(x) for x in t.vox_lin[b, :nv]]
+    index = {l: i for i, l in enumerate(vl)}
+    rvs, mv = t.sample_rvs(M, seed)
+    m = int(mv[b])
+    inc = [index[int(l)] for l in rvs[b, :m]]
+    initial = set(inc)
+    challengers = [v for v in range(nv) if v not in initial]
+    states = []
+    for tch, v in enumerate(challengers):
+        d = int(dec[b, tch])
+        j = d if d >= 0 else -d - 1
+        # the slot draw, from an independent hash: hi32(h(seed, 3, b, t)) mod m
+        assert j == (pins.py_chain(seed, 3, b, tch) >> 32) % m
+        if d >= 0:
+            inc[j] = v
+        states.append((d >= 0, list(inc)))
+    return vl, inc, states
+
+
+@pytest.mark.parametrize("seed", [0, 5, 9])
+def test_cas_swap_decisions_replay_and_coverage_grows(seed):
+    """beta = 0 (Sec. 3.2): every accepted replacement strictly enlarges the
+    covered occupied space, recomputed from scratch from the replayed
+    incumbent sets; refusals leave it unchanged; the replay ends at the
+    emitted centers."""
+    w = W.get_workload("object")
+    L = w.layers[0]
+    t = oracle.Table(w.points()[:3], oracle.grid_from_spec(L.grid))
+    M = 200
+    cl, mv, dec, ns = t.sample_cas_swap(M, seed)
+    total = 0
+    for b in range(t.B):
+        vl, inc, states = _replay_swaps(t, b, M, seed, dec)
+        nbr = pins.neighbourhood_sets(vl, t.grid.dims, 1)
+        rvs, _ = t.sample_rvs(M, seed)
+        index = {l: i for i, l in enumerate(vl)}
+        prev = pins.coverage(nbr, [index[int(l)] for l in rvs[b, :mv[b]]])
+        swaps = 0
+        for accepted, cur in states:
+            cov = pins.coverage(nbr, cur)
+            if accepted:
+                assert cov > prev
+                swaps += 1
+            else:
+                assert cov == prev
+            prev = cov
+        assert swaps == ns[b]
+        assert sorted(vl[v] for v in inc) == list(cl[b, :mv[b]])
+        total += swaps
+    assert total > 0
+
+
+def test_cas_swap_hand_worked_row():
+    """Occupied voxels x = 0, 2, 3, 4 of one grid row, r = 1, M = 1. From
+    Eqs. 2-3 by hand: starting at x = 0, challenger 2 has H_add = 2 (x = 2,
+    3 uncovered) against H_rmv = 1 and replaces it, after which 3 and 4
+    gain 1 against 2; starting at 2, 3 or 4 no challenger wins. So the
+    result is 2, 2, 3, 4 for a start at 0, 2, 3, 4."""
+    pts = [[(x + 0.5) * 0.25, 0.1, 0.1] for x in (0, 2, 3, 4)]
+    P = np.array([pts], np.float32)
+    t = oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (8, 1, 1), 4, 1))
+    expect = {0: 2, 2: 2, 3: 3, 4: 4}
+    seen = set()
+    for seed in range(40):
+        rvs, _ = t.sample_rvs(1, seed)
+        cl, mv, dec, ns = t.sample_cas_swap(1, seed)
+        start = int(rvs[0, 0])
+        assert int(cl[0, 0]) == expect[start]
+        assert ns[0] == (1 if start == 0 else 0)
+        seen.add(start)
+    assert 0 in seen  # the swapping case was exercised
+
+
+def test_cas_swap_never_swaps_isolated_voxels():
+    """pi(v) = {v} for every voxel: H_add = 1 = H_rmv, so no challenger wins
+    and the result is the RVS choice."""
+    pts = [[(x + 0.5) * 0.25, (y + 0.5) * 0.25, 0.1] for x in range(0, 16, 2) for y in range(0, 16, 2)]
+    P = np.array([pts], np.float32)
+    t = oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (16, 16, 1), 4, 1))
+    for seed in range(3):
+        cl, mv, dec, ns = t.sample_cas_swap(10, seed)
+        rvs, _ = t.sample_rvs(10, seed)
+        assert ns[0] == 0
+        assert np.array_equal(cl, rvs)
+
+
+def test_cas_swap_takes_everything_when_m_exceeds_occupancy():
+    t = _small_table(3, npts=10)
+    nv = int(t.nvox[0])
+    cl, mv, dec, ns = t.sample_cas_swap(nv + 5, 1)
+    assert mv[0] == nv and ns[0] == 0
+    assert list(cl[0, :nv]) == list(t.vox_lin[0, :nv])
+
+
 # ---------------------------------------------------------------- query
 
 def _context_bruteforce(P, lin, tb, center_lin, dims, r):
