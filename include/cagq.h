@@ -55,6 +55,7 @@ extern "C" {
 
 #define CAGQ_SAMPLE_RVS 0   /* Random Voxel Sampling (Sec. 3.2) */
 #define CAGQ_SAMPLE_CAS 1   /* Coverage-Aware Sampling, greedy (Sec. 3.2, Eqs. 1-2) */
+#define CAGQ_SAMPLE_CAS_SWAP 2  /* Coverage-Aware Sampling, challenger / incumbent swaps (Sec. 3.2, Eqs. 2-3) */
 #define CAGQ_QUERY_CUBE 0   /* Cube Query (Sec. 3.2) */
 #define CAGQ_QUERY_KNN 1    /* k-NN among the context points (Sec. 3.2) */
 
@@ -151,6 +152,20 @@ CAGQ_API int cagq_build_grid(const float* points, int32_t B, int32_t N, const ca
  *     workgroup per cloud holds the whole state) the call is asynchronous;
  *     otherwise its round count is data dependent and it waits on the host
  *     for the rounds to finish (without synchronising `stream` as a whole).
+ *   mode CAGQ_SAMPLE_CAS_SWAP: the paper's own procedure (Eqs. 2-3). The
+ *     m_valid incumbents start as the RVS choice for `seed`, held in slots
+ *     0..m_valid-1 in ascending lin; every other occupied voxel C, in
+ *     ascending lin, challenges slot hi32(h(seed,3,b,t)) mod m_valid (t =
+ *     0, 1, ... counts the challenges) holding incumbent I, and replaces it
+ *     when
+ *       2^16*lambda*#{V in pi(C): C_V = 0} - beta_q16 * sum_{V in pi(C)} C_V
+ *         > 2^16*lambda*#{V in pi(I): C_V = 1}
+ *     with C_V the incumbents whose neighbourhood holds V. A replaced
+ *     incumbent does not challenge again. The procedure is sequential (one
+ *     workgroup per cloud walks the challengers); the call only enqueues.
+ *     Both sides are compared as 64-bit integers (any beta_q16, r <= 3).
+ *     Requires 4*M + 4*ceil(N/32) + (r <= 2 ? 1 : 2) * N <= 159728 bytes
+ *     (the state one workgroup holds), else returns CAGQ_ERR_CAPACITY.
  *   center_lin  device int32 [B][M];  m_valid  device int32 [B]
  */
 CAGQ_API int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t seed,

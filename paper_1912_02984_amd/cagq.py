@@ -26,7 +26,7 @@ ERR_CAPACITY = -5
 ERR_HIP = -6
 ERR_CENTER_NOT_OCCUPIED = -7
 
-SAMPLE = {"rvs": 0, "cas": 1}
+SAMPLE = {"rvs": 0, "cas": 1, "cas_swap": 2}
 QUERY = {"cube": 0, "knn": 1}
 MAX_K = 64
 MAX_NV = 64
@@ -180,7 +180,9 @@ def build_grid(points: torch.Tensor, desc: GridDesc, workspace: Optional[torch.T
 def sample_centers(grid: Grid, M: int, mode: str, seed: int, beta_q16: int = 0,
                    center_lin: Optional[torch.Tensor] = None, m_valid: Optional[torch.Tensor] = None,
                    stream: Optional[torch.cuda.Stream] = None):
-    """M center voxels per cloud by RVS or CAS (cagq_sample_centers)."""
+    """M center voxels per cloud by RVS, CAS (greedy) or CAS with the paper's
+    challenger / incumbent swaps (cagq_sample_centers; mode "rvs", "cas" or
+    "cas_swap")."""
     dev = grid.points.device
     if center_lin is None:
         center_lin = torch.empty((grid.B, M), dtype=torch.int32, device=dev)

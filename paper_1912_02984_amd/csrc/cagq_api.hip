@@ -136,6 +136,12 @@ int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t se
         hipError_t e = launch_select(L, g->workspace, M, 0, seed, center_lin, m_valid, (hipStream_t)stream);
         return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
     }
+    if (mode == CAGQ_SAMPLE_CAS_SWAP) {  // 64-bit comparisons: no range limit on beta
+        if (!cas_swap_fits(L, g->desc, M)) return CAGQ_ERR_CAPACITY;
+        hipError_t e = launch_cas_swap(L, g->desc, g->workspace, M, seed, beta_q16, center_lin, m_valid,
+                                       (hipStream_t)stream);
+        return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+    }
     if (mode != CAGQ_SAMPLE_CAS) return CAGQ_ERR_INVALID_ARG;
     const int64_t side = 2 * (int64_t)g->desc.radius + 1;
     const int64_t lam = side * side * side;

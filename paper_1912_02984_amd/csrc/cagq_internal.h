@@ -337,6 +337,12 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
 hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
                          int32_t* center_lin, int32_t* m_valid, hipStream_t s);
 
+// The paper's challenger / incumbent CAS: RVS incumbents, then one
+// workgroup per cloud walks the challengers.
+bool cas_swap_fits(const Layout& L, const cagq_grid_desc& d, int32_t M);
+hipError_t launch_cas_swap(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, uint64_t seed,
+                           uint32_t beta_q16, int32_t* center_lin, int32_t* m_valid, hipStream_t s);
+
 // Writes the CAS neighbour lists of the grid in whichever format the layout
 // holds (has_nbr16 or has_nbr32).
 hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s);

@@ -123,7 +123,7 @@ def test_sample_rejects_bad_arguments():
     g = _grid_record()
     p = C.c_void_p(0x300000)
     assert L.cagq_sample_centers(C.byref(g), 0, 0, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
-    assert L.cagq_sample_centers(C.byref(g), 8, 2, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_sample_centers(C.byref(g), 8, 3, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG
     assert L.cagq_sample_centers(C.byref(g), 8, 0, 1, 0, None, p, None) == cagq.ERR_INVALID_ARG
     assert L.cagq_sample_centers(C.byref(g), 8, 0, 1, 0, p, None, None) == cagq.ERR_INVALID_ARG
     assert L.cagq_sample_centers(None, 8, 0, 1, 0, p, p, None) == cagq.ERR_INVALID_ARG

@@ -55,6 +55,8 @@ def run_both(P, grid_spec, M, K, sample, query, seed, weights=None, beta_q16=0, 
     ot = oracle.Table(P, oracle.grid_from_spec(grid_spec))
     if sample == "rvs":
         ocl, omv = ot.sample_rvs(M, seed)
+    elif sample == "cas_swap":
+        ocl, omv, _, _ = ot.sample_cas_swap(M, seed, beta_q16)
     else:
         ocl, omv, _, _ = ot.sample_cas(M, beta_q16)
     qo = ot.query(ocl, omv, K, query, seed, weights=weights)
@@ -193,6 +195,39 @@ def test_cas_single_workgroup_limits(N, dims):
     if dims in ((16, 16, 16), (12, 12, 12)):
         spec2 = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8, 2)
         run_both(P, spec2, 700, 8, "cas", "knn", 0, where=f"N={N} dims={dims} r=2")
+
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room"])
+def test_cas_swap_workloads(name):
+    """The paper's challenger / incumbent CAS on the small workloads, each
+    layer fed by the previous one's centers."""
+    w = W.get_workload(name)
+    P = w.points()[:4]
+    wts = None
+    for li, L in enumerate(w.layers):
+        qo = run_both(P, L.grid, L.M, L.K, "cas_swap", L.query, L.seed, weights=wts, where=f"{name} L{li}")
+        P, wts = qo["center_xyz"], qo["center_w"]
+
+
+@pytest.mark.parametrize("r,beta_q16", [(1, 65536 // 4), (2, 0), (3, 0)])
+def test_cas_swap_radius_and_penalty(r, beta_q16):
+    rng = np.random.default_rng(r)
+    P = rng.random((2, 1500, 3), dtype=np.float32) * np.float32(0.999)
+    spec = _spec((0, 0, 0), (1 / 16,) * 3, (16, 16, 16), 8, r)
+    run_both(P, spec, 100, 8, "cas_swap", "cube", 11, beta_q16=beta_q16, where=f"r={r} beta={beta_q16}")
+
+
+def test_cas_swap_more_centers_than_voxels_and_capacity():
+    rng = np.random.default_rng(4)
+    P = rng.random((2, 60, 3), dtype=np.float32) * np.float32(0.5)
+    spec = _spec((0, 0, 0), (0.25,) * 3, (2, 2, 2), 8)
+    run_both(P, spec, 20, 8, "cas_swap", "knn", 3, where="M>nvox")
+    # a cloud too large for one workgroup's state is refused before anything runs
+    big = torch.zeros((1, 200000, 3), device=DEV)
+    g = cagq.build_grid(big, cagq.desc_from_spec(_spec((0, 0, 0), (1.0,) * 3, (4, 4, 4), 8)))
+    with pytest.raises(cagq.CagqError) as ei:
+        cagq.sample_centers(g, 40000, "cas_swap", 0)
+    assert ei.value.code == cagq.ERR_CAPACITY
 
 
 @pytest.mark.parametrize("beta_q16", [1, 65536 // 4, 3 * 65536])
