@@ -120,6 +120,40 @@ def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
     return "\n".join(lines) + "\n"
 
 
+def measure_cas_swap(P, P_np, B: int, N: int, L, with_oracle: bool, reps: int = 3) -> dict:
+    """The paper's challenger / incumbent CAS (a sequential procedure, so
+    latency-bound: reported in ms and challenges per second) on the layer-1
+    grid of the bench batch, with the oracle on one scene beside it."""
+    import torch
+    from paper_1912_02984_amd import cagq
+    desc = cagq.desc_from_spec(L.grid)
+    g = cagq.build_grid(P, desc)
+    cl, mv = cagq.sample_centers(g, L.M, "cas_swap", L.seed)
+    torch.cuda.synchronize()
+    nvox = g.table()["nvox"].cpu().numpy()
+    challenges = int(sum(int(n) - min(L.M, int(n)) for n in nvox))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        cagq.sample_centers(g, L.M, "cas_swap", L.seed, center_lin=cl, m_valid=mv)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    row = {"workload": f"layer 1 of the bench batch: B={B} x {N} pts, M={L.M}, r={L.grid.radius}",
+           "ms": round(ms, 3), "challenges": challenges,
+           "challenges_per_s": round(challenges / (ms / 1e3), 1), "bound": "latency (sequential challenges)"}
+    if with_oracle:
+        import oracle
+        t0 = time.perf_counter()
+        ot = oracle.Table(P_np[:1], oracle.grid_from_spec(L.grid))
+        ot.sample_cas_swap(L.M, L.seed)
+        dt = time.perf_counter() - t0
+        ch1 = int(ot.nvox[0]) - min(L.M, int(ot.nvox[0]))
+        row["oracle"] = {"ms": round(dt * 1e3, 2), "challenges": ch1, "challenges_per_s": round(ch1 / dt, 1),
+                         "cores": 1, "sample": "1 of the scenes, table build included"}
+    return row
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -130,6 +164,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time to accumulate for the CPU baseline")
+    ap.add_argument("--no-next", action="store_true",
+                    help="skip the measurement of the rows beyond the hot path")
     ap.add_argument("--copy-probe", action="store_true",
                     help="run one fp32 copy kernel of known size first (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "COMMAND"),
@@ -270,6 +306,11 @@ def main():
                 "per_variant": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                                 for k, v in roof.items()}}
 
+    # rows beyond the hot path, measured on the layer-1 grid of the same batch
+    next_rows = None
+    if not args.no_next:
+        next_rows = {"cas_swap": measure_cas_swap(P, P_np, B, N, wls[0].layers[0], with_oracle=not args.no_cpu_baseline)}
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -311,6 +352,7 @@ def main():
         "wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "next_rows": next_rows,
     }
     print(json.dumps(line), flush=True)
 

@@ -18,44 +18,9 @@ namespace {
 
 constexpr int kNbrThreads = 256;
 
-struct Dims {
-    int32_t D[3];
-};
-
-struct Row {
-    uint32_t first;  // slot of the first occupied voxel at or after the segment's start
-    uint32_t mask;   // bit j: voxel x - h + j occupied (0 outside the grid)
-};
-
-// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz).
-// Branch-free: rows outside the grid are clamped into it for the loads and
-// get an empty mask, and the second word is always loaded (the same word
-// unless the segment crosses a word boundary), so the loads of many rows are
-// in flight together.
-__device__ __forceinline__ Row load_row(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
-                                        const Dims& g, int32_t x, int32_t yy, int32_t zz, int32_t h) {
-    const bool inside = yy >= 0 && yy < g.D[1] && zz >= 0 && zz < g.D[2];
-    const int32_t yc = yy < 0 ? 0 : (yy >= g.D[1] ? g.D[1] - 1 : yy);
-    const int32_t zc = zz < 0 ? 0 : (zz >= g.D[2] ? g.D[2] - 1 : zz);
-    const int32_t xs = x - h;
-    const int32_t lo_x = xs < 0 ? 0 : xs;
-    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
-    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
-    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
-    const uint32_t w0 = lo >> 6, o = lo & 63;
-    const uint64_t a = bm[w0];
-    const uint64_t c = bm[hi >> 6];
-    // when both ends share a word, the bits shifted in from c lie above the segment
-    const uint64_t bits = (a >> o) | (o ? c << (64 - o) : 0ull);
-    Row r;
-    r.mask = inside ? (uint32_t)(bits & ((1ull << (hi_x - lo_x + 1)) - 1)) << (lo_x - xs) : 0u;
-    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
-    return r;
-}
-
 // E: entry type, ST: entries per voxel (header included), HDR: header entries.
 template <int RAD, typename E, int ST, int HDR>
-__global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, int64_t W, Dims g,
+__global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, int64_t W, GridDims g,
                                                          const int32_t* __restrict__ nvox,
                                                          const uint32_t* __restrict__ vox_lin,
                                                          const uint64_t* __restrict__ bitmap,
@@ -65,10 +30,8 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
     if (gid >= B * N) return;
     const int32_t b = gid / N, s = gid - b * N;
     if (s >= nvox[b]) return;
-    const uint32_t lin = vox_lin[gid];
-    const int32_t x = (int32_t)(lin % (uint32_t)g.D[0]);
-    const int32_t y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
-    const int32_t z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
+    int32_t x, y, z;
+    decode_lin(vox_lin[gid], g, x, y, z);
     const uint64_t* bm = bitmap + (size_t)b * W;
     const uint32_t* wr = word_rank + (size_t)b * W;
     E* out = nbr + (size_t)gid * ST;
@@ -77,7 +40,7 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
     constexpr uint32_t kInner = ((1u << (2 * RAD + 1)) - 1) << (H - RAD);
     if constexpr (RAD == 1) {
         // all 25 rows of the window at once
-        Row rows[S2 * S2];
+        GridRow rows[S2 * S2];
 #pragma unroll
         for (int j = 0; j < S2 * S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j % S2 - H, z + j / S2 - H, H);
 #pragma unroll
@@ -104,7 +67,7 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
     } else {
         // one plane of rows at a time, the window within r first
         for (int dz = -RAD; dz <= RAD; ++dz) {
-            Row rows[2 * RAD + 1];
+            GridRow rows[2 * RAD + 1];
 #pragma unroll
             for (int j = 0; j < 2 * RAD + 1; ++j) rows[j] = load_row(bm, wr, g, x, y + j - RAD, z + dz, RAD);
 #pragma unroll
@@ -113,7 +76,7 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
         }
         const uint32_t n_r = n - HDR;
         for (int dz = -H; dz <= H; ++dz) {
-            Row rows[S2];
+            GridRow rows[S2];
 #pragma unroll
             for (int j = 0; j < S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j - H, z + dz, H);
 #pragma unroll
@@ -134,7 +97,7 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
 }  // namespace
 
 hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s) {
-    Dims g;
+    GridDims g;
     for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
     const unsigned blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
     const int32_t* nvox = at<int32_t>(ws, L.nvox);

@@ -291,6 +291,50 @@ __device__ __forceinline__ int32_t slot_of(const uint64_t* bm, const uint32_t* w
     return (int32_t)(wr[lin >> 6] + __popcll(w & (bit - 1)));
 }
 
+struct GridDims {
+    int32_t D[3];
+};
+
+// One grid-row segment of a cloud's occupancy: the slot of the first occupied
+// voxel at or after the segment's start, and bit j set when voxel x - h + j
+// of the segment is occupied (clear outside the grid).
+struct GridRow {
+    uint32_t first;
+    uint32_t mask;
+};
+
+// The segment x' in [x - h, x + h] of grid row (yy, zz), h <= 15. Branch-free:
+// rows outside the grid are clamped into it for the loads and get an empty
+// mask, and the second word is always loaded (the same word unless the
+// segment crosses a word boundary), so the loads of many rows are in flight
+// together.
+__device__ __forceinline__ GridRow load_row(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
+                                            const GridDims& g, int32_t x, int32_t yy, int32_t zz, int32_t h) {
+    const bool inside = yy >= 0 && yy < g.D[1] && zz >= 0 && zz < g.D[2];
+    const int32_t yc = yy < 0 ? 0 : (yy >= g.D[1] ? g.D[1] - 1 : yy);
+    const int32_t zc = zz < 0 ? 0 : (zz >= g.D[2] ? g.D[2] - 1 : zz);
+    const int32_t xs = x - h;
+    const int32_t lo_x = xs < 0 ? 0 : xs;
+    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
+    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
+    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
+    const uint32_t w0 = lo >> 6, o = lo & 63;
+    const uint64_t a = bm[w0];
+    const uint64_t c = bm[hi >> 6];
+    // when both ends share a word, the bits shifted in from c lie above the segment
+    const uint64_t bits = (a >> o) | (o ? c << (64 - o) : 0ull);
+    GridRow r;
+    r.mask = inside ? (uint32_t)(bits & ((1ull << (hi_x - lo_x + 1)) - 1)) << (lo_x - xs) : 0u;
+    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
+    return r;
+}
+
+__device__ __forceinline__ void decode_lin(uint32_t lin, const GridDims& g, int32_t& x, int32_t& y, int32_t& z) {
+    x = (int32_t)(lin % (uint32_t)g.D[0]);
+    y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
+    z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
+}
+
 // Calls f(slot) for every occupied voxel within Chebyshev distance `rad` of
 // grid cell (x, y, z), in ascending linear id, one occupancy word per grid
 // row segment; stops early (returning false) when f returns false.

@@ -351,54 +351,12 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_mb_final(int32_t B, const 
     if (threadIdx.x == 0) thr[b] = sel_pack(st.bound, st.need);
 }
 
-struct GridDims {
-    int32_t D[3];
-};
-
-__device__ __forceinline__ void decode(uint32_t lin, const GridDims& g, int32_t* x, int32_t* y, int32_t* z) {
-    *x = (int32_t)(lin % (uint32_t)g.D[0]);
-    *y = (int32_t)((lin / (uint32_t)g.D[0]) % (uint32_t)g.D[1]);
-    *z = (int32_t)(lin / ((uint32_t)g.D[0] * (uint32_t)g.D[1]));
-}
-
-// Occupancy of the grid-row segment x' in [x - h, x + h] at (yy, zz): bit j of
-// `mask` stands for x' = x - h + j (0 outside the grid); `first` is the slot
-// of the first occupied voxel at or after the segment's start, so bit j's
-// slot is first + popcount(mask below bit j). Branch-free: rows outside the
-// grid are clamped into it for the loads and get an empty mask, so the loads
-// of all rows of a window are issued together.
-struct RowDesc {
-    uint32_t first;
-    uint32_t mask;
-};
-
-__device__ __forceinline__ RowDesc row_desc(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
-                                            const GridDims& g, int32_t x, int32_t yy, int32_t zz, int32_t h) {
-    const bool inside = yy >= 0 && yy < g.D[1] && zz >= 0 && zz < g.D[2];
-    const int32_t yc = yy < 0 ? 0 : (yy >= g.D[1] ? g.D[1] - 1 : yy);
-    const int32_t zc = zz < 0 ? 0 : (zz >= g.D[2] ? g.D[2] - 1 : zz);
-    const int32_t xs = x - h;
-    const int32_t lo_x = xs < 0 ? 0 : xs;
-    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
-    const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
-    const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
-    const uint32_t w0 = lo >> 6, w1 = hi >> 6, o = lo & 63;
-    const uint64_t a = bm[w0];
-    const uint64_t c = bm[w1];  // the same word unless the segment crosses a word boundary (then o > 0)
-    const uint64_t bits = (a >> o) | (w1 != w0 ? c << (64 - o) : 0ull);
-    const uint32_t width = hi - lo + 1;
-    RowDesc r;
-    r.mask = inside ? (uint32_t)(bits & ((1ull << width) - 1)) << (lo_x - xs) : 0u;
-    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
-    return r;
-}
-
 // Slot of bit j of a row, or `self` when bit j is clear (a harmless address).
-__device__ __forceinline__ uint32_t row_slot_or(const RowDesc& r, int j, uint32_t self) {
+__device__ __forceinline__ uint32_t row_slot_or(const GridRow& r, int j, uint32_t self) {
     return ((r.mask >> j) & 1u) ? r.first + (uint32_t)__popc(r.mask & ((1u << j) - 1)) : self;
 }
 
-__device__ __forceinline__ uint32_t row_slot(const RowDesc& r, int j) {
+__device__ __forceinline__ uint32_t row_slot(const GridRow& r, int j) {
     return r.first + (uint32_t)__popc(r.mask & ((1u << j) - 1));
 }
 
@@ -545,12 +503,12 @@ __global__ __launch_bounds__(256) void k_cas_score(
                 const uint64_t* bm = bitmap + (size_t)b * W;
                 const uint32_t* wr = word_rank + (size_t)b * W;
                 int32_t x, y, z;
-                decode(lin, g, &x, &y, &z);
+                decode_lin(lin, g, x, y, z);
                 constexpr int S = 2 * RAD + 1;
-                RowDesc rows[S * S];
+                GridRow rows[S * S];
 #pragma unroll
                 for (int j = 0; j < S * S; ++j)
-                    rows[j] = row_desc(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
+                    rows[j] = load_row(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
                 // every coverage count of the window loaded at once, then masked
                 uint32_t c[S * S * S];
 #pragma unroll
@@ -649,15 +607,15 @@ __global__ __launch_bounds__(256) void k_cas_pick(
                             if (found < 0 && kk[j] > my) found = (int32_t)u4(q[j / 4], j % 4);
                     }
                 } else {
-                    decode(vox_lin[gid], g, &x, &y, &z);
+                    decode_lin(vox_lin[gid], g, x, y, z);
                     // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
                     // row descriptors, then all keys are loaded before comparing (a
                     // clear bit loads the voxel's own key, which never beats it)
                     for (int p = 0; p < S2 && found < 0; ++p) {
                         const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
-                        RowDesc rows[S2];
+                        GridRow rows[S2];
 #pragma unroll
-                        for (int j = 0; j < S2; ++j) rows[j] = row_desc(bm, wr, g, x, y + j - H, z + dz, H);
+                        for (int j = 0; j < S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j - H, z + dz, H);
                         uint32_t sl[S2 * S2];
                         uint64_t kk[S2 * S2];
 #pragma unroll
@@ -730,7 +688,7 @@ __global__ __launch_bounds__(256) void k_cas_pick(
             const uint32_t* wwr = word_rank + (size_t)wb * W;
             for (int j = lane_id(); j < S2 * S2; j += kWave) {
                 const int dy = j % S2 - H, dz = j / S2 - H;
-                const RowDesc r = row_desc(wbm, wwr, g, wx, wy + dy, wz + dz, H);
+                const GridRow r = load_row(wbm, wwr, g, wx, wy + dy, wz + dz, H);
                 const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
 #pragma unroll
                 for (int q = 0; q < S2; ++q) {
