@@ -61,8 +61,11 @@ def lib():
         L.orc_sample_cas_swap.argtypes = [C.POINTER(_Table), C.c_int32, C.c_uint64, C.c_uint32, P, P, P, P]
         L.orc_query.argtypes = [C.POINTER(_Table), P, P, P, P, C.c_int32, C.c_int32,
                                 C.c_int32, C.c_uint64, P, P, P, P, P, P]
+        L.orc_query_points.argtypes = [C.POINTER(_Table), P, P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64,
+                                       P, P, P, P, P]
+        L.orc_context_list.argtypes = [C.POINTER(_Table), P, C.c_int32, P, P, C.c_int64]
         for f in ("orc_voxelize", "orc_build_table", "orc_sample_rvs", "orc_sample_cas", "orc_sample_cas_swap",
-                  "orc_query"):
+                  "orc_query", "orc_query_points", "orc_context_list"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -187,6 +190,39 @@ class Table:
                                _ptr(out["n_valid"]), _ptr(out["center_xyz"]), _ptr(out["center_w"]),
                                _ptr(out["ctx_count"])), "orc_query")
         return out
+
+    def query_points(self, centers: np.ndarray, K: int, mode: str, seed: int,
+                     points: Optional[np.ndarray] = None, allow_nonfinite: bool = False) -> Dict[str, np.ndarray]:
+        """Upsampling query: K nodes around given center points [B][M][3]."""
+        P = self.points if points is None else np.ascontiguousarray(points, np.float32)
+        Q = np.ascontiguousarray(centers, np.float32)
+        B, M = Q.shape[:2]
+        out = dict(
+            node_idx=np.zeros((B, M, K), np.int32),
+            node_xyz=np.zeros((B, M, K, 3), np.float32),
+            n_valid=np.zeros((B, M), np.int32),
+            ctx_count=np.zeros((B, M), np.int32),
+            center_lin=np.zeros((B, M), np.int32),
+        )
+        m = {"cube": 0, "knn": 1}[mode]
+        rc = lib().orc_query_points(C.byref(self._t), _ptr(P), _ptr(Q), M, K, m, C.c_uint64(seed),
+                                    _ptr(out["node_idx"]), _ptr(out["node_xyz"]), _ptr(out["n_valid"]),
+                                    _ptr(out["ctx_count"]), _ptr(out["center_lin"]))
+        if not (allow_nonfinite and rc == -4):
+            _check(rc, "orc_query_points")
+        return out
+
+    def context_list(self, center_lin: np.ndarray):
+        """Context lists of center voxels [B][M]: (ctx_off [B*M+1] int64,
+        ctx_idx [total] int32)."""
+        cl = np.ascontiguousarray(center_lin, np.int32)
+        B, M = cl.shape
+        off = np.zeros(B * M + 1, np.int64)
+        _check(lib().orc_context_list(C.byref(self._t), _ptr(cl), M, _ptr(off), None, 0), "orc_context_list")
+        idx = np.zeros(max(int(off[-1]), 1), np.int32)
+        _check(lib().orc_context_list(C.byref(self._t), _ptr(cl), M, _ptr(off), _ptr(idx), int(off[-1])),
+               "orc_context_list")
+        return off, idx[: int(off[-1])]
 
 
 def run_layer(points: np.ndarray, layer, weights: Optional[np.ndarray] = None):

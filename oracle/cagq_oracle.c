@@ -49,6 +49,14 @@
  *   center    Appendix E, Eqs. 7-8: w_c = sum w_j, chi_c = sum w_j chi_j /
  *             w_c over the n valid nodes. Reading: the fp32 sum is pairwise
  *             in node order (stride 1, 2, 4, ...), then one fp32 divide.
+ *   upsample  Sec. 3.1: centers given from outside, only nodes queried.
+ *             Reading: a center point's voxel v by the voxelize rule (v need
+ *             not be occupied); context and cube key as for query; the k-NN
+ *             reference is the center point itself; an empty context gives
+ *             n = 0 and index -1 in every slot.
+ *   context   Sec. 3.3, grid context pooling: every context point of a
+ *             center. Reading: voxels of pi(v) in ascending lin, stored
+ *             points ascending, concatenated over the batch (CSR offsets).
  *   h         splitmix64 chain: h(seed, tag, a1..ak) =
  *             sm64(...sm64(sm64(seed ^ tag) ^ a1)... ^ ak), tags RVS=1,
  *             CUBE=2, CAS-P=3 (splitmix64: Steele, Lea, Flood, OOPSLA 2014).
@@ -63,7 +71,10 @@
  * incumbent sets), slot draws vs an independent hash, no swap among
  * isolated voxels, hand-worked examples; k-NN vs brute force and vs
  * global k-NN when the cap never binds; cube subset / frequency checks;
- * centers vs closed forms and an fp64 error bound.
+ * centers vs closed forms and an fp64 error bound; upsampling k-NN vs a
+ * numpy brute force over the block around each center point, and vs
+ * global k-NN; context lists vs a numpy enumeration of the block's stored
+ * points.
  */
 #include "cagq_oracle.h"
 
@@ -73,6 +84,7 @@
 
 #define ORC_EINVAL (-1)
 #define ORC_ENONFINITE (-4)
+#define ORC_ECAPACITY (-5)
 #define ORC_ENOTOCC (-7)
 
 uint64_t orc_splitmix64(uint64_t x) {
@@ -503,5 +515,122 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
     free(nbs);
     free(key);
     free(term);
+    return rc;
+}
+
+/* Upsampling query (Sec. 3.1: in the upsampling layers the centers arrive
+ * through long-range connections and CAGQ only queries their node points).
+ * Each given center point falls into voxel v by the voxelize rule (v need
+ * not be occupied); its context is the stored points of pi(v); the min(K, c)
+ * context points of smallest key are kept. Cube key as for orc_query (it
+ * depends on v only); k-NN key bits(d^2) << 32 | i with d measured from the
+ * center point itself. An empty context gives n = 0 and every slot -1 (xyz
+ * 0); otherwise slots k >= n repeat slot 0.
+ *   centers [B][M][3]; center_lin [B][M] (may be NULL) receives lin(v). */
+int orc_query_points(const orc_table* t, const float* pts, const float* centers, int32_t M, int32_t K,
+                     int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz, int32_t* n_valid,
+                     int32_t* ctx_count, int32_t* center_lin) {
+    if (!table_ok(t) || !pts || !centers || M < 1 || K < 1) return ORC_EINVAL;
+    if (mode != 0 && mode != 1) return ORC_EINVAL;
+    if (!node_idx || !n_valid) return ORC_EINVAL;
+    int32_t rad = t->g.radius;
+    int32_t side = 2 * rad + 1;
+    int32_t lambda = side * side * side;
+    int32_t* nbs = (int32_t*)malloc(sizeof(int32_t) * (size_t)lambda);
+    uint64_t* key = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)lambda * (size_t)t->g.n_v);
+    if (!nbs || !key) { free(nbs); free(key); return ORC_EINVAL; }
+    int rc = 0;
+    for (int32_t b = 0; b < t->B; ++b) {
+        const float* P = pts + (size_t)b * t->N * 3;
+        const uint32_t* vo = t->vox_off + (size_t)b * (t->N + 1);
+        const uint32_t* pl = t->pt_list + (size_t)b * t->N;
+        uint64_t hb = orc_splitmix64(orc_splitmix64(seed ^ 2ull) ^ (uint64_t)b);
+        for (int32_t j = 0; j < M; ++j) {
+            size_t cj = (size_t)b * M + j;
+            const float* q = centers + cj * 3;
+            uint32_t l;
+            int vr = orc_voxelize(q, 1, &t->g, &l);
+            if (vr != 0) rc = vr;
+            if (center_lin) center_lin[cj] = (int32_t)l;
+            /* context points: the stored lists of every voxel of pi(v) */
+            int32_t nn = neighbours(t, b, l, rad, nbs);
+            int32_t c = 0;
+            for (int32_t e = 0; e < nn; ++e)
+                for (uint32_t u = vo[nbs[e]]; u < vo[nbs[e] + 1]; ++u) key[c++] = pl[u];
+            if (mode == 0) {
+                uint64_t hc = orc_splitmix64(hb ^ (uint64_t)l);
+                for (int32_t e = 0; e < c; ++e) {
+                    uint64_t i = key[e];
+                    uint64_t h = orc_splitmix64(hc ^ i);
+                    key[e] = ((h >> 32) << 32) | i;
+                }
+            } else {
+                for (int32_t e = 0; e < c; ++e) {
+                    uint64_t i = key[e];
+                    float dx = P[3 * i + 0] - q[0];
+                    float dy = P[3 * i + 1] - q[1];
+                    float dz = P[3 * i + 2] - q[2];
+                    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+                    float sxy = xx + yy;
+                    float d2 = sxy + zz;
+                    key[e] = ((uint64_t)float_bits(d2) << 32) | i;
+                }
+            }
+            qsort(key, (size_t)c, sizeof(uint64_t), cmp_u64);
+            int32_t n = c < K ? c : K;
+            int32_t* ni = node_idx + cj * K;
+            for (int32_t k = 0; k < K; ++k) ni[k] = n ? (int32_t)(key[k < n ? k : 0] & 0xFFFFFFFFu) : -1;
+            if (node_xyz)
+                for (int32_t k = 0; k < K; ++k)
+                    for (int a = 0; a < 3; ++a)
+                        node_xyz[(cj * K + k) * 3 + a] = n ? P[3 * (size_t)ni[k] + a] : 0.0f;
+            n_valid[cj] = n;
+            if (ctx_count) ctx_count[cj] = c;
+        }
+    }
+    free(nbs);
+    free(key);
+    return rc;
+}
+
+/* Context lists for grid context pooling (Sec. 3.3: the context feature is
+ * pooled over every context point of a group, the points CAGQ already
+ * associated with the center voxel). Per center voxel v (any voxel of the
+ * grid, occupied or not): the stored points of the occupied voxels of
+ * pi(v), voxels in ascending lin, each voxel's stored points ascending.
+ *   ctx_off [B*M + 1]: ctx_off[b*M + j] = number of context points of the
+ *   centers before (b, j) in batch order; ctx_off[B*M] = the total.
+ *   ctx_idx [capacity] (may be NULL): the lists, concatenated in the same
+ *   order; entries past capacity are not written (returns -5 then).
+ * A lin outside the grid gets an empty list and returns -7. */
+int orc_context_list(const orc_table* t, const int32_t* center_lin, int32_t M, int64_t* ctx_off,
+                     int32_t* ctx_idx, int64_t capacity) {
+    if (!table_ok(t) || !center_lin || M < 1 || !ctx_off || capacity < 0) return ORC_EINVAL;
+    int32_t rad = t->g.radius;
+    int32_t side = 2 * rad + 1;
+    int32_t* nbs = (int32_t*)malloc(sizeof(int32_t) * (size_t)(side * side * side));
+    if (!nbs) return ORC_EINVAL;
+    const int64_t V = (int64_t)t->g.dims[0] * t->g.dims[1] * t->g.dims[2];
+    int rc = 0;
+    int64_t total = 0;
+    for (int32_t b = 0; b < t->B; ++b) {
+        const uint32_t* vo = t->vox_off + (size_t)b * (t->N + 1);
+        const uint32_t* pl = t->pt_list + (size_t)b * t->N;
+        for (int32_t j = 0; j < M; ++j) {
+            size_t cj = (size_t)b * M + j;
+            ctx_off[cj] = total;
+            int32_t l = center_lin[cj];
+            if (l < 0 || (int64_t)l >= V) { rc = ORC_ENOTOCC; continue; }
+            int32_t nn = neighbours(t, b, (uint32_t)l, rad, nbs);
+            for (int32_t e = 0; e < nn; ++e)
+                for (uint32_t u = vo[nbs[e]]; u < vo[nbs[e] + 1]; ++u) {
+                    if (ctx_idx && total < capacity) ctx_idx[total] = (int32_t)pl[u];
+                    ++total;
+                }
+        }
+    }
+    ctx_off[(size_t)t->B * M] = total;
+    free(nbs);
+    if (rc == 0 && ctx_idx && total > capacity) rc = ORC_ECAPACITY;
     return rc;
 }

@@ -10,7 +10,8 @@
  *
  * All pointers are host pointers. Shapes are row-major. Every function
  * returns 0 on success or a negative code:
- *   -1 invalid argument, -4 non-finite coordinate, -7 center voxel not occupied.
+ *   -1 invalid argument, -4 non-finite coordinate, -5 output capacity
+ *   exceeded, -7 center voxel not occupied (or outside the grid).
  *
  * Parity pins (what each function is checked against, beyond itself) are
  * listed in the header comment of cagq_oracle.c.
@@ -79,6 +80,20 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
               int32_t mode, uint64_t seed,
               int32_t* node_idx, float* node_xyz, int32_t* n_valid,
               float* center_xyz, uint32_t* center_w, int32_t* ctx_count);
+
+/* Upsampling query (Sec. 3.1): node points around given center points
+ * [B][M][3]; k-NN distances from the center point; an empty context gives
+ * n_valid 0 and -1 in every node slot. ctx_count, center_lin [B][M] and
+ * node_xyz may be NULL. */
+int orc_query_points(const orc_table* t, const float* pts, const float* centers, int32_t M, int32_t K,
+                     int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz, int32_t* n_valid,
+                     int32_t* ctx_count, int32_t* center_lin);
+
+/* Context lists (Sec. 3.3, grid context pooling): ctx_off [B*M + 1] CSR
+ * offsets over the batch, ctx_idx [capacity] (may be NULL) the point
+ * indices, per center the voxels of pi(v) in ascending lin. */
+int orc_context_list(const orc_table* t, const int32_t* center_lin, int32_t M, int64_t* ctx_off,
+                     int32_t* ctx_idx, int64_t capacity);
 
 #ifdef __cplusplus
 }

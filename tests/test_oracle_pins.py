@@ -554,3 +554,164 @@ def test_query_rejects_unoccupied_center():
     empty = next(l for l in range(6 * 6 * 3) if l not in occupied)
     with pytest.raises(oracle.OracleError, match="-7"):
         t.query(np.array([[empty]], np.int32), np.array([1], np.int32), 4, "cube", 0)
+
+
+# ---------------------------------------------------------------- upsampling query
+
+def _upsampling_centers(P, gs, n, seed):
+    """Center points of three kinds: points of the cloud, uniform points in
+    the grid's box, and points just outside it (clamped onto border voxels)."""
+    rng = np.random.default_rng(seed)
+    lo = np.asarray(gs.origin, np.float64)
+    hi = lo + np.asarray(gs.voxel_size, np.float64) * np.asarray(gs.dims)
+    own = P[rng.integers(0, P.shape[0], n // 3)]
+    box = rng.uniform(lo, hi, (n // 3, 3))
+    out = rng.uniform(lo - 0.3, hi + 0.3, (n - 2 * (n // 3), 3))
+    return np.concatenate([own, box, out]).astype(np.float32)
+
+
+@pytest.mark.parametrize("n_v", [32, 3])
+def test_query_points_knn_matches_bruteforce(n_v):
+    """Sec. 3.1 upsampling: the nodes of a given center point are its K
+    nearest stored points of the block around the voxel it falls in, the
+    distance measured from the point itself (numpy lexsort on (i, d^2) in
+    the same fp32 order); an empty block gives n = 0 and -1 everywhere."""
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.make_grid(gs.origin, gs.voxel_size, gs.dims, n_v, 1)
+    t = oracle.Table(P, grid)
+    Q = _upsampling_centers(P[0], gs, 300, 3)[None]
+    K = 16
+    q = t.query_points(Q, K, "knn", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, n_v)
+    qlin = oracle.voxelize(Q, grid)[0]
+    empty = 0
+    for j in range(Q.shape[1]):
+        assert q["center_lin"][0, j] == qlin[j]
+        ctx = _context_bruteforce(P[0], lin, tb, int(qlin[j]), gs.dims, 1)
+        assert q["ctx_count"][0, j] == len(ctx)
+        d = P[0, ctx] - Q[0, j]
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        order = np.lexsort((ctx, d2.view(np.uint32)))
+        n = min(K, len(ctx))
+        assert q["n_valid"][0, j] == n
+        if n == 0:
+            empty += 1
+            assert np.all(q["node_idx"][0, j] == -1) and np.all(q["node_xyz"][0, j] == 0)
+            continue
+        assert list(q["node_idx"][0, j, :n]) == list(ctx[order[:n]])
+        assert np.all(q["node_idx"][0, j, n:] == q["node_idx"][0, j, 0])
+        assert np.array_equal(q["node_xyz"][0, j].view(np.uint32), P[0, q["node_idx"][0, j]].view(np.uint32))
+    assert 0 < empty < Q.shape[1] // 2
+
+
+def test_query_points_equals_global_knn_when_the_block_suffices():
+    """The block around a center point reaches at least r voxel edges past
+    it on every side: when the K-th nearest of all N points is closer than
+    that and the cap never binds, the upsampling k-NN is the ordinary k-NN."""
+    P = W.uniform_cube(1, 4000, 23)
+    size = 0.1
+    grid = oracle.make_grid((0, 0, 0), (size,) * 3, (10, 10, 10), 64, 1)
+    t = oracle.Table(P, grid)
+    assert t.vox_count.max() <= 64
+    Q = np.random.default_rng(8).random((1, 300, 3)).astype(np.float32)
+    K = 8
+    q = t.query_points(Q, K, "knn", 0)
+    checked = 0
+    for j in range(300):
+        d = np.sqrt(((P[0].astype(np.float64) - Q[0, j]) ** 2).sum(1))
+        order = np.argsort(d, kind="stable")
+        if d[order[K - 1]] < size - 1e-3 and d[order[K]] - d[order[K - 1]] > 1e-5:
+            assert set(q["node_idx"][0, j]) == set(order[:K])
+            checked += 1
+    assert checked > 100
+
+
+def test_query_points_cube_is_a_subset_of_the_block_and_depends_on_the_voxel():
+    """Cube Query around a given point: distinct context points, the whole
+    context when c <= K; two points in one voxel get the same nodes."""
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.grid_from_spec(gs)
+    t = oracle.Table(P, grid)
+    Q = _upsampling_centers(P[0], gs, 200, 4)[None]
+    Q2 = Q.copy()
+    # a second point in the same voxel: the lower corner's side of the first
+    g = pins.grid_coords_f64(Q[0], gs.origin, gs.voxel_size, gs.dims)
+    inner = np.all((Q[0] - gs.origin) / gs.voxel_size - g > 0.05, axis=1) & np.all(
+        (Q[0] - gs.origin) / gs.voxel_size - g < 0.95, axis=1)
+    Q2[0, inner] = (np.asarray(gs.origin) + (g[inner] + 0.5) * np.asarray(gs.voxel_size)).astype(np.float32)
+    K = 8
+    a = t.query_points(Q, K, "cube", 5)
+    b = t.query_points(Q2, K, "cube", 5)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, gs.n_v)
+    for j in range(200):
+        ctx = set(_context_bruteforce(P[0], lin, tb, int(a["center_lin"][0, j]), gs.dims, 1))
+        n = min(K, len(ctx))
+        got = list(a["node_idx"][0, j, :n])
+        assert len(set(got)) == n and set(got) <= ctx
+        if len(ctx) <= K:
+            assert set(got) == ctx
+        if inner[j]:
+            assert b["center_lin"][0, j] == a["center_lin"][0, j]
+            assert list(b["node_idx"][0, j]) == list(a["node_idx"][0, j])
+
+
+def test_query_points_nonfinite_center_is_an_error():
+    t = _small_table(0)
+    Q = np.array([[[np.nan, 0.1, 0.1]]], np.float32)
+    with pytest.raises(oracle.OracleError, match="-4"):
+        t.query_points(Q, 4, "knn", 0)
+    q = t.query_points(Q, 4, "knn", 0, allow_nonfinite=True)
+    assert q["center_lin"][0, 0] % t.grid.dims[0] == 0
+
+
+# ---------------------------------------------------------------- context lists
+
+@pytest.mark.parametrize("n_v", [32, 3])
+def test_context_list_matches_block_enumeration(n_v):
+    """Sec. 3.3 grid context pooling reads every context point: per center,
+    the stored points of the occupied voxels of the block, ordered by
+    (voxel lin, point index) -- a numpy enumeration over all points -- and
+    concatenated with CSR offsets over the batch. Unoccupied center voxels
+    have a context too."""
+    w = W.get_workload("room")
+    P = w.points(B=2)
+    gs = w.layers[0].grid
+    grid = oracle.make_grid(gs.origin, gs.voxel_size, gs.dims, n_v, 1)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(120, 6)
+    rng = np.random.default_rng(1)
+    V = int(np.prod(gs.dims))
+    cl = np.concatenate([cl, rng.integers(0, V, (2, 40)).astype(np.int32)], axis=1)
+    off, idx = t.context_list(cl)
+    assert off[0] == 0 and np.all(np.diff(off) >= 0) and off[-1] == len(idx)
+    M = cl.shape[1]
+    for b in range(2):
+        lin = oracle.voxelize(P[b], grid)
+        tb = pins.table_numpy(lin, n_v)
+        for j in range(M):
+            ctx = _context_bruteforce(P[b], lin, tb, int(cl[b, j]), gs.dims, 1)
+            ctx = ctx[np.lexsort((ctx, lin[ctx]))]
+            k = b * M + j
+            assert list(idx[off[k]:off[k + 1]]) == list(ctx)
+
+
+def test_context_list_counts_equal_the_query_context_counts():
+    w = W.get_workload("object")
+    L = w.layers[0]
+    t = oracle.Table(w.points()[:4], oracle.grid_from_spec(L.grid))
+    cl, mv = t.sample_rvs(L.M, 2)
+    q = t.query(cl, mv, L.K, "knn", 0)
+    off, _ = t.context_list(cl)
+    assert np.array_equal(np.diff(off).reshape(cl.shape), q["ctx_count"])
+
+
+def test_context_list_rejects_a_lin_outside_the_grid():
+    t = _small_table(0)
+    with pytest.raises(oracle.OracleError, match="-7"):
+        t.context_list(np.array([[6 * 6 * 3]], np.int32))
