@@ -154,6 +154,79 @@ def measure_cas_swap(P, P_np, B: int, N: int, L, with_oracle: bool, reps: int = 
     return row
 
 
+def _timed(fn, reps: int):
+    """Average ms of fn() over reps calls, HIP events on the current stream."""
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / reps
+
+
+def measure_upsampling(P, P_np, B: int, N: int, wl, with_oracle: bool, reps: int = 20) -> dict:
+    """The upsampling query (centers given: the N input points of each scene)
+    against the grid of the layer-1 centers, with the layer-2 grid spec and K,
+    and the context lists of the layer-1 centers on the layer-1 grid."""
+    import torch
+    from paper_1912_02984_amd import cagq
+    L0, L1 = wl.layers[0], wl.layers[1]
+    # the coarse points: the layer-1 group centers of the same batch
+    g0 = cagq.build_grid(P, cagq.desc_from_spec(L0.grid))
+    cl0, _ = cagq.sample_centers(g0, L0.M, L0.sample, L0.seed)
+    q0 = cagq.query_context(g0, cl0, L0.K, L0.query, L0.seed)
+    coarse = q0["center_xyz"].contiguous()
+    g1 = cagq.build_grid(coarse, cagq.desc_from_spec(L1.grid))
+    out = cagq.query_points(g1, P, L1.K, "knn", 1)
+    ms = _timed(lambda: cagq.query_points(g1, P, L1.K, "knn", 1, out=out), reps)
+    ctx = int(out["ctx_count"].sum().item())
+    M = B * N
+    # algorithmic bytes: center xyz in; per node index and xyz out; n_valid,
+    # ctx_count and lin out; the context points' xyz + index (16 B each)
+    alg = M * (12 + 16 * L1.K + 12) + 16 * ctx
+    up = {"workload": f"B={B} x {N} centers (the input points) on the grid of the {L0.M} layer-1 centers, "
+                      f"{tuple(L1.grid.dims)} voxels of {L1.grid.voxel_size[0]:.2f} m, K={L1.K}, k-NN",
+          "ms": round(ms, 4), "centers_per_s": round(M / (ms / 1e3), 1),
+          "roofline": {"bound": "hbm", "achieved": round(alg / (ms / 1e3) / 1e9, 1), "peak": 8000.0,
+                       "unit": "GB/s", "frac": round(alg / (ms / 1e3) / 1e9 / 8000.0, 4), "traffic": None}}
+    # context lists of the layer-1 centers
+    off = cagq.context_offsets(g0, cl0)
+    idx = cagq.context_list(g0, cl0, off)
+    total = int(off[-1].item())
+
+    def ctx_once():
+        cagq.context_offsets(g0, cl0, out=off)
+        cagq.context_list(g0, cl0, off, out=idx, capacity=total)
+    ms_c = _timed(ctx_once, reps)
+    alg_c = 8 * total + B * L0.M * (4 + 8)
+    cx = {"workload": f"B={B} x {L0.M} layer-1 centers, {tuple(L0.grid.dims)} voxels, r={L0.grid.radius}: "
+                      f"{total} context entries",
+          "ms": round(ms_c, 4), "entries_per_s": round(total / (ms_c / 1e3), 1),
+          "roofline": {"bound": "hbm", "achieved": round(alg_c / (ms_c / 1e3) / 1e9, 1), "peak": 8000.0,
+                       "unit": "GB/s", "frac": round(alg_c / (ms_c / 1e3) / 1e9 / 8000.0, 4), "traffic": None}}
+    if with_oracle:
+        import oracle
+        t0 = time.perf_counter()
+        ot0 = oracle.Table(P_np[:1], oracle.grid_from_spec(L0.grid))
+        ocl, omv = ot0.sample(L0.M, L0.sample, L0.seed)
+        oq = ot0.query(ocl, omv, L0.K, L0.query, L0.seed)
+        t1 = time.perf_counter()
+        ot1 = oracle.Table(oq["center_xyz"], oracle.grid_from_spec(L1.grid))
+        ot1.query_points(P_np[:1], L1.K, "knn", 1)
+        t2 = time.perf_counter()
+        _, oidx = ot0.context_list(ocl)
+        t3 = time.perf_counter()
+        up["oracle"] = {"ms": round((t2 - t1) * 1e3, 2), "centers_per_s": round(N / (t2 - t1), 1), "cores": 1,
+                        "sample": "1 of the scenes, coarse table build included"}
+        cx["oracle"] = {"ms": round((t3 - t2) * 1e3, 2), "entries_per_s": round(len(oidx) / (t3 - t2), 1),
+                        "cores": 1, "sample": "1 of the scenes"}
+    return {"query_points": up, "context_list": cx}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -310,6 +383,7 @@ def main():
     next_rows = None
     if not args.no_next:
         next_rows = {"cas_swap": measure_cas_swap(P, P_np, B, N, wls[0].layers[0], with_oracle=not args.no_cpu_baseline)}
+        next_rows.update(measure_upsampling(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline))
 
     cpu = None
     if not args.no_cpu_baseline:

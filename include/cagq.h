@@ -49,9 +49,9 @@ extern "C" {
 #define CAGQ_ERR_GRID_TOO_LARGE (-2)    /* D_x*D_y*D_z > 2^31-1 */
 #define CAGQ_ERR_WORKSPACE_TOO_SMALL (-3)
 #define CAGQ_ERR_NONFINITE_INPUT (-4)   /* device-side: a NaN/Inf coordinate */
-#define CAGQ_ERR_CAPACITY (-5)          /* device-side: an internal table overflowed */
+#define CAGQ_ERR_CAPACITY (-5)          /* device-side: an internal table or an output overflowed */
 #define CAGQ_ERR_HIP (-6)               /* a HIP runtime call failed */
-#define CAGQ_ERR_CENTER_NOT_OCCUPIED (-7) /* device-side: a query center is not in O_v */
+#define CAGQ_ERR_CENTER_NOT_OCCUPIED (-7) /* device-side: a query center is not in O_v (or not in the grid) */
 
 #define CAGQ_SAMPLE_RVS 0   /* Random Voxel Sampling (Sec. 3.2) */
 #define CAGQ_SAMPLE_CAS 1   /* Coverage-Aware Sampling, greedy (Sec. 3.2, Eqs. 1-2) */
@@ -202,6 +202,56 @@ CAGQ_API int cagq_query_context(const cagq_grid* g, const uint32_t* weights, con
                        int32_t* node_idx, float* node_xyz, int32_t* n_valid,
                        float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
                        void* stream);
+
+/*
+ * Upsampling query (Sec. 3.1: in the upsampling layers the group centers
+ * arrive through long-range connections, and CAGQ only queries their node
+ * points). Center point q falls into voxel v by the voxelize rule of
+ * cagq_grid_desc; v need not be occupied. The context is the stored points
+ * of the occupied voxels of pi(v), c points; the n = min(K, c) of smallest
+ * 64-bit key are kept in ascending key order:
+ *   CAGQ_QUERY_CUBE: key = (hi32(h(seed,2,b,lin(v),i)) << 32) | i, as in
+ *                    cagq_query_context (it depends on v only)
+ *   CAGQ_QUERY_KNN:  key = (bits(d2) << 32) | i, d2 = (dx*dx + dy*dy) + dz*dz
+ *                    in fp32 with d = p_i - q, the center point itself
+ * Node slots k >= n repeat slot 0; an empty context (c = 0) gives n = 0, -1
+ * in every node slot and zero coordinates. No group center is formed.
+ *   centers     device float [B][M][3]
+ *   node_idx    device int32 [B][M][K]
+ *   node_xyz    device float [B][M][K][3] or NULL; bit copies of the points
+ *   n_valid     device int32 [B][M]
+ *   ctx_count   device int32 [B][M] or NULL; c
+ *   center_lin  device int32 [B][M] or NULL; lin(v), for cagq_context_*
+ * 1 <= K <= CAGQ_MAX_K. A non-finite center coordinate maps to voxel 0 on
+ * that axis and raises CAGQ_ERR_NONFINITE_INPUT in the device status.
+ */
+CAGQ_API int cagq_query_points(const cagq_grid* g, const float* centers, int32_t M, int32_t K, int32_t mode,
+                               uint64_t seed, int32_t* node_idx, float* node_xyz, int32_t* n_valid,
+                               int32_t* ctx_count, int32_t* center_lin, void* stream);
+
+/*
+ * Context lists for grid context pooling (Sec. 3.3: a group's context
+ * feature is pooled over all of its context points, which CAGQ has already
+ * associated with the center voxel). The context of center voxel v (any
+ * voxel of the grid, occupied or not) is the stored points of the occupied
+ * voxels of pi(v), voxels in ascending lin, each voxel's stored points in
+ * ascending index. Two calls:
+ *   cagq_context_offsets writes ctx_off, device int64 [B*M + 1]:
+ *     ctx_off[b*M + j] = the number of context points of all centers before
+ *     (b, j) in batch order, ctx_off[B*M] = the total T.
+ *   cagq_context_list writes ctx_idx, device int32 [capacity]: entries
+ *     [ctx_off[b*M+j], ctx_off[b*M+j+1]) hold the context of center (b, j)
+ *     as point indices 0..N-1 of cloud b. ctx_off must hold the offsets of
+ *     the same centers (enqueued before on the stream). Entries at or past
+ *     `capacity` are not written; then CAGQ_ERR_CAPACITY is raised in the
+ *     device status. Read ctx_off[B*M] to size ctx_idx.
+ *   center_lin  device int32 [B][M]; a lin outside [0, D_x*D_y*D_z) gets an
+ *               empty context and raises CAGQ_ERR_CENTER_NOT_OCCUPIED.
+ */
+CAGQ_API int cagq_context_offsets(const cagq_grid* g, const int32_t* center_lin, int32_t M, int64_t* ctx_off,
+                                  void* stream);
+CAGQ_API int cagq_context_list(const cagq_grid* g, const int32_t* center_lin, int32_t M, const int64_t* ctx_off,
+                               int32_t* ctx_idx, int64_t capacity, void* stream);
 
 /* Synchronises `stream` and returns the first device-side error recorded in
  * g's workspace since it was last built (CAGQ_OK if none). */

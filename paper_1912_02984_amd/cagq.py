@@ -72,11 +72,16 @@ def lib() -> C.CDLL:
                                           P, P, P]
         L.cagq_query_context.argtypes = [C.POINTER(GridC), P, P, C.c_int32, C.c_int32, C.c_int32,
                                          C.c_uint64, P, P, P, P, P, P, P]
+        L.cagq_query_points.argtypes = [C.POINTER(GridC), P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64,
+                                        P, P, P, P, P, P]
+        L.cagq_context_offsets.argtypes = [C.POINTER(GridC), P, C.c_int32, P, P]
+        L.cagq_context_list.argtypes = [C.POINTER(GridC), P, C.c_int32, P, P, C.c_int64, P]
         L.cagq_get_device_status.argtypes = [C.POINTER(GridC), P]
         L.cagq_status_string.argtypes = [C.c_int]
         L.cagq_status_string.restype = C.c_char_p
         for f in ("cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
-                  "cagq_query_context", "cagq_get_device_status"):
+                  "cagq_query_context", "cagq_query_points", "cagq_context_offsets", "cagq_context_list",
+                  "cagq_get_device_status"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -227,6 +232,61 @@ def query_context(grid: Grid, center_lin: torch.Tensor, K: int, mode: str, seed:
         C.byref(grid.rec), _ptr(weights), _ptr(center_lin), M, K, QUERY[mode], C.c_uint64(seed & (2**64 - 1)),
         _ptr(out["node_idx"]), _ptr(out.get("node_xyz")), _ptr(out["n_valid"]), _ptr(out["center_xyz"]),
         _ptr(out["center_w"]), _ptr(out.get("ctx_count")), _stream_ptr(stream)), "cagq_query_context")
+    return out
+
+
+def query_points(grid: Grid, centers: torch.Tensor, K: int, mode: str, seed: int,
+                 out: Optional[Dict[str, torch.Tensor]] = None, want_xyz: bool = True,
+                 stream: Optional[torch.cuda.Stream] = None) -> Dict[str, torch.Tensor]:
+    """Upsampling query: K node points around given center points [B, M, 3]
+    (cagq_query_points). Also returns ctx_count and each center's voxel lin."""
+    B, M = int(centers.shape[0]), int(centers.shape[1])
+    _need(centers, torch.float32, (B, M, 3), "centers")
+    dev = grid.points.device
+    if out is None:
+        out = dict(
+            node_idx=torch.empty((B, M, K), dtype=torch.int32, device=dev),
+            node_xyz=torch.empty((B, M, K, 3), dtype=torch.float32, device=dev) if want_xyz else None,
+            n_valid=torch.empty((B, M), dtype=torch.int32, device=dev),
+            ctx_count=torch.empty((B, M), dtype=torch.int32, device=dev),
+            center_lin=torch.empty((B, M), dtype=torch.int32, device=dev),
+        )
+    _check(lib().cagq_query_points(
+        C.byref(grid.rec), _ptr(centers), M, K, QUERY[mode], C.c_uint64(seed & (2**64 - 1)),
+        _ptr(out["node_idx"]), _ptr(out.get("node_xyz")), _ptr(out["n_valid"]), _ptr(out.get("ctx_count")),
+        _ptr(out.get("center_lin")), _stream_ptr(stream)), "cagq_query_points")
+    return out
+
+
+def context_offsets(grid: Grid, center_lin: torch.Tensor, out: Optional[torch.Tensor] = None,
+                    stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """CSR offsets [B*M + 1] (int64) of the centers' context lists."""
+    B, M = int(center_lin.shape[0]), int(center_lin.shape[1])
+    _need(center_lin, torch.int32, (B, M), "center_lin")
+    if out is None:
+        out = torch.empty(B * M + 1, dtype=torch.int64, device=grid.points.device)
+    _need(out, torch.int64, (B * M + 1,), "ctx_off")
+    _check(lib().cagq_context_offsets(C.byref(grid.rec), _ptr(center_lin), M, _ptr(out), _stream_ptr(stream)),
+           "cagq_context_offsets")
+    return out
+
+
+def context_list(grid: Grid, center_lin: torch.Tensor, ctx_off: torch.Tensor,
+                 out: Optional[torch.Tensor] = None, capacity: Optional[int] = None,
+                 stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """The context lists (int32 point indices) laid out by ``ctx_off``. Without
+    ``out`` the total is read back from ``ctx_off`` to size it."""
+    B, M = int(center_lin.shape[0]), int(center_lin.shape[1])
+    _need(center_lin, torch.int32, (B, M), "center_lin")
+    _need(ctx_off, torch.int64, (B * M + 1,), "ctx_off")
+    if out is None:
+        total = int(ctx_off[-1].item())
+        out = torch.empty(max(total, 1), dtype=torch.int32, device=grid.points.device)
+        capacity = total
+    if capacity is None:
+        capacity = int(out.numel())
+    _check(lib().cagq_context_list(C.byref(grid.rec), _ptr(center_lin), M, _ptr(ctx_off), _ptr(out),
+                                   int(capacity), _stream_ptr(stream)), "cagq_context_list")
     return out
 
 

@@ -175,6 +175,44 @@ int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_
     return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
 }
 
+int cagq_query_points(const cagq_grid* g, const float* centers, int32_t M, int32_t K, int32_t mode, uint64_t seed,
+                      int32_t* node_idx, float* node_xyz, int32_t* n_valid, int32_t* ctx_count,
+                      int32_t* center_lin, void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    if (K < 1 || K > CAGQ_MAX_K) return CAGQ_ERR_INVALID_ARG;
+    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN) return CAGQ_ERR_INVALID_ARG;
+    if (!centers || !node_idx || !n_valid) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_query_points(L, g->desc, g->workspace, centers, M, K, mode, seed, node_idx, node_xyz,
+                                       n_valid, ctx_count, center_lin, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_context_offsets(const cagq_grid* g, const int32_t* center_lin, int32_t M, int64_t* ctx_off,
+                         void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    if (!center_lin || !ctx_off) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_context_offsets(L, g->desc, g->workspace, center_lin, M, ctx_off, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_context_list(const cagq_grid* g, const int32_t* center_lin, int32_t M, const int64_t* ctx_off,
+                      int32_t* ctx_idx, int64_t capacity, void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    if (!center_lin || !ctx_off || capacity < 0 || (capacity > 0 && !ctx_idx)) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_context_list(L, g->desc, g->workspace, center_lin, M, ctx_off, ctx_idx, capacity,
+                                       (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
 int cagq_get_device_status(const cagq_grid* g, void* stream) {
     Layout L;
     int rc = grid_layout(g, &L);

@@ -35,18 +35,6 @@ GridArgs grid_args(const cagq_grid_desc& d) {
     return g;
 }
 
-// clamp(floor((p - o) / s), 0, D - 1): one rounded subtract, one correctly
-// rounded divide, an exact floor and an exact clamp.
-__device__ __forceinline__ int32_t axis_index(float p, float o, float s, int32_t D) {
-    float diff = p - o;
-    float t = diff / s;
-    float f = floorf(t);
-    if (f < 0.0f) return 0;
-    if (f >= 2147483648.0f) return D - 1;
-    int32_t gi = (int32_t)f;
-    return gi > D - 1 ? D - 1 : gi;
-}
-
 __global__ void k_clear(uint4* __restrict__ p, size_t n16) {
     size_t stride = (size_t)gridDim.x * blockDim.x;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)

@@ -28,6 +28,7 @@ enum StatusSlot {
     kStTicketOff = 2,  // tile tickets of the offsets scan
     kStBigCount = 3,   // number of voxels with more than kBigVoxel points
     kStTicketSel = 4,  // tile tickets of the center compaction scan
+    kStTicketCtx = 5,  // tile tickets of the context-offsets scan
     kStSlots = 16
 };
 
@@ -217,25 +218,27 @@ constexpr uint64_t kDescAgg = 1ull << 62;
 constexpr uint64_t kDescInc = 2ull << 62;
 constexpr uint64_t kDescVal = (1ull << 62) - 1;
 
-// Exclusive prefix of `agg` over the tiles before `tile` in one segment.
-// Every thread of the block calls it; wave 0 publishes and looks back. Tiles
-// are numbered by a ticket taken at block start, so every predecessor has
-// started and will publish: the spin always ends.
-__device__ inline uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
+// Exclusive prefix of `agg` over the tiles before `tile` in one segment;
+// desc(t) is the address of tile t's descriptor. Every thread of the block
+// calls it; wave 0 publishes and looks back. Tiles are numbered by a ticket
+// taken at block start, so every predecessor has started and will publish:
+// the spin always ends.
+template <typename F>
+__device__ inline uint64_t tile_lookback_at(F desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
     if (threadIdx.x < kWave) {
         const int lane = lane_id();
         uint64_t excl = 0;
         if (tile == 0) {
-            if (lane == 0) st_release(desc, kDescInc | agg);
+            if (lane == 0) st_release(desc(0), kDescInc | agg);
         } else {
-            if (lane == 0) st_release(desc + tile, kDescAgg | agg);
+            if (lane == 0) st_release(desc(tile), kDescAgg | agg);
             int64_t base = tile - 1;
             while (true) {
                 int64_t idx = base - lane;
                 uint64_t d = kDescInc;  // before the first tile: an inclusive zero
                 if (idx >= 0) {
                     do {
-                        d = ld_acquire(desc + idx);
+                        d = ld_acquire(desc(idx));
                     } while ((d >> 62) == 0);
                 }
                 uint64_t inc = __ballot((d >> 62) == 2);
@@ -247,12 +250,17 @@ __device__ inline uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t 
                 excl += wave_sum<uint64_t>(d & kDescVal);
                 base -= kWave;
             }
-            if (lane == 0) st_release(desc + tile, kDescInc | (excl + agg));
+            if (lane == 0) st_release(desc(tile), kDescInc | (excl + agg));
         }
         if (lane == 0) *s_out = excl;
     }
     __syncthreads();
     return *s_out;
+}
+
+// The same over a contiguous descriptor array.
+__device__ inline uint64_t tile_lookback(uint64_t* desc, int64_t tile, uint64_t agg, uint64_t* s_out) {
+    return tile_lookback_at([desc](int64_t t) { return desc + t; }, tile, agg, s_out);
 }
 
 // Exclusive scan of one 64-bit value per thread across a kScanThreads block;
@@ -289,6 +297,18 @@ __device__ __forceinline__ int32_t slot_of(const uint64_t* bm, const uint32_t* w
     uint64_t bit = 1ull << (lin & 63);
     if (!(w & bit)) return -1;
     return (int32_t)(wr[lin >> 6] + __popcll(w & (bit - 1)));
+}
+
+// clamp(floor((p - o) / s), 0, D - 1): one rounded subtract, one correctly
+// rounded divide, an exact floor and an exact clamp.
+__device__ __forceinline__ int32_t axis_index(float p, float o, float s, int32_t D) {
+    float diff = p - o;
+    float t = diff / s;
+    float f = floorf(t);
+    if (f < 0.0f) return 0;
+    if (f >= 2147483648.0f) return D - 1;
+    int32_t gi = (int32_t)f;
+    return gi > D - 1 ? D - 1 : gi;
 }
 
 struct GridDims {
@@ -400,6 +420,19 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
 bool cas_lds_fits(const Layout& L, const cagq_grid_desc& d, uint32_t beta_q16);
 hipError_t launch_cas_lds(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, int32_t* center_lin,
                           int32_t* m_valid, hipStream_t s);
+
+// Context lists (Sec. 3.3, grid context pooling): CSR offsets over the batch
+// of every center's context count, then the lists themselves.
+hipError_t launch_context_offsets(const Layout& L, const cagq_grid_desc& d, void* ws, const int32_t* center_lin,
+                                  int32_t M, int64_t* ctx_off, hipStream_t s);
+hipError_t launch_context_list(const Layout& L, const cagq_grid_desc& d, void* ws, const int32_t* center_lin,
+                               int32_t M, const int64_t* ctx_off, int32_t* ctx_idx, int64_t capacity,
+                               hipStream_t s);
+
+// Upsampling query around given center points [B][M][3] (Sec. 3.1).
+hipError_t launch_query_points(const Layout& L, const cagq_grid_desc& d, void* ws, const float* centers, int32_t M,
+                               int32_t K, int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz,
+                               int32_t* n_valid, int32_t* ctx_count, int32_t* center_lin, hipStream_t s);
 
 hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* points, void* ws,
                         const uint32_t* weights, const int32_t* center_lin, int32_t M, int32_t K,

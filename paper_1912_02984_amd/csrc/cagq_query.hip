@@ -18,6 +18,12 @@
 //   4. node coordinates are bit copies re-read from the copy; w_c is the
 //      integer sum of the node weights and chi_c the pairwise fp32 sum of
 //      w_k * p_k (shuffle-down tree: stride 1, 2, 4, ...) divided by w_c.
+//
+// The upsampling variant (Sec. 3.1: centers arrive through long-range
+// connections, only their nodes are queried) takes center points instead:
+// v is the voxel a point falls in (it need not be occupied), k-NN distances
+// are measured from the point itself, an empty context gives index -1, and
+// no group center is formed.
 #include "cagq_internal.h"
 
 namespace cagq {
@@ -165,13 +171,14 @@ __device__ __forceinline__ void gmerge_low(uint64_t& bk, uint32_t& bp, uint64_t 
     for (int j = G >> 1; j > 0; j >>= 1) gcx(bk, bp, j, (lg & j) == 0);
 }
 
-template <int MODE, int G, int RAD>
+template <int MODE, int G, int RAD, bool UP>
 __global__ __launch_bounds__(kQueryThreads) void k_query(
     const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
     int64_t W, const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
     const uint32_t* __restrict__ vox_off, const float4* __restrict__ pt4, const int32_t* __restrict__ center_lin,
-    uint64_t seed, int32_t* __restrict__ node_idx, float* __restrict__ node_xyz, int32_t* __restrict__ n_valid,
-    float* __restrict__ center_xyz, uint32_t* __restrict__ center_w, int32_t* __restrict__ ctx_count,
+    const float* __restrict__ center_pts, uint64_t seed, int32_t* __restrict__ node_idx,
+    float* __restrict__ node_xyz, int32_t* __restrict__ n_valid, float* __restrict__ center_xyz,
+    uint32_t* __restrict__ center_w, int32_t* __restrict__ ctx_count, int32_t* __restrict__ lin_out,
     int* __restrict__ status) {
     extern __shared__ uint32_t smem[];
     constexpr int GPB = kQueryThreads / G;  // groups per block
@@ -189,18 +196,34 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     const int32_t c_id = live ? cid : 0;
     const int32_t b = (int32_t)udiv((uint32_t)c_id, g.mm);
     const size_t cK = (size_t)c_id * K;
-    const int32_t lin_s = center_lin[c_id];
-    const int64_t V = (int64_t)g.D[0] * g.D[1] * g.D[2];
     const uint64_t* bm = bitmap + (size_t)b * W;
     const uint32_t* wr = word_rank + (size_t)b * W;
     const uint32_t* vo = vox_off + (size_t)b * (N + 1);
     const float4* p4 = pt4 + (size_t)b * N;
-    const bool in_grid = lin_s >= 0 && (int64_t)lin_s < V;
-    const uint32_t lin = in_grid ? (uint32_t)lin_s : 0u;
-    const uint32_t zq = udiv(lin, g.d01);
-    const uint32_t rem = lin - zq * (uint32_t)g.D[0] * (uint32_t)g.D[1];
-    const uint32_t yq = udiv(rem, g.d0);
-    const int32_t gx = (int32_t)(rem - yq * (uint32_t)g.D[0]), gy = (int32_t)yq, gz = (int32_t)zq;
+    bool in_grid = true;
+    uint32_t lin;
+    int32_t gx, gy, gz;
+    float px = 0.f, py = 0.f, pz = 0.f;  // the given center point (upsampling)
+    if constexpr (UP) {
+        px = center_pts[(size_t)c_id * 3 + 0];
+        py = center_pts[(size_t)c_id * 3 + 1];
+        pz = center_pts[(size_t)c_id * 3 + 2];
+        const bool bad = !isfinite(px) || !isfinite(py) || !isfinite(pz);
+        gx = isfinite(px) ? axis_index(px, g.o[0], g.s[0], g.D[0]) : 0;
+        gy = isfinite(py) ? axis_index(py, g.o[1], g.s[1], g.D[1]) : 0;
+        gz = isfinite(pz) ? axis_index(pz, g.o[2], g.s[2], g.D[2]) : 0;
+        lin = (uint32_t)gx + (uint32_t)g.D[0] * ((uint32_t)gy + (uint32_t)g.D[1] * (uint32_t)gz);
+        if (live && bad && lg == 0) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+    } else {
+        const int32_t lin_s = center_lin[c_id];
+        const int64_t V = (int64_t)g.D[0] * g.D[1] * g.D[2];
+        in_grid = lin_s >= 0 && (int64_t)lin_s < V;
+        lin = in_grid ? (uint32_t)lin_s : 0u;
+        const uint32_t zq = udiv(lin, g.d01);
+        const uint32_t rem = lin - zq * (uint32_t)g.D[0] * (uint32_t)g.D[1];
+        const uint32_t yq = udiv(rem, g.d0);
+        gx = (int32_t)(rem - yq * (uint32_t)g.D[0]), gy = (int32_t)yq, gz = (int32_t)zq;
+    }
 
     // 1. occupied voxels of pi(v), compacted in ascending linear id; the
     // center voxel is one of them (q = nnb / 2), so its own check costs
@@ -238,11 +261,14 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         c += gbcast<G>(incl, G - 1);
         nocc += (uint32_t)__popcll(mask);
     }
-    // an unoccupied center has an empty context and gets zeros
-    if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
-    if (!occupied) {
-        nocc = 0;
-        c = 0;
+    // a sampled center that is not occupied has an empty context and gets
+    // zeros (an upsampling center's voxel may be empty)
+    if (!UP) {
+        if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
+        if (!occupied) {
+            nocc = 0;
+            c = 0;
+        }
     }
     if (lg == 0) s_pre[nocc] = c;
     wave_lds_sync();
@@ -252,6 +278,10 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     float qx = 0.f, qy = 0.f, qz = 0.f;
     if (MODE == CAGQ_QUERY_CUBE) {
         hc = sm64(sm64(sm64(seed ^ 2ull) ^ (uint64_t)b) ^ (uint64_t)lin);
+    } else if (UP) {
+        qx = px;
+        qy = py;
+        qz = pz;
     } else {
         qx = g.o[0] + ((float)gx + 0.5f) * g.s[0];
         qy = g.o[1] + ((float)gy + 0.5f) * g.s[1];
@@ -337,6 +367,22 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         x = y = z = 0.0f;
         w = 1u;
     }
+    if (UP) {
+        if (live && lg < K) {
+            node_idx[cK + lg] = n ? (int32_t)idx : -1;
+            if (node_xyz) {
+                node_xyz[(cK + lg) * 3 + 0] = x;
+                node_xyz[(cK + lg) * 3 + 1] = y;
+                node_xyz[(cK + lg) * 3 + 2] = z;
+            }
+        }
+        if (live && lg == 0) {
+            n_valid[cid] = (int32_t)n;
+            if (ctx_count) ctx_count[cid] = (int32_t)c;
+            if (lin_out) lin_out[cid] = (int32_t)lin;
+        }
+        return;
+    }
     if (live && lg < K) {
         node_idx[cK + lg] = (int32_t)idx;
         if (node_xyz) {
@@ -372,50 +418,67 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     }
 }
 
-template <int MODE, int G, int RAD>
-void launch_g(const Layout& L, const QGrid& g, void* ws, const uint32_t* weights,
-              const int32_t* center_lin, int32_t M, int32_t K, uint64_t seed, int32_t* node_idx, float* node_xyz,
-              int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count, hipStream_t s) {
+// The pointers of one query launch.
+struct QueryIO {
+    const uint32_t* weights;
+    const int32_t* center_lin;
+    const float* center_pts;
+    int32_t* node_idx;
+    float* node_xyz;
+    int32_t* n_valid;
+    float* center_xyz;
+    uint32_t* center_w;
+    int32_t* ctx_count;
+    int32_t* lin_out;
+};
+
+template <int MODE, int G, int RAD, bool UP>
+void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int32_t M, int32_t K, uint64_t seed,
+              hipStream_t s) {
     constexpr int GPB = kQueryThreads / G;
     const int32_t total = L.B * M;
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
     constexpr int side = 2 * RAD + 1;
     const size_t lds = (size_t)GPB * (2 * side * side * side + 1) * sizeof(uint32_t);
-    k_query<MODE, G, RAD><<<blocks, kQueryThreads, lds, s>>>(
-        weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
-        at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), center_lin, seed, node_idx, node_xyz, n_valid,
-        center_xyz, center_w, ctx_count, at<int>(ws, L.status));
+    k_query<MODE, G, RAD, UP><<<blocks, kQueryThreads, lds, s>>>(
+        io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
+        at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
+        io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status));
 }
 
-template <int MODE, int G>
-void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const uint32_t* weights,
-              const int32_t* center_lin, int32_t M, int32_t K, uint64_t seed, int32_t* node_idx, float* node_xyz,
-              int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count, hipStream_t s) {
+template <int MODE, int G, bool UP>
+void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const QueryIO& io, int32_t M, int32_t K,
+              uint64_t seed, hipStream_t s) {
     if (rad == 1)
-        launch_g<MODE, G, 1>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
-                             center_w, ctx_count, s);
+        launch_g<MODE, G, 1, UP>(L, g, ws, io, M, K, seed, s);
     else if (rad == 2)
-        launch_g<MODE, G, 2>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
-                             center_w, ctx_count, s);
+        launch_g<MODE, G, 2, UP>(L, g, ws, io, M, K, seed, s);
     else
-        launch_g<MODE, G, 3>(L, g, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid, center_xyz,
-                             center_w, ctx_count, s);
+        launch_g<MODE, G, 3, UP>(L, g, ws, io, M, K, seed, s);
 }
 
-template <int MODE>
-void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const uint32_t* weights,
-                 const int32_t* center_lin, int32_t M, int32_t K, uint64_t seed, int32_t* node_idx,
-                 float* node_xyz, int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
-                 hipStream_t s) {
+template <int MODE, bool UP>
+void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const QueryIO& io, int32_t M, int32_t K,
+                 uint64_t seed, hipStream_t s) {
     if (K <= 16)
-        launch_r<MODE, 16>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
-                           center_xyz, center_w, ctx_count, s);
+        launch_r<MODE, 16, UP>(L, g, rad, ws, io, M, K, seed, s);
     else if (K <= 32)
-        launch_r<MODE, 32>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
-                           center_xyz, center_w, ctx_count, s);
+        launch_r<MODE, 32, UP>(L, g, rad, ws, io, M, K, seed, s);
     else
-        launch_r<MODE, 64>(L, g, rad, ws, weights, center_lin, M, K, seed, node_idx, node_xyz, n_valid,
-                           center_xyz, center_w, ctx_count, s);
+        launch_r<MODE, 64, UP>(L, g, rad, ws, io, M, K, seed, s);
+}
+
+QGrid make_qgrid(const cagq_grid_desc& d, int32_t M) {
+    QGrid g;
+    for (int a = 0; a < 3; ++a) {
+        g.o[a] = d.origin[a];
+        g.s[a] = d.voxel_size[a];
+        g.D[a] = d.dims[a];
+    }
+    g.d0 = make_magic((uint32_t)d.dims[0]);
+    g.d01 = make_magic((uint32_t)d.dims[0] * (uint32_t)d.dims[1]);
+    g.mm = make_magic((uint32_t)M);
+    return g;
 }
 
 }  // namespace
@@ -426,21 +489,26 @@ hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* p
                         int32_t* n_valid, float* center_xyz, uint32_t* center_w, int32_t* ctx_count,
                         hipStream_t s) {
     (void)points;  // node coordinates are bit copies read from the slot-ordered copy
-    QGrid g;
-    for (int a = 0; a < 3; ++a) {
-        g.o[a] = d.origin[a];
-        g.s[a] = d.voxel_size[a];
-        g.D[a] = d.dims[a];
-    }
-    g.d0 = make_magic((uint32_t)d.dims[0]);
-    g.d01 = make_magic((uint32_t)d.dims[0] * (uint32_t)d.dims[1]);
-    g.mm = make_magic((uint32_t)M);
+    const QGrid g = make_qgrid(d, M);
+    const QueryIO io{weights, center_lin, nullptr, node_idx, node_xyz, n_valid, center_xyz, center_w, ctx_count,
+                     nullptr};
     if (mode == CAGQ_QUERY_CUBE)
-        launch_mode<CAGQ_QUERY_CUBE>(L, g, d.radius, ws, weights, center_lin, M, K, seed, node_idx, node_xyz,
-                                     n_valid, center_xyz, center_w, ctx_count, s);
+        launch_mode<CAGQ_QUERY_CUBE, false>(L, g, d.radius, ws, io, M, K, seed, s);
     else
-        launch_mode<CAGQ_QUERY_KNN>(L, g, d.radius, ws, weights, center_lin, M, K, seed, node_idx, node_xyz,
-                                    n_valid, center_xyz, center_w, ctx_count, s);
+        launch_mode<CAGQ_QUERY_KNN, false>(L, g, d.radius, ws, io, M, K, seed, s);
+    return hipGetLastError();
+}
+
+hipError_t launch_query_points(const Layout& L, const cagq_grid_desc& d, void* ws, const float* centers, int32_t M,
+                               int32_t K, int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz,
+                               int32_t* n_valid, int32_t* ctx_count, int32_t* center_lin, hipStream_t s) {
+    const QGrid g = make_qgrid(d, M);
+    const QueryIO io{nullptr, nullptr, centers, node_idx, node_xyz, n_valid, nullptr, nullptr, ctx_count,
+                     center_lin};
+    if (mode == CAGQ_QUERY_CUBE)
+        launch_mode<CAGQ_QUERY_CUBE, true>(L, g, d.radius, ws, io, M, K, seed, s);
+    else
+        launch_mode<CAGQ_QUERY_KNN, true>(L, g, d.radius, ws, io, M, K, seed, s);
     return hipGetLastError();
 }
 

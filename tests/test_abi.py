@@ -148,3 +148,35 @@ def test_query_rejects_bad_arguments():
     assert args(cx=None) == cagq.ERR_INVALID_ARG
     assert args(cw=None) == cagq.ERR_INVALID_ARG
     assert args(cl=None) == cagq.ERR_INVALID_ARG
+
+
+def test_query_points_rejects_bad_arguments():
+    L = cagq.lib()
+    g = _grid_record()
+    p = C.c_void_p(0x300000)
+    args = lambda K=16, mode=1, M=8, c=p, ni=p, nv=p: L.cagq_query_points(
+        C.byref(g), c, M, K, mode, 1, ni, None, nv, None, None, None)
+    assert args(K=0) == cagq.ERR_INVALID_ARG
+    assert args(K=65) == cagq.ERR_INVALID_ARG
+    assert args(mode=2) == cagq.ERR_INVALID_ARG
+    assert args(M=0) == cagq.ERR_INVALID_ARG
+    assert args(c=None) == cagq.ERR_INVALID_ARG
+    assert args(ni=None) == cagq.ERR_INVALID_ARG
+    assert args(nv=None) == cagq.ERR_INVALID_ARG
+
+
+def test_context_calls_reject_bad_arguments():
+    L = cagq.lib()
+    g = _grid_record()
+    p = C.c_void_p(0x300000)
+    assert L.cagq_context_offsets(C.byref(g), p, 0, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_offsets(C.byref(g), None, 8, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_offsets(C.byref(g), p, 8, None, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_offsets(None, p, 8, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_list(C.byref(g), p, 8, p, p, -1, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_list(C.byref(g), p, 8, p, None, 16, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_list(C.byref(g), p, 8, None, p, 16, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_list(C.byref(g), None, 8, p, p, 16, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_context_list(C.byref(g), p, 0, p, p, 16, None) == cagq.ERR_INVALID_ARG
+    small = _grid_record(ws_bytes=1024)
+    assert L.cagq_context_offsets(C.byref(small), p, 8, p, None) == cagq.ERR_WORKSPACE_TOO_SMALL

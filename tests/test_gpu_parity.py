@@ -288,3 +288,138 @@ def test_unoccupied_center_is_reported():
     assert cagq.get_device_status(g) == cagq.ERR_CENTER_NOT_OCCUPIED
     assert int(q["n_valid"][0, 0]) > 0 and int(q["n_valid"][0, 1]) == 0
     assert torch.all(q["node_idx"][0, 1] == 0) and torch.all(q["center_xyz"][0, 1] == 0)
+
+
+# ---------------------------------------------------------------- upsampling query and context lists
+
+def run_up(P, grid_spec, Q, K, mode, seed, where="", context=True):
+    """Upsampling query (and the context lists of the centers' voxels) on
+    both sides: grid on P [B,N,3], given centers Q [B,M,3]."""
+    P = np.ascontiguousarray(P, np.float32)
+    Q = np.ascontiguousarray(Q, np.float32)
+    ot = oracle.Table(P, oracle.grid_from_spec(grid_spec))
+    qo = ot.query_points(Q, K, mode, seed)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(grid_spec))
+    qg = cagq.query_points(g, torch.from_numpy(Q).to(DEV), K, mode, seed)
+    assert cagq.get_device_status(g) == 0, where
+    for k in ("node_idx", "n_valid", "ctx_count", "center_lin"):
+        assert np.array_equal(_np(qg[k]), qo[k]), (where, k)
+    assert np.array_equal(_bits(_np(qg["node_xyz"])), _bits(qo["node_xyz"])), where
+    if context:
+        assert_context(g, ot, qg["center_lin"], where)
+    return qo
+
+
+def assert_context(g, ot, center_lin, where=""):
+    off_o, idx_o = ot.context_list(_np(center_lin))
+    off = cagq.context_offsets(g, center_lin)
+    idx = cagq.context_list(g, center_lin, off)
+    assert cagq.get_device_status(g) == 0, where
+    assert np.array_equal(_np(off), off_o), where
+    assert np.array_equal(_np(idx)[: len(idx_o)], idx_o), where
+
+
+@pytest.mark.parametrize("name", ["object", "room", "bigroom/cas-knn"])
+def test_query_points_workloads(name):
+    """The upsampling step of a segmentation network: the grid holds the
+    centers of layer 1, and every input point of layer 0 is a center whose
+    nodes are queried among them (K of the layer, both query modes)."""
+    w = W.get_workload(name)
+    P = w.points()
+    # a one-layer workload queries its centers on the same grid
+    L0, L1 = w.layers[0], w.layers[min(1, len(w.layers) - 1)]
+    t, cl, mv, q = oracle.run_layer(P, L0)
+    coarse = q["center_xyz"]
+    for mode in ("knn", "cube"):
+        print(f"[parity] upsampling {name} {mode}: B={P.shape[0]} N={coarse.shape[1]} M={P.shape[1]} K={L1.K}",
+              flush=True)
+        run_up(coarse, L1.grid, P, L1.K, mode, 7, where=f"{name} {mode}", context=(mode == "knn"))
+
+
+@pytest.mark.parametrize("r", [1, 2, 3])
+@pytest.mark.parametrize("K", [1, 16, 33, 64])
+def test_query_points_radius_and_node_counts(r, K):
+    """Centers of three kinds (cloud points, points in the box, points
+    outside it, clamped): contexts from empty to a few hundred points."""
+    rng = np.random.default_rng(10 * r + K)
+    B, N, M = 2, 3000, 1111
+    # the points fill [0, 0.7)^3 of the grid's unit box, densest near 0
+    P = (rng.random((B, N, 3), dtype=np.float32) ** 2 * np.float32(0.7)).astype(np.float32)
+    Q = np.concatenate([P[:, :300], rng.random((B, 500, 3), dtype=np.float32),
+                        (rng.random((B, M - 800, 3), dtype=np.float32) * np.float32(1.6) - np.float32(0.3))], 1)
+    spec = _spec((0, 0, 0), (0.05,) * 3, (20, 20, 20), 8, r)
+    qo = run_up(P, spec, Q, K, "knn", 1, where=f"r={r} K={K}")
+    assert (qo["n_valid"] == 0).any() and (qo["ctx_count"] > 64).any()
+    run_up(P, spec, Q, K, "cube", 2, where=f"cube r={r} K={K}", context=False)
+
+
+def test_query_points_nonfinite_center_is_reported():
+    rng = np.random.default_rng(3)
+    P = rng.random((1, 500, 3), dtype=np.float32)
+    Q = rng.random((1, 40, 3), dtype=np.float32)
+    Q[0, 5, 2] = np.inf
+    Q[0, 9, 0] = np.nan
+    spec = _spec((0, 0, 0), (0.1,) * 3, (10, 10, 10), 8)
+    ot = oracle.Table(P, oracle.grid_from_spec(spec))
+    qo = ot.query_points(Q, 8, "knn", 0, allow_nonfinite=True)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(spec))
+    qg = cagq.query_points(g, torch.from_numpy(Q).to(DEV), 8, "knn", 0)
+    assert cagq.get_device_status(g) == cagq.ERR_NONFINITE_INPUT
+    for k in ("node_idx", "n_valid", "ctx_count", "center_lin"):
+        assert np.array_equal(_np(qg[k]), qo[k]), k
+
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room", "bigroom/cas-knn", "lidar"])
+def test_context_lists_of_sampled_centers(name):
+    """The context lists of each workload's layer-1 centers, at full size."""
+    w = W.get_workload(name)
+    P = w.points()
+    L = w.layers[0]
+    print(f"[parity] context lists {name}: B={P.shape[0]} N={P.shape[1]} M={L.M}", flush=True)
+    ot = oracle.Table(P, oracle.grid_from_spec(L.grid))
+    ocl, _ = ot.sample_rvs(L.M, L.seed)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(L.grid))
+    cl, _ = cagq.sample_centers(g, L.M, "rvs", L.seed)
+    assert np.array_equal(_np(cl), ocl)
+    assert_context(g, ot, cl, name)
+
+
+@pytest.mark.parametrize("BM", [1, 1023, 1024, 1025, 3073])
+def test_context_offsets_at_scan_tile_edges(BM):
+    """Center counts on both sides of the offsets scan's tile size, with
+    unoccupied center voxels and repeated centers."""
+    rng = np.random.default_rng(BM)
+    P = rng.random((1, 4000, 3), dtype=np.float32)
+    spec = _spec((0, 0, 0), (0.05,) * 3, (20, 20, 20), 4)
+    cl = rng.integers(0, 8000, (1, BM)).astype(np.int32)
+    ot = oracle.Table(P, oracle.grid_from_spec(spec))
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(spec))
+    assert_context(g, ot, torch.from_numpy(cl).to(DEV), f"BM={BM}")
+
+
+def test_context_list_capacity_and_outside_lin():
+    rng = np.random.default_rng(4)
+    P = rng.random((2, 2000, 3), dtype=np.float32)
+    spec = _spec((0, 0, 0), (0.1,) * 3, (10, 10, 10), 8)
+    ot = oracle.Table(P, oracle.grid_from_spec(spec))
+    cl = rng.integers(0, 1000, (2, 50)).astype(np.int32)
+    off_o, idx_o = ot.context_list(cl)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(spec))
+    clt = torch.from_numpy(cl).to(DEV)
+    off = cagq.context_offsets(g, clt)
+    cap = len(idx_o) // 2
+    out = torch.full((len(idx_o),), -9, dtype=torch.int32, device=DEV)
+    cagq.context_list(g, clt, off, out=out, capacity=cap)
+    assert cagq.get_device_status(g) == cagq.ERR_CAPACITY
+    got = _np(out)
+    assert np.array_equal(got[:cap], idx_o[:cap]) and np.all(got[cap:] == -9)
+    # a lin outside the grid: empty context, reported
+    g2 = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.desc_from_spec(spec))
+    bad = clt.clone()
+    bad[1, 7] = 1000
+    off2 = cagq.context_offsets(g2, bad)
+    assert cagq.get_device_status(g2) == cagq.ERR_CENTER_NOT_OCCUPIED
+    o2 = _np(off2)
+    assert o2[57 + 1] == o2[57]
+    with pytest.raises(oracle.OracleError, match="-7"):
+        ot.context_list(_np(bad))
