@@ -44,6 +44,8 @@ class _Table(C.Structure):
 
 _lib = None
 
+QUERY_MODES = {"cube": 0, "knn": 1, "knn_ring": 2}
+
 
 def lib():
     global _lib
@@ -184,7 +186,7 @@ class Table:
             center_w=np.zeros((B, M), np.uint32),
             ctx_count=np.zeros((B, M), np.int32),
         )
-        m = {"cube": 0, "knn": 1}[mode]
+        m = QUERY_MODES[mode]
         _check(lib().orc_query(C.byref(self._t), _ptr(P), _ptr(W), _ptr(cl), _ptr(mv), M, K, m,
                                C.c_uint64(seed), _ptr(out["node_idx"]), _ptr(out["node_xyz"]),
                                _ptr(out["n_valid"]), _ptr(out["center_xyz"]), _ptr(out["center_w"]),
@@ -204,7 +206,7 @@ class Table:
             ctx_count=np.zeros((B, M), np.int32),
             center_lin=np.zeros((B, M), np.int32),
         )
-        m = {"cube": 0, "knn": 1}[mode]
+        m = QUERY_MODES[mode]
         rc = lib().orc_query_points(C.byref(self._t), _ptr(P), _ptr(Q), M, K, m, C.c_uint64(seed),
                                     _ptr(out["node_idx"]), _ptr(out["node_xyz"]), _ptr(out["n_valid"]),
                                     _ptr(out["ctx_count"]), _ptr(out["center_lin"]))

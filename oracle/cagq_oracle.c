@@ -46,6 +46,12 @@
  *             hi32(h(seed, 2, b, lin(v), i)) << 32 | i, k-NN key
  *             bits(d^2) << 32 | i with d measured from the center of voxel
  *             v and d^2 = (dx*dx + dy*dy) + dz*dz. Slots k >= n repeat slot 0.
+ *   k-NN by   Appendix D, "CAGQ k-NN" (mode 2): levels 0, 1, ..., r of pi(v)
+ *   levels    (Chebyshev distance exactly i); a level that fits in what is
+ *             left of K is appended whole, in gathering order (voxels by
+ *             ascending lin, stored points ascending), otherwise its nearest
+ *             points by the k-NN key; stop at K. Not exact: a level-1 point
+ *             can be nearer than a level-0 one.
  *   center    Appendix E, Eqs. 7-8: w_c = sum w_j, chi_c = sum w_j chi_j /
  *             w_c over the n valid nodes. Reading: the fp32 sum is pairwise
  *             in node order (stride 1, 2, 4, ...), then one fp32 divide.
@@ -74,7 +80,9 @@
  * centers vs closed forms and an fp64 error bound; upsampling k-NN vs a
  * numpy brute force over the block around each center point, and vs
  * global k-NN; context lists vs a numpy enumeration of the block's stored
- * points.
+ * points; level-wise k-NN vs a hand-worked example of the algorithm, the
+ * K nearest of the center voxel when it holds K points, the whole context
+ * in level order when it holds at most K.
  */
 #include "cagq_oracle.h"
 
@@ -424,13 +432,70 @@ static uint32_t float_bits(float f) {
     return u;
 }
 
+/* k-NN key of point i from reference q: bits(d^2) << 32 | i. */
+static uint64_t knn_key(const float* P, uint64_t i, const float* q) {
+    float dx = P[3 * i + 0] - q[0];
+    float dy = P[3 * i + 1] - q[1];
+    float dz = P[3 * i + 2] - q[2];
+    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+    float s = xx + yy;
+    float d2 = s + zz;
+    return ((uint64_t)float_bits(d2) << 32) | i;
+}
+
+/* Appendix D, "CAGQ k-NN" (the level-wise procedure). Level i of pi(v) is
+ * the voxels at Chebyshev distance exactly i from v. For level 0, 1, ...:
+ * gather the level's stored points (voxels in ascending lin, each voxel's
+ * points ascending), kl of them; topkl = min(K - counter, kl); when topkl is
+ * kl the whole level is appended as gathered, otherwise the topkl nearest
+ * to q (by knn_key, ascending); stop once counter reaches K. The appended
+ * points go to nodes[0..counter); layer has room for one level. */
+static int32_t knn_by_levels(const orc_table* t, int32_t b, uint32_t l, const float* P, const float* q,
+                             int32_t K, uint64_t* layer, int32_t* nodes) {
+    const int32_t* D = t->g.dims;
+    const int32_t rad = t->g.radius;
+    const uint32_t* vo = t->vox_off + (size_t)b * (t->N + 1);
+    const uint32_t* pl = t->pt_list + (size_t)b * t->N;
+    int32_t gx = (int32_t)(l % (uint32_t)D[0]);
+    int32_t gy = (int32_t)((l / (uint32_t)D[0]) % (uint32_t)D[1]);
+    int32_t gz = (int32_t)(l / ((uint32_t)D[0] * (uint32_t)D[1]));
+    int32_t counter = 0;
+    for (int32_t lev = 0; lev <= rad; ++lev) {
+        int32_t kl = 0;
+        for (int32_t dz = -lev; dz <= lev; ++dz)
+            for (int32_t dy = -lev; dy <= lev; ++dy)
+                for (int32_t dx = -lev; dx <= lev; ++dx) {
+                    int32_t m = abs(dx) > abs(dy) ? abs(dx) : abs(dy);
+                    m = abs(dz) > m ? abs(dz) : m;
+                    if (m != lev) continue;
+                    int32_t x = gx + dx, y = gy + dy, z = gz + dz;
+                    if (x < 0 || y < 0 || z < 0 || x >= D[0] || y >= D[1] || z >= D[2]) continue;
+                    uint32_t nl = (uint32_t)x + (uint32_t)D[0] * ((uint32_t)y + (uint32_t)D[1] * (uint32_t)z);
+                    int32_t sl = find_slot(t, b, nl);
+                    if (sl < 0) continue;
+                    for (uint32_t u = vo[sl]; u < vo[sl + 1]; ++u) layer[kl++] = pl[u];
+                }
+        int32_t topkl = K - counter < kl ? K - counter : kl;
+        if (topkl == kl) {
+            for (int32_t e = 0; e < kl; ++e) nodes[counter + e] = (int32_t)layer[e];
+        } else {
+            for (int32_t e = 0; e < kl; ++e) layer[e] = knn_key(P, layer[e], q);
+            qsort(layer, (size_t)kl, sizeof(uint64_t), cmp_u64);
+            for (int32_t e = 0; e < topkl; ++e) nodes[counter + e] = (int32_t)(layer[e] & 0xFFFFFFFFu);
+        }
+        counter += topkl;
+        if (counter >= K) break;
+    }
+    return counter;
+}
+
 int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
               const int32_t* center_lin, const int32_t* m_valid, int32_t M, int32_t K,
               int32_t mode, uint64_t seed,
               int32_t* node_idx, float* node_xyz, int32_t* n_valid,
               float* center_xyz, uint32_t* center_w, int32_t* ctx_count) {
     if (!table_ok(t) || !pts || !center_lin || !m_valid || M < 1 || K < 1) return ORC_EINVAL;
-    if (mode != 0 && mode != 1) return ORC_EINVAL;
+    if (mode < 0 || mode > 2) return ORC_EINVAL;
     if (!node_idx || !n_valid || !center_xyz || !center_w) return ORC_EINVAL;
     int32_t rad = t->g.radius;
     int32_t side = 2 * rad + 1;
@@ -438,7 +503,8 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
     int32_t* nbs = (int32_t*)malloc(sizeof(int32_t) * (size_t)lambda);
     uint64_t* key = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)lambda * (size_t)t->g.n_v);
     float* term = (float*)malloc(sizeof(float) * 3 * (size_t)K);
-    if (!nbs || !key || !term) { free(nbs); free(key); free(term); return ORC_EINVAL; }
+    int32_t* nodes = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
+    if (!nbs || !key || !term || !nodes) { free(nbs); free(key); free(term); free(nodes); return ORC_EINVAL; }
     const int32_t* D = t->g.dims;
     int rc = 0;
     for (int32_t b = 0; b < t->B; ++b) {
@@ -453,7 +519,7 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
             if (center_lin[cj] < 0 || find_slot(t, b, l) < 0) { rc = ORC_ENOTOCC; continue; }
             /* context points: the stored lists of every voxel of pi(v) */
             int32_t nn = neighbours(t, b, l, rad, nbs);
-            int32_t c = 0;
+            int32_t c = 0, nlev = 0;
             for (int32_t q = 0; q < nn; ++q)
                 for (uint32_t e = vo[nbs[q]]; e < vo[nbs[q] + 1]; ++e) key[c++] = pl[e];
             if (mode == 0) {
@@ -474,19 +540,17 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
                     float off = gc * t->g.voxel_size[a];
                     q[a] = t->g.origin[a] + off;
                 }
-                for (int32_t e = 0; e < c; ++e) {
-                    uint64_t i = key[e];
-                    float dx = P[3 * i + 0] - q[0];
-                    float dy = P[3 * i + 1] - q[1];
-                    float dz = P[3 * i + 2] - q[2];
-                    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-                    float s = xx + yy;
-                    float d2 = s + zz;
-                    key[e] = ((uint64_t)float_bits(d2) << 32) | i;
-                }
+                if (mode == 1)
+                    for (int32_t e = 0; e < c; ++e) key[e] = knn_key(P, key[e], q);
+                else
+                    nlev = knn_by_levels(t, b, l, P, q, K, key, nodes);
             }
-            qsort(key, (size_t)c, sizeof(uint64_t), cmp_u64);
+            if (mode != 2) qsort(key, (size_t)c, sizeof(uint64_t), cmp_u64);
             int32_t n = c < K ? c : K;
+            if (mode == 2) {
+                n = nlev;
+                for (int32_t k = 0; k < n; ++k) key[k] = (uint64_t)(uint32_t)nodes[k];
+            }
             int32_t* ni = node_idx + cj * K;
             for (int32_t k = 0; k < K; ++k) ni[k] = (int32_t)(key[k < n ? k : 0] & 0xFFFFFFFFu);
             if (node_xyz)
@@ -515,6 +579,7 @@ int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
     free(nbs);
     free(key);
     free(term);
+    free(nodes);
     return rc;
 }
 
@@ -531,14 +596,15 @@ int orc_query_points(const orc_table* t, const float* pts, const float* centers,
                      int32_t mode, uint64_t seed, int32_t* node_idx, float* node_xyz, int32_t* n_valid,
                      int32_t* ctx_count, int32_t* center_lin) {
     if (!table_ok(t) || !pts || !centers || M < 1 || K < 1) return ORC_EINVAL;
-    if (mode != 0 && mode != 1) return ORC_EINVAL;
+    if (mode < 0 || mode > 2) return ORC_EINVAL;
     if (!node_idx || !n_valid) return ORC_EINVAL;
     int32_t rad = t->g.radius;
     int32_t side = 2 * rad + 1;
     int32_t lambda = side * side * side;
     int32_t* nbs = (int32_t*)malloc(sizeof(int32_t) * (size_t)lambda);
     uint64_t* key = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)lambda * (size_t)t->g.n_v);
-    if (!nbs || !key) { free(nbs); free(key); return ORC_EINVAL; }
+    int32_t* nodes = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
+    if (!nbs || !key || !nodes) { free(nbs); free(key); free(nodes); return ORC_EINVAL; }
     int rc = 0;
     for (int32_t b = 0; b < t->B; ++b) {
         const float* P = pts + (size_t)b * t->N * 3;
@@ -564,20 +630,16 @@ int orc_query_points(const orc_table* t, const float* pts, const float* centers,
                     uint64_t h = orc_splitmix64(hc ^ i);
                     key[e] = ((h >> 32) << 32) | i;
                 }
-            } else {
-                for (int32_t e = 0; e < c; ++e) {
-                    uint64_t i = key[e];
-                    float dx = P[3 * i + 0] - q[0];
-                    float dy = P[3 * i + 1] - q[1];
-                    float dz = P[3 * i + 2] - q[2];
-                    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
-                    float sxy = xx + yy;
-                    float d2 = sxy + zz;
-                    key[e] = ((uint64_t)float_bits(d2) << 32) | i;
-                }
+            } else if (mode == 1) {
+                for (int32_t e = 0; e < c; ++e) key[e] = knn_key(P, key[e], q);
             }
-            qsort(key, (size_t)c, sizeof(uint64_t), cmp_u64);
             int32_t n = c < K ? c : K;
+            if (mode == 2) {
+                n = knn_by_levels(t, b, l, P, q, K, key, nodes);
+                for (int32_t k = 0; k < n; ++k) key[k] = (uint64_t)(uint32_t)nodes[k];
+            } else {
+                qsort(key, (size_t)c, sizeof(uint64_t), cmp_u64);
+            }
             int32_t* ni = node_idx + cj * K;
             for (int32_t k = 0; k < K; ++k) ni[k] = n ? (int32_t)(key[k < n ? k : 0] & 0xFFFFFFFFu) : -1;
             if (node_xyz)
@@ -590,6 +652,7 @@ int orc_query_points(const orc_table* t, const float* pts, const float* centers,
     }
     free(nbs);
     free(key);
+    free(nodes);
     return rc;
 }
 

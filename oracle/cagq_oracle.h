@@ -73,7 +73,8 @@ int orc_sample_cas(const orc_table* t, int32_t M, uint32_t beta_q16,
 int orc_sample_cas_swap(const orc_table* t, int32_t M, uint64_t seed, uint32_t beta_q16,
                         int32_t* center_lin, int32_t* m_valid, int32_t* decision, int32_t* n_swaps);
 
-/* Node query (Sec. 3.2: Cube Query when mode == 0, k-NN when mode == 1) and
+/* Node query (Sec. 3.2: Cube Query when mode == 0, k-NN when mode == 1, the
+ * level-wise k-NN of Appendix D when mode == 2) and
  * group centers (Appendix E). weights [B][N] may be NULL (all 1). */
 int orc_query(const orc_table* t, const float* pts, const uint32_t* weights,
               const int32_t* center_lin, const int32_t* m_valid, int32_t M, int32_t K,

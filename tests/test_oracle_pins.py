@@ -715,3 +715,132 @@ def test_context_list_rejects_a_lin_outside_the_grid():
     t = _small_table(0)
     with pytest.raises(oracle.OracleError, match="-7"):
         t.context_list(np.array([[6 * 6 * 3]], np.int32))
+
+
+# ---------------------------------------------------------------- level-wise k-NN (Appendix D)
+
+def _ring_table():
+    """Voxels of edge 1, center voxel (2,2,2). Points by index: 0 E in
+    (2,3,2), 1 A at the center voxel's far corner, 2 C just past its +x face,
+    3 B inside it, 4 D just past its -x face. Distances from the voxel center
+    (2.5,2.5,2.5): A 0.779, B 0.4, C 0.55, D 0.6, E 1.1."""
+    P = np.array([[[2.5, 3.6, 2.5], [2.95, 2.95, 2.95], [3.05, 2.5, 2.5], [2.5, 2.5, 2.9],
+                   [1.9, 2.5, 2.5]]], np.float32)
+    t = oracle.Table(P, oracle.make_grid((0, 0, 0), (1, 1, 1), (5, 5, 5), 8, 1))
+    return t, np.array([[2 + 5 * (2 + 5 * 2)]], np.int32), np.array([1], np.int32)
+
+
+@pytest.mark.parametrize("K,nodes", [
+    (1, [3]),                # level 0 holds 2 > K: its nearest, B
+    (2, [1, 3]),             # level 0 fits exactly: appended as gathered (A, B)
+    (3, [1, 3, 2]),          # then the nearest of level 1: C
+    (5, [1, 3, 4, 2, 0]),    # level 1 fits: gathered by voxel lin (D, C, E)
+    (6, [1, 3, 4, 2, 0, 1]),  # c = 5 < K: slots past n repeat slot 0
+])
+def test_knn_ring_hand_worked(K, nodes):
+    """The level-wise k-NN of Appendix D, worked by hand on five points.
+    K = 2 shows the paper's early-exit claim failing: C (0.55) is nearer
+    than A (0.78), yet the whole of level 0 is taken first."""
+    t, cl, mv = _ring_table()
+    q = t.query(cl, mv, K, "knn_ring", 0)
+    assert list(q["node_idx"][0, 0]) == nodes
+    assert q["n_valid"][0, 0] == min(K, 5)
+    exact = t.query(cl, mv, K, "knn", 0)
+    if K == 2:
+        assert list(exact["node_idx"][0, 0]) == [3, 2]
+
+
+def test_knn_ring_is_the_center_voxels_knn_when_it_holds_k_points():
+    """When the center voxel stores at least K points, level 0 alone is
+    searched: the result is the ordinary K nearest of its stored points."""
+    rng = np.random.default_rng(2)
+    P = (rng.random((1, 3000, 3)) * np.float32(0.5)).astype(np.float32)
+    grid = oracle.make_grid((0, 0, 0), (0.125,) * 3, (4, 4, 4), 64, 1)
+    t = oracle.Table(P, grid)
+    nv = int(t.nvox[0])
+    cl = t.vox_lin[:, :nv].astype(np.int32)
+    K = 16
+    q = t.query(cl, np.array([nv], np.int32), K, "knn_ring", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, 64)
+    checked = 0
+    for j in range(nv):
+        s = int(np.searchsorted(tb["vox_lin"], cl[0, j]))
+        own = tb["pt_list"][tb["vox_off"][s]:tb["vox_off"][s + 1]]
+        if len(own) < K:
+            continue
+        g = np.array(pins.decode(int(cl[0, j]), (4, 4, 4)), np.float32)
+        c = (g + np.float32(0.5)) * np.float32(0.125)
+        d = P[0, own] - c
+        d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+        order = np.lexsort((own, d2.view(np.uint32)))
+        assert list(q["node_idx"][0, j]) == list(own[order[:K]])
+        checked += 1
+    assert checked >= 4
+
+
+def test_knn_ring_takes_the_whole_context_in_level_order_when_it_fits():
+    """c <= K: every context point, levels ascending, each level in gathering
+    order (voxel lin, then point index) -- a numpy sort of the block."""
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.make_grid(gs.origin, gs.voxel_size, gs.dims, 4, 2)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(300, 3)
+    K = 64
+    q = t.query(cl, mv, K, "knn_ring", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, 4)
+    g_all = np.stack([lin % gs.dims[0], (lin // gs.dims[0]) % gs.dims[1], lin // (gs.dims[0] * gs.dims[1])], -1)
+    checked = 0
+    for j in range(300):
+        ctx = _context_bruteforce(P[0], lin, tb, int(cl[0, j]), gs.dims, 2)
+        if len(ctx) > K:
+            continue
+        gc = np.array(pins.decode(int(cl[0, j]), gs.dims))
+        level = np.abs(g_all[ctx] - gc).max(axis=1)
+        order = np.lexsort((ctx, lin[ctx], level))
+        assert list(q["node_idx"][0, j, :len(ctx)]) == list(ctx[order])
+        checked += 1
+    assert checked > 50
+
+
+def test_knn_ring_levels_before_the_last_are_whole_and_the_last_is_nearest_first():
+    """On a workload: the chosen nodes take every point of the levels before
+    the last level used, and from that level the nearest by (d^2, index)."""
+    w = W.get_workload("room")
+    P = w.points(B=1)
+    gs = w.layers[0].grid
+    grid = oracle.grid_from_spec(gs)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(400, 9)
+    K = 32
+    q = t.query(cl, mv, K, "knn_ring", 0)
+    lin = oracle.voxelize(P, grid)[0]
+    tb = pins.table_numpy(lin, gs.n_v)
+    g_all = np.stack([lin % gs.dims[0], (lin // gs.dims[0]) % gs.dims[1], lin // (gs.dims[0] * gs.dims[1])], -1)
+    o, s = np.float32(gs.origin), np.float32(gs.voxel_size)
+    partial = 0
+    for j in range(400):
+        ctx = _context_bruteforce(P[0], lin, tb, int(cl[0, j]), gs.dims, 1)
+        gc = np.array(pins.decode(int(cl[0, j]), gs.dims))
+        level = np.abs(g_all[ctx] - gc).max(axis=1)
+        n = int(q["n_valid"][0, j])
+        got = q["node_idx"][0, j, :n]
+        assert n == min(K, len(ctx)) and len(set(got)) == n and set(got) <= set(ctx)
+        lv = dict(zip(ctx, level))
+        last = max(lv[i] for i in got)
+        for i, l in zip(ctx, level):
+            if l < last:
+                assert i in set(got)
+        inlast = ctx[level == last]
+        if len(inlast) > sum(1 for i in got if lv[i] == last):
+            partial += 1
+            c = o + (gc.astype(np.float32) + np.float32(0.5)) * s
+            d = P[0, inlast] - c
+            d2 = (d[:, 0] * d[:, 0] + d[:, 1] * d[:, 1]) + d[:, 2] * d[:, 2]
+            take = sum(1 for i in got if lv[i] == last)
+            best = inlast[np.lexsort((inlast, d2.view(np.uint32)))[:take]]
+            assert list(got[n - take:]) == list(best)
+    assert partial > 20
