@@ -227,6 +227,60 @@ def measure_upsampling(P, P_np, B: int, N: int, wl, with_oracle: bool, reps: int
     return {"query_points": up, "context_list": cx}
 
 
+def measure_knn_ring(P, P_np, B: int, N: int, wl, with_oracle: bool, reps: int = 20) -> dict:
+    """The level-wise k-NN of Appendix D against the exact context k-NN on the
+    layer-1 centers of the bench batch: time per launch, and how far its nodes
+    are from the exact ones (recall, centers with the same node set, and the
+    ratio of the K-th node distance from the voxel center)."""
+    import torch
+    from paper_1912_02984_amd import cagq
+    L = wl.layers[0]
+    g = cagq.build_grid(P, cagq.desc_from_spec(L.grid))
+    cl, _ = cagq.sample_centers(g, L.M, L.sample, L.seed)
+    ex = cagq.query_context(g, cl, L.K, "knn", L.seed)
+    rg = cagq.query_context(g, cl, L.K, "knn_ring", L.seed)
+    ms_ex = _timed(lambda: cagq.query_context(g, cl, L.K, "knn", L.seed, out=ex), reps)
+    ms_rg = _timed(lambda: cagq.query_context(g, cl, L.K, "knn_ring", L.seed, out=rg), reps)
+    # K-th node distance from the center voxel's center (float64)
+    dims = torch.tensor(L.grid.dims, device=P.device, dtype=torch.int64)
+    lin = cl.long()
+    gxyz = torch.stack([lin % dims[0], (lin // dims[0]) % dims[1], lin // (dims[0] * dims[1])], -1).double()
+    q = torch.tensor(L.grid.origin, device=P.device, dtype=torch.float64) + (gxyz + 0.5) * torch.tensor(
+        L.grid.voxel_size, device=P.device, dtype=torch.float64)
+
+    def deviation(exact, ring, K):
+        full = exact["n_valid"] == K
+        a, b_ = ring["node_idx"].long(), exact["node_idx"].long()
+        hit = (a[..., :, None] == b_[..., None, :]).any(-1).sum(-1).float()
+
+        def kth(out):
+            return (out["node_xyz"].double() - q[..., None, :]).norm(dim=-1).max(-1).values
+
+        ratio = kth(ring)[full] / kth(exact)[full].clamp_min(1e-12)
+        return {"K": K, "centers_with_K_nodes": int(full.sum().item()),
+                "recall_vs_exact": round((hit[full] / K).mean().item(), 5),
+                "same_node_set": round((hit[full] == K).float().mean().item(), 5),
+                "kth_distance_ratio_mean": round(ratio.mean().item(), 5),
+                "kth_distance_ratio_max": round(ratio.max().item(), 5)}
+
+    dev = [deviation(ex, rg, L.K)]
+    k2 = max(1, L.K // 4)
+    dev.append(deviation(cagq.query_context(g, cl, k2, "knn", L.seed),
+                         cagq.query_context(g, cl, k2, "knn_ring", L.seed), k2))
+    row = {"workload": f"layer 1 of the bench batch: B={B} x {L.M} centers, K={L.K}, r={L.grid.radius}",
+           "ms": round(ms_rg, 4), "ms_exact": round(ms_ex, 4), "deviation": dev}
+    if with_oracle:
+        import oracle
+        ot = oracle.Table(P_np[:1], oracle.grid_from_spec(L.grid))
+        ocl = np.ascontiguousarray(cl[:1].cpu().numpy())
+        omv = np.full(1, min(L.M, int(ot.nvox[0])), np.int32)
+        t0 = time.perf_counter()
+        ot.query(ocl, omv, L.K, "knn_ring", L.seed)
+        t1 = time.perf_counter()
+        row["oracle"] = {"ms": round((t1 - t0) * 1e3, 2), "cores": 1, "sample": "the centers of 1 of the scenes"}
+    return row
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -384,6 +438,7 @@ def main():
     if not args.no_next:
         next_rows = {"cas_swap": measure_cas_swap(P, P_np, B, N, wls[0].layers[0], with_oracle=not args.no_cpu_baseline)}
         next_rows.update(measure_upsampling(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline))
+        next_rows["knn_ring"] = measure_knn_ring(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline)
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -58,6 +58,7 @@ extern "C" {
 #define CAGQ_SAMPLE_CAS_SWAP 2  /* Coverage-Aware Sampling, challenger / incumbent swaps (Sec. 3.2, Eqs. 2-3) */
 #define CAGQ_QUERY_CUBE 0   /* Cube Query (Sec. 3.2) */
 #define CAGQ_QUERY_KNN 1    /* k-NN among the context points (Sec. 3.2) */
+#define CAGQ_QUERY_KNN_RING 2  /* level-wise k-NN (Appendix D, "CAGQ k-NN"); approximate */
 
 /* Library limits (checked on the host). */
 #define CAGQ_MAX_K 64       /* node points per group */
@@ -181,6 +182,14 @@ CAGQ_API int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, ui
  *   CAGQ_QUERY_CUBE: key = (hi32(h(seed,2,b,lin(v),i)) << 32) | i  (random subset)
  *   CAGQ_QUERY_KNN:  key = (bits(d2) << 32) | i, d2 = (dx*dx + dy*dy) + dz*dz
  *                    in fp32 from q_a = origin_a + ((float)g_a + 0.5f) * voxel_size_a
+ *   CAGQ_QUERY_KNN_RING: the level-wise procedure of Appendix D. Level l of
+ *                    pi(v) is the voxels at Chebyshev distance exactly l; for
+ *                    l = 0, 1, ..., r a level whose points fit in what is
+ *                    left of K is taken whole, in gathering order (voxels by
+ *                    ascending lin, stored points ascending), otherwise its
+ *                    nearest points by the CAGQ_QUERY_KNN key; the search
+ *                    stops at K. Approximate: a level-1 point can be nearer
+ *                    than a level-0 one. Nodes are kept in that order.
  * Node slots k >= n repeat slot 0. Group center (Eqs. 7-8):
  *   w_c = sum of the n node weights (uint32);
  *   chi_c = S / (float)w_c per axis, S the fp32 pairwise sum of
@@ -214,6 +223,8 @@ CAGQ_API int cagq_query_context(const cagq_grid* g, const uint32_t* weights, con
  *                    cagq_query_context (it depends on v only)
  *   CAGQ_QUERY_KNN:  key = (bits(d2) << 32) | i, d2 = (dx*dx + dy*dy) + dz*dz
  *                    in fp32 with d = p_i - q, the center point itself
+ *   CAGQ_QUERY_KNN_RING: the level-wise procedure (see cagq_query_context)
+ *                    with distances from q
  * Node slots k >= n repeat slot 0; an empty context (c = 0) gives n = 0, -1
  * in every node slot and zero coordinates. No group center is formed.
  *   centers     device float [B][M][3]

@@ -27,7 +27,7 @@ ERR_HIP = -6
 ERR_CENTER_NOT_OCCUPIED = -7
 
 SAMPLE = {"rvs": 0, "cas": 1, "cas_swap": 2}
-QUERY = {"cube": 0, "knn": 1}
+QUERY = {"cube": 0, "knn": 1, "knn_ring": 2}
 MAX_K = 64
 MAX_NV = 64
 MAX_RADIUS = 3

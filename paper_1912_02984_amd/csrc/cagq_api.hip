@@ -167,7 +167,7 @@ int cagq_query_context(const cagq_grid* g, const uint32_t* weights, const int32_
     if (rc != CAGQ_OK) return rc;
     if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
     if (K < 1 || K > CAGQ_MAX_K) return CAGQ_ERR_INVALID_ARG;
-    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN) return CAGQ_ERR_INVALID_ARG;
+    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN && mode != CAGQ_QUERY_KNN_RING) return CAGQ_ERR_INVALID_ARG;
     if (!center_lin || !node_idx || !n_valid || !center_xyz || !center_w) return CAGQ_ERR_INVALID_ARG;
     hipError_t e = launch_query(L, g->desc, g->points, g->workspace, weights, center_lin, M, K, mode, seed,
                                 node_idx, node_xyz, n_valid, center_xyz, center_w, ctx_count,
@@ -183,7 +183,7 @@ int cagq_query_points(const cagq_grid* g, const float* centers, int32_t M, int32
     if (rc != CAGQ_OK) return rc;
     if (M < 1 || (int64_t)g->B * M > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
     if (K < 1 || K > CAGQ_MAX_K) return CAGQ_ERR_INVALID_ARG;
-    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN) return CAGQ_ERR_INVALID_ARG;
+    if (mode != CAGQ_QUERY_CUBE && mode != CAGQ_QUERY_KNN && mode != CAGQ_QUERY_KNN_RING) return CAGQ_ERR_INVALID_ARG;
     if (!centers || !node_idx || !n_valid) return CAGQ_ERR_INVALID_ARG;
     hipError_t e = launch_query_points(L, g->desc, g->workspace, centers, M, K, mode, seed, node_idx, node_xyz,
                                        n_valid, ctx_count, center_lin, (hipStream_t)stream);

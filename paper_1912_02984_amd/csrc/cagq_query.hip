@@ -19,6 +19,16 @@
 //      integer sum of the node weights and chi_c the pairwise fp32 sum of
 //      w_k * p_k (shuffle-down tree: stride 1, 2, 4, ...) divided by w_c.
 //
+// The level-wise k-NN (Appendix D, "CAGQ k-NN": levels 0..r of pi(v), a
+// level that fits in what is left of K taken whole as gathered, otherwise its
+// nearest points) probes the block level by level, so that the context is
+// compacted level-major and the levels' cumulative counts fall out of the
+// probe. With L* the first level whose cumulative count reaches K, only the
+// entries up to the end of L* are streamed; entry e gets the key e (gathering
+// order) before L*'s first entry, or throughout when L* fits exactly, and
+// (1 << 62) | (bits(d^2) << 31) | i inside a level L* that does not fit: the
+// K smallest keys are the procedure's nodes, in its order.
+//
 // The upsampling variant (Sec. 3.1: centers arrive through long-range
 // connections, only their nodes are queried) takes center points instead:
 // v is the voxel a point falls in (it need not be occupied), k-NN distances
@@ -50,6 +60,32 @@ Magic make_magic(uint32_t d) {
 __device__ __forceinline__ uint32_t udiv(uint32_t n, const Magic& g) {
     return (uint32_t)(((uint64_t)n * g.m) >> g.sh);
 }
+
+constexpr int kRing = CAGQ_QUERY_KNN_RING;  // the level-wise k-NN mode
+
+// The voxels of the (2R+1)^3 block, R = 3, level by level (Chebyshev distance
+// 0, 1, 2, 3), each level in ascending (dz, dy, dx); packed (dx+3) |
+// (dy+3) << 4 | (dz+3) << 8. The first (2r+1)^3 entries are the block of
+// radius r in the same order.
+struct Shells {
+    uint32_t v[343];
+};
+
+constexpr Shells make_shells() {
+    Shells t{};
+    int n = 0;
+    for (int lev = 0; lev <= 3; ++lev)
+        for (int dz = -lev; dz <= lev; ++dz)
+            for (int dy = -lev; dy <= lev; ++dy)
+                for (int dx = -lev; dx <= lev; ++dx) {
+                    const int ax = dx < 0 ? -dx : dx, ay = dy < 0 ? -dy : dy, az = dz < 0 ? -dz : dz;
+                    const int m = ax > ay ? (ax > az ? ax : az) : (ay > az ? ay : az);
+                    if (m == lev) t.v[n++] = (uint32_t)(dx + 3) | (uint32_t)(dy + 3) << 4 | (uint32_t)(dz + 3) << 8;
+                }
+    return t;
+}
+
+__constant__ Shells kShells = make_shells();
 
 struct QGrid {
     float o[3];
@@ -229,6 +265,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     // center voxel is one of them (q = nnb / 2), so its own check costs
     // nothing extra
     uint32_t nocc = 0, c = 0;
+    uint32_t cum[RAD + 1];  // level-wise mode: context points of levels 0..l
     bool occupied = false;
     const int gshift = lane & ~(G - 1);
     const uint64_t gmask = G == 64 ? ~0ull : ((1ull << G) - 1);
@@ -237,9 +274,17 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         bool occ = false;
         uint32_t st = 0, cnt = 0;
         if (in_grid && q < nnb) {
-            const int32_t x = gx + q % side - rad;
-            const int32_t y = gy + (q / side) % side - rad;
-            const int32_t z = gz + q / (side * side) - rad;
+            int32_t x, y, z;
+            if (MODE == kRing) {
+                const uint32_t o = kShells.v[q];
+                x = gx + (int32_t)(o & 15u) - 3;
+                y = gy + (int32_t)((o >> 4) & 15u) - 3;
+                z = gz + (int32_t)(o >> 8) - 3;
+            } else {
+                x = gx + q % side - rad;
+                y = gy + (q / side) % side - rad;
+                z = gz + q / (side * side) - rad;
+            }
             if (x >= 0 && y >= 0 && z >= 0 && x < g.D[0] && y < g.D[1] && z < g.D[2]) {
                 const uint32_t nl = (uint32_t)x + (uint32_t)g.D[0] * ((uint32_t)y + (uint32_t)g.D[1] * (uint32_t)z);
                 const int32_t sl = slot_of(bm, wr, nl);
@@ -251,12 +296,21 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             }
         }
         const uint64_t mask = (__ballot(occ) >> gshift) & gmask;
-        if (nnb / 2 >= q0 && nnb / 2 < q0 + G) occupied = (mask >> (nnb / 2 - q0)) & 1ull;
+        constexpr int qc = MODE == kRing ? 0 : nnb / 2;  // the center voxel's probe index
+        if (qc >= q0 && qc < q0 + G) occupied = (mask >> (qc - q0)) & 1ull;
         const uint32_t pos = nocc + (uint32_t)__popcll(mask & ((1ull << lg) - 1));
         const uint32_t incl = gscan_incl<G>(cnt, lg);
         if (occ) {
             s_st[pos] = st;
             s_pre[pos] = c + incl - cnt;
+        }
+        if (MODE == kRing) {
+            // level l ends at probe index (2l+1)^3 - 1
+#pragma unroll
+            for (int l = 0; l <= RAD; ++l) {
+                const int last = (2 * l + 1) * (2 * l + 1) * (2 * l + 1) - 1;
+                if (last >= q0 && last < q0 + G) cum[l] = c + (uint32_t)__shfl((int)incl, last - q0, G);
+            }
         }
         c += gbcast<G>(incl, G - 1);
         nocc += (uint32_t)__popcll(mask);
@@ -287,10 +341,27 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         qy = g.o[1] + ((float)gy + 0.5f) * g.s[1];
         qz = g.o[2] + ((float)gz + 0.5f) * g.s[2];
     }
+    // the entries streamed: all c, or in the level-wise mode those up to the
+    // end of L*, the first level whose cumulative count reaches K; `base` is
+    // where L* starts, `part` whether L* is cut
+    uint32_t cs = c, base = 0;
+    bool part = false;
+    if (MODE == kRing && c >= (uint32_t)K) {
+        int ls = RAD;
+#pragma unroll
+        for (int l = RAD - 1; l >= 0; --l)
+            if (cum[l] >= (uint32_t)K) ls = l;
+        cs = cum[ls];
+        base = 0;
+#pragma unroll
+        for (int l = 0; l < RAD; ++l)
+            if (l + 1 == ls) base = cum[l];
+        part = cs > (uint32_t)K;
+    }
     uint64_t bk = ~0ull;
     uint32_t bp = 0;
     // the chunk loop runs the same number of times for every group of the wave
-    uint32_t cmax = c;
+    uint32_t cmax = cs;
 #pragma unroll
     for (int d = G; d < kWave; d <<= 1) {
         const uint32_t o = xlane(cmax, d);
@@ -299,7 +370,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     // a context of at most G points is one chunk: its points and weights stay
     // in the lanes that loaded them, and the sort carries the lane (entry)
     // instead of the position in the copy
-    const bool one = c <= (uint32_t)G;
+    const bool one = cs <= (uint32_t)G;
     // the sort levels that matter: up to the smallest power of two >= cmax
     uint32_t top = 2;
     while (top < cmax && top < (uint32_t)G) top <<= 1;
@@ -309,7 +380,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         const uint32_t e = e0 + lg;
         uint64_t key = ~0ull;
         uint32_t pos = 0;
-        if (e < c) {
+        if (e < cs) {
             // the compacted voxel holding context entry e
             uint32_t lo = 0, hi = nocc - 1;
             while (lo < hi) {
@@ -331,7 +402,11 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
                 const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
                 const float sxy = xx + yy;
                 const float d2 = sxy + zz;
-                key = ((uint64_t)__float_as_uint(d2) << 32) | i;
+                if (MODE == kRing)
+                    key = (part && e >= base) ? (1ull << 62) | ((uint64_t)__float_as_uint(d2) << 31) | i
+                                              : (uint64_t)e;
+                else
+                    key = ((uint64_t)__float_as_uint(d2) << 32) | i;
             }
         }
         gsort<G>(key, pos, lg, top);
@@ -350,22 +425,27 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     const uint64_t k0 = ((uint64_t)gbcast<G>((uint32_t)(bk >> 32), 0) << 32) | gbcast<G>((uint32_t)bk, 0);
     const uint64_t mine = own ? bk : k0;
     const uint32_t mpos = own ? bp : gbcast<G>(bp, 0);
-    const uint32_t idx = n ? (uint32_t)mine : 0u;
+    // the node's point index is the key's low half, except in the level-wise
+    // mode, whose keys order by position: there it comes with the point
+    uint32_t idx = n ? (uint32_t)mine : 0u;
     // a one-chunk context reads node point and weight from the lane holding
     // them; a longer one reads them again
     const int from = one ? (int)mpos : 0;
     float x = __shfl(v0.x, from, G), y = __shfl(v0.y, from, G), z = __shfl(v0.z, from, G);
     uint32_t w = (uint32_t)__shfl((int)w0, from, G);
+    if (MODE == kRing) idx = (uint32_t)__shfl((int)__float_as_uint(v0.w), from, G);
     if (!one) {
         const float4 pv = p4[mpos];
         x = pv.x;
         y = pv.y;
         z = pv.z;
+        if (MODE == kRing) idx = __float_as_uint(pv.w);
         w = Wt ? Wt[(size_t)b * N + idx] : 1u;
     }
     if (!n) {
         x = y = z = 0.0f;
         w = 1u;
+        idx = 0u;
     }
     if (UP) {
         if (live && lg < K) {
@@ -494,8 +574,10 @@ hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* p
                      nullptr};
     if (mode == CAGQ_QUERY_CUBE)
         launch_mode<CAGQ_QUERY_CUBE, false>(L, g, d.radius, ws, io, M, K, seed, s);
-    else
+    else if (mode == CAGQ_QUERY_KNN)
         launch_mode<CAGQ_QUERY_KNN, false>(L, g, d.radius, ws, io, M, K, seed, s);
+    else
+        launch_mode<kRing, false>(L, g, d.radius, ws, io, M, K, seed, s);
     return hipGetLastError();
 }
 
@@ -507,8 +589,10 @@ hipError_t launch_query_points(const Layout& L, const cagq_grid_desc& d, void* w
                      center_lin};
     if (mode == CAGQ_QUERY_CUBE)
         launch_mode<CAGQ_QUERY_CUBE, true>(L, g, d.radius, ws, io, M, K, seed, s);
-    else
+    else if (mode == CAGQ_QUERY_KNN)
         launch_mode<CAGQ_QUERY_KNN, true>(L, g, d.radius, ws, io, M, K, seed, s);
+    else
+        launch_mode<kRing, true>(L, g, d.radius, ws, io, M, K, seed, s);
     return hipGetLastError();
 }
 

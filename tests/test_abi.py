@@ -141,7 +141,7 @@ def test_query_rejects_bad_arguments():
         C.byref(g), None, cl, M, K, mode, 1, ni, None, nv, cx, cw, None, None)
     assert args(K=0) == cagq.ERR_INVALID_ARG
     assert args(K=65) == cagq.ERR_INVALID_ARG
-    assert args(mode=2) == cagq.ERR_INVALID_ARG
+    assert args(mode=3) == cagq.ERR_INVALID_ARG
     assert args(M=0) == cagq.ERR_INVALID_ARG
     assert args(ni=None) == cagq.ERR_INVALID_ARG
     assert args(nv=None) == cagq.ERR_INVALID_ARG
@@ -158,7 +158,7 @@ def test_query_points_rejects_bad_arguments():
         C.byref(g), c, M, K, mode, 1, ni, None, nv, None, None, None)
     assert args(K=0) == cagq.ERR_INVALID_ARG
     assert args(K=65) == cagq.ERR_INVALID_ARG
-    assert args(mode=2) == cagq.ERR_INVALID_ARG
+    assert args(mode=3) == cagq.ERR_INVALID_ARG
     assert args(M=0) == cagq.ERR_INVALID_ARG
     assert args(c=None) == cagq.ERR_INVALID_ARG
     assert args(ni=None) == cagq.ERR_INVALID_ARG

@@ -423,3 +423,49 @@ def test_context_list_capacity_and_outside_lin():
     assert o2[57 + 1] == o2[57]
     with pytest.raises(oracle.OracleError, match="-7"):
         ot.context_list(_np(bad))
+
+
+# ---------------------------------------------------------------- level-wise k-NN (Appendix D)
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room", "bigroom/cas-knn", "lidar"])
+def test_knn_ring_workloads(name):
+    """Layer 1 of each workload with the level-wise k-NN, at full size."""
+    w = W.get_workload(name)
+    P = w.points()
+    L = w.layers[0]
+    print(f"[parity] knn_ring {name}: B={P.shape[0]} N={P.shape[1]} M={L.M} K={L.K} r={L.grid.radius}", flush=True)
+    run_both(P, L.grid, L.M, L.K, L.sample, "knn_ring", L.seed, where=f"{name} ring")
+
+
+@pytest.mark.parametrize("r", [1, 2, 3])
+@pytest.mark.parametrize("K", [1, 5, 32, 64])
+def test_knn_ring_radius_and_node_counts(r, K):
+    """Levels cut at every position: clustered points with small and large
+    voxel populations, n_v binding, weights."""
+    rng = np.random.default_rng(100 * r + K)
+    B, N = 2, 4000
+    P = (rng.random((B, N, 3), dtype=np.float32) ** 3).astype(np.float32)
+    spec = _spec((0, 0, 0), (0.05,) * 3, (20, 20, 20), 16, r)
+    wts = rng.integers(1, 9, (B, N)).astype(np.uint32)
+    run_both(P, spec, 300, K, "rvs", "knn_ring", 4, weights=wts, where=f"ring r={r} K={K}")
+
+
+def test_knn_ring_hand_worked_on_gpu():
+    """The five-point example worked by hand for the oracle's pins."""
+    P = np.array([[[2.5, 3.6, 2.5], [2.95, 2.95, 2.95], [3.05, 2.5, 2.5], [2.5, 2.5, 2.9],
+                   [1.9, 2.5, 2.5]]], np.float32)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.make_desc((0, 0, 0), (1, 1, 1), (5, 5, 5), 8, 1))
+    cl = torch.tensor([[62]], dtype=torch.int32, device=DEV)
+    for K, nodes in [(1, [3]), (2, [1, 3]), (3, [1, 3, 2]), (5, [1, 3, 4, 2, 0]), (6, [1, 3, 4, 2, 0, 1])]:
+        q = cagq.query_context(g, cl, K, "knn_ring", 0)
+        assert _np(q["node_idx"])[0, 0].tolist() == nodes, K
+    assert cagq.get_device_status(g) == 0
+
+
+@pytest.mark.parametrize("r", [1, 2])
+def test_query_points_knn_ring(r):
+    rng = np.random.default_rng(r)
+    P = (rng.random((2, 3000, 3), dtype=np.float32) ** 2 * np.float32(0.7)).astype(np.float32)
+    Q = rng.random((2, 900, 3), dtype=np.float32)
+    spec = _spec((0, 0, 0), (0.05,) * 3, (20, 20, 20), 8, r)
+    run_up(P, spec, Q, 16, "knn_ring", 0, where=f"up ring r={r}", context=False)
