@@ -66,8 +66,12 @@ def lib():
         L.orc_query_points.argtypes = [C.POINTER(_Table), P, P, C.c_int32, C.c_int32, C.c_int32, C.c_uint64,
                                        P, P, P, P, P]
         L.orc_context_list.argtypes = [C.POINTER(_Table), P, C.c_int32, P, P, C.c_int64]
+        L.orc_sample_points.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, P]
+        L.orc_ball_query.argtypes = [P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32, C.c_float, P, P]
+        L.orc_coverage.argtypes = [C.POINTER(_Table), P, P, P, C.c_int32, C.c_int32, P]
         for f in ("orc_voxelize", "orc_build_table", "orc_sample_rvs", "orc_sample_cas", "orc_sample_cas_swap",
-                  "orc_query", "orc_query_points", "orc_context_list"):
+                  "orc_query", "orc_query_points", "orc_context_list", "orc_sample_points", "orc_ball_query",
+                  "orc_coverage"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -225,6 +229,42 @@ class Table:
         _check(lib().orc_context_list(C.byref(self._t), _ptr(cl), M, _ptr(off), _ptr(idx), int(off[-1])),
                "orc_context_list")
         return off, idx[: int(off[-1])]
+
+    def coverage(self, node_idx: np.ndarray, n_valid: np.ndarray, points: Optional[np.ndarray] = None) -> np.ndarray:
+        """Occupied voxels [B] holding a valid node point (Sec. 4)."""
+        P = self.points if points is None else np.ascontiguousarray(points, np.float32)
+        ni = np.ascontiguousarray(node_idx, np.int32)
+        nv = np.ascontiguousarray(n_valid, np.int32)
+        B, M, K = ni.shape
+        out = np.zeros(B, np.int32)
+        _check(lib().orc_coverage(C.byref(self._t), _ptr(P), _ptr(ni), _ptr(nv), M, K, _ptr(out)), "orc_coverage")
+        return out
+
+
+SAMPLE_POINT_MODES = {"rps": 0, "fps": 1}
+
+
+def sample_points(points: np.ndarray, M: int, mode: str, seed: int = 0) -> np.ndarray:
+    """Random / Farthest Point Sampling: center point indices [B][M]."""
+    P = np.ascontiguousarray(points, np.float32)
+    B, N = P.shape[:2]
+    out = np.zeros((B, M), np.int32)
+    _check(lib().orc_sample_points(_ptr(P), B, N, M, SAMPLE_POINT_MODES[mode], C.c_uint64(seed), _ptr(out)),
+           "orc_sample_points")
+    return out
+
+
+def ball_query(points: np.ndarray, center_idx: np.ndarray, K: int, radius2: float):
+    """Ball Query: (node_idx [B][M][K], n_valid [B][M])."""
+    P = np.ascontiguousarray(points, np.float32)
+    ci = np.ascontiguousarray(center_idx, np.int32)
+    B, N = P.shape[:2]
+    M = ci.shape[1]
+    ni = np.zeros((B, M, K), np.int32)
+    nv = np.zeros((B, M), np.int32)
+    _check(lib().orc_ball_query(_ptr(P), B, N, _ptr(ci), M, K, C.c_float(radius2), _ptr(ni), _ptr(nv)),
+           "orc_ball_query")
+    return ni, nv
 
 
 def run_layer(points: np.ndarray, layer, weights: Optional[np.ndarray] = None):

@@ -63,9 +63,15 @@
  *   context   Sec. 3.3, grid context pooling: every context point of a
  *             center. Reading: voxels of pi(v) in ascending lin, stored
  *             points ascending, concatenated over the batch (CSR offsets).
+ *   RPS, FPS, Ball Query (Sec. 4, the comparison methods): RPS = the M
+ *             points of smallest key hi32(h(seed, 4, b, i)) << 32 | i in
+ *             ascending index; FPS from point 0, farthest by d^2 to the
+ *             chosen set, ties to the lowest index, pick order; Ball Query =
+ *             the first K points in index order with d^2 < R^2.
+ *   coverage  Sec. 4: occupied voxels holding a node point / |O_v|.
  *   h         splitmix64 chain: h(seed, tag, a1..ak) =
  *             sm64(...sm64(sm64(seed ^ tag) ^ a1)... ^ ak), tags RVS=1,
- *             CUBE=2, CAS-P=3 (splitmix64: Steele, Lea, Flood, OOPSLA 2014).
+ *             CUBE=2, CAS-P=3, RPS=4 (splitmix64: Steele, Lea, Flood, OOPSLA 2014).
  *
  * Pins (tests marked "not gpu"): splitmix64 published outputs; voxelize vs
  * a numpy fp32 re-derivation and hand-placed boundary points; the table vs
@@ -695,5 +701,117 @@ int orc_context_list(const orc_table* t, const int32_t* center_lin, int32_t M, i
     ctx_off[(size_t)t->B * M] = total;
     free(nbs);
     if (rc == 0 && ctx_idx && total > capacity) rc = ORC_ECAPACITY;
+    return rc;
+}
+
+/* ------------------------------------------------------------------------
+ * Comparison methods of Sec. 4 (tab:query): Random Point Sampling, Farthest
+ * Point Sampling and Ball Query, and the occupied-space coverage metric.
+ * They are what CAGQ is measured against, not CAGQ.
+ * ------------------------------------------------------------------------ */
+
+/* d^2 between points a and b, fp32: (dx*dx + dy*dy) + dz*dz. */
+static float dist2(const float* a, const float* b) {
+    float dx = a[0] - b[0], dy = a[1] - b[1], dz = a[2] - b[2];
+    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+    float s = xx + yy;
+    return s + zz;
+}
+
+/* RPS (mode 0): M input points, every point equally likely -- the M points
+ * of smallest key (hi32(h(seed, 4, b, i)) << 32) | i, in ascending index.
+ * FPS (mode 1): start at point 0; each next center is the point farthest
+ * (largest d^2 to its nearest chosen center; ties to the lowest index) from
+ * the chosen ones, in pick order. 1 <= M <= N. center_idx [B][M]. */
+int orc_sample_points(const float* pts, int32_t B, int32_t N, int32_t M, int32_t mode, uint64_t seed,
+                      int32_t* center_idx) {
+    if (!pts || !center_idx || B < 1 || N < 1 || M < 1 || M > N || (mode != 0 && mode != 1)) return ORC_EINVAL;
+    uint64_t* key = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)N);
+    float* dmin = (float*)malloc(sizeof(float) * (size_t)N);
+    if (!key || !dmin) { free(key); free(dmin); return ORC_EINVAL; }
+    for (int32_t b = 0; b < B; ++b) {
+        const float* P = pts + (size_t)b * N * 3;
+        int32_t* c = center_idx + (size_t)b * M;
+        if (mode == 0) {
+            uint64_t hb = orc_splitmix64(orc_splitmix64(seed ^ 4ull) ^ (uint64_t)b);
+            for (int32_t i = 0; i < N; ++i) key[i] = ((orc_splitmix64(hb ^ (uint64_t)i) >> 32) << 32) | (uint32_t)i;
+            qsort(key, (size_t)N, sizeof(uint64_t), cmp_u64);
+            for (int32_t j = 0; j < M; ++j) key[j] &= 0xFFFFFFFFu;
+            qsort(key, (size_t)M, sizeof(uint64_t), cmp_u64);
+            for (int32_t j = 0; j < M; ++j) c[j] = (int32_t)key[j];
+        } else {
+            int32_t cur = 0;
+            for (int32_t i = 0; i < N; ++i) dmin[i] = INFINITY;
+            for (int32_t j = 0; j < M; ++j) {
+                c[j] = cur;
+                int32_t best = 0;
+                float bd = -1.0f;
+                for (int32_t i = 0; i < N; ++i) {
+                    float d = dist2(P + 3 * (size_t)i, P + 3 * (size_t)cur);
+                    if (d < dmin[i]) dmin[i] = d;
+                    if (dmin[i] > bd) { bd = dmin[i]; best = i; }
+                }
+                cur = best;
+            }
+        }
+    }
+    free(key);
+    free(dmin);
+    return 0;
+}
+
+/* Ball Query: per center point, the first K points in index order with
+ * d^2 < radius2 (fp32 as dist2) among all N points of its cloud; n_valid =
+ * their number; slots k >= n repeat slot 0 (n >= 1 when the center is one
+ * of the points). center_idx [B][M], node_idx [B][M][K], n_valid [B][M]. */
+int orc_ball_query(const float* pts, int32_t B, int32_t N, const int32_t* center_idx, int32_t M, int32_t K,
+                   float radius2, int32_t* node_idx, int32_t* n_valid) {
+    if (!pts || !center_idx || !node_idx || !n_valid || B < 1 || N < 1 || M < 1 || K < 1) return ORC_EINVAL;
+    for (int32_t b = 0; b < B; ++b) {
+        const float* P = pts + (size_t)b * N * 3;
+        for (int32_t j = 0; j < M; ++j) {
+            size_t cj = (size_t)b * M + j;
+            int32_t ci = center_idx[cj];
+            if (ci < 0 || ci >= N) return ORC_EINVAL;
+            int32_t* ni = node_idx + cj * K;
+            int32_t n = 0;
+            for (int32_t i = 0; i < N && n < K; ++i)
+                if (dist2(P + 3 * (size_t)i, P + 3 * (size_t)ci) < radius2) ni[n++] = i;
+            for (int32_t k = n; k < K; ++k) ni[k] = n ? ni[0] : -1;
+            n_valid[cj] = n;
+        }
+    }
+    return 0;
+}
+
+/* Occupied-space coverage (Sec. 4): per cloud, the number of occupied
+ * voxels holding at least one valid node point of any group (the metric is
+ * this over |O_v|). node_idx [B][M][K] point indices, n_valid [B][M];
+ * covered [B]. */
+int orc_coverage(const orc_table* t, const float* pts, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
+                 int32_t K, int32_t* covered) {
+    if (!table_ok(t) || !pts || !node_idx || !n_valid || !covered || M < 1 || K < 1) return ORC_EINVAL;
+    uint32_t* lin = (uint32_t*)malloc(sizeof(uint32_t) * (size_t)t->N);
+    uint8_t* hit = (uint8_t*)malloc((size_t)t->N);
+    if (!lin || !hit) { free(lin); free(hit); return ORC_EINVAL; }
+    int rc = 0;
+    for (int32_t b = 0; b < t->B; ++b) {
+        orc_voxelize(pts + (size_t)b * t->N * 3, t->N, &t->g, lin);
+        memset(hit, 0, (size_t)t->N);
+        for (int32_t j = 0; j < M; ++j) {
+            size_t cj = (size_t)b * M + j;
+            for (int32_t k = 0; k < n_valid[cj] && k < K; ++k) {
+                int32_t i = node_idx[cj * K + k];
+                if (i < 0 || i >= t->N) { rc = ORC_EINVAL; continue; }
+                int32_t s = find_slot(t, b, lin[i]);
+                if (s >= 0) hit[s] = 1;
+            }
+        }
+        int32_t n = 0;
+        for (int32_t s = 0; s < t->nvox[b]; ++s) n += hit[s];
+        covered[b] = n;
+    }
+    free(lin);
+    free(hit);
     return rc;
 }

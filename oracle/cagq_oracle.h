@@ -96,6 +96,23 @@ int orc_query_points(const orc_table* t, const float* pts, const float* centers,
 int orc_context_list(const orc_table* t, const int32_t* center_lin, int32_t M, int64_t* ctx_off,
                      int32_t* ctx_idx, int64_t capacity);
 
+/* Comparison methods of Sec. 4 and the coverage metric (not CAGQ).
+ * orc_sample_points: mode 0 Random Point Sampling (M smallest
+ * hi32(h(seed,4,b,i)) << 32 | i, ascending index), mode 1 Farthest Point
+ * Sampling from point 0 (pick order); 1 <= M <= N; center_idx [B][M]. */
+int orc_sample_points(const float* pts, int32_t B, int32_t N, int32_t M, int32_t mode, uint64_t seed,
+                      int32_t* center_idx);
+
+/* Ball Query: the first K points in index order with d^2 < radius2 around
+ * each center point; slots past n repeat slot 0 (-1 when n = 0). */
+int orc_ball_query(const float* pts, int32_t B, int32_t N, const int32_t* center_idx, int32_t M, int32_t K,
+                   float radius2, int32_t* node_idx, int32_t* n_valid);
+
+/* Occupied-space coverage (Sec. 4): covered [B] = occupied voxels holding a
+ * valid node point (the metric is covered / nvox). */
+int orc_coverage(const orc_table* t, const float* pts, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
+                 int32_t K, int32_t* covered);
+
 #ifdef __cplusplus
 }
 #endif

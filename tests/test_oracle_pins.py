@@ -844,3 +844,94 @@ def test_knn_ring_levels_before_the_last_are_whole_and_the_last_is_nearest_first
             best = inlast[np.lexsort((inlast, d2.view(np.uint32)))[:take]]
             assert list(got[n - take:]) == list(best)
     assert partial > 20
+
+
+# ---------------------------------------------------------------- comparison methods and coverage (Sec. 4)
+
+def test_rps_is_the_m_smallest_keys_in_index_order():
+    P = W.uniform_cube(2, 700, 3)
+    c = oracle.sample_points(P, 90, "rps", 17)
+    for b in range(2):
+        keys = [((pins.py_chain(17, 4, b, i) >> 32) << 32) | i for i in range(700)]
+        assert list(c[b]) == sorted(int(k & 0xFFFFFFFF) for k in sorted(keys)[:90])
+
+
+def _fps_numpy(P, M):
+    """Farthest point sampling in numpy fp32, from point 0."""
+    d = np.full(P.shape[0], np.inf, np.float32)
+    out, cur = [], 0
+    for _ in range(M):
+        out.append(cur)
+        v = P - P[cur]
+        d2 = (v[:, 0] * v[:, 0] + v[:, 1] * v[:, 1]) + v[:, 2] * v[:, 2]
+        d = np.minimum(d, d2)
+        cur = int(np.argmax(d))  # first maximum: ties to the lowest index
+    return out
+
+
+def test_fps_matches_numpy_farthest_point_sampling():
+    P = W.uniform_cube(2, 600, 8)
+    P[1, 100:140] = P[1, 0]  # duplicates: ties and zero distances
+    c = oracle.sample_points(P, 120, "fps", 0)
+    for b in range(2):
+        assert list(c[b]) == _fps_numpy(P[b], 120)
+
+
+def test_fps_picks_are_farthest_and_spread_shrinks():
+    """Each pick maximises the distance to the chosen set, so the sequence of
+    pick distances never increases (Gonzalez's 2-approximation property)."""
+    P = W.get_workload("object").points()[:1]
+    c = oracle.sample_points(P, 64, "fps", 0)[0]
+    X = P[0].astype(np.float64)
+    prev = np.inf
+    for j in range(1, 64):
+        dj = np.min(((X[c[:j]] - X[c[j]]) ** 2).sum(1))
+        dall = np.min(((X[c[:j], None, :] - X[None, :, :]) ** 2).sum(-1), axis=0).max()
+        assert dj <= prev + 1e-9 and abs(dj - dall) <= 1e-6 * max(1.0, dall)
+        prev = dj
+
+
+def test_ball_query_is_the_first_k_inside_the_radius():
+    P = W.get_workload("room").points(B=1)
+    c = oracle.sample_points(P, 200, "rps", 1)
+    r2 = np.float32(0.186) ** 2
+    K = 16
+    ni, nv = oracle.ball_query(P, c, K, float(r2))
+    for j in range(200):
+        v = P[0] - P[0, c[0, j]]
+        d2 = (v[:, 0] * v[:, 0] + v[:, 1] * v[:, 1]) + v[:, 2] * v[:, 2]
+        inside = np.nonzero(d2 < r2)[0][:K]
+        n = len(inside)
+        assert nv[0, j] == n >= 1
+        assert list(ni[0, j, :n]) == list(inside) and np.all(ni[0, j, n:] == inside[0])
+
+
+def test_coverage_is_the_share_of_occupied_voxels_holding_a_node():
+    w = W.get_workload("room")
+    P = w.points(B=2)
+    grid = oracle.grid_from_spec(w.layers[0].grid)
+    t = oracle.Table(P, grid)
+    cl, mv = t.sample_rvs(300, 2)
+    q = t.query(cl, mv, 16, "cube", 2)
+    cov = t.coverage(q["node_idx"], q["n_valid"])
+    lin = oracle.voxelize(P, grid)
+    for b in range(2):
+        nodes = np.concatenate([q["node_idx"][b, j, :q["n_valid"][b, j]] for j in range(300)])
+        assert cov[b] == len(np.unique(lin[b, nodes]))
+        assert t.nvox[b] == len(np.unique(lin[b]))
+
+
+@pytest.mark.parametrize("name", ["object", "room"])
+def test_cas_covers_more_than_rvs(name):
+    """Sec. 4: CAS leads the occupied-space coverage (beta = 0), as in every
+    row of the paper's latency/coverage tables."""
+    w = W.get_workload(name)
+    L = w.layers[0]
+    P = w.points()[:4]
+    t = oracle.Table(P, oracle.grid_from_spec(L.grid))
+    M = max(8, int(t.nvox.min()) // 8)
+    cas, mc, _, _ = t.sample_cas(M)
+    rvs, mr = t.sample_rvs(M, 3)
+    a = t.query(cas, mc, L.K, "cube", 0)
+    b = t.query(rvs, mr, L.K, "cube", 0)
+    assert np.all(t.coverage(a["node_idx"], a["n_valid"]) > t.coverage(b["node_idx"], b["n_valid"]))
