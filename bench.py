@@ -281,6 +281,46 @@ def measure_knn_ring(P, P_np, B: int, N: int, wl, with_oracle: bool, reps: int =
     return row
 
 
+def measure_coverage(P, B: int, N: int, wl, reps: int = 3) -> dict:
+    """Sec. 4's comparison on the layer-1 shape of the bench batch: latency of
+    the whole data structuring (sampling + query; CAGQ includes its grid
+    build) and the occupied-space coverage of the nodes, for RPS / FPS with
+    Ball Query (radius giving the ball the cube's volume) and for RVS / CAS
+    with Cube Query and k-NN. Coverage is the mean over the clouds of the
+    occupied voxels holding a node over all occupied voxels."""
+    import math
+    import torch
+    from paper_1912_02984_amd import cagq
+    L = wl.layers[0]
+    desc = cagq.desc_from_spec(L.grid)
+    g = cagq.build_grid(P, desc)
+    nvox = g.table()["nvox"].double()
+    edge = (2 * L.grid.radius + 1) * L.grid.voxel_size[0]
+    radius = edge * (3.0 / (4.0 * math.pi)) ** (1.0 / 3.0)
+    r2 = float(np.float32(radius) ** 2)
+    rows = {}
+
+    def cagq_run(sample, query):
+        gg = cagq.build_grid(P, desc)
+        cl, _ = cagq.sample_centers(gg, L.M, sample, L.seed)
+        return cagq.query_context(gg, cl, L.K, query, L.seed)
+
+    def base_run(sample, query):
+        c = cagq.sample_points(P, L.M, sample, L.seed)
+        return cagq.ball_query(P, c, L.K, r2)
+
+    for name, fn in [("RPS+Ball", lambda: base_run("rps", "ball")), ("FPS+Ball", lambda: base_run("fps", "ball")),
+                     ("RVS+Cube", lambda: cagq_run("rvs", "cube")), ("CAS+Cube", lambda: cagq_run("cas", "cube")),
+                     ("RVS+kNN", lambda: cagq_run("rvs", "knn")), ("CAS+kNN", lambda: cagq_run("cas", "knn"))]:
+        ms = _timed(fn, reps)
+        out = fn()
+        cov = cagq.coverage(g, out["node_idx"], out["n_valid"]).double() / nvox
+        rows[name] = {"ms": round(ms, 3), "coverage": round(cov.mean().item(), 4)}
+    return {"workload": f"B={B} x {N} points, M={L.M}, K={L.K}, {tuple(L.grid.dims)} voxels of "
+                        f"{L.grid.voxel_size[0]:.2f} m, r={L.grid.radius}; ball radius {radius:.4f} m",
+            "methods": rows}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -439,6 +479,7 @@ def main():
         next_rows = {"cas_swap": measure_cas_swap(P, P_np, B, N, wls[0].layers[0], with_oracle=not args.no_cpu_baseline)}
         next_rows.update(measure_upsampling(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline))
         next_rows["knn_ring"] = measure_knn_ring(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline)
+        next_rows["coverage"] = measure_coverage(P, B, N, wls[0])
 
     cpu = None
     if not args.no_cpu_baseline:

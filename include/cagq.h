@@ -60,6 +60,9 @@ extern "C" {
 #define CAGQ_QUERY_KNN 1    /* k-NN among the context points (Sec. 3.2) */
 #define CAGQ_QUERY_KNN_RING 2  /* level-wise k-NN (Appendix D, "CAGQ k-NN"); approximate */
 
+#define CAGQ_POINTS_RPS 0   /* Random Point Sampling (comparison method, Sec. 4) */
+#define CAGQ_POINTS_FPS 1   /* Farthest Point Sampling (comparison method, Sec. 4) */
+
 /* Library limits (checked on the host). */
 #define CAGQ_MAX_K 64       /* node points per group */
 #define CAGQ_MAX_NV 64      /* points stored per voxel */
@@ -263,6 +266,44 @@ CAGQ_API int cagq_context_offsets(const cagq_grid* g, const int32_t* center_lin,
                                   void* stream);
 CAGQ_API int cagq_context_list(const cagq_grid* g, const int32_t* center_lin, int32_t M, const int64_t* ctx_off,
                                int32_t* ctx_idx, int64_t capacity, void* stream);
+
+/*
+ * The comparison methods of Sec. 4 (the latency and coverage tables): what
+ * CAGQ replaces, provided to measure it against. They work on raw points
+ * and need no grid.
+ * cagq_sample_points chooses M of the N points of each cloud:
+ *   CAGQ_POINTS_RPS: Random Point Sampling, every point equally likely: the
+ *     M points of smallest key (hi32(h(seed,4,b,i)) << 32) | i (h as in
+ *     cagq_sample_centers), in ascending index;
+ *   CAGQ_POINTS_FPS: Farthest Point Sampling from point 0: each next center
+ *     is the point whose d^2 to its nearest chosen center is largest (ties
+ *     to the lowest index), in pick order; one workgroup per cloud keeps
+ *     the distances in registers, so N <= 81920.
+ *   points [B][N][3], center_idx [B][M] (point indices), 1 <= M <= N.
+ * cagq_ball_query: per center point p_c, the first K points in index order
+ *   with d^2 < radius2 among all N points of its cloud (the O(MN) search);
+ *   n_valid = their number; slots k >= n repeat slot 0. A center index
+ *   outside [0, N) gets n = 0 and -1 in every slot.
+ *   center_idx [B][M], node_idx [B][M][K], n_valid [B][M].
+ * d^2 = (dx*dx + dy*dy) + dz*dz in fp32 throughout.
+ */
+CAGQ_API int cagq_sample_points(const float* points, int32_t B, int32_t N, int32_t M, int32_t mode, uint64_t seed,
+                                int32_t* center_idx, void* stream);
+CAGQ_API int cagq_ball_query(const float* points, int32_t B, int32_t N, const int32_t* center_idx, int32_t M,
+                             int32_t K, float radius2, int32_t* node_idx, int32_t* n_valid, void* stream);
+
+/*
+ * Occupied-space coverage (Sec. 4: the voxels occupied by the node points of
+ * all groups over the voxels occupied by the N points), on the voxels of a
+ * built grid: covered[b] = the occupied voxels of cloud b holding at least
+ * one valid node point (node slots k < n_valid); the metric is covered[b] /
+ * nvox[b]. Node indices refer to the grid's points; any method's nodes
+ * qualify (cagq_query_*, cagq_ball_query).
+ *   node_idx device int32 [B][M][K], n_valid device int32 [B][M],
+ *   covered  device int32 [B]. Uses the grid's workspace.
+ */
+CAGQ_API int cagq_coverage(const cagq_grid* g, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
+                           int32_t K, int32_t* covered, void* stream);
 
 /* Synchronises `stream` and returns the first device-side error recorded in
  * g's workspace since it was last built (CAGQ_OK if none). */

@@ -76,12 +76,15 @@ def lib() -> C.CDLL:
                                         P, P, P, P, P, P]
         L.cagq_context_offsets.argtypes = [C.POINTER(GridC), P, C.c_int32, P, P]
         L.cagq_context_list.argtypes = [C.POINTER(GridC), P, C.c_int32, P, P, C.c_int64, P]
+        L.cagq_sample_points.argtypes = [P, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_uint64, P, P]
+        L.cagq_ball_query.argtypes = [P, C.c_int32, C.c_int32, P, C.c_int32, C.c_int32, C.c_float, P, P, P]
+        L.cagq_coverage.argtypes = [C.POINTER(GridC), P, P, C.c_int32, C.c_int32, P, P]
         L.cagq_get_device_status.argtypes = [C.POINTER(GridC), P]
         L.cagq_status_string.argtypes = [C.c_int]
         L.cagq_status_string.restype = C.c_char_p
         for f in ("cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
                   "cagq_query_context", "cagq_query_points", "cagq_context_offsets", "cagq_context_list",
-                  "cagq_get_device_status"):
+                  "cagq_sample_points", "cagq_ball_query", "cagq_coverage", "cagq_get_device_status"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -287,6 +290,51 @@ def context_list(grid: Grid, center_lin: torch.Tensor, ctx_off: torch.Tensor,
         capacity = int(out.numel())
     _check(lib().cagq_context_list(C.byref(grid.rec), _ptr(center_lin), M, _ptr(ctx_off), _ptr(out),
                                    int(capacity), _stream_ptr(stream)), "cagq_context_list")
+    return out
+
+
+POINTS = {"rps": 0, "fps": 1}
+
+
+def sample_points(points: torch.Tensor, M: int, mode: str, seed: int = 0, out: Optional[torch.Tensor] = None,
+                  stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Random / Farthest Point Sampling (comparison methods): [B, M] point indices."""
+    B, N = int(points.shape[0]), int(points.shape[1])
+    _need(points, torch.float32, (B, N, 3), "points")
+    if out is None:
+        out = torch.empty((B, M), dtype=torch.int32, device=points.device)
+    _check(lib().cagq_sample_points(_ptr(points), B, N, M, POINTS[mode], C.c_uint64(seed & (2**64 - 1)), _ptr(out),
+                                    _stream_ptr(stream)), "cagq_sample_points")
+    return out
+
+
+def ball_query(points: torch.Tensor, center_idx: torch.Tensor, K: int, radius2: float,
+               out: Optional[Dict[str, torch.Tensor]] = None,
+               stream: Optional[torch.cuda.Stream] = None) -> Dict[str, torch.Tensor]:
+    """Ball Query (comparison method): the first K points within the radius."""
+    B, N = int(points.shape[0]), int(points.shape[1])
+    M = int(center_idx.shape[1])
+    _need(points, torch.float32, (B, N, 3), "points")
+    _need(center_idx, torch.int32, (B, M), "center_idx")
+    if out is None:
+        out = dict(node_idx=torch.empty((B, M, K), dtype=torch.int32, device=points.device),
+                   n_valid=torch.empty((B, M), dtype=torch.int32, device=points.device))
+    _check(lib().cagq_ball_query(_ptr(points), B, N, _ptr(center_idx), M, K, C.c_float(radius2),
+                                 _ptr(out["node_idx"]), _ptr(out["n_valid"]), _stream_ptr(stream)),
+           "cagq_ball_query")
+    return out
+
+
+def coverage(grid: Grid, node_idx: torch.Tensor, n_valid: torch.Tensor, out: Optional[torch.Tensor] = None,
+             stream: Optional[torch.cuda.Stream] = None) -> torch.Tensor:
+    """Occupied voxels [B] holding a valid node point (divide by nvox for the metric)."""
+    B, M, K = (int(x) for x in node_idx.shape)
+    _need(node_idx, torch.int32, (B, M, K), "node_idx")
+    _need(n_valid, torch.int32, (B, M), "n_valid")
+    if out is None:
+        out = torch.empty(B, dtype=torch.int32, device=node_idx.device)
+    _check(lib().cagq_coverage(C.byref(grid.rec), _ptr(node_idx), _ptr(n_valid), M, K, _ptr(out),
+                               _stream_ptr(stream)), "cagq_coverage")
     return out
 
 

@@ -73,6 +73,7 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_nbr32 = take(L->has_nbr32 ? 4 * BN * (size_t)kNbr32Stride : 0);
     L->sel_thr = take(8 * (size_t)B);
     L->sel_hist = take(4 * (size_t)kSelPasses * B * kSelBins);
+    L->cov_mark = take((BN + 15) / 16 * 16);
     L->total = off;
     return true;
 }
@@ -210,6 +211,38 @@ int cagq_context_list(const cagq_grid* g, const int32_t* center_lin, int32_t M, 
     if (!center_lin || !ctx_off || capacity < 0 || (capacity > 0 && !ctx_idx)) return CAGQ_ERR_INVALID_ARG;
     hipError_t e = launch_context_list(L, g->desc, g->workspace, center_lin, M, ctx_off, ctx_idx, capacity,
                                        (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_sample_points(const float* points, int32_t B, int32_t N, int32_t M, int32_t mode, uint64_t seed,
+                       int32_t* center_idx, void* stream) {
+    if (!points || !center_idx || B < 1 || N < 1 || (int64_t)B * N > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    if (M < 1 || M > N || (mode != CAGQ_POINTS_RPS && mode != CAGQ_POINTS_FPS)) return CAGQ_ERR_INVALID_ARG;
+    if (mode == CAGQ_POINTS_FPS && N > kFpsMaxN) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_sample_points(points, B, N, M, mode, seed, center_idx, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_ball_query(const float* points, int32_t B, int32_t N, const int32_t* center_idx, int32_t M, int32_t K,
+                    float radius2, int32_t* node_idx, int32_t* n_valid, void* stream) {
+    if (!points || !center_idx || !node_idx || !n_valid) return CAGQ_ERR_INVALID_ARG;
+    if (B < 1 || N < 1 || (int64_t)B * N > 2147483647LL || M < 1 || (int64_t)B * M > 2147483647LL)
+        return CAGQ_ERR_INVALID_ARG;
+    if (K < 1 || (int64_t)B * M * K > 2147483647LL || !(radius2 >= 0.0f) || radius2 == __builtin_inff())
+        return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_ball_query(points, B, N, center_idx, M, K, radius2, node_idx, n_valid,
+                                     (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_coverage(const cagq_grid* g, const int32_t* node_idx, const int32_t* n_valid, int32_t M, int32_t K,
+                  int32_t* covered, void* stream) {
+    Layout L;
+    int rc = grid_layout(g, &L);
+    if (rc != CAGQ_OK) return rc;
+    if (!node_idx || !n_valid || !covered || M < 1 || K < 1) return CAGQ_ERR_INVALID_ARG;
+    if ((int64_t)g->B * M * K > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
+    hipError_t e = launch_coverage(L, g->workspace, node_idx, n_valid, M, K, covered, (hipStream_t)stream);
     return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
 }
 

@@ -69,6 +69,7 @@ struct Layout {
     bool has_nbr16, has_nbr32;
     size_t sel_thr;       // u64 [B] selection threshold, see sel_pack
     size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
+    size_t cov_mark;      // u8  [B][N] coverage metric: 1 when the slot holds a node point
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };
 
@@ -428,6 +429,15 @@ hipError_t launch_context_offsets(const Layout& L, const cagq_grid_desc& d, void
 hipError_t launch_context_list(const Layout& L, const cagq_grid_desc& d, void* ws, const int32_t* center_lin,
                                int32_t M, const int64_t* ctx_off, int32_t* ctx_idx, int64_t capacity,
                                hipStream_t s);
+
+// Comparison methods of Sec. 4 and the coverage metric.
+hipError_t launch_sample_points(const float* points, int32_t B, int32_t N, int32_t M, int32_t mode, uint64_t seed,
+                                int32_t* center_idx, hipStream_t s);
+hipError_t launch_ball_query(const float* points, int32_t B, int32_t N, const int32_t* center_idx, int32_t M,
+                             int32_t K, float radius2, int32_t* node_idx, int32_t* n_valid, hipStream_t s);
+hipError_t launch_coverage(const Layout& L, void* ws, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
+                           int32_t K, int32_t* covered, hipStream_t s);
+constexpr int32_t kFpsMaxN = 80 * 1024;  // points per cloud Farthest Point Sampling keeps in registers
 
 // Upsampling query around given center points [B][M][3] (Sec. 3.1).
 hipError_t launch_query_points(const Layout& L, const cagq_grid_desc& d, void* ws, const float* centers, int32_t M,

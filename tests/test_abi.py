@@ -180,3 +180,30 @@ def test_context_calls_reject_bad_arguments():
     assert L.cagq_context_list(C.byref(g), p, 0, p, p, 16, None) == cagq.ERR_INVALID_ARG
     small = _grid_record(ws_bytes=1024)
     assert L.cagq_context_offsets(C.byref(small), p, 8, p, None) == cagq.ERR_WORKSPACE_TOO_SMALL
+
+
+def test_comparison_methods_reject_bad_arguments():
+    L = cagq.lib()
+    g = _grid_record()
+    p = C.c_void_p(0x300000)
+    sp = lambda B=1, N=100, M=10, mode=0, pts=p, out=p: L.cagq_sample_points(pts, B, N, M, mode, 1, out, None)
+    assert sp(M=0) == cagq.ERR_INVALID_ARG
+    assert sp(M=101) == cagq.ERR_INVALID_ARG
+    assert sp(mode=2) == cagq.ERR_INVALID_ARG
+    assert sp(B=0) == cagq.ERR_INVALID_ARG
+    assert sp(pts=None) == cagq.ERR_INVALID_ARG
+    assert sp(out=None) == cagq.ERR_INVALID_ARG
+    assert sp(N=81921, M=5, mode=1) == cagq.ERR_INVALID_ARG  # FPS keeps at most 81920 points per cloud
+    bq = lambda K=8, r2=0.01, c=p, ni=p, nv=p: L.cagq_ball_query(p, 1, 100, c, 10, K, C.c_float(r2), ni, nv, None)
+    assert bq(K=0) == cagq.ERR_INVALID_ARG
+    assert bq(r2=-1.0) == cagq.ERR_INVALID_ARG
+    assert bq(r2=float("nan")) == cagq.ERR_INVALID_ARG
+    assert bq(r2=float("inf")) == cagq.ERR_INVALID_ARG
+    assert bq(c=None) == cagq.ERR_INVALID_ARG
+    assert bq(ni=None) == cagq.ERR_INVALID_ARG
+    assert bq(nv=None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_coverage(C.byref(g), p, p, 0, 8, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_coverage(C.byref(g), p, p, 8, 0, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_coverage(C.byref(g), None, p, 8, 8, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_coverage(C.byref(g), p, None, 8, 8, p, None) == cagq.ERR_INVALID_ARG
+    assert L.cagq_coverage(C.byref(g), p, p, 8, 8, None, None) == cagq.ERR_INVALID_ARG

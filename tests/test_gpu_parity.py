@@ -469,3 +469,56 @@ def test_query_points_knn_ring(r):
     Q = rng.random((2, 900, 3), dtype=np.float32)
     spec = _spec((0, 0, 0), (0.05,) * 3, (20, 20, 20), 8, r)
     run_up(P, spec, Q, 16, "knn_ring", 0, where=f"up ring r={r}", context=False)
+
+
+# ---------------------------------------------------------------- comparison methods and coverage (Sec. 4)
+
+@pytest.mark.parametrize("B,N,M", [(1, 1, 1), (2, 1000, 1000), (3, 5000, 77), (2, 70000, 8192), (1, 81920, 1)])
+def test_rps_matches_oracle(B, N, M):
+    P = W.uniform_cube(B, N, N % 97)
+    c = cagq.sample_points(torch.from_numpy(P).to(DEV), M, "rps", 5)
+    assert np.array_equal(_np(c), oracle.sample_points(P, M, "rps", 5))
+
+
+@pytest.mark.parametrize("B,N,M", [(1, 1, 1), (2, 1000, 1000), (2, 3000, 500), (1, 20000, 300), (2, 81920, 2048)])
+def test_fps_matches_oracle(B, N, M):
+    rng = np.random.default_rng(N)
+    P = rng.random((B, N, 3), dtype=np.float32)
+    P[:, N // 2:N // 2 + min(50, N // 2)] = P[:, :1]  # duplicate points: ties and zero distances
+    print(f"[parity] fps B={B} N={N} M={M}", flush=True)
+    c = cagq.sample_points(torch.from_numpy(P).to(DEV), M, "fps")
+    assert np.array_equal(_np(c), oracle.sample_points(P, M, "fps"))
+
+
+@pytest.mark.parametrize("K", [1, 16, 64])
+def test_ball_query_matches_oracle(K):
+    w = W.get_workload("room")
+    P = w.points()
+    c = oracle.sample_points(P, 500, "rps", 3)
+    c[0, :5] = [-1, P.shape[1], 0, 1, 2]  # out-of-range centers get nothing
+    r2 = float(np.float32(0.186) ** 2)
+    q = cagq.ball_query(torch.from_numpy(P).to(DEV), torch.from_numpy(c).to(DEV), K, r2)
+    ni_o, nv_o = oracle.ball_query(P, np.where((c >= 0) & (c < P.shape[1]), c, 0), K, r2)
+    ni_o[0, :2], nv_o[0, :2] = -1, 0
+    assert np.array_equal(_np(q["node_idx"]), ni_o)
+    assert np.array_equal(_np(q["n_valid"]), nv_o)
+
+
+@pytest.mark.parametrize("name", ["room", "bigroom/cas-knn"])
+def test_coverage_matches_oracle(name):
+    """Coverage of CAGQ nodes and of RPS + Ball Query nodes, on the layer-1 grid."""
+    w = W.get_workload(name)
+    P = w.points()
+    L = w.layers[0]
+    ot = oracle.Table(P, oracle.grid_from_spec(L.grid))
+    Pt = torch.from_numpy(P).to(DEV)
+    g = cagq.build_grid(Pt, cagq.desc_from_spec(L.grid))
+    cl, mv = cagq.sample_centers(g, L.M, "rvs", 1)
+    q = cagq.query_context(g, cl, L.K, "cube", 1)
+    cov = cagq.coverage(g, q["node_idx"], q["n_valid"])
+    assert np.array_equal(_np(cov), ot.coverage(_np(q["node_idx"]), _np(q["n_valid"])))
+    c = cagq.sample_points(Pt, L.M, "rps", 1)
+    bq = cagq.ball_query(Pt, c, L.K, float(np.float32(0.1) ** 2))
+    cov2 = cagq.coverage(g, bq["node_idx"], bq["n_valid"])
+    assert np.array_equal(_np(cov2), ot.coverage(_np(bq["node_idx"]), _np(bq["n_valid"])))
+    assert cagq.get_device_status(g) == 0
