@@ -104,7 +104,7 @@ def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
     sf, sw = COPY_PROBE_BYTES / (cf * 1024), COPY_PROBE_BYTES / (cw * 1024)
 
     def layer1(rows, mode):
-        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+(?:, \d+)?>", r["Kernel_Name"])]
+        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+(?:, \d+)?(?:, false)?>", r["Kernel_Name"])]
         g = max(int(r["Grid_Size"]) for r in q)
         return [float(r["Counter_Value"]) for r in q if int(r["Grid_Size"]) == g]
     lines = [f"Calibration: a {COPY_PROBE_BYTES >> 20} MiB fp32 copy kernel reads FETCH_SIZE {cf:.0f} KiB "
