@@ -33,6 +33,9 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 COPY_PROBE_BYTES = 1 << 30  # the calibration copy reads and writes this many bytes
+SLEEP_CYCLES = 1_000_000  # about 0.4 ms of the GPU clock before each bracketed launch
+QUERY_REPS = 10  # layer-1 query launches between the roofline's events
+ROOF_PASSES = 3  # variant passes that time them
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_query_bigroom_b4_traffic.md")
 QUERY_SOURCES = ("paper_1912_02984_amd/csrc/cagq_query.hip", "paper_1912_02984_amd/csrc/cagq_internal.h")
 QUERY_NAMES = {"0": "k_query<cube>", "1": "k_query<knn>"}
@@ -104,7 +107,7 @@ def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
     sf, sw = COPY_PROBE_BYTES / (cf * 1024), COPY_PROBE_BYTES / (cw * 1024)
 
     def layer1(rows, mode):
-        q = [r for r in rows if re.search(rf"k_query<{mode}, \d+(?:, \d+)?(?:, false)?>", r["Kernel_Name"])]
+        q = [r for r in rows if re.search(rf"k_query(?:_r2)?<{mode}, \d+(?:, \d+)?(?:, false)?>", r["Kernel_Name"])]
         g = max(int(r["Grid_Size"]) for r in q)
         return [float(r["Counter_Value"]) for r in q if int(r["Grid_Size"]) == g]
     lines = [f"Calibration: a {COPY_PROBE_BYTES >> 20} MiB fp32 copy kernel reads FETCH_SIZE {cf:.0f} KiB "
@@ -155,17 +158,22 @@ def measure_cas_swap(P, P_np, B: int, N: int, L, with_oracle: bool, reps: int = 
 
 
 def _timed(fn, reps: int):
-    """Average ms of fn() over reps calls, HIP events on the current stream."""
+    """Average ms of fn() over reps calls, each bracketed by HIP events on the
+    current stream after a bounded GPU-side delay (so the host has enqueued
+    the calls before the GPU reaches the start event)."""
     import torch
     fn()
     torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
+    pairs = []
     for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        e0.record()
         fn()
-    e1.record()
+        e1.record()
+        pairs.append((e0, e1))
     torch.cuda.synchronize()
-    return e0.elapsed_time(e1) / reps
+    return sum(a.elapsed_time(b) for a, b in pairs) / reps
 
 
 def measure_upsampling(P, P_np, B: int, N: int, wl, with_oracle: bool, reps: int = 20) -> dict:
@@ -395,7 +403,14 @@ def main():
             if record and li == 0:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
+                # a bounded GPU-side delay first: the host enqueues the start
+                # event, QUERY_REPS identical launches and the end event while
+                # the stream is still busy, so the events bracket the kernels
+                # alone, back to back, and not the host's time to issue them
+                torch.cuda._sleep(SLEEP_CYCLES)
                 e0.record()
+                for _ in range(QUERY_REPS - 1):
+                    cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
             cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
             if record and li == 0:
                 e1.record()
@@ -438,8 +453,7 @@ def main():
     ms_step = t_ev0.elapsed_time(t_ev1) / args.steps
     points_per_s = B * N / (ms_step / 1e3)
 
-    # per-variant times, one variant at a time on the default stream; the
-    # layer-1 query launches of these passes give the roofline entry
+    # per-variant times, one variant at a time on the default stream
     variant_ms = {}
     reps = max(5, args.steps // 2)
     for plan in plans:
@@ -449,16 +463,22 @@ def main():
         torch.cuda.synchronize()
         e0.record()
         for _ in range(reps):
-            run_variant(plan, record=True)
+            run_variant(plan)
         e1.record()
         torch.cuda.synchronize()
         variant_ms[plan[0].name] = e0.elapsed_time(e1) / reps
+    # then passes whose layer-1 query runs QUERY_REPS times between events:
+    # the roofline entry
+    for plan in plans:
+        for _ in range(ROOF_PASSES):
+            run_variant(plan, record=True)
+    torch.cuda.synchronize()
 
     # roofline of the layer-1 query kernel, per variant
     roof = {}
     for w, layers in plans:
         L, desc, ws, out, cl, mv = layers[0]
-        durs = [a.elapsed_time(b) for name, a, b in q_events if name == w.name]
+        durs = [a.elapsed_time(b) / QUERY_REPS for name, a, b in q_events if name == w.name]
         t_ms = float(np.mean(durs))
         ctx_total = int(out["ctx_count"].sum().item())
         alg = query_alg_bytes(B * L.M, L.K, ctx_total)

@@ -155,13 +155,6 @@ __device__ __forceinline__ uint32_t gscan_incl(uint32_t v, int lg) {
     return v;
 }
 
-template <int G>
-__device__ __forceinline__ uint32_t gsum(uint32_t v) {
-#pragma unroll
-    for (int d = 1; d < G; d <<= 1) v += xlane(v, d);
-    return v;
-}
-
 // Compare-exchange of (key, payload) with the partner lane lg ^ j: this lane
 // keeps the smaller key when keep_min, else the larger.
 __device__ __forceinline__ void gcx(uint64_t& k, uint32_t& p, int j, bool keep_min) {
@@ -367,6 +360,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         const uint32_t o = xlane(cmax, d);
         cmax = o > cmax ? o : cmax;
     }
+    cmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)cmax);  // the same in every lane
     // a context of at most G points is one chunk: its points and weights stay
     // in the lanes that loaded them, and the sort carries the lane (entry)
     // instead of the position in the copy
@@ -471,12 +465,17 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             node_xyz[(cK + lg) * 3 + 2] = z;
         }
     }
+    // n <= top: the levels at and above `top` add nothing
     const bool valid = (uint32_t)lg < n;
-    const uint32_t wc = gsum<G>(valid ? w : 0u);
+    uint32_t wc = valid ? w : 0u;
+#pragma unroll
+    for (int d = 1; d < G; d <<= 1)
+        if ((uint32_t)d < top) wc += xlane(wc, d);
     const float wf = (float)w;
     float tx = wf * x, ty = wf * y, tz = wf * z;
 #pragma unroll
     for (int h = 1; h < G; h <<= 1) {
+        if ((uint32_t)h >= top) break;
         // the lanes that add (multiples of 2h) read lane + h = lane ^ h
         const float ox = xlanef(tx, h);
         const float oy = xlanef(ty, h);
@@ -487,11 +486,361 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             tz = tz + oz;
         }
     }
+    // lanes 0, 1, 2 of the group each divide one of lane 0's sums
+    const float sx = __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(tx), 0x00, 0xF, 0xF, true));
+    const float sy = __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(ty), 0x00, 0xF, 0xF, true));
+    const float sz = __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(tz), 0x00, 0xF, 0xF, true));
+    const uint32_t sw = (uint32_t)__builtin_amdgcn_mov_dpp((int)wc, 0x00, 0xF, 0xF, true);  // quad_perm 0,0,0,0
+    if (live && lg < 3) {
+        const float num = lg == 0 ? sx : (lg == 1 ? sy : sz);
+        center_xyz[(size_t)cid * 3 + lg] = n ? num / (float)sw : 0.0f;
+    }
     if (live && lg == 0) {
-        const float wcf = (float)wc;
-        center_xyz[(size_t)cid * 3 + 0] = n ? tx / wcf : 0.0f;
-        center_xyz[(size_t)cid * 3 + 1] = n ? ty / wcf : 0.0f;
-        center_xyz[(size_t)cid * 3 + 2] = n ? tz / wcf : 0.0f;
+        center_w[cid] = wc;
+        n_valid[cid] = (int32_t)n;
+        if (ctx_count) ctx_count[cid] = (int32_t)c;
+    }
+}
+
+// Value of lane 15 - l within the 16-lane row (DPP row_mirror).
+__device__ __forceinline__ uint32_t mirror(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, true);
+}
+
+__device__ __forceinline__ uint64_t mirror64(uint64_t v) {
+    return ((uint64_t)mirror((uint32_t)(v >> 32)) << 32) | mirror((uint32_t)v);
+}
+
+// Value of lane 0 of this lane's 16-lane row.
+__device__ __forceinline__ uint32_t row0(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x150, 0xF, 0xF, true);  // row_share:0
+}
+
+// Bitonic half-cleaners j = 8, 4, 2, 1 over a 16-lane row: a bitonic
+// sequence ends ascending.
+__device__ __forceinline__ void clean16(uint64_t& k, uint32_t& p, int lg) {
+#pragma unroll
+    for (int j = 8; j > 0; j >>= 1) gcx(k, p, j, (lg & j) == 0);
+}
+
+// Sampled centers with 16 < K <= 32, Cube Query or k-NN: 16 lanes per center
+// (four per wave), two result registers per lane, ranks 0..15 in `b0` and
+// 16..31 in `b1`.
+//   1. Each group probes the (2r+1)^2 grid rows of its center's block, one
+//      lane per row: a row segment of the block holds consecutive slots,
+//      whose stored points are contiguous in the slot-ordered copy, so the
+//      context is (2r+1)^2 ranges (some empty). Their starts and prefix
+//      counts go to LDS, with the center's facts (lin, cloud, reference
+//      point, context size).
+//   2. The block's 16 centers are ranked by context size and group g takes
+//      the center of rank g, so each wave works on four centers of similar
+//      size and its chunk loop and sort depth follow them.
+//   3. Chunks of 16 entries are sorted across the group; the first is the
+//      running best, each later one is merged in: the 16 smallest of b1 and
+//      the chunk (elementwise minimum against the chunk reversed, then
+//      half-cleaners), then b0 and that merged the same way into the new b0
+//      (smaller half) and b1 (larger half).
+//   4. Node slot k is b0 lane k or b1 lane k - 16; slots k >= n repeat slot 0.
+//      The center's pairwise sum runs strides 1..8 inside each half, then
+//      node 16 into node 0 -- the order of the single-register tree.
+template <int MODE, int RAD, bool UP>
+__global__ __launch_bounds__(kQueryThreads) void k_query_r2(
+    const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
+    int64_t W, const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
+    const uint32_t* __restrict__ vox_off, const float4* __restrict__ pt4, const int32_t* __restrict__ center_lin,
+    const float* __restrict__ center_pts, uint64_t seed, int32_t* __restrict__ node_idx,
+    float* __restrict__ node_xyz, int32_t* __restrict__ n_valid, float* __restrict__ center_xyz,
+    uint32_t* __restrict__ center_w, int32_t* __restrict__ ctx_count, int32_t* __restrict__ lin_out,
+    int* __restrict__ status) {
+    constexpr int G = 16, GPB = kQueryThreads / G;
+    constexpr int S = 2 * RAD + 1, NR = S * S;
+    __shared__ uint32_t s_st[GPB][NR];
+    __shared__ uint32_t s_pre[GPB][NR + 1];
+    __shared__ uint32_t s_c[GPB], s_lin[GPB], s_b[GPB];
+    __shared__ float s_q[GPB][3];
+    __shared__ uint32_t s_src[GPB];
+    const int lane = lane_id();
+    const int lg = lane & (G - 1);
+    const int gb = threadIdx.x / G;
+    const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
+
+    // 1. this group's own center
+    {
+        const int32_t cid = (int32_t)blk * GPB + gb;
+        const bool live = cid < total;
+        const int32_t c_id = live ? cid : 0;
+        const int32_t b = (int32_t)udiv((uint32_t)c_id, g.mm);
+        const uint64_t* bm = bitmap + (size_t)b * W;
+        const uint32_t* wr = word_rank + (size_t)b * W;
+        const uint32_t* vo = vox_off + (size_t)b * (N + 1);
+        bool in_grid = true;
+        uint32_t lin;
+        int32_t gx, gy, gz;
+        float qx, qy, qz;
+        if constexpr (UP) {
+            qx = center_pts[(size_t)c_id * 3 + 0];
+            qy = center_pts[(size_t)c_id * 3 + 1];
+            qz = center_pts[(size_t)c_id * 3 + 2];
+            const bool bad = !isfinite(qx) || !isfinite(qy) || !isfinite(qz);
+            gx = isfinite(qx) ? axis_index(qx, g.o[0], g.s[0], g.D[0]) : 0;
+            gy = isfinite(qy) ? axis_index(qy, g.o[1], g.s[1], g.D[1]) : 0;
+            gz = isfinite(qz) ? axis_index(qz, g.o[2], g.s[2], g.D[2]) : 0;
+            lin = (uint32_t)gx + (uint32_t)g.D[0] * ((uint32_t)gy + (uint32_t)g.D[1] * (uint32_t)gz);
+            if (live && bad && lg == 0) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+        } else {
+            const int32_t lin_s = center_lin[c_id];
+            const int64_t V = (int64_t)g.D[0] * g.D[1] * g.D[2];
+            in_grid = lin_s >= 0 && (int64_t)lin_s < V;
+            lin = in_grid ? (uint32_t)lin_s : 0u;
+            const uint32_t zq = udiv(lin, g.d01);
+            const uint32_t rem = lin - zq * (uint32_t)g.D[0] * (uint32_t)g.D[1];
+            const uint32_t yq = udiv(rem, g.d0);
+            gx = (int32_t)(rem - yq * (uint32_t)g.D[0]), gy = (int32_t)yq, gz = (int32_t)zq;
+            qx = g.o[0] + ((float)gx + 0.5f) * g.s[0];
+            qy = g.o[1] + ((float)gy + 0.5f) * g.s[1];
+            qz = g.o[2] + ((float)gz + 0.5f) * g.s[2];
+        }
+        // the block's rows: each a range [st, st + len) of the copy
+        GridDims gd;
+        gd.D[0] = g.D[0], gd.D[1] = g.D[1], gd.D[2] = g.D[2];
+        uint32_t c = 0;
+        bool occupied = false;
+#pragma unroll
+        for (int q0 = 0; q0 < NR; q0 += G) {
+            const int q = q0 + lg;
+            uint32_t st = 0, len = 0, mask = 0;
+            if (q < NR) {
+                const GridRow r = load_row(bm, wr, gd, gx, gy + q % S - RAD, gz + q / S - RAD, RAD);
+                mask = in_grid ? r.mask : 0u;
+                st = vo[r.first];
+                len = mask ? vo[r.first + (uint32_t)__popc(mask)] - st : 0u;
+            }
+            if (NR / 2 >= q0 && NR / 2 < q0 + G)
+                occupied = (__shfl((int)mask, NR / 2 - q0, G) >> RAD) & 1;
+            // inclusive scan of the lengths across the row of 16 lanes
+            uint32_t incl = len;
+#pragma unroll
+            for (int d = 1; d < G; d <<= 1) {
+                const uint32_t o = (uint32_t)__shfl_up((int)incl, d, G);
+                if (lg >= d) incl += o;
+            }
+            if (q < NR) {
+                s_st[gb][q] = st;
+                s_pre[gb][q] = c + incl - len;
+            }
+            c += (uint32_t)__shfl((int)incl, G - 1, G);
+        }
+        // a sampled center that is not occupied has an empty context and
+        // gets zeros (an upsampling center's voxel may be empty)
+        if (!UP) {
+            if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
+            if (!occupied) c = 0;
+        }
+        if (lg == 0) {
+            s_pre[gb][NR] = c;
+            s_c[gb] = live ? c : 0u;
+            s_lin[gb] = lin;
+            s_b[gb] = (uint32_t)b;
+            s_q[gb][0] = qx, s_q[gb][1] = qy, s_q[gb][2] = qz;
+        }
+    }
+    __syncthreads();
+    // 2. the block's centers by context size (ties by group): group g takes
+    // the center of rank g
+    if (lg == 0) {
+        const uint32_t mine = s_c[gb];
+        uint32_t r = 0;
+#pragma unroll
+        for (int h = 0; h < GPB; ++h) {
+            const uint32_t o = s_c[h];
+            r += (o < mine || (o == mine && h < gb)) ? 1u : 0u;
+        }
+        s_src[r] = (uint32_t)gb;
+    }
+    __syncthreads();
+    const int src = (int)s_src[gb];
+    const int32_t cid = (int32_t)blk * GPB + src;
+    const bool live = cid < total;
+    const uint32_t c = s_c[src];
+    const uint32_t lin = s_lin[src];
+    const int32_t b = (int32_t)s_b[src];
+    const float qx = s_q[src][0], qy = s_q[src][1], qz = s_q[src][2];
+    const uint32_t* s_pr = s_pre[src];
+    const uint32_t* s_sr = s_st[src];
+    const float4* p4 = pt4 + (size_t)b * N;
+    const size_t cK = (size_t)(live ? cid : 0) * K;
+
+    // 3. keys, sorted 16 at a time and merged into the best 32
+    uint64_t hc = 0;
+    if (MODE == CAGQ_QUERY_CUBE) hc = sm64(sm64(sm64(seed ^ 2ull) ^ (uint64_t)b) ^ (uint64_t)lin);
+    uint32_t cmax = c;
+#pragma unroll
+    for (int d = G; d < kWave; d <<= 1) {
+        const uint32_t o = xlane(cmax, d);
+        cmax = o > cmax ? o : cmax;
+    }
+    cmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)cmax);
+    const bool one = c <= (uint32_t)G;
+    uint32_t top = 2;
+    while (top < cmax && top < (uint32_t)G) top <<= 1;
+    uint64_t b0k = ~0ull, b1k = ~0ull;
+    uint32_t b0p = 0, b1p = 0;
+    float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f);
+    uint32_t w0 = 1u;
+    for (uint32_t e0 = 0; e0 < cmax; e0 += G) {
+        const uint32_t e = e0 + lg;
+        uint64_t key = ~0ull;
+        uint32_t pos = 0;
+        if (e < c) {
+            // the row holding entry e: the last range starting at or before it
+            uint32_t lo = 0, hi = NR - 1;
+            while (lo < hi) {
+                const uint32_t mid = (lo + hi + 1) >> 1;
+                if (s_pr[mid] <= e) lo = mid; else hi = mid - 1;
+            }
+            pos = s_sr[lo] + (e - s_pr[lo]);
+            const float4 v = p4[pos];
+            const uint32_t i = __float_as_uint(v.w);
+            if (one) {
+                v0 = v;
+                if (Wt) w0 = Wt[(size_t)b * N + i];
+                pos = (uint32_t)lg;
+            }
+            if (MODE == CAGQ_QUERY_CUBE) {
+                key = (sm64(hc ^ (uint64_t)i) & 0xFFFFFFFF00000000ull) | i;
+            } else {
+                const float dx = v.x - qx, dy = v.y - qy, dz = v.z - qz;
+                const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+                const float sxy = xx + yy;
+                const float d2 = sxy + zz;
+                key = ((uint64_t)__float_as_uint(d2) << 32) | i;
+            }
+        }
+        gsort<G>(key, pos, lg, e0 == 0 ? top : (uint32_t)G);
+        if (e0 == 0) {
+            b0k = key;
+            b0p = pos;
+        } else {
+            // the 16 smallest of b1 and the chunk
+            uint64_t rk = mirror64(key);
+            uint32_t rp = mirror(pos);
+            if (rk < b1k) {
+                b1k = rk;
+                b1p = rp;
+            }
+            clean16(b1k, b1p, lg);
+            // b0 and those: smaller half to b0, larger to b1
+            rk = mirror64(b1k);
+            rp = mirror(b1p);
+            const bool sw = rk < b0k;
+            b1k = sw ? b0k : rk;
+            b1p = sw ? b0p : rp;
+            b0k = sw ? rk : b0k;
+            b0p = sw ? rp : b0p;
+            clean16(b0k, b0p, lg);
+            clean16(b1k, b1p, lg);
+        }
+    }
+
+    // 4. outputs (an empty context gives n = 0)
+    const uint32_t n = c < (uint32_t)K ? c : (uint32_t)K;
+    uint32_t nmax = n;
+#pragma unroll
+    for (int d = G; d < kWave; d <<= 1) {
+        const uint32_t o = xlane(nmax, d);
+        nmax = o > nmax ? o : nmax;
+    }
+    nmax = (uint32_t)__builtin_amdgcn_readfirstlane((int)nmax);
+    const uint64_t s0k = ((uint64_t)row0((uint32_t)(b0k >> 32)) << 32) | row0((uint32_t)b0k);
+    const uint32_t s0p = row0(b0p);
+    float tx = 0.f, ty = 0.f, tz = 0.f, ux = 0.f, uy = 0.f, uz = 0.f;
+    uint32_t wsum = 0;
+    // slot lg (from b0) and slot 16 + lg (from b1, written only when K > 16 + lg)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const uint32_t k = (uint32_t)(h * G + lg);
+        const bool own = k < n;
+        const uint64_t mk = own ? (h ? b1k : b0k) : s0k;
+        const uint32_t mp = own ? (h ? b1p : b0p) : s0p;
+        const uint32_t idx = n ? (uint32_t)mk : 0u;
+        const int from = one ? (int)mp : 0;
+        float x = __shfl(v0.x, from, G), y = __shfl(v0.y, from, G), z = __shfl(v0.z, from, G);
+        uint32_t w = (uint32_t)__shfl((int)w0, from, G);
+        if (!one) {
+            const float4 pv = p4[mp];
+            x = pv.x;
+            y = pv.y;
+            z = pv.z;
+            if (!UP) w = Wt ? Wt[(size_t)b * N + idx] : 1u;
+        }
+        if (!n) {
+            x = y = z = 0.0f;
+            w = 1u;
+        }
+        if (live && k < (uint32_t)K) {
+            node_idx[cK + k] = UP ? (n ? (int32_t)idx : -1) : (int32_t)idx;
+            if (node_xyz) {
+                node_xyz[(cK + k) * 3 + 0] = x;
+                node_xyz[(cK + k) * 3 + 1] = y;
+                node_xyz[(cK + k) * 3 + 2] = z;
+            }
+        }
+        if (!UP) {
+            const float wf = (float)w;
+            if (h == 0) {
+                tx = wf * x, ty = wf * y, tz = wf * z;
+            } else {
+                ux = wf * x, uy = wf * y, uz = wf * z;
+            }
+            wsum += own ? w : 0u;
+        }
+    }
+    if (UP) {
+        if (live && lg == 0) {
+            n_valid[cid] = (int32_t)n;
+            if (ctx_count) ctx_count[cid] = (int32_t)c;
+            if (lin_out) lin_out[cid] = (int32_t)lin;
+        }
+        return;
+    }
+    uint32_t wc = wsum;
+#pragma unroll
+    for (int d = 1; d < G; d <<= 1) wc += xlane(wc, d);
+    // strides 1..8 inside each half (only as far as the wave's largest n
+    // reaches), then node 16 into node 0
+#pragma unroll
+    for (int hh = 1; hh < G; hh <<= 1) {
+        if ((uint32_t)hh >= nmax) break;
+        const bool lead = (lg & (2 * hh - 1)) == 0;
+        const float ox = xlanef(tx, hh), oy = xlanef(ty, hh), oz = xlanef(tz, hh);
+        if (lead && (uint32_t)(lg + hh) < n) {
+            tx = tx + ox;
+            ty = ty + oy;
+            tz = tz + oz;
+        }
+        if (nmax > (uint32_t)G) {
+            const float px = xlanef(ux, hh), py = xlanef(uy, hh), pz = xlanef(uz, hh);
+            if (lead && (uint32_t)(G + lg + hh) < n) {
+                ux = ux + px;
+                uy = uy + py;
+                uz = uz + pz;
+            }
+        }
+    }
+    if (n > (uint32_t)G) {  // lane 0 holds nodes 0 and 16
+        tx = tx + ux;
+        ty = ty + uy;
+        tz = tz + uz;
+    }
+    // lanes 0, 1, 2 of the group each divide one of lane 0's sums
+    const float sx = __uint_as_float(row0(__float_as_uint(tx)));
+    const float sy = __uint_as_float(row0(__float_as_uint(ty)));
+    const float sz = __uint_as_float(row0(__float_as_uint(tz)));
+    if (live && lg < 3) {
+        const float num = lg == 0 ? sx : (lg == 1 ? sy : sz);
+        center_xyz[(size_t)cid * 3 + lg] = n ? num / (float)wc : 0.0f;
+    }
+    if (live && lg == 0) {
         center_w[cid] = wc;
         n_valid[cid] = (int32_t)n;
         if (ctx_count) ctx_count[cid] = (int32_t)c;
@@ -537,9 +886,31 @@ void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const Quer
         launch_g<MODE, G, 3, UP>(L, g, ws, io, M, K, seed, s);
 }
 
+template <int MODE, int RAD, bool UP>
+void launch_r2(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int32_t M, int32_t K, uint64_t seed,
+               hipStream_t s) {
+    constexpr int GPB = kQueryThreads / 16;
+    const int32_t total = L.B * M;
+    const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
+    k_query_r2<MODE, RAD, UP><<<blocks, kQueryThreads, 0, s>>>(
+        io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
+        at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
+        io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status));
+}
+
 template <int MODE, bool UP>
 void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const QueryIO& io, int32_t M, int32_t K,
                  uint64_t seed, hipStream_t s) {
+    if (MODE != kRing && K > 16 && K <= 32) {
+        // 16 lanes and two result registers per center
+        if (rad == 1)
+            launch_r2<MODE, 1, UP>(L, g, ws, io, M, K, seed, s);
+        else if (rad == 2)
+            launch_r2<MODE, 2, UP>(L, g, ws, io, M, K, seed, s);
+        else
+            launch_r2<MODE, 3, UP>(L, g, ws, io, M, K, seed, s);
+        return;
+    }
     if (K <= 16)
         launch_r<MODE, 16, UP>(L, g, rad, ws, io, M, K, seed, s);
     else if (K <= 32)

@@ -157,7 +157,7 @@ def test_more_centers_than_occupied_voxels():
     run_both(P, spec, 20, 16, "cas", "cube", 7, where="M>nvox cas")
 
 
-@pytest.mark.parametrize("K", [1, 2, 31, 33, 64])
+@pytest.mark.parametrize("K", [1, 2, 16, 17, 24, 31, 32, 33, 64])
 def test_node_counts(K):
     w = W.get_workload("room")
     L = w.layers[0]
@@ -337,7 +337,7 @@ def test_query_points_workloads(name):
 
 
 @pytest.mark.parametrize("r", [1, 2, 3])
-@pytest.mark.parametrize("K", [1, 16, 33, 64])
+@pytest.mark.parametrize("K", [1, 16, 17, 32, 33, 64])
 def test_query_points_radius_and_node_counts(r, K):
     """Centers of three kinds (cloud points, points in the box, points
     outside it, clamped): contexts from empty to a few hundred points."""
@@ -522,3 +522,19 @@ def test_coverage_matches_oracle(name):
     cov2 = cagq.coverage(g, bq["node_idx"], bq["n_valid"])
     assert np.array_equal(_np(cov2), ot.coverage(_np(bq["node_idx"]), _np(bq["n_valid"])))
     assert cagq.get_device_status(g) == 0
+
+
+@pytest.mark.parametrize("r", [1, 2, 3])
+@pytest.mark.parametrize("K", [17, 32])
+def test_sixteen_lane_query_with_large_contexts(r, K):
+    """Contexts from empty to several hundred points in one block of 16
+    centers (the query sorts the block's centers by context size), weights,
+    K between 17 and 32: several chunks merged into two result registers."""
+    rng = np.random.default_rng(7 * r + K)
+    B, N = 2, 6000
+    P = (rng.random((B, N, 3), dtype=np.float32) ** 4).astype(np.float32)
+    spec = _spec((0, 0, 0), (0.04,) * 3, (25, 25, 25), 32, r)
+    wts = rng.integers(1, 50, (B, N)).astype(np.uint32)
+    for q in ("knn", "cube"):
+        qo = run_both(P, spec, 333, K, "rvs", q, 3, weights=wts, where=f"r={r} K={K} {q}")
+    assert qo["ctx_count"].max() > 64 and qo["ctx_count"].min() < 16
