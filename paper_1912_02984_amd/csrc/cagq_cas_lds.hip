@@ -34,6 +34,7 @@ constexpr int kKS = kCasLdsMaxN / kT;      // owned slots per thread
 constexpr int kKeyShift = 25;              // key = (U << 25) | (2^25 - 1 - slot)
 constexpr uint32_t kSlotMask = (1u << kKeyShift) - 1;
 constexpr uint16_t kNone = 0xFFFF;
+constexpr int kPre = 4;                    // entry groups of 8 loaded with a list's header
 
 __device__ __forceinline__ uint32_t wmax32(uint32_t v) {
 #pragma unroll
@@ -184,9 +185,19 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         for (uint32_t i = tid; i < qa; i += kT) {
             const uint32_t s = que[i];
             const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
-            const uint32_t n_r = e[0].x & 0xFFFFu;
+            // the header and the first kPre groups of entries are loaded
+            // together (every list has room for them), so a list within r
+            // of up to 8 * kPre entries costs one load latency
+            uint4 pre[kPre];
+            const uint4 h = e[0];
+#pragma unroll
+            for (int c = 0; c < kPre; ++c) pre[c] = e[1 + c];
+            const uint32_t n_r = h.x & 0xFFFFu;
             uint32_t U = 0;
-            for (uint32_t c = 0; c * 8 < n_r; ++c) U += uncovered(e[1 + c], c * 8, n_r, cov);
+#pragma unroll
+            for (int c = 0; c < kPre; ++c)
+                if ((uint32_t)c * 8 < n_r) U += uncovered(pre[c], c * 8, n_r, cov);
+            for (uint32_t c = kPre; c * 8 < n_r; ++c) U += uncovered(e[1 + c], c * 8, n_r, cov);
             const uint32_t kv = (U << kKeyShift) | (kSlotMask - s);
             key[s] = kv;
             lmax = kv > lmax ? kv : lmax;
@@ -231,11 +242,14 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
             const uint32_t s = que[i];
             const uint32_t my = key[s];
             const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
+            uint4 pre[kPre];
             const uint4 h = e[0];
+#pragma unroll
+            for (int c = 0; c < kPre; ++c) pre[c] = e[1 + c];
             const uint32_t n_r = h.x & 0xFFFFu, n2 = h.x >> 16;
             int32_t found = -1;
             for (uint32_t c = 0; c * 8 < n2 && found < 0; ++c) {
-                const uint4 v = e[1 + c];
+                const uint4 v = c < (uint32_t)kPre ? pre[c < (uint32_t)kPre ? c : 0] : e[1 + c];
                 uint32_t sl[8], kk[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(v, j) : s;
