@@ -339,6 +339,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time to accumulate for the CPU baseline")
+    ap.add_argument("--rvs-after-layer", type=int, default=3,
+                    help="a step issues RVS+cube once CAS+kNN has enqueued this layer's sampling (0-3)")
     ap.add_argument("--no-next", action="store_true",
                     help="skip the measurement of the rows beyond the hot path")
     ap.add_argument("--copy-probe", action="store_true",
@@ -394,12 +396,14 @@ def main():
     streams = [torch.cuda.Stream() for _ in plans]
     q_events = []  # (variant, start, end) around layer-1 query launches
 
-    def run_variant(plan, record=False):
+    def run_variant(plan, record=False, hook=None, hook_layer=-1):
         w, layers = plan
         pts, wts = P, None
         for li, (L, desc, ws, out, cl, mv) in enumerate(layers):
             g = cagq.build_grid(pts, desc, ws)
             cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
+            if li == hook_layer and hook is not None:
+                hook()
             if record and li == 0:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
@@ -421,13 +425,27 @@ def main():
         main = torch.cuda.current_stream()
         start = torch.cuda.Event()
         start.record(main)
-        # RVS+cube is issued first: it only enqueues; CAS+kNN polls its rounds
-        order = sorted(range(len(plans)), key=lambda i: plans[i][0].layers[0].sample != "rvs")
-        for i in order:
-            st = streams[i]
+        for st in streams:
             st.wait_event(start)
-            with torch.cuda.stream(st):
-                run_variant(plans[i])
+        # CAS+kNN waits on the host for the rounds of its two large layers.
+        # RVS+cube only enqueues; it is issued from inside CAS+kNN once a
+        # layer's sampling is enqueued (by default the last layer's: its
+        # single-workgroup CAS holds four CUs for ~0.1 ms and RVS+cube's
+        # kernels fill the others, where beside the large layers' rounds they
+        # delay each round's launches)
+        cas = [i for i in range(len(plans)) if plans[i][0].layers[0].sample != "rvs"]
+        rvs = [i for i in range(len(plans)) if plans[i][0].layers[0].sample == "rvs"]
+
+        def issue_rvs():
+            for i in rvs:
+                with torch.cuda.stream(streams[i]):
+                    run_variant(plans[i])
+
+        if cas:
+            with torch.cuda.stream(streams[cas[0]]):
+                run_variant(plans[cas[0]], hook=issue_rvs, hook_layer=args.rvs_after_layer)
+        else:
+            issue_rvs()
         for st in streams:
             main.wait_stream(st)
 
