@@ -339,8 +339,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum oracle time to accumulate for the CPU baseline")
-    ap.add_argument("--rvs-after-layer", type=int, default=3,
+    ap.add_argument("--rvs-after-layer", type=int, default=2,
                     help="a step issues RVS+cube once CAS+kNN has enqueued this layer's sampling (0-3)")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="issue RVS+cube's kernels one by one instead of replaying its captured graph")
     ap.add_argument("--no-next", action="store_true",
                     help="skip the measurement of the rows beyond the hot path")
     ap.add_argument("--copy-probe", action="store_true",
@@ -421,6 +423,21 @@ def main():
                 q_events.append((w.name, e0, e1))
             pts, wts = out["center_xyz"], out["center_w"]
 
+    # RVS+cube never waits on the host, so it is captured once in a HIP graph
+    # (kernel launches only) and a step replays it: one launch from the host
+    graphs = {}
+    if not args.no_graph:
+        for i, (w, layers) in enumerate(plans):
+            if w.layers[0].sample == "rvs":
+                with torch.cuda.stream(streams[i]):
+                    run_variant(plans[i])  # eager once, outside the capture
+                torch.cuda.synchronize()
+                gr = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(gr, stream=streams[i]):
+                    run_variant(plans[i])
+                torch.cuda.synchronize()
+                graphs[i] = gr
+
     def step():
         main = torch.cuda.current_stream()
         start = torch.cuda.Event()
@@ -429,17 +446,20 @@ def main():
             st.wait_event(start)
         # CAS+kNN waits on the host for the rounds of its two large layers.
         # RVS+cube only enqueues; it is issued from inside CAS+kNN once a
-        # layer's sampling is enqueued (by default the last layer's: its
-        # single-workgroup CAS holds four CUs for ~0.1 ms and RVS+cube's
-        # kernels fill the others, where beside the large layers' rounds they
-        # delay each round's launches)
+        # layer's sampling is enqueued (by default the third layer's: the
+        # single-workgroup CAS of the last two layers holds four CUs for
+        # ~0.25 ms and RVS+cube's kernels fill the others, where beside the
+        # large layers' rounds they delay each round's launches)
         cas = [i for i in range(len(plans)) if plans[i][0].layers[0].sample != "rvs"]
         rvs = [i for i in range(len(plans)) if plans[i][0].layers[0].sample == "rvs"]
 
         def issue_rvs():
             for i in rvs:
                 with torch.cuda.stream(streams[i]):
-                    run_variant(plans[i])
+                    if i in graphs:
+                        graphs[i].replay()
+                    else:
+                        run_variant(plans[i])
 
         if cas:
             with torch.cuda.stream(streams[cas[0]]):

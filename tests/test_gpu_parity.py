@@ -538,3 +538,80 @@ def test_sixteen_lane_query_with_large_contexts(r, K):
     for q in ("knn", "cube"):
         qo = run_both(P, spec, 333, K, "rvs", q, 3, weights=wts, where=f"r={r} K={K} {q}")
     assert qo["ctx_count"].max() > 64 and qo["ctx_count"].min() < 16
+
+
+# ---------------------------------------------------------------- HIP graph replay
+
+def _rvs_plan(w, B, dev):
+    plan, n = [], w.N
+    for L in w.layers:
+        desc = cagq.desc_from_spec(L.grid)
+        lay = cagq.workspace_layout(B, n, desc)
+        plan.append((L, desc, torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev),
+                     cagq.alloc_query_outputs(B, L.M, L.K, dev), torch.empty((B, L.M), dtype=torch.int32, device=dev),
+                     torch.empty((B,), dtype=torch.int32, device=dev)))
+        n = L.M
+    return plan
+
+
+def _run_plan(P, plan):
+    pts, wts = P, None
+    for (L, desc, ws, out, cl, mv) in plan:
+        g = cagq.build_grid(pts, desc, ws)
+        cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
+        cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
+        pts, wts = out["center_xyz"], out["center_w"]
+
+
+def _snapshot(plan):
+    return [(_np(cl).copy(), _np(mv).copy(), {k: _np(v).copy() for k, v in out.items() if v is not None})
+            for (L, desc, ws, out, cl, mv) in plan]
+
+
+def test_graph_replay_of_the_rvs_cube_path():
+    """The four RVS + Cube Query layers of the indoor scenes, captured once in
+    a HIP graph (all kernels, no memory-set nodes) and replayed three times,
+    with eager runs of the same path on other inputs and synchronizations in
+    between: every replay equals the eager result bit for bit, and layer 1
+    equals the oracle."""
+    w = W.get_workload("bigroom/rvs-cube")
+    B = 4
+    P_np = w.points(B=B)
+    P = torch.from_numpy(P_np).to(DEV)
+    plan = _rvs_plan(w, B, DEV)
+    _run_plan(P, plan)
+    torch.cuda.synchronize()
+    ref = _snapshot(plan)
+    # layer 1 against the oracle
+    L = w.layers[0]
+    ot = oracle.Table(P_np, oracle.grid_from_spec(L.grid))
+    ocl, omv = ot.sample_rvs(L.M, L.seed)
+    assert np.array_equal(ref[0][0], ocl)
+    qo = ot.query(ocl, omv, L.K, L.query, L.seed)
+    assert np.array_equal(ref[0][2]["node_idx"], qo["node_idx"])
+    assert np.array_equal(_bits(ref[0][2]["center_xyz"]), _bits(qo["center_xyz"]))
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        _run_plan(P, plan)
+    torch.cuda.synchronize()
+    other = _rvs_plan(w, B, DEV)
+    P2 = (P * 0.5).contiguous()
+    for rep in range(3):
+        for (L, desc, ws, out, cl, mv) in plan:  # scribble over the outputs first
+            cl.fill_(-5)
+            for v in out.values():
+                if v is not None:
+                    v.fill_(7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = _snapshot(plan)
+        for li, ((a_cl, a_mv, a_out), (b_cl, b_mv, b_out)) in enumerate(zip(ref, got)):
+            assert np.array_equal(a_cl, b_cl) and np.array_equal(a_mv, b_mv), (rep, li)
+            for k in a_out:
+                assert np.array_equal(_bits(a_out[k]), _bits(b_out[k])), (rep, li, k)
+        _run_plan(P2, other)  # the program's own eager work between replays
+        torch.cuda.synchronize()
