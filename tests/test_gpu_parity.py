@@ -178,12 +178,13 @@ def test_wider_neighbourhoods(r):
         run_both(P, spec, 300, 32, "cas", "knn", 8, where=f"r={r} cas")
 
 
-@pytest.mark.parametrize("N,dims", [(4096, (96, 96, 40)), (4097, (32, 32, 16)), (3000, (16, 16, 16)),
+@pytest.mark.parametrize("N,dims", [(1024, (10, 10, 10)), (1025, (40, 40, 20)), (700, (48, 48, 24)),
+                                    (4096, (96, 96, 40)), (4097, (32, 32, 16)), (3000, (16, 16, 16)),
                                     (4096, (12, 12, 12)), (8192, (16, 16, 16))])
 def test_cas_single_workgroup_limits(N, dims):
     """CAS with beta = 0 runs in one workgroup per cloud up to N = 4096 and in
     the many-kernel rounds (with neighbour lists for r = 1) beyond: clouds on
-    both sides of the limit, one whose every voxel is chosen (M >= nvox, so
+    both sides of the limit, small ones, one whose every voxel is chosen (M >= nvox, so
     the best unpicked key ends at 0), and dense grids whose voxels have full
     neighbour lists, with r = 1 and r = 2."""
     rng = np.random.default_rng(N + dims[2])
@@ -192,7 +193,7 @@ def test_cas_single_workgroup_limits(N, dims):
     spec = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8)
     M = 5000 if dims == (16, 16, 16) and N == 3000 else 1500
     run_both(P, spec, M, 8, "cas", "knn", 0, where=f"N={N} dims={dims}")
-    if dims in ((16, 16, 16), (12, 12, 12)):
+    if dims in ((16, 16, 16), (12, 12, 12), (10, 10, 10)):
         spec2 = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8, 2)
         run_both(P, spec2, 700, 8, "cas", "knn", 0, where=f"N={N} dims={dims} r=2")
 
