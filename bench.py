@@ -329,6 +329,173 @@ def measure_coverage(P, B: int, N: int, wl, reps: int = 3) -> dict:
             "methods": rows}
 
 
+CONFIGS = ("tiny", "object", "room", "bigroom/cas-knn", "bigroom/rvs-cube", "lidar")
+
+
+def _host_info() -> dict:
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "nproc": os.cpu_count()}
+
+
+class _OneCore:
+    """Pins this process to one core of those it may use (the oracle is
+    single-threaded; pinning keeps it on one core while it is timed)."""
+
+    def __init__(self):
+        self.saved = None
+        self.where = "no core (affinity unavailable)"
+
+    def __enter__(self):
+        if hasattr(os, "sched_getaffinity"):
+            self.saved = os.sched_getaffinity(0)
+            core = max(self.saved)
+            os.sched_setaffinity(0, {core})
+            self.where = f"core {core}"
+        return self
+
+    def __exit__(self, *exc):
+        if self.saved is not None:
+            os.sched_setaffinity(0, self.saved)
+
+
+def measure_configs(dev, with_oracle: bool, reps: int = 50, reps_big: int = 20) -> dict:
+    """Every workload config, each layer chained as in the parity tests:
+    median and interquartile range of the whole pass (build + sample + query
+    of every layer) between two events after a GPU-side delay, the median of
+    each call bracketed on its own (which adds the events' overhead), a
+    replay of the pass captured in a HIP graph where no layer waits on the
+    host, points/s, and algorithmic bytes per pass (per cloud and layer:
+    12N (+4N with weights) + 20S + 24|O_v| + 16MK + 28M, S the stored points)
+    over the median time. The oracle runs the same pass on one core."""
+    import torch
+    from paper_1912_02984_amd import cagq
+    from paper_1912_02984_amd import workloads as W
+
+    def ev():
+        return torch.cuda.Event(enable_timing=True)
+
+    out_all = {}
+    for name in CONFIGS:
+        w = W.get_workload(name)
+        P_np = w.points()
+        B, N = P_np.shape[0], P_np.shape[1]
+        P = torch.from_numpy(P_np).to(dev)
+        plan, n = [], N
+        for L in w.layers:
+            desc = cagq.desc_from_spec(L.grid)
+            lay = cagq.workspace_layout(B, n, desc)
+            plan.append((L, desc, torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev),
+                         cagq.alloc_query_outputs(B, L.M, L.K, dev), torch.empty((B, L.M), dtype=torch.int32, device=dev),
+                         torch.empty((B,), dtype=torch.int32, device=dev)))
+            n = L.M
+        grids = []
+
+        def run(marks=None):
+            grids.clear()
+            pts, wts = P, None
+            for (L, desc, ws, out, cl, mv) in plan:
+                g = cagq.build_grid(pts, desc, ws)
+                if marks is not None:
+                    marks.append(ev()); marks[-1].record()
+                cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
+                if marks is not None:
+                    marks.append(ev()); marks[-1].record()
+                cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
+                if marks is not None:
+                    marks.append(ev()); marks[-1].record()
+                grids.append(g)
+                pts, wts = out["center_xyz"], out["center_w"]
+
+        for _ in range(5):
+            run()
+        torch.cuda.synchronize()
+        nrep = reps_big if N * B > 1_000_000 else reps
+        pairs = []
+        for _ in range(nrep):
+            a, b = ev(), ev()
+            torch.cuda._sleep(SLEEP_CYCLES)
+            a.record()
+            run()
+            b.record()
+            pairs.append((a, b))
+        torch.cuda.synchronize()
+        tot = np.array([a.elapsed_time(b) for a, b in pairs])
+        # per call, each bracketed by events
+        calls = []
+        for _ in range(max(5, nrep // 4)):
+            marks = [ev()]
+            torch.cuda._sleep(SLEEP_CYCLES)
+            marks[0].record()
+            run(marks)
+            calls.append(marks)
+        torch.cuda.synchronize()
+        d = np.array([[m[i].elapsed_time(m[i + 1]) for i in range(len(m) - 1)] for m in calls])
+        med = np.median(d, axis=0)
+        layers = []
+        alg = 0
+        for li, (L, desc, ws, out, cl, mv) in enumerate(plan):
+            tb = grids[li].table()
+            nv = tb["nvox"].cpu().numpy().astype(np.int64)
+            S = np.array([int(tb["vox_off"][b_, int(nv[b_])]) for b_ in range(B)], np.int64)
+            n_in = N if li == 0 else plan[li - 1][0].M
+            per = 12 * n_in + (4 * n_in if li > 0 else 0) + 20 * S + 24 * nv + 16 * L.M * L.K + 28 * L.M
+            alg += int(per.sum())
+            layers.append({"sample": L.sample, "query": L.query, "M": L.M, "K": L.K,
+                           "build_ms": round(float(med[3 * li]), 4), "sample_ms": round(float(med[3 * li + 1]), 4),
+                           "query_ms": round(float(med[3 * li + 2]), 4)})
+        t_med = float(np.median(tot))
+        row = {"B": B, "N": N, "layers": layers, "ms_median": round(t_med, 4),
+               "ms_iqr": [round(float(np.percentile(tot, 25)), 4), round(float(np.percentile(tot, 75)), 4)],
+               "reps": nrep, "points_per_s": round(B * N / (t_med / 1e3), 1), "alg_bytes": alg,
+               "alg_gbs": round(alg / (t_med / 1e3) / 1e9, 1)}
+        # a HIP graph of the pass, where nothing in it waits on the host
+        host_rounds = any(L.sample == "cas" and n_l > 4096
+                          for L, n_l in zip(w.layers, [N] + [L.M for L in w.layers[:-1]]))
+        if not host_rounds:
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=side):
+                run()
+            torch.cuda.synchronize()
+            pairs = []
+            for _ in range(nrep):
+                a, b = ev(), ev()
+                torch.cuda._sleep(SLEEP_CYCLES)
+                a.record()
+                gr.replay()
+                b.record()
+                pairs.append((a, b))
+            torch.cuda.synchronize()
+            row["graph_ms_median"] = round(float(np.median([a.elapsed_time(b) for a, b in pairs])), 4)
+            del gr
+        if with_oracle and name not in ("bigroom/cas-knn", "bigroom/rvs-cube"):
+            import oracle
+            times = []
+            with _OneCore():
+                for _ in range(3 if B * N <= 100_000 else 1):
+                    t0 = time.perf_counter()
+                    pts, wts = P_np, None
+                    for L in w.layers:
+                        _, ocl, omv, oq = oracle.run_layer(pts, L, weights=wts)
+                        pts, wts = oq["center_xyz"], oq["center_w"]
+                    times.append(time.perf_counter() - t0)
+            row["oracle_ms"] = round(float(np.median(times)) * 1e3, 2)
+            row["oracle_cores"] = 1
+        out_all[name] = row
+        del plan, grids
+        torch.cuda.synchronize()
+    return out_all
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -343,6 +510,8 @@ def main():
                     help="a step issues RVS+cube once CAS+kNN has enqueued this layer's sampling (0-3)")
     ap.add_argument("--no-graph", action="store_true",
                     help="issue RVS+cube's kernels one by one instead of replaying its captured graph")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the timing of every workload config")
     ap.add_argument("--no-next", action="store_true",
                     help="skip the measurement of the rows beyond the hot path")
     ap.add_argument("--copy-probe", action="store_true",
@@ -539,9 +708,17 @@ def main():
         next_rows["knn_ring"] = measure_knn_ring(P, P_np, B, N, wls[0], with_oracle=not args.no_cpu_baseline)
         next_rows["coverage"] = measure_coverage(P, B, N, wls[0])
 
+    # every workload config (the C4 step above is the headline)
+    configs = None
+    if not args.no_configs:
+        configs = measure_configs(dev, with_oracle=not args.no_cpu_baseline)
+        configs["host"] = _host_info()
+
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
+        pin = _OneCore()
+        pin.__enter__()
         t0 = time.perf_counter()
         done = 0
         while True:
@@ -554,10 +731,12 @@ def main():
             if time.perf_counter() - t0 >= args.cpu_seconds or done >= 32:
                 break
         dt = time.perf_counter() - t0
+        pin.__exit__(None, None, None)
         cpu = {"value": round(done * N / dt, 1), "unit": "points/s", "cores": 1, "kind": "oracle",
                "sample": f"{done} pass(es) of the same hot path (all layers, "
                          f"{'both variants' if len(wls) == 2 else variants[0]}) over 1 of the {B} scenes, "
-                         f"single-threaded C oracle, {dt:.1f} s"}
+                         f"single-threaded C oracle pinned to {pin.where}, {dt:.1f} s",
+               **_host_info()}
 
     line = {
         "metric": METRIC,
@@ -581,6 +760,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "next_rows": next_rows,
+        "configs": configs,
     }
     print(json.dumps(line), flush=True)
 
