@@ -93,6 +93,27 @@ def summarize_stats(stats_csv: str, command: str) -> str:
     return "\n".join([f"Command: `{command}`", ""] + out) + "\n"
 
 
+def summarize_counters(csv_path: str) -> str:
+    """Per kernel, the dispatches and the average of every counter per
+    dispatch, from a rocprofv3 --pmc counter collection."""
+    rows = list(csv.DictReader(open(csv_path)))
+    sums, disp, names = {}, {}, []
+    for r in rows:
+        m = re.search(r"(k_\w+(?:<[^>]*>)?|at::native::\w+|__amd_\w+)", r["Kernel_Name"])
+        k = m.group(1) if m else r["Kernel_Name"][:40]
+        c = r["Counter_Name"]
+        if c not in names:
+            names.append(c)
+        sums.setdefault(k, {}).setdefault(c, 0.0)
+        sums[k][c] += float(r["Counter_Value"])
+        disp.setdefault(k, set()).add(r["Dispatch_Id"])
+    out = ["| Kernel | Dispatches | " + " | ".join(names) + " |", "|---|---|" + "---|" * len(names)]
+    for k in sorted(sums, key=lambda k: -sums[k].get(names[0], 0.0) / len(disp[k])):
+        n = len(disp[k])
+        out.append(f"| {k} | {n} | " + " | ".join(f"{sums[k].get(c, 0.0) / n:.1f}" for c in names) + " |")
+    return "\n".join(out) + "\n"
+
+
 def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
     """HBM bytes per launch of the layer-1 query kernels from a FETCH_SIZE
     and a WRITE_SIZE pass, each scaled by what the same counter reads for
@@ -518,11 +539,16 @@ def main():
                     help="run one fp32 copy kernel of known size first (counter calibration)")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("STATS_CSV", "COMMAND"),
                     help="print a markdown table of a rocprofv3 kernel summary and exit")
+    ap.add_argument("--summarize-counters", metavar="COUNTER_CSV",
+                    help="print a markdown table of a rocprofv3 --pmc collection per kernel and exit")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the query kernels' HBM bytes from two counter passes and exit")
     args = ap.parse_args()
     if args.summarize_stats:
         print(summarize_stats(*args.summarize_stats), end="")
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters), end="")
         return
     if args.summarize_traffic:
         print(summarize_traffic(*args.summarize_traffic), end="")
