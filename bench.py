@@ -720,9 +720,26 @@ def main():
                             ctx_total=ctx_total)
     dom = max(roof.values(), key=lambda r: r["us"])
     traffic = load_traffic().get(dom["kernel"])
+    # what a plain streaming copy reaches on this GPU, for context: a 1 GiB
+    # fp32 copy (read + write), timed like the query
+    src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    cps = []
+    for _ in range(3):
+        a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(SLEEP_CYCLES)
+        a.record()
+        dst.copy_(src)
+        b_.record()
+        cps.append((a, b_))
+    torch.cuda.synchronize()
+    copy_gbs = 2 * COPY_PROBE_BYTES / (min(a.elapsed_time(b_) for a, b_ in cps) / 1e3) / 1e9
+    del src, dst
     roofline = {"bound": "hbm", "achieved": round(dom["achieved_gbs"], 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(dom["achieved_gbs"] / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "kernel": dom["kernel"], "launch_us": round(dom["us"], 2), "alg_bytes": dom["alg_bytes"],
+                "copy_gbs": round(copy_gbs, 1),
                 "per_variant": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
                                 for k, v in roof.items()}}
 
