@@ -197,7 +197,15 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
 #pragma unroll
             for (int c = 0; c < kPre; ++c)
                 if ((uint32_t)c * 8 < n_r) U += uncovered(pre[c], c * 8, n_r, cov);
-            for (uint32_t c = kPre; c * 8 < n_r; ++c) U += uncovered(e[1 + c], c * 8, n_r, cov);
+            const uint32_t ncr = (n_r + 7) / 8;
+            for (uint32_t c0 = kPre; c0 < ncr; c0 += kPre) {
+                uint4 q[kPre];
+#pragma unroll
+                for (int j = 0; j < kPre; ++j) q[j] = e[1 + (c0 + j < ncr ? c0 + j : ncr - 1)];
+#pragma unroll
+                for (int j = 0; j < kPre; ++j)
+                    if (c0 + j < ncr) U += uncovered(q[j], (c0 + j) * 8, n_r, cov);
+            }
             const uint32_t kv = (U << kKeyShift) | (kSlotMask - s);
             key[s] = kv;
             lmax = kv > lmax ? kv : lmax;
@@ -247,17 +255,31 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
 #pragma unroll
             for (int c = 0; c < kPre; ++c) pre[c] = e[1 + c];
             const uint32_t n_r = h.x & 0xFFFFu, n2 = h.x >> 16;
+            const uint32_t nch = (n2 + 7) / 8;  // groups of 8 entries (n2 >= 1: the voxel itself)
             int32_t found = -1;
-            for (uint32_t c = 0; c * 8 < n2 && found < 0; ++c) {
-                const uint4 v = c < (uint32_t)kPre ? pre[c < (uint32_t)kPre ? c : 0] : e[1 + c];
-                uint32_t sl[8], kk[8];
+            // kPre groups at a time: the first came with the header, each
+            // later batch is loaded in one go (clamped to the list's last
+            // group), so a long list costs one load latency per kPre groups
+            for (uint32_t c0 = 0; c0 < nch && found < 0; c0 += kPre) {
+                uint4 q[kPre];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(v, j) : s;
+                for (int j = 0; j < kPre; ++j) {
+                    const uint32_t cj = c0 + j < nch ? c0 + j : nch - 1;
+                    q[j] = c0 == 0 ? pre[j] : e[1 + cj];
+                }
 #pragma unroll
-                for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+                for (int jj = 0; jj < kPre; ++jj) {
+                    const uint32_t c = c0 + jj;
+                    if (c >= nch || found >= 0) break;
+                    uint32_t sl[8], kk[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j)
-                    if (found < 0 && kk[j] > my) found = (int32_t)sl[j];
+                    for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(q[jj], j) : s;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        if (found < 0 && kk[j] > my) found = (int32_t)sl[j];
+                }
             }
             if (found >= 0) {
                 blk[s] = (uint16_t)found;
@@ -270,7 +292,17 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
             rnd[s] = cur;
             blk[s] = (uint16_t)(my >> 16);
             dty[s] = (uint16_t)(my & 0xFFFFu);
-            for (uint32_t c = 0; c * 8 < n2; ++c) mark(e[1 + c], c * 8, n_r, n2, s, cur, rnd, dty, cov);
+            for (uint32_t c0 = 0; c0 < nch; c0 += kPre) {
+                uint4 q[kPre];
+#pragma unroll
+                for (int j = 0; j < kPre; ++j) {
+                    const uint32_t cj = c0 + j < nch ? c0 + j : nch - 1;
+                    q[j] = c0 == 0 ? pre[j] : e[1 + cj];
+                }
+#pragma unroll
+                for (int jj = 0; jj < kPre; ++jj)
+                    if (c0 + jj < nch) mark(q[jj], (c0 + jj) * 8, n_r, n2, s, cur, rnd, dty, cov);
+            }
         }
     }
     if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
