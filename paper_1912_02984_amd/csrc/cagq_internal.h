@@ -73,14 +73,16 @@ struct Layout {
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };
 
-// CAS control block, placed at Layout::cas_ctl: per round parity and cloud,
+// CAS control block, placed at Layout::cas_ctl: per round buffer (a round
+// writes one, reads the previous one and clears the next) and cloud,
 // kCasParts partial maxima / counts (spreading the atomics of one round over
 // several addresses), then per cloud a done flag, then the number of clouds
-// done:  u64 gpart[2][B][kCasParts]; u32 cpart[2][B][kCasParts]; u32 done[B];
+// done:  u64 gpart[3][B][kCasParts]; u32 cpart[3][B][kCasParts]; u32 done[B];
 // u32 ndone.
 constexpr int kCasParts = 128;
+constexpr int kCasBufs = 3;
 struct CasCtl {
-    static size_t bytes(int B) { return (size_t)B * (2 * kCasParts * 12 + 4) + 64; }
+    static size_t bytes(int B) { return (size_t)B * (kCasBufs * kCasParts * 12 + 4) + 64; }
 };
 
 // Neighbour lists of the single-workgroup CAS (clouds of at most kCasLdsMaxN

@@ -23,6 +23,14 @@
 // whose key exceeds the best unpicked key number at least m: those are the
 // sequential greedy's first picks, and the m largest keys among them are
 // its first m picks. They are emitted in ascending linear id.
+//
+// With neighbour lists (r = 1, clouds above the single-workgroup size) a
+// round is one kernel: each pick lowers the keys its coverage changes, so
+// no voxel is rescored (k_cas_round). Without lists a round is a scoring
+// kernel that recomputes the keys near the last picks from the occupancy
+// rows and a picking kernel (k_cas_score, k_cas_pick).
+#include <chrono>
+
 #include "cagq_internal.h"
 
 namespace cagq {
@@ -33,8 +41,8 @@ constexpr int kSelThreads = 1024;
 constexpr int32_t kSelManyBlockMin = 16384;  // clouds of this many points use the many-block select
 
 struct CasPtrs {
-    uint64_t* gpart;  // [2][B][kCasParts] partial maxima of the unpicked keys, per round parity
-    uint32_t* cpart;  // [2][B][kCasParts] partial counts of picks above that maximum
+    uint64_t* gpart;  // [kCasBufs][B][kCasParts] partial maxima of the unpicked keys, per round buffer
+    uint32_t* cpart;  // [kCasBufs][B][kCasParts] partial counts of picks above a maximum
     uint32_t* done;   // [B]
     uint32_t* ndone;  // clouds done
     uint32_t* host;       // pinned host words (or null): [0] = 1 once every cloud is done,
@@ -43,7 +51,7 @@ struct CasPtrs {
 
 CasPtrs cas_ptrs(const Layout& L, void* ws) {
     char* base = static_cast<char*>(ws) + L.cas_ctl;
-    const size_t parts = (size_t)2 * L.B * kCasParts;
+    const size_t parts = (size_t)kCasBufs * L.B * kCasParts;
     CasPtrs c;
     c.gpart = reinterpret_cast<uint64_t*>(base);
     c.cpart = reinterpret_cast<uint32_t*>(base + parts * 8);
@@ -418,10 +426,20 @@ struct CasState {
     uint64_t* pick;     // key at pick time, 0 = unpicked
     uint32_t* round;    // round that picked the voxel + 1, 0 = unpicked
     int32_t* blocker;   // a neighbour whose key beat the voxel's last time, -1 = none
-    uint32_t* dirty;    // round whose scoring must recompute the voxel's key
+    uint32_t* dirty;    // round whose scoring must recompute the voxel's key (row-scan rounds)
 };
 
-__global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
+// The key of a voxel of score `score` and linear id `lin`: (score, -lin) as
+// one unsigned 64-bit word, the score offset by 2^31.
+__device__ __forceinline__ uint64_t cas_key(int64_t score, uint32_t lin) {
+    return ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
+}
+
+// Clears the state and the control block. With lists (nbr != null) also sets
+// every occupied voxel's key for round 0: nothing is covered yet, so every
+// voxel within r is uncovered and the score is 2^16 * lambda * n_r.
+__global__ void k_cas_init(int32_t BN, int32_t B, int32_t N, CasState st, CasPtrs ctl, const uint32_t* __restrict__ nbr,
+                           const uint32_t* __restrict__ vox_lin, const int32_t* __restrict__ nvox, int64_t unit) {
     int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < BN) {
         st.cover[gid] = 0;
@@ -429,8 +447,10 @@ __global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
         st.round[gid] = 0;
         st.blocker[gid] = -1;
         st.dirty[gid] = 0;
+        if (nbr && gid - (gid / N) * N < nvox[gid / N])
+            st.key[gid] = cas_key(unit * (int64_t)nbr[(size_t)gid * kNbr32Stride], vox_lin[gid]);
     }
-    if (gid < 2 * B * kCasParts) {
+    if (gid < kCasBufs * B * kCasParts) {
         ctl.gpart[gid] = 0;
         ctl.cpart[gid] = 0;
     }
@@ -442,11 +462,11 @@ __global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
 // and wherever a pick of round R-1 came within distance 2r) and their
 // maximum per cloud. Also retires a cloud once round R-1 found enough picks
 // above the best unpicked key.
-template <int RAD, bool LIST>
+template <int RAD>
 __global__ __launch_bounds__(256) void k_cas_score(
     int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, int64_t lam, uint32_t beta_q16, int32_t M,
     const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
-    const uint32_t* __restrict__ word_rank, const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
+    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
     // no early exit: every lane takes part in the wave reductions
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
@@ -482,51 +502,31 @@ __global__ __launch_bounds__(256) void k_cas_score(
             const uint32_t* cv = st.cover + (size_t)b * N;
             const uint32_t lin = lin0;
             int64_t U = 0, cs = 0;
-            if constexpr (LIST) {
-                // the voxels within r head the list: at most 27 of them
-                static_assert(RAD == 1, "lists of the many-kernel path are for r = 1");
-                const uint4* e = reinterpret_cast<const uint4*>(nbr + (size_t)gid * kNbr32Stride);
-                uint4 q[8];
+            const uint64_t* bm = bitmap + (size_t)b * W;
+            const uint32_t* wr = word_rank + (size_t)b * W;
+            int32_t x, y, z;
+            decode_lin(lin, g, x, y, z);
+            constexpr int S = 2 * RAD + 1;
+            GridRow rows[S * S];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) q[j] = e[j];
-                const uint32_t n_r = q[0].x;
-                uint32_t c[28];
+            for (int j = 0; j < S * S; ++j)
+                rows[j] = load_row(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
+            // every coverage count of the window loaded at once, then masked
+            uint32_t c[S * S * S];
 #pragma unroll
-                for (int j = 0; j < 28; ++j) c[j] = cv[(uint32_t)j < n_r ? u4(q[1 + j / 4], j % 4) : (uint32_t)s];
+            for (int j = 0; j < S * S; ++j)
 #pragma unroll
-                for (int j = 0; j < 28; ++j) {
-                    const bool occ = (uint32_t)j < n_r;
-                    U += (occ && c[j] == 0) ? 1 : 0;
-                    cs += occ ? c[j] : 0u;
+                for (int q = 0; q < S; ++q) c[j * S + q] = cv[row_slot_or(rows[j], q, (uint32_t)s)];
+#pragma unroll
+            for (int j = 0; j < S * S; ++j)
+#pragma unroll
+                for (int q = 0; q < S; ++q) {
+                    const bool occ = (rows[j].mask >> q) & 1u;
+                    const uint32_t cc = occ ? c[j * S + q] : 0u;
+                    U += (occ && cc == 0) ? 1 : 0;
+                    cs += cc;
                 }
-            } else {
-                const uint64_t* bm = bitmap + (size_t)b * W;
-                const uint32_t* wr = word_rank + (size_t)b * W;
-                int32_t x, y, z;
-                decode_lin(lin, g, x, y, z);
-                constexpr int S = 2 * RAD + 1;
-                GridRow rows[S * S];
-#pragma unroll
-                for (int j = 0; j < S * S; ++j)
-                    rows[j] = load_row(bm, wr, g, x, y + j % S - RAD, z + j / S - RAD, RAD);
-                // every coverage count of the window loaded at once, then masked
-                uint32_t c[S * S * S];
-#pragma unroll
-                for (int j = 0; j < S * S; ++j)
-#pragma unroll
-                    for (int q = 0; q < S; ++q) c[j * S + q] = cv[row_slot_or(rows[j], q, (uint32_t)s)];
-#pragma unroll
-                for (int j = 0; j < S * S; ++j)
-#pragma unroll
-                    for (int q = 0; q < S; ++q) {
-                        const bool occ = (rows[j].mask >> q) & 1u;
-                        const uint32_t cc = occ ? c[j * S + q] : 0u;
-                        U += (occ && cc == 0) ? 1 : 0;
-                        cs += cc;
-                    }
-            }
-            const int64_t score = 65536ll * lam * U - (int64_t)beta_q16 * cs;
-            k = ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
+            k = cas_key(65536ll * lam * U - (int64_t)beta_q16 * cs, lin);
             st.key[gid] = k;
         } else {
             k = key0;
@@ -550,11 +550,11 @@ __global__ __launch_bounds__(256) void k_cas_score(
 // and scans its 2r-neighbourhood, one z-plane at a time, only when that one
 // no longer does. Also counts earlier picks whose key beats this round's
 // best unpicked key.
-template <int RAD, bool LIST>
+template <int RAD>
 __global__ __launch_bounds__(256) void k_cas_pick(
     int32_t R, int32_t B, int32_t N, int64_t W, GridDims g, const int32_t* __restrict__ nvox,
     const uint32_t* __restrict__ vox_lin, const uint64_t* __restrict__ bitmap,
-    const uint32_t* __restrict__ word_rank, const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
+    const uint32_t* __restrict__ word_rank, CasState st, CasPtrs ctl) {
     constexpr int H = 2 * RAD;      // half-width of the competition window
     constexpr int S2 = 2 * H + 1;
     // no early exit: every lane takes part in the wave-wide steps
@@ -590,42 +590,24 @@ __global__ __launch_bounds__(256) void k_cas_pick(
             const bool beaten = bl >= 0 && ky[bl] > my;
             if (!beaten) {
                 int32_t found = -1;
-                if constexpr (LIST) {
-                    // 16 entries of the list at a time (a voxel's own key
-                    // stands in past its end: it never beats itself)
-                    const uint4* e = reinterpret_cast<const uint4*>(nbr + (size_t)gid * kNbr32Stride);
-                    const uint32_t n2 = e[0].y;
-                    for (uint32_t c0 = 0; c0 < n2 && found < 0; c0 += 16) {
-                        uint4 q[4];
+                decode_lin(vox_lin[gid], g, x, y, z);
+                // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
+                // row descriptors, then all keys are loaded before comparing (a
+                // clear bit loads the voxel's own key, which never beats it)
+                for (int p = 0; p < S2 && found < 0; ++p) {
+                    const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
+                    GridRow rows[S2];
 #pragma unroll
-                        for (int j = 0; j < 4; ++j) q[j] = e[1 + c0 / 4 + j];
-                        uint64_t kk[16];
+                    for (int j = 0; j < S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j - H, z + dz, H);
+                    uint32_t sl[S2 * S2];
+                    uint64_t kk[S2 * S2];
 #pragma unroll
-                        for (int j = 0; j < 16; ++j) kk[j] = ky[c0 + j < n2 ? u4(q[j / 4], j % 4) : (uint32_t)s];
+                    for (int i = 0; i < S2 * S2; ++i) sl[i] = row_slot_or(rows[i / S2], i % S2, (uint32_t)s);
 #pragma unroll
-                        for (int j = 0; j < 16; ++j)
-                            if (found < 0 && kk[j] > my) found = (int32_t)u4(q[j / 4], j % 4);
-                    }
-                } else {
-                    decode_lin(vox_lin[gid], g, x, y, z);
-                    // planes in the order dz = 0, -1, +1, -2, +2, ...; per plane all
-                    // row descriptors, then all keys are loaded before comparing (a
-                    // clear bit loads the voxel's own key, which never beats it)
-                    for (int p = 0; p < S2 && found < 0; ++p) {
-                        const int32_t dz = (p & 1) ? -((p + 1) >> 1) : (p >> 1);
-                        GridRow rows[S2];
+                    for (int i = 0; i < S2 * S2; ++i) kk[i] = ky[sl[i]];
 #pragma unroll
-                        for (int j = 0; j < S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j - H, z + dz, H);
-                        uint32_t sl[S2 * S2];
-                        uint64_t kk[S2 * S2];
-#pragma unroll
-                        for (int i = 0; i < S2 * S2; ++i) sl[i] = row_slot_or(rows[i / S2], i % S2, (uint32_t)s);
-#pragma unroll
-                        for (int i = 0; i < S2 * S2; ++i) kk[i] = ky[sl[i]];
-#pragma unroll
-                        for (int i = 0; i < S2 * S2; ++i)
-                            if (found < 0 && kk[i] > my) found = (int32_t)sl[i];
-                    }
+                    for (int i = 0; i < S2 * S2; ++i)
+                        if (found < 0 && kk[i] > my) found = (int32_t)sl[i];
                 }
                 if (found >= 0) {
                     st.blocker[gid] = found;
@@ -640,42 +622,9 @@ __global__ __launch_bounds__(256) void k_cas_pick(
     // Marks of the winners: rescoring flags within 2r, coverage counts
     // within r. Winners of a round are more than 2r apart, so their
     // r-neighbourhoods are disjoint and no count is raised twice in a round:
-    // plain read-modify-write is exact. Without lists the whole wave marks
-    // each winner's window, one grid row per lane.
-    if constexpr (LIST) {
-        // the wave marks all (winner, list entry) pairs of its winners, 64
-        // at a time: the entries of one list are contiguous, so a winner's
-        // marks are coalesced, and the wave waits for two dependent loads
-        // per 64 pairs, not per winner
-        const uint32_t n2w = winner ? nbr[(size_t)gid * kNbr32Stride + 1] : 0u;
-        const uint32_t n_rw = winner ? nbr[(size_t)gid * kNbr32Stride] : 0u;
-        const uint32_t incl = wave_incl_scan<uint32_t>(n2w);
-        const uint32_t total = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
-        for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
-            const uint32_t p = p0 + (uint32_t)lane_id();
-            // owner: the first lane whose inclusive count exceeds p
-            int lo = 0;
-#pragma unroll
-            for (int step = kWave / 2; step > 0; step >>= 1) {
-                const uint32_t v = (uint32_t)__shfl((int)incl, lo + step - 1, kWave);
-                if (v <= p) lo += step;
-            }
-            const int owner = lo < kWave ? lo : kWave - 1;
-            const uint32_t o_incl = (uint32_t)__shfl((int)incl, owner, kWave);
-            const uint32_t o_n2 = (uint32_t)__shfl((int)n2w, owner, kWave);
-            const uint32_t o_nr = (uint32_t)__shfl((int)n_rw, owner, kWave);
-            const int32_t o_gid = __shfl(gid, owner, kWave);
-            const int32_t o_b = __shfl(b, owner, kWave);
-            if (p < total) {
-                const uint32_t j = p - (o_incl - o_n2);
-                const uint32_t sl = nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
-                uint32_t* cv = st.cover + (size_t)o_b * N;
-                st.dirty[(size_t)o_b * N + sl] = cur;
-                if (j < o_nr) cv[sl] = cv[sl] + 1u;
-            }
-        }
-    }
-    uint64_t wins = LIST ? 0ull : __ballot(winner);
+    // plain read-modify-write is exact. The whole wave marks each winner's
+    // window, one grid row per lane.
+    uint64_t wins = __ballot(winner);
     while (wins) {
         const int wl = __ffsll((unsigned long long)wins) - 1;
         wins &= wins - 1;
@@ -708,6 +657,230 @@ __global__ __launch_bounds__(256) void k_cas_pick(
         if (lane_id() == 0 && tot) atomicAdd(&cp[(size_t)b * kCasParts + part_slot()], tot);
     } else if (above) {
         atomicAdd(&cp[(size_t)b * kCasParts + part_slot()], above);
+    }
+}
+
+// The lane of the wave whose inclusive count is the first to exceed p.
+__device__ __forceinline__ int pair_owner(uint32_t incl, uint32_t p) {
+    int lo = 0;
+#pragma unroll
+    for (int step = kWave / 2; step > 0; step >>= 1) {
+        const uint32_t v = (uint32_t)__shfl((int)incl, lo + step - 1, kWave);
+        if (v <= p) lo += step;
+    }
+    return lo < kWave ? lo : kWave - 1;
+}
+
+// The first of entries 16c..16c+15 of a list of n2 entries (held in q) that
+// is a competitor and whose key beats `my`, or -1. Positions past the list's
+// end read the voxel's own slot `self`, whose key never beats its own.
+__device__ __forceinline__ int32_t beats(const uint4 (&q)[4], uint32_t c, uint32_t n2, uint32_t self, uint64_t my,
+                                         uint32_t cur, const uint64_t* __restrict__ ky,
+                                         const uint32_t* __restrict__ rd) {
+    uint32_t sl[16], rr[16];
+    uint64_t kk[16];
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sl[j] = 16 * c + j < n2 ? u4(q[j / 4], j % 4) : self;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        kk[j] = ky[sl[j]];
+        rr[j] = rd[sl[j]];
+    }
+    int32_t found = -1;
+#pragma unroll
+    for (int j = 0; j < 16; ++j)
+        if (found < 0 && kk[j] > my && (rr[j] == 0 || rr[j] == cur)) found = (int32_t)sl[j];
+    return found;
+}
+
+// One round of CAS on neighbour lists (r = 1), in one kernel: the keys stay
+// exact without rescoring. A winner raises the coverage count of every voxel
+// u within r of it, and the score of every voxel v within r of such a u
+// falls by beta_q16 (its coverage sum rose by one), and by 2^16 * lambda
+// more when u was uncovered (v lost an uncovered neighbour): the winner
+// subtracts that from v's key with an atomic add, so every key equals the
+// score formula on the current counts once the round's kernel has ended.
+//
+// Keys fall while other lanes of the same round read them, which keeps the
+// round exact:
+// * a voxel's key is lowered only by winners within distance 2r of it;
+// * two winners within 2r of each other cannot happen: of such pairs take
+//   the winner z of largest key. Any winner near z read z's key below its
+//   own, hence below z's, so a winner near z had lowered it before, after
+//   reading it below its own key in turn, and so on backwards in time
+//   through finitely many winners: a contradiction. So a winner's own key is
+//   exact, and it keeps that key for the whole round (it is never lowered);
+// * for a winner w and a voxel u within 2r of it, take the winner x near u
+//   with key below w's that read u first. It read u lowered only by winners
+//   with keys above w's, and still below its own key. So u's key, with every
+//   winner above w applied, is below w's, and stays below: w is picked by
+//   the sequential greedy, after those winners, with its very key.
+// A voxel picked in an earlier round keeps its key in the array; competitors
+// tell it apart by its pick round. The round's best unpicked key (read at the
+// round's start) bounds every later pick, so round R counts the picks above
+// round R-1's bound and round R+1 retires the cloud: the stopping rule of the
+// two-kernel rounds, one round later.
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_cas_round(int32_t R, int32_t B, int32_t N, int64_t unit, uint32_t beta_q16,
+                                                   int32_t M, const int32_t* __restrict__ nvox,
+                                                   const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
+    // no early exit: every lane takes part in the wave-wide steps
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    const bool in_range = gid < B * N;
+    const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
+    // the voxel's own state is loaded up front, together with the cloud's
+    const uint32_t rnd0 = in_range ? st.round[gid] : 0u;
+    const uint64_t pk0 = in_range ? st.pick[gid] : 0ull;
+    const uint64_t my0 = in_range ? st.key[gid] : 0ull;
+    const int32_t bl0 = in_range ? st.blocker[gid] : -1;
+    bool active = in_range && ctl.done[b] == 0;
+    if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
+        __hip_atomic_store(ctl.host + 1, (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    const int32_t nv = nvox[b];
+    const size_t part = (size_t)B * kCasParts;
+    const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) % kCasBufs) * part, b) : 0u;
+    if (active && prev >= (uint32_t)(M < nv ? M : nv)) {
+        if (s == 0) {
+            ctl.done[b] = 1;
+            // the last cloud to finish tells the host, without a copy on the stream
+            if (atomicAdd(ctl.ndone, 1u) + 1 == (uint32_t)B && ctl.host)
+                __hip_atomic_store(ctl.host, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+        active = false;
+    }
+    if (active)  // the next round's partials start from zero
+        for (int32_t i = s; i < kCasParts; i += N) {
+            const size_t o = (size_t)((R + 1) % kCasBufs) * part + (size_t)b * kCasParts + i;
+            ctl.gpart[o] = 0;
+            ctl.cpart[o] = 0;
+        }
+    const uint64_t G = R > 0 ? parts_max(ctl.gpart + (size_t)((R - 1) % kCasBufs) * part, b) : ~0ull;
+    const uint32_t cur = (uint32_t)R + 1;
+    const size_t cb = (size_t)b * N;
+    uint64_t k = 0;
+    uint32_t above = 0;
+    bool winner = false;
+    // A voxel unpicked at the round's start is beaten when its blocker
+    // still beats it, or else when an entry of its 2r-list does; the
+    // competitors are the voxels unpicked at the round's start or picked in
+    // this round (their keys stay in the array, their pick round tells them
+    // apart). Each lane checks its blocker and its list's first 16 entries;
+    // longer lists not yet decided are then scanned by the whole wave, one
+    // (voxel, 16 entries) pair per lane, so that no lane walks a long list
+    // alone.
+    const uint64_t* ky = st.key + cb;
+    const uint32_t* rd = st.round + cb;
+    const uint4* el = reinterpret_cast<const uint4*>(nbr + (size_t)(in_range ? gid : 0) * kNbr32Stride);
+    int32_t found = -2;  // -2: not competing, -1: no entry beats it so far
+    uint32_t n2 = 0;
+    if (active && s < nv) {
+        if (rnd0 != 0) {
+            above = pk0 > G ? 1u : 0u;
+        } else {
+            k = my0;
+            // the list's header and first entries are loaded with the blocker's state
+            const uint4 h = el[0];
+            uint4 q[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) q[j] = el[1 + j];
+            bool beaten = false;
+            if (bl0 >= 0) {
+                const uint64_t kb = ky[bl0];
+                const uint32_t rb = rd[bl0];
+                beaten = kb > my0 && (rb == 0 || rb == cur);
+            }
+            n2 = h.y;
+            if (!beaten) found = beats(q, 0, n2, (uint32_t)s, my0, cur, ky, rd);
+        }
+    }
+    const uint32_t nrest = found == -1 && n2 > 16 ? (n2 - 1) / 16 : 0u;  // chunks 1.. still to scan
+    const uint32_t sincl = wave_incl_scan<uint32_t>(nrest);
+    const uint32_t stot = (uint32_t)__shfl((int)sincl, kWave - 1, kWave);
+    if (stot) {
+        __shared__ int32_t s_found[256];
+        const int wbase = threadIdx.x & ~(kWave - 1);
+        s_found[threadIdx.x] = -1;
+        for (uint32_t p0 = 0; p0 < stot; p0 += kWave) {
+            const uint32_t p = p0 + (uint32_t)lane_id();
+            const int owner = pair_owner(sincl, p);
+            const uint32_t o_incl = (uint32_t)__shfl((int)sincl, owner, kWave);
+            const uint32_t o_n = (uint32_t)__shfl((int)nrest, owner, kWave);
+            const uint32_t o_n2 = (uint32_t)__shfl((int)n2, owner, kWave);
+            const int32_t o_gid = __shfl(gid, owner, kWave);
+            const int32_t o_b = __shfl(b, owner, kWave);
+            const uint64_t o_my = shfl64(my0, owner);
+            if (p < stot) {
+                const uint32_t c = 1 + p - (o_incl - o_n);
+                const size_t ob = (size_t)o_b * N;
+                const uint4* e = reinterpret_cast<const uint4*>(nbr + (size_t)o_gid * kNbr32Stride);
+                uint4 q[4];
+#pragma unroll
+                for (int j = 0; j < 4; ++j) q[j] = e[1 + 4 * c + j];
+                const int32_t f = beats(q, c, o_n2, (uint32_t)((size_t)o_gid - ob), o_my, cur, st.key + ob,
+                                        st.round + ob);
+                if (f >= 0) s_found[wbase + owner] = f;  // any beating entry will do
+            }
+        }
+        if (nrest) found = s_found[threadIdx.x];
+    }
+    if (found >= 0) {
+        st.blocker[gid] = found;
+    } else if (found == -1) {
+        winner = true;
+        st.round[gid] = cur;
+        st.pick[gid] = my0;
+    }
+    // The winners' coverage counts and key updates, by the whole wave over
+    // all (winner, u) pairs with u within r of the winner, 64 at a time.
+    // Winners are more than 2r apart, so no count is raised twice in a
+    // round: a plain read-modify-write is exact. A lane whose u was raised
+    // then walks u's own list within r and lowers those keys.
+    const uint32_t nrw = winner ? nbr[(size_t)gid * kNbr32Stride] : 0u;
+    const uint32_t incl = wave_incl_scan<uint32_t>(nrw);
+    const uint32_t total = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+    for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
+        const uint32_t p = p0 + (uint32_t)lane_id();
+        const int owner = pair_owner(incl, p);
+        const uint32_t o_incl = (uint32_t)__shfl((int)incl, owner, kWave);
+        const uint32_t o_nr = (uint32_t)__shfl((int)nrw, owner, kWave);
+        const int32_t o_gid = __shfl(gid, owner, kWave);
+        const int32_t o_b = __shfl(b, owner, kWave);
+        if (p < total) {
+            const uint32_t j = p - (o_incl - o_nr);
+            const size_t ob = (size_t)o_b * N;
+            const uint32_t u = nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
+            uint32_t* cv = st.cover + ob;
+            const uint32_t c = cv[u];
+            cv[u] = c + 1u;
+            const int64_t d = (c == 0 ? unit : 0) + (int64_t)beta_q16;
+            if (d != 0) {
+                const uint64_t dec = (uint64_t)(-d) << 32;  // the score field falls by d
+                const uint32_t o_s = (uint32_t)((size_t)o_gid - ob);
+                const uint4* lu = reinterpret_cast<const uint4*>(nbr + (ob + u) * kNbr32Stride);
+                const uint32_t n_ru = lu[0].x;
+                for (uint32_t c0 = 0; c0 < n_ru; c0 += 8) {
+                    const uint4 q0 = lu[1 + c0 / 4], q1 = lu[2 + c0 / 4];
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) {
+                        const uint32_t v = u4(jj < 4 ? q0 : q1, jj % 4);
+                        if (c0 + jj < n_ru && v != o_s)
+                            atomicAdd((unsigned long long*)&st.key[ob + v], (unsigned long long)dec);
+                    }
+                }
+            }
+        }
+    }
+    // per-cloud maximum of the unpicked keys and count of picks above the
+    // previous round's maximum, into this round's partial slots
+    const size_t mine = (size_t)(R % kCasBufs) * part;
+    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
+    if (b0 == b1) {
+        const uint64_t mx = wave_max64(k);
+        const uint32_t tot = wave_sum<uint32_t>(above);
+        if (lane_id() == 0 && mx) atomicMax((unsigned long long*)&ctl.gpart[mine + (size_t)b * kCasParts + part_slot()], mx);
+        if (lane_id() == 0 && tot) atomicAdd(&ctl.cpart[mine + (size_t)b * kCasParts + part_slot()], tot);
+    } else {
+        if (k) atomicMax((unsigned long long*)&ctl.gpart[mine + (size_t)b * kCasParts + part_slot()], k);
+        if (above) atomicAdd(&ctl.cpart[mine + (size_t)b * kCasParts + part_slot()], above);
     }
 }
 
@@ -775,44 +948,43 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     }
     const int64_t side = 2 * rad + 1;
     const int64_t lam = side * side * side;
-    const int32_t init_n = BN > 2 * B * kCasParts ? BN : 2 * B * kCasParts;
-    k_cas_init<<<(init_n + 255) / 256, 256, 0, s>>>(BN, B, st, ctl);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-
     const int32_t* nvox = at<int32_t>(ws, L.nvox);
     const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
     const uint64_t* bitmap = at<uint64_t>(ws, L.bitmap);
     const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
-    int64_t R = 0;
-    // neighbour lists replace the row scans where the layout holds them
+    hipError_t e = hipSuccess;
+    // neighbour lists replace the row scans where the layout holds them, and
+    // then a round is one kernel that keeps the keys exact by itself
     const bool lists = L.has_nbr32 && rad == 1;
     if (lists && (e = launch_cas_nbr(L, d, ws, s)) != hipSuccess) return e;
     const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
+    const int32_t init_n = BN > kCasBufs * B * kCasParts ? BN : kCasBufs * B * kCasParts;
+    k_cas_init<<<(init_n + 255) / 256, 256, 0, s>>>(BN, B, N, st, ctl, nbr, vox_lin, nvox, 65536 * lam);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+
+    int64_t R = 0;
     auto launch_batch = [&](int rounds) {
         for (int i = 0; i < rounds; ++i, ++R) {
             if (lists) {
-                k_cas_score<1, true><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox, vox_lin,
-                                                        bitmap, word_rank, nbr, st, ctl);
-                k_cas_pick<1, true><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
-                                                       word_rank, nbr, st, ctl);
+                k_cas_round<<<pb, 256, 0, s>>>((int32_t)R, B, N, 65536 * lam, beta_q16, M, nvox, nbr, st, ctl);
             } else if (rad == 1) {
-                k_cas_score<1, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
-                                                         vox_lin, bitmap, word_rank, nullptr, st, ctl);
-                k_cas_pick<1, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
-                                                        word_rank, nullptr, st, ctl);
+                k_cas_score<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
+                                                         vox_lin, bitmap, word_rank, st, ctl);
+                k_cas_pick<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
+                                                        word_rank, st, ctl);
             } else {
-                k_cas_score<2, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
-                                                         vox_lin, bitmap, word_rank, nullptr, st, ctl);
-                k_cas_pick<2, false><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
-                                                        word_rank, nullptr, st, ctl);
+                k_cas_score<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
+                                                         vox_lin, bitmap, word_rank, st, ctl);
+                k_cas_pick<2><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, nvox, vox_lin, bitmap,
+                                                        word_rank, st, ctl);
             }
         }
         return hipGetLastError();
     };
-    // every round picks at least the best unpicked voxel, so min(M, N) + 2
-    // rounds always suffice (the last one only records that the cloud is done)
-    const int64_t max_rounds = (int64_t)(M < N ? M : N) + 2;
+    // every round picks at least the best unpicked voxel, so min(M, N) + 3
+    // rounds always suffice (the last ones only count and record that the
+    // cloud is done)
+    const int64_t max_rounds = (int64_t)(M < N ? M : N) + 3;
     // every cloud needs several rounds: the first batches are long, later ones
     // short so that few rounds run after the last cloud is done
     const int first_batch = 6, batch = 2;
@@ -842,6 +1014,8 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     words[1] = 0;
     ctl.host = static_cast<uint32_t*>(dev_words);
     if ((e = launch_batch(first_batch)) != hipSuccess) return e;
+    uint32_t seen = ~0u;
+    auto seen_at = std::chrono::steady_clock::now();
     for (uint64_t spins = 1;; ++spins) {
         if (words[0] == 1u) return hipSuccess;
         if ((int64_t)words[1] + ahead >= R) {  // fewer than `ahead` rounds still queued
@@ -852,9 +1026,20 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
             if ((e = launch_batch(batch)) != hipSuccess) return e;
             continue;
         }
-        if (spins % 1024 == 0) {  // a failed stream ends the wait
-            const hipError_t q = hipStreamQuery(s);
-            if (q != hipSuccess && q != hipErrorNotReady) return q;
+        // A failed stream ends the wait. The stream is queried only once no
+        // round has started for a millisecond: a query of a busy stream puts
+        // a marker into its queue, which holds back the next round by ~5 us.
+        if ((spins & 1023) == 0) {
+            const uint32_t w = words[1];
+            const auto now = std::chrono::steady_clock::now();
+            if (w != seen) {
+                seen = w;
+                seen_at = now;
+            } else if (now - seen_at > std::chrono::milliseconds(1)) {
+                const hipError_t q = hipStreamQuery(s);
+                if (q != hipSuccess && q != hipErrorNotReady) return q;
+                seen_at = now;
+            }
         }
     }
 }

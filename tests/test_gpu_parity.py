@@ -193,7 +193,7 @@ def test_cas_single_workgroup_limits(N, dims):
     spec = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8)
     M = 5000 if dims == (16, 16, 16) and N == 3000 else 1500
     run_both(P, spec, M, 8, "cas", "knn", 0, where=f"N={N} dims={dims}")
-    if dims in ((16, 16, 16), (12, 12, 12), (10, 10, 10)):
+    if dims in ((16, 16, 16), (12, 12, 12), (10, 10, 10), (48, 48, 24)):
         spec2 = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8, 2)
         run_both(P, spec2, 700, 8, "cas", "knn", 0, where=f"N={N} dims={dims} r=2")
 
