@@ -83,13 +83,27 @@ def _short(name: str) -> str:
 
 
 def summarize_stats(stats_csv: str, command: str) -> str:
-    """Markdown table of a rocprofv3 --stats kernel summary."""
+    """Markdown table of a rocprofv3 --stats kernel summary, and, when the
+    run's kernel trace sits beside it, the query launches by grid size."""
     rows = list(csv.DictReader(open(stats_csv)))
     out = ["| Kernel | Calls | Total (us) | Avg (us) | Min (us) | Max (us) | % |", "|---|---|---|---|---|---|---|"]
     for r in rows:
         out.append(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e3:.1f} | "
                    f"{float(r['AverageNs']) / 1e3:.2f} | {float(r['MinNs']) / 1e3:.2f} | "
                    f"{float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.2f} |")
+    trace_csv = stats_csv.replace("_kernel_stats.csv", "_kernel_trace.csv")
+    if trace_csv != stats_csv and os.path.exists(trace_csv):
+        by = {}
+        for r in csv.DictReader(open(trace_csv)):
+            if "k_query" not in r["Kernel_Name"]:
+                continue
+            blocks = int(r["Grid_Size_X"]) // max(1, int(r["Workgroup_Size_X"]))
+            d = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            by.setdefault((_short(r["Kernel_Name"]), blocks), []).append(d)
+        out += ["", "Query launches by grid size (from the kernel trace of the same run):", "",
+                "| Kernel | Blocks | Launches | Avg (us) | Min (us) |", "|---|---|---|---|---|"]
+        for (name, blocks), ds in sorted(by.items(), key=lambda kv: (kv[0][0], -kv[0][1])):
+            out.append(f"| {name} | {blocks} | {len(ds)} | {sum(ds) / len(ds):.2f} | {min(ds):.2f} |")
     return "\n".join([f"Command: `{command}`", ""] + out) + "\n"
 
 
