@@ -985,24 +985,25 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     // rounds always suffice (the last ones only count and record that the
     // cloud is done)
     const int64_t max_rounds = (int64_t)(M < N ? M : N) + 3;
-    // every cloud needs several rounds: the first batches are long, later ones
+    // every cloud needs several rounds: the first batch is long, later ones
     // short so that few rounds run after the last cloud is done
-    const int first_batch = 6, batch = 2;
+    const int first_batch = 6, batch = 1;
     uint32_t* poll = poll_buffer();
     if (!poll) {
-        // synchronous polling
+        // synchronous polling, a few rounds per copy of the done count
+        const int sync_batch = 4;
         while (true) {
-            if ((e = launch_batch(batch)) != hipSuccess) return e;
+            if ((e = launch_batch(sync_batch)) != hipSuccess) return e;
             uint32_t nd = 0;
             if ((e = hipMemcpyAsync(&nd, ctl.ndone, sizeof nd, hipMemcpyDeviceToHost, s)) != hipSuccess) return e;
             if ((e = hipStreamSynchronize(s)) != hipSuccess) return e;
             if (nd == (uint32_t)B) return hipSuccess;
-            if (R > max_rounds + 2 * batch) break;
+            if (R > max_rounds + 2 * sync_batch) break;
         }
         *status_out = CAGQ_ERR_CAPACITY;
         return hipSuccess;
     }
-    const int ahead = 3;
+    const int ahead = 2;
     // The scoring kernel publishes its round and, once every cloud is done,
     // a done flag in pinned host memory. The host keeps at least `ahead`
     // rounds queued until it sees the flag: no copies and no events on the
