@@ -544,7 +544,7 @@ def main():
     ap.add_argument("--rvs-after-layer", type=int, default=2,
                     help="a step issues RVS+cube once CAS+kNN has enqueued this layer's sampling (0-3)")
     ap.add_argument("--no-graph", action="store_true",
-                    help="issue RVS+cube's kernels one by one instead of replaying its captured graph")
+                    help="issue every kernel one by one instead of replaying the captured graphs of the layers that do not wait on the host")
     ap.add_argument("--no-configs", action="store_true",
                     help="skip the timing of every workload config")
     ap.add_argument("--no-next", action="store_true",
@@ -607,10 +607,17 @@ def main():
     streams = [torch.cuda.Stream() for _ in plans]
     q_events = []  # (variant, start, end) around layer-1 query launches
 
-    def run_variant(plan, record=False, hook=None, hook_layer=-1):
+    def run_variant(plan, record=False, hook=None, hook_layer=-1, first=0, last=None):
+        """Layers [first, last) of a variant; a later layer reads the
+        previous layer's outputs, which stay at fixed addresses."""
         w, layers = plan
-        pts, wts = P, None
-        for li, (L, desc, ws, out, cl, mv) in enumerate(layers):
+        if first == 0:
+            pts, wts = P, None
+        else:
+            prev = layers[first - 1][3]
+            pts, wts = prev["center_xyz"], prev["center_w"]
+        for li in range(first, len(layers) if last is None else last):
+            L, desc, ws, out, cl, mv = layers[li]
             g = cagq.build_grid(pts, desc, ws)
             cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
             if li == hook_layer and hook is not None:
@@ -632,20 +639,45 @@ def main():
                 q_events.append((w.name, e0, e1))
             pts, wts = out["center_xyz"], out["center_w"]
 
-    # RVS+cube never waits on the host, so it is captured once in a HIP graph
-    # (kernel launches only) and a step replays it: one launch from the host
+    def host_layers(w):
+        """Leading layers whose sampling waits on the host: CAS outside the
+        single-workgroup kernel (more than 4096 points or r > 2) issues its
+        rounds from the host until every cloud is done."""
+        n, k = N, 0
+        for li, L in enumerate(w.layers):
+            if L.sample == "cas" and not (n <= 4096 and L.grid.radius in (1, 2)):
+                k = li + 1
+            n = L.M
+        return k
+
+    # The layers after the last one that waits on the host only enqueue
+    # kernels, so they are captured once in a HIP graph (kernel launches only)
+    # and a step replays it: one launch from the host instead of ~10 per layer
+    # (all of RVS+cube; layers 3-4 of CAS+kNN)
     graphs = {}
     if not args.no_graph:
         for i, (w, layers) in enumerate(plans):
-            if w.layers[0].sample == "rvs":
-                with torch.cuda.stream(streams[i]):
-                    run_variant(plans[i])  # eager once, outside the capture
-                torch.cuda.synchronize()
-                gr = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(gr, stream=streams[i]):
-                    run_variant(plans[i])
-                torch.cuda.synchronize()
-                graphs[i] = gr
+            t = host_layers(w)
+            if t >= len(layers):
+                continue
+            with torch.cuda.stream(streams[i]):
+                run_variant(plans[i])  # eager once, outside the capture
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr, stream=streams[i]):
+                run_variant(plans[i], first=t)
+            torch.cuda.synchronize()
+            graphs[i] = (t, gr)
+
+    def run_planned(i, hook=None, hook_layer=-1):
+        """A variant as a step runs it: its host-driven layers eagerly, the
+        rest from its graph."""
+        t, gr = graphs.get(i, (len(plans[i][1]), None))
+        run_variant(plans[i], hook=hook, hook_layer=hook_layer, last=t)
+        if gr is not None:
+            gr.replay()
+            if hook is not None and hook_layer >= t:
+                hook()
 
     def step():
         main = torch.cuda.current_stream()
@@ -655,24 +687,22 @@ def main():
             st.wait_event(start)
         # CAS+kNN waits on the host for the rounds of its two large layers.
         # RVS+cube only enqueues; it is issued from inside CAS+kNN once a
-        # layer's sampling is enqueued (by default the third layer's: the
-        # single-workgroup CAS of the last two layers holds four CUs for
-        # ~0.25 ms and RVS+cube's kernels fill the others, where beside the
-        # large layers' rounds they delay each round's launches)
+        # layer's sampling is enqueued (by default the third layer's, which
+        # comes with the graph of the last two: their single-workgroup CAS
+        # holds four CUs for ~0.25 ms and RVS+cube's kernels fill the others,
+        # where beside the large layers' rounds they delay each round's
+        # launches)
         cas = [i for i in range(len(plans)) if plans[i][0].layers[0].sample != "rvs"]
         rvs = [i for i in range(len(plans)) if plans[i][0].layers[0].sample == "rvs"]
 
         def issue_rvs():
             for i in rvs:
                 with torch.cuda.stream(streams[i]):
-                    if i in graphs:
-                        graphs[i].replay()
-                    else:
-                        run_variant(plans[i])
+                    run_planned(i)
 
         if cas:
             with torch.cuda.stream(streams[cas[0]]):
-                run_variant(plans[cas[0]], hook=issue_rvs, hook_layer=args.rvs_after_layer)
+                run_planned(cas[0], hook=issue_rvs, hook_layer=args.rvs_after_layer)
         else:
             issue_rvs()
         for st in streams:

@@ -555,9 +555,9 @@ def _rvs_plan(w, B, dev):
     return plan
 
 
-def _run_plan(P, plan):
-    pts, wts = P, None
-    for (L, desc, ws, out, cl, mv) in plan:
+def _run_plan(P, plan, first=0):
+    pts, wts = (P, None) if first == 0 else (plan[first - 1][3]["center_xyz"], plan[first - 1][3]["center_w"])
+    for (L, desc, ws, out, cl, mv) in plan[first:]:
         g = cagq.build_grid(pts, desc, ws)
         cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
         cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
@@ -611,6 +611,51 @@ def test_graph_replay_of_the_rvs_cube_path():
         torch.cuda.synchronize()
         got = _snapshot(plan)
         for li, ((a_cl, a_mv, a_out), (b_cl, b_mv, b_out)) in enumerate(zip(ref, got)):
+            assert np.array_equal(a_cl, b_cl) and np.array_equal(a_mv, b_mv), (rep, li)
+            for k in a_out:
+                assert np.array_equal(_bits(a_out[k]), _bits(b_out[k])), (rep, li, k)
+        _run_plan(P2, other)  # the program's own eager work between replays
+        torch.cuda.synchronize()
+
+
+def test_graph_replay_of_the_single_workgroup_cas_layers():
+    """Layers 3-4 of the CAS + k-NN indoor path (2048 and 512 points per
+    cloud: single-workgroup CAS, no host round trips), captured in a HIP graph
+    after eager layers 1-2 and replayed three times with eager work and
+    synchronizations between: every replay equals the eager result bit for
+    bit, and layer 3's centers equal the oracle's CAS on layer 2's output."""
+    w = W.get_workload("bigroom/cas-knn")
+    B = 4
+    P = torch.from_numpy(w.points(B=B)).to(DEV)
+    plan = _rvs_plan(w, B, DEV)
+    _run_plan(P, plan)
+    torch.cuda.synchronize()
+    ref = _snapshot(plan)
+    L3 = w.layers[2]
+    ot = oracle.Table(_np(plan[1][3]["center_xyz"]).copy(), oracle.grid_from_spec(L3.grid))
+    ocl, omv, _, _ = ot.sample_cas(L3.M)
+    assert np.array_equal(ref[2][0], ocl) and np.array_equal(ref[2][1], omv)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=side):
+        _run_plan(P, plan, first=2)
+    torch.cuda.synchronize()
+    other = _rvs_plan(w, B, DEV)
+    P2 = (P * 0.5).contiguous()
+    for rep in range(3):
+        for (L, desc, ws, out, cl, mv) in plan[2:]:  # scribble over the outputs first
+            cl.fill_(-5)
+            for v in out.values():
+                if v is not None:
+                    v.fill_(7)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        got = _snapshot(plan)
+        for li in (2, 3):
+            (a_cl, a_mv, a_out), (b_cl, b_mv, b_out) = ref[li], got[li]
             assert np.array_equal(a_cl, b_cl) and np.array_equal(a_mv, b_mv), (rep, li)
             for k in a_out:
                 assert np.array_equal(_bits(a_out[k]), _bits(b_out[k])), (rep, li, k)
