@@ -203,12 +203,16 @@ __device__ __forceinline__ uint64_t wave_merge_low64(uint64_t best, uint64_t add
 }
 
 // Agent-scope atomics for the cross-workgroup scan descriptors (the 8 XCDs
-// have separate L2s, so these must reach the coherent level).
-__device__ __forceinline__ uint64_t ld_acquire(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT);
+// have separate L2s, so these must reach the coherent level). Relaxed: a
+// descriptor carries its value and status in one word, and no tile reads
+// another tile's other output within the kernel, so no ordering with other
+// memory is needed (an agent-scope release or acquire would also write back
+// or invalidate the XCD's L2 at every descriptor).
+__device__ __forceinline__ uint64_t ld_desc(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void st_release(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+__device__ __forceinline__ void st_desc(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 __device__ __forceinline__ void raise_error(int* status, int code) {
@@ -232,16 +236,16 @@ __device__ inline uint64_t tile_lookback_at(F desc, int64_t tile, uint64_t agg, 
         const int lane = lane_id();
         uint64_t excl = 0;
         if (tile == 0) {
-            if (lane == 0) st_release(desc(0), kDescInc | agg);
+            if (lane == 0) st_desc(desc(0), kDescInc | agg);
         } else {
-            if (lane == 0) st_release(desc(tile), kDescAgg | agg);
+            if (lane == 0) st_desc(desc(tile), kDescAgg | agg);
             int64_t base = tile - 1;
             while (true) {
                 int64_t idx = base - lane;
                 uint64_t d = kDescInc;  // before the first tile: an inclusive zero
                 if (idx >= 0) {
                     do {
-                        d = ld_acquire(desc(idx));
+                        d = ld_desc(desc(idx));
                     } while ((d >> 62) == 0);
                 }
                 uint64_t inc = __ballot((d >> 62) == 2);
@@ -253,7 +257,7 @@ __device__ inline uint64_t tile_lookback_at(F desc, int64_t tile, uint64_t agg, 
                 excl += wave_sum<uint64_t>(d & kDescVal);
                 base -= kWave;
             }
-            if (lane == 0) st_release(desc(tile), kDescInc | (excl + agg));
+            if (lane == 0) st_desc(desc(tile), kDescInc | (excl + agg));
         }
         if (lane == 0) *s_out = excl;
     }
