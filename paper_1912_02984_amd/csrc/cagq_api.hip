@@ -155,7 +155,7 @@ int cagq_sample_centers(const cagq_grid* g, int32_t M, int32_t mode, uint64_t se
     hipError_t e = run_cas(L, g->desc, g->workspace, M, beta_q16, (hipStream_t)stream, &status);
     if (e != hipSuccess) return CAGQ_ERR_HIP;
     if (status != CAGQ_OK) return status;
-    e = launch_select(L, g->workspace, M, 1, seed, center_lin, m_valid, (hipStream_t)stream);
+    e = launch_select_cas(L, g->desc, g->workspace, M, beta_q16, center_lin, m_valid, (hipStream_t)stream);
     return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
 }
 

@@ -77,12 +77,17 @@ struct Layout {
 // writes one, reads the previous one and clears the next) and cloud,
 // kCasParts partial maxima / counts (spreading the atomics of one round over
 // several addresses), then per cloud a done flag, then the number of clouds
-// done:  u64 gpart[3][B][kCasParts]; u32 cpart[3][B][kCasParts]; u32 done[B];
-// u32 ndone.
+// done, then the number of clouds done, then per cloud kCasParts partial
+// histograms of the picks' uncovered counts U (rounds on lists with beta = 0):
+// u64 gpart[3][B][kCasParts]; u32 cpart[3][B][kCasParts]; u32 done[B];
+// u32 ndone; u32 uhist[B][kCasParts][kCasUBins].
 constexpr int kCasParts = 128;
 constexpr int kCasBufs = 3;
+constexpr int kCasUBins = 32;  // U <= 27 with r = 1
 struct CasCtl {
-    static size_t bytes(int B) { return (size_t)B * (kCasBufs * kCasParts * 12 + 4) + 64; }
+    static size_t bytes(int B) {
+        return (size_t)B * (kCasBufs * kCasParts * 12 + 4 + 4 * kCasParts * kCasUBins) + 64;
+    }
 };
 
 // Neighbour lists of the single-workgroup CAS (clouds of at most kCasLdsMaxN
@@ -407,6 +412,12 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
 // key_mode 0: RVS keys from `seed`; key_mode 1: CAS pick keys (largest first).
 hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uint64_t seed,
                          int32_t* center_lin, int32_t* m_valid, hipStream_t s);
+
+// The selection after run_cas: the m largest pick keys. Rounds on lists with
+// beta = 0 kept a histogram of the picks' U, which gives the bound at once;
+// otherwise the radix select of launch_select.
+hipError_t launch_select_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, uint32_t beta_q16,
+                             int32_t* center_lin, int32_t* m_valid, hipStream_t s);
 
 // The paper's challenger / incumbent CAS: RVS incumbents, then one
 // workgroup per cloud walks the challengers.

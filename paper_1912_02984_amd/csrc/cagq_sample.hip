@@ -29,6 +29,7 @@
 // no voxel is rescored (k_cas_round). Without lists a round is a scoring
 // kernel that recomputes the keys near the last picks from the occupancy
 // rows and a picking kernel (k_cas_score, k_cas_pick).
+#include <algorithm>
 #include <chrono>
 
 #include "cagq_internal.h"
@@ -45,6 +46,7 @@ struct CasPtrs {
     uint32_t* cpart;  // [kCasBufs][B][kCasParts] partial counts of picks above a maximum
     uint32_t* done;   // [B]
     uint32_t* ndone;  // clouds done
+    uint32_t* uhist;  // [B][kCasParts][kCasUBins] picks per uncovered count U (lists, beta = 0)
     uint32_t* host;       // pinned host words (or null): [0] = 1 once every cloud is done,
                           // [1] = the round being scored (all earlier rounds have finished)
 };
@@ -57,6 +59,7 @@ CasPtrs cas_ptrs(const Layout& L, void* ws) {
     c.cpart = reinterpret_cast<uint32_t*>(base + parts * 8);
     c.done = reinterpret_cast<uint32_t*>(base + parts * 12);
     c.ndone = c.done + L.B;
+    c.uhist = c.ndone + 1;
     c.host = nullptr;
     return c;
 }
@@ -455,6 +458,7 @@ __global__ void k_cas_init(int32_t BN, int32_t B, int32_t N, CasState st, CasPtr
         ctl.cpart[gid] = 0;
     }
     if (gid < B) ctl.done[gid] = 0;
+    if (gid < B * kCasParts * kCasUBins) ctl.uhist[gid] = 0;
     if (gid == 0) *ctl.ndone = 0;
 }
 
@@ -828,6 +832,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
         winner = true;
         st.round[gid] = cur;
         st.pick[gid] = my0;
+        if (beta_q16 == 0) {  // the score is unit * U: the pick's U, for the selection
+            const uint32_t u = (uint32_t)(((int64_t)(my0 >> 32) - 2147483648ll) / unit);
+            atomicAdd(&ctl.uhist[((size_t)b * kCasParts + part_slot()) * kCasUBins + u], 1u);
+        }
     }
     // The winners' coverage counts and key updates, by the whole wave over
     // all (winner, u) pairs with u within r of the winner, 64 at a time.
@@ -884,6 +892,51 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
     }
 }
 
+// Bound and tie count of the m largest pick keys from the histogram of the
+// picks' U (beta = 0: a pick key is (unit * U + 2^31, ~lin), so the m
+// largest are the picks with U > U* and, of those with U = U*, the lowest
+// slots, U* being the largest U with at least m picks at or above it). Also
+// clears the scan state of the compaction that follows.
+__global__ void k_sel_cas_u(int64_t tiles_s, const int32_t* __restrict__ nvox, int32_t M,
+                            const uint32_t* __restrict__ uhist, int64_t unit, uint64_t* __restrict__ thr,
+                            int32_t* __restrict__ m_valid, uint64_t* __restrict__ desc_s, int* __restrict__ status) {
+    const int32_t b = blockIdx.x;
+    for (int64_t t = threadIdx.x; t < tiles_s; t += blockDim.x) desc_s[(size_t)b * tiles_s + t] = 0;
+    if (b == 0 && threadIdx.x == 0) status[kStTicketSel] = 0;
+    // bin totals over the partial histograms: lane l sums bin l % 32 over
+    // half of the partials, the two halves then add up
+    __shared__ uint32_t s_h[kCasUBins];
+    static_assert(2 * kCasUBins == kWave, "two lanes per bin");
+    {
+        const int bin = threadIdx.x % kCasUBins, half = threadIdx.x / kCasUBins;
+        const uint32_t* h0 = uhist + ((size_t)b * kCasParts + (size_t)half * (kCasParts / 2)) * kCasUBins + bin;
+        uint32_t h = 0;
+#pragma unroll 16
+        for (int i = 0; i < kCasParts / 2; ++i) h += h0[(size_t)i * kCasUBins];
+        h += (uint32_t)__shfl_down((int)h, kCasUBins, kWave);
+        if (threadIdx.x < kCasUBins) s_h[threadIdx.x] = h;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        const int32_t nv = nvox[b];
+        const uint32_t m = (uint32_t)(M < nv ? M : nv);
+        uint32_t run = 0, need = 0;
+        uint64_t bound = 0;
+        for (int u = kCasUBins - 1; u >= 0 && m > 0; --u) {
+            const uint32_t h = s_h[u];
+            if (run + h >= m) {
+                // the select key is the complement of the pick key: its top half
+                bound = 0xFFFFFFFFull - (uint64_t)(unit * u + 2147483648ll);
+                need = m - run;
+                break;
+            }
+            run += h;
+        }
+        thr[b] = sel_pack(bound, need);
+        m_valid[b] = (int32_t)m;
+    }
+}
+
 // A small pinned host buffer per calling thread for polling the number of
 // clouds done without stalling the stream. Allocated on first use, kept for
 // the life of the process.
@@ -926,6 +979,25 @@ hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uin
     return hipGetLastError();
 }
 
+hipError_t launch_select_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, uint32_t beta_q16,
+                             int32_t* center_lin, int32_t* m_valid, hipStream_t s) {
+    if (!(L.has_nbr32 && d.radius == 1 && beta_q16 == 0))
+        return launch_select(L, ws, M, 1, 0, center_lin, m_valid, s);
+    const CasPtrs ctl = cas_ptrs(L, ws);
+    const int64_t side = 2 * (int64_t)d.radius + 1;
+    uint64_t* thr = at<uint64_t>(ws, L.sel_thr);
+    uint64_t* desc_s = at<uint64_t>(ws, L.desc_s);
+    int* status = at<int>(ws, L.status);
+    const int32_t* nvox = at<int32_t>(ws, L.nvox);
+    k_sel_cas_u<<<L.B, kWave, 0, s>>>(L.tiles_s, nvox, M, ctl.uhist, 65536 * side * side * side, thr, m_valid,
+                                      desc_s, status);
+    k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(L.N, L.tiles_s, nvox,
+                                                                   at<uint32_t>(ws, L.vox_lin), M, 1, 0,
+                                                                   at<uint64_t>(ws, L.cas_pick), thr, center_lin,
+                                                                   desc_s, status);
+    return hipGetLastError();
+}
+
 hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, uint32_t beta_q16,
                    hipStream_t s, int* status_out) {
     *status_out = CAGQ_OK;
@@ -958,7 +1030,7 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     const bool lists = L.has_nbr32 && rad == 1;
     if (lists && (e = launch_cas_nbr(L, d, ws, s)) != hipSuccess) return e;
     const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
-    const int32_t init_n = BN > kCasBufs * B * kCasParts ? BN : kCasBufs * B * kCasParts;
+    const int32_t init_n = std::max(BN, B * kCasParts * kCasUBins);
     k_cas_init<<<(init_n + 255) / 256, 256, 0, s>>>(BN, B, N, st, ctl, nbr, vox_lin, nvox, 65536 * lam);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
