@@ -775,7 +775,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
     const uint32_t* rd = st.round + cb;
     const uint4* el = reinterpret_cast<const uint4*>(nbr + (size_t)(in_range ? gid : 0) * kNbr32Stride);
     int32_t found = -2;  // -2: not competing, -1: no entry beats it so far
-    uint32_t n2 = 0;
+    uint32_t n2 = 0, n_r = 0;
+    // a possible winner's first 16 list entries (its voxels within r come
+    // first), kept for the wave's coverage pass below
+    __shared__ uint32_t s_ent[256][16];
     if (active && s < nv) {
         if (rnd0 != 0) {
             above = pk0 > G ? 1u : 0u;
@@ -793,7 +796,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
                 beaten = kb > my0 && (rb == 0 || rb == cur);
             }
             n2 = h.y;
+            n_r = h.x;
             if (!beaten) found = beats(q, 0, n2, (uint32_t)s, my0, cur, ky, rd);
+            if (found == -1) {
+                uint4* se = reinterpret_cast<uint4*>(s_ent[threadIdx.x]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) se[j] = q[j];
+            }
         }
     }
     const uint32_t nrest = found == -1 && n2 > 16 ? (n2 - 1) / 16 : 0u;  // chunks 1.. still to scan
@@ -838,13 +847,15 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
         }
     }
     // The winners' coverage counts and key updates, by the whole wave over
-    // all (winner, u) pairs with u within r of the winner, 64 at a time.
-    // Winners are more than 2r apart, so no count is raised twice in a
-    // round: a plain read-modify-write is exact. A lane whose u was raised
-    // then walks u's own list within r and lowers those keys.
-    const uint32_t nrw = winner ? nbr[(size_t)gid * kNbr32Stride] : 0u;
+    // all (winner, u) pairs with u within r of the winner, 64 at a time (u
+    // from the winner's entries in LDS). Winners are more than 2r apart, so no
+    // count is raised twice in a round: a plain read-modify-write is exact.
+    // A lane loads u's count and u's list within r together, and when u was
+    // uncovered (or beta > 0) lowers the keys on that list.
+    const uint32_t nrw = winner ? n_r : 0u;
     const uint32_t incl = wave_incl_scan<uint32_t>(nrw);
     const uint32_t total = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+    const int wb = threadIdx.x & ~(kWave - 1);
     for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
         const uint32_t p = p0 + (uint32_t)lane_id();
         const int owner = pair_owner(incl, p);
@@ -855,22 +866,32 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
         if (p < total) {
             const uint32_t j = p - (o_incl - o_nr);
             const size_t ob = (size_t)o_b * N;
-            const uint32_t u = nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
+            const uint32_t u = j < 16 ? s_ent[wb + owner][j] : nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
             uint32_t* cv = st.cover + ob;
+            const uint4* lu = reinterpret_cast<const uint4*>(nbr + (ob + u) * kNbr32Stride);
+            uint4 lq[5];  // header and entries 0..15 (a list within r holds at most 27)
+#pragma unroll
+            for (int i = 0; i < 5; ++i) lq[i] = lu[i];
             const uint32_t c = cv[u];
             cv[u] = c + 1u;
             const int64_t d = (c == 0 ? unit : 0) + (int64_t)beta_q16;
             if (d != 0) {
                 const uint64_t dec = (uint64_t)(-d) << 32;  // the score field falls by d
                 const uint32_t o_s = (uint32_t)((size_t)o_gid - ob);
-                const uint4* lu = reinterpret_cast<const uint4*>(nbr + (ob + u) * kNbr32Stride);
-                const uint32_t n_ru = lu[0].x;
-                for (uint32_t c0 = 0; c0 < n_ru; c0 += 8) {
-                    const uint4 q0 = lu[1 + c0 / 4], q1 = lu[2 + c0 / 4];
+                const uint32_t n_ru = lq[0].x;
 #pragma unroll
-                    for (int jj = 0; jj < 8; ++jj) {
-                        const uint32_t v = u4(jj < 4 ? q0 : q1, jj % 4);
-                        if (c0 + jj < n_ru && v != o_s)
+                for (int i = 0; i < 16; ++i) {
+                    const uint32_t v = u4(lq[1 + i / 4], i % 4);
+                    if ((uint32_t)i < n_ru && v != o_s)
+                        atomicAdd((unsigned long long*)&st.key[ob + v], (unsigned long long)dec);
+                }
+                if (n_ru > 16) {
+#pragma unroll
+                    for (int i = 0; i < 3; ++i) lq[1 + i] = lu[5 + i];
+#pragma unroll
+                    for (int i = 16; i < 28; ++i) {
+                        const uint32_t v = u4(lq[1 + (i - 16) / 4], i % 4);
+                        if ((uint32_t)i < n_ru && v != o_s)
                             atomicAdd((unsigned long long*)&st.key[ob + v], (unsigned long long)dec);
                     }
                 }
