@@ -191,7 +191,7 @@ def test_cas_single_workgroup_limits(N, dims):
     P = rng.random((2, N, 3), dtype=np.float32) * np.float32(0.999)
     P[1, : N // 2] *= np.float32(0.3)  # a denser half in the second cloud
     spec = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8)
-    M = 5000 if dims == (16, 16, 16) and N == 3000 else 1500
+    M = 5000 if dims == (16, 16, 16) and N in (3000, 8192) else 1500  # M above the occupied voxels
     run_both(P, spec, M, 8, "cas", "knn", 0, where=f"N={N} dims={dims}")
     if dims in ((16, 16, 16), (12, 12, 12), (10, 10, 10), (48, 48, 24)):
         spec2 = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 8, 2)
@@ -231,11 +231,17 @@ def test_cas_swap_more_centers_than_voxels_and_capacity():
     assert ei.value.code == cagq.ERR_CAPACITY
 
 
+@pytest.mark.parametrize("name", ["object", "room"])
 @pytest.mark.parametrize("beta_q16", [1, 65536 // 4, 3 * 65536])
-def test_cas_with_overcoverage_penalty(beta_q16):
-    w = W.get_workload("object")
+def test_cas_with_overcoverage_penalty(name, beta_q16):
+    """beta > 0 on small clouds (the two-kernel rounds over occupancy rows)
+    and on 8192-point clouds (the one-kernel rounds on neighbour lists, whose
+    key lowering then also subtracts beta per raised count, and the radix
+    selection instead of the U histogram)."""
+    w = W.get_workload(name)
     L = w.layers[0]
-    run_both(w.points()[:4], L.grid, L.M, L.K, "cas", "knn", 0, beta_q16=beta_q16, where=f"beta={beta_q16}")
+    run_both(w.points()[:2 if name == "room" else 4], L.grid, L.M, L.K, "cas", "knn", 0, beta_q16=beta_q16,
+             where=f"{name} beta={beta_q16}")
 
 
 def test_weighted_centers():
