@@ -274,6 +274,220 @@ __global__ __launch_bounds__(256) void k_finalize(
     }
 }
 
+// ---- small clouds: the whole build in one workgroup per cloud.
+// For clouds of at most kSmallN points whose grid has at most kSmallW
+// occupancy words, every step above runs in one 1024-thread workgroup with
+// the bitmap, the ranks, the counts and offsets and the buckets in LDS, so
+// the seven launches (and their dependent round trips to memory) become one.
+// The outputs are those of the steps above, bit for bit: the same bitmap,
+// ranks, slots and linear ids, counts and offsets, and per voxel the n_v
+// lowest point indices in ascending order (ranked against the voxel's
+// bucket, or selected by a wave for voxels of more than kBigVoxel points).
+// The threads exchange data through LDS only, so the barriers do not wait for
+// the global stores of the steps before them.
+constexpr int kSmallT = 1024;
+constexpr int kSmallPts = 8;   // points per thread
+constexpr int kSmallWd = 4;    // occupancy words per thread
+constexpr int32_t kSmallN = kSmallT * kSmallPts;
+constexpr int64_t kSmallW = kSmallT * kSmallWd;
+constexpr int kSmallBig = kSmallN / (kBigVoxel + 1) + 1;  // voxels of more than kBigVoxel points
+
+// Exclusive scan of one value per thread over the kSmallT threads.
+__device__ __forceinline__ uint64_t small_excl_scan(uint64_t v, uint64_t* s_wave, uint64_t* total) {
+    const uint64_t incl = wave_incl_scan<uint64_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    lds_barrier();
+    uint64_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kSmallT / kWave; ++i) {
+        const uint64_t x = s_wave[i];
+        off += i < wv ? x : 0ull;
+        tot += x;
+    }
+    *total = tot;
+    lds_barrier();
+    return off + incl - v;
+}
+
+size_t small_lds_bytes(int32_t N, int64_t W) { return (size_t)12 * W + (size_t)4 * (2 * (size_t)N + 1); }
+
+__global__ __launch_bounds__(kSmallT) void k_build_small(
+    const float* __restrict__ P, int32_t N, GridArgs g, int64_t W, uint32_t n_v, uint32_t* __restrict__ pt_slot,
+    uint64_t* __restrict__ bitmap, uint32_t* __restrict__ word_rank, uint32_t* __restrict__ vox_lin,
+    uint32_t* __restrict__ vox_count, int32_t* __restrict__ nvox, uint32_t* __restrict__ vox_off,
+    uint32_t* __restrict__ pt_list, float4* __restrict__ pt4, int* __restrict__ status) {
+    extern __shared__ __align__(16) unsigned char lds[];
+    uint64_t* s_bm = reinterpret_cast<uint64_t*>(lds);   // [W] occupancy words
+    uint32_t* s_wr = reinterpret_cast<uint32_t*>(s_bm + W);  // [W] ranks
+    uint32_t* s_off = s_wr + W;  // [N + 1] counts, then (full offset << 16) | stored offset
+    uint32_t* s_bk = s_off + N + 1;  // [N] point indices grouped by slot (arrival order)
+    __shared__ uint64_t s_wave[kSmallT / kWave];
+    __shared__ uint32_t s_big[kSmallBig];
+    __shared__ uint32_t s_nbig;
+    const int32_t b = blockIdx.x;
+    const int tid = threadIdx.x;
+    const size_t pb = (size_t)b * N;
+
+    for (int64_t w = tid; w < W; w += kSmallT) s_bm[w] = 0ull;
+    for (int32_t i = tid; i <= N; i += kSmallT) s_off[i] = 0u;
+    if (tid == 0) s_nbig = 0;
+    lds_barrier();
+
+    // voxelize: linear id, occupancy bit
+    uint32_t lin[kSmallPts];
+#pragma unroll
+    for (int k = 0; k < kSmallPts; ++k) {
+        const int32_t i = tid + k * kSmallT;
+        lin[k] = 0;
+        if (i >= N) continue;
+        const float* p = P + (pb + i) * 3;
+        const float c[3] = {p[0], p[1], p[2]};
+        uint32_t gg[3];
+        bool bad = false;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) {
+            if (!isfinite(c[a])) {
+                bad = true;
+                gg[a] = 0;
+            } else {
+                gg[a] = (uint32_t)axis_index(c[a], g.o[a], g.s[a], g.D[a]);
+            }
+        }
+        lin[k] = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
+        atomicOr(reinterpret_cast<unsigned long long*>(&s_bm[lin[k] >> 6]), 1ull << (lin[k] & 63));
+        if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+    }
+    lds_barrier();
+
+    // ranks of the words; the linear id of every occupied voxel at its slot
+    uint64_t wd[kSmallWd];
+    uint32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallWd; ++j) {
+        const int64_t w = (int64_t)tid * kSmallWd + j;
+        wd[j] = w < W ? s_bm[w] : 0ull;
+        cnt += (uint32_t)__popcll(wd[j]);
+    }
+    uint64_t total;
+    uint32_t r = (uint32_t)small_excl_scan(cnt, s_wave, &total);
+    const uint32_t nv = (uint32_t)total;
+#pragma unroll
+    for (int j = 0; j < kSmallWd; ++j) {
+        const int64_t w = (int64_t)tid * kSmallWd + j;
+        if (w >= W) break;
+        s_wr[w] = r;
+        bitmap[(size_t)b * W + w] = wd[j];
+        word_rank[(size_t)b * W + w] = r;
+        for (uint64_t m = wd[j]; m; m &= m - 1) vox_lin[pb + r++] = (uint32_t)(w * 64 + __ffsll((unsigned long long)m) - 1);
+    }
+    if (tid == 0) nvox[b] = (int32_t)nv;
+    lds_barrier();
+
+    // slot and arrival position of every point, packed as slot << 16 | position
+    uint32_t sp[kSmallPts];
+#pragma unroll
+    for (int k = 0; k < kSmallPts; ++k) {
+        const int32_t i = tid + k * kSmallT;
+        sp[k] = 0;
+        if (i >= N) continue;
+        const uint32_t w = lin[k] >> 6;
+        const uint32_t sl = s_wr[w] + (uint32_t)__popcll(s_bm[w] & ((1ull << (lin[k] & 63)) - 1));
+        sp[k] = (sl << 16) | atomicAdd(&s_off[sl], 1u);
+        pt_slot[pb + i] = sl;
+    }
+    lds_barrier();
+
+    // offsets: (full << 31) | stored, scanned over the slots [0, nv)
+    uint32_t c8[kSmallPts];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kSmallPts; ++j) {
+        const uint32_t sl = (uint32_t)tid * kSmallPts + j;
+        c8[j] = sl < nv ? s_off[sl] : 0u;
+        sum += ((uint64_t)c8[j] << 31) | (c8[j] < n_v ? c8[j] : n_v);
+    }
+    uint64_t run = small_excl_scan(sum, s_wave, &total);
+    uint32_t* vo = vox_off + (size_t)b * (N + 1);
+#pragma unroll
+    for (int j = 0; j < kSmallPts; ++j) {
+        const uint32_t sl = (uint32_t)tid * kSmallPts + j;
+        if (sl >= nv) break;
+        const uint32_t full = (uint32_t)(run >> 31), stored = (uint32_t)(run & 0x7FFFFFFFu);
+        vo[sl] = stored;
+        vox_count[pb + sl] = c8[j];
+        s_off[sl] = (full << 16) | stored;
+        if (c8[j] > kBigVoxel) s_big[atomicAdd(&s_nbig, 1u)] = sl;
+        run += ((uint64_t)c8[j] << 31) | (c8[j] < n_v ? c8[j] : n_v);
+    }
+    if (tid == 0) {
+        vo[nv] = (uint32_t)(total & 0x7FFFFFFFu);
+        s_off[nv] = ((uint32_t)(total >> 31) << 16) | (uint32_t)(total & 0x7FFFFFFFu);
+    }
+    lds_barrier();
+
+    // buckets
+#pragma unroll
+    for (int k = 0; k < kSmallPts; ++k) {
+        const int32_t i = tid + k * kSmallT;
+        if (i < N) s_bk[(s_off[sp[k] >> 16] >> 16) + (sp[k] & 0xFFFFu)] = (uint32_t)i;
+    }
+    lds_barrier();
+
+    // stored lists: a point of a voxel of at most kBigVoxel points by its rank
+#pragma unroll
+    for (int k = 0; k < kSmallPts; ++k) {
+        const int32_t i = tid + k * kSmallT;
+        if (i >= N) continue;
+        const uint32_t o0 = s_off[sp[k] >> 16], o1 = s_off[(sp[k] >> 16) + 1];
+        const uint32_t f0 = o0 >> 16, cnt_v = (o1 >> 16) - f0;
+        if (cnt_v > kBigVoxel) continue;
+        uint32_t rank = 0;
+        for (uint32_t j = 0; j < cnt_v; ++j) rank += s_bk[f0 + j] < (uint32_t)i ? 1u : 0u;
+        if (rank < n_v) {
+            const size_t dst = pb + (o0 & 0xFFFFu) + rank;
+            const float* p = P + (pb + i) * 3;
+            pt_list[dst] = (uint32_t)i;
+            pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float((uint32_t)i));
+        }
+    }
+    // larger voxels: one wave each, the n_v smallest indices by bitonic selection
+    const int lane = lane_id();
+    for (uint32_t v = (uint32_t)(tid / kWave); v < s_nbig; v += kSmallT / kWave) {
+        const uint32_t sl = s_big[v];
+        const uint32_t o0 = s_off[sl], f0 = o0 >> 16, cnt_v = (s_off[sl + 1] >> 16) - f0;
+        uint64_t best = ~0ull;
+        for (uint32_t c0 = 0; c0 < cnt_v; c0 += kWave) {
+            uint64_t key = (c0 + lane < cnt_v) ? (uint64_t)s_bk[f0 + c0 + lane] : ~0ull;
+            key = wave_sort64(key);
+            best = c0 == 0 ? key : wave_merge_low64(best, key);
+        }
+        if ((uint32_t)lane < n_v) {
+            const uint32_t i = (uint32_t)best;
+            const size_t dst = pb + (o0 & 0xFFFFu) + lane;
+            const float* p = P + (pb + i) * 3;
+            pt_list[dst] = i;
+            pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+        }
+    }
+}
+
+// Dynamic LDS a workgroup of k_build_small may take on the current device, or -1.
+int64_t small_lds_avail() {
+    static int64_t avail[64];  // per device, 0 until known
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return -1;
+    if (avail[dev] == 0) {
+        int max_sh = 0;
+        hipFuncAttributes fa{};
+        if (hipDeviceGetAttribute(&max_sh, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+            hipFuncGetAttributes(&fa, (const void*)k_build_small) != hipSuccess)
+            return -1;
+        avail[dev] = (int64_t)max_sh - (int64_t)fa.sharedSizeBytes;
+    }
+    return avail[dev];
+}
+
 }  // namespace
 
 hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_desc& d, void* ws,
@@ -281,6 +495,20 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
     const int32_t B = L.B, N = L.N, BN = B * N;
     const GridArgs g = grid_args(d);
     int* status = at<int>(ws, L.status);
+    if (N <= kSmallN && L.W <= kSmallW && (int64_t)small_lds_bytes(N, L.W) <= small_lds_avail()) {
+        // the status words only: the small build uses no scan descriptors or occupancy bytes
+        k_clear<<<1, 256, 0, s>>>(at<uint4>(ws, L.status), (4 * kStSlots + 15) / 16);
+        const size_t bytes = small_lds_bytes(N, L.W);
+        hipError_t e = hipFuncSetAttribute((const void*)k_build_small, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)bytes);
+        if (e != hipSuccess) return e;
+        k_build_small<<<B, kSmallT, bytes, s>>>(points, N, g, L.W, (uint32_t)d.n_v, at<uint32_t>(ws, L.pt_slot),
+                                                at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
+                                                at<uint32_t>(ws, L.vox_lin), at<uint32_t>(ws, L.vox_count),
+                                                at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_off),
+                                                at<uint32_t>(ws, L.pt_list), at<float4>(ws, L.pt4), status);
+        return hipGetLastError();
+    }
     size_t n16 = (L.clear_end - L.status) / 16;
     int cb = (int)((n16 + 255) / 256);
     if (cb > 4096) cb = 4096;

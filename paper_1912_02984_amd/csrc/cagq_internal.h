@@ -220,6 +220,16 @@ __device__ __forceinline__ void st_desc(uint64_t* p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// A workgroup barrier that orders LDS accesses only: the global stores issued
+// before it are not waited for (__syncthreads also waits for those, a full
+// memory round trip). For kernels whose threads exchange data through LDS
+// alone.
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 __device__ __forceinline__ void raise_error(int* status, int code) {
     atomicCAS(status + kStError, 0, code);
 }
