@@ -101,11 +101,13 @@ def _spec(origin, size, dims, n_v, r=1):
     return W.GridSpec(tuple(origin), tuple(size), tuple(dims), n_v, r)
 
 
-def test_capped_and_big_voxels():
+@pytest.mark.parametrize("N", [5000, 12000])
+def test_capped_and_big_voxels(N):
     """Voxels holding up to a few hundred points: the cap keeps the lowest
-    indices, through both the per-point ranking and the wave selection."""
+    indices, through both the per-point ranking and the wave selection, in
+    the one-workgroup build (5000 points) and the seven-kernel build (12000)."""
     rng = np.random.default_rng(5)
-    B, N = 3, 5000
+    B = 3
     P = rng.random((B, N, 3), dtype=np.float32)
     # a third of each cloud crowds into three voxels
     P[:, : N // 3] = (np.float32(0.01) + rng.random((B, N // 3, 3), dtype=np.float32) * np.float32(0.02))
