@@ -724,7 +724,8 @@ __device__ __forceinline__ int32_t beats(const uint4 (&q)[4], uint32_t c, uint32
 // round's start) bounds every later pick, so round R counts the picks above
 // round R-1's bound and round R+1 retires the cloud: the stopping rule of the
 // two-kernel rounds, one round later.
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k_cas_round(int32_t R, int32_t B, int32_t N, int64_t unit, uint32_t beta_q16,
+constexpr int kRoundThreads = 64;  // one wave per block: the blocks spread over every CU
+__global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5))) void k_cas_round(int32_t R, int32_t B, int32_t N, int64_t unit, uint32_t beta_q16,
                                                    int32_t M, const int32_t* __restrict__ nvox,
                                                    const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
     // no early exit: every lane takes part in the wave-wide steps
@@ -778,7 +779,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
     uint32_t n2 = 0, n_r = 0;
     // a possible winner's first 16 list entries (its voxels within r come
     // first), kept for the wave's coverage pass below
-    __shared__ uint32_t s_ent[256][16];
+    __shared__ uint32_t s_ent[kRoundThreads][16];
     if (active && s < nv) {
         if (rnd0 != 0) {
             above = pk0 > G ? 1u : 0u;
@@ -809,7 +810,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(5))) void k
     const uint32_t sincl = wave_incl_scan<uint32_t>(nrest);
     const uint32_t stot = (uint32_t)__shfl((int)sincl, kWave - 1, kWave);
     if (stot) {
-        __shared__ int32_t s_found[256];
+        __shared__ int32_t s_found[kRoundThreads];
         const int wbase = threadIdx.x & ~(kWave - 1);
         s_found[threadIdx.x] = -1;
         for (uint32_t p0 = 0; p0 < stot; p0 += kWave) {
@@ -1059,7 +1060,8 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     auto launch_batch = [&](int rounds) {
         for (int i = 0; i < rounds; ++i, ++R) {
             if (lists) {
-                k_cas_round<<<pb, 256, 0, s>>>((int32_t)R, B, N, 65536 * lam, beta_q16, M, nvox, nbr, st, ctl);
+                k_cas_round<<<(BN + kRoundThreads - 1) / kRoundThreads, kRoundThreads, 0, s>>>(
+                    (int32_t)R, B, N, 65536 * lam, beta_q16, M, nvox, nbr, st, ctl);
             } else if (rad == 1) {
                 k_cas_score<1><<<pb, 256, 0, s>>>((int32_t)R, B, N, L.W, g, lam, beta_q16, M, nvox,
                                                          vox_lin, bitmap, word_rank, st, ctl);
