@@ -16,7 +16,7 @@ namespace cagq {
 
 namespace {
 
-constexpr int kNbrThreads = 256;
+constexpr int kNbrThreads = 64;  // one wave per block: small clouds spread over every CU
 
 // E: entry type, ST: entries per voxel (header included), HDR: header entries.
 template <int RAD, typename E, int ST, int HDR>

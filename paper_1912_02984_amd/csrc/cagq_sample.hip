@@ -1053,7 +1053,7 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     if (lists && (e = launch_cas_nbr(L, d, ws, s)) != hipSuccess) return e;
     const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
     const int32_t init_n = std::max(BN, B * kCasParts * kCasUBins);
-    k_cas_init<<<(init_n + 255) / 256, 256, 0, s>>>(BN, B, N, st, ctl, nbr, vox_lin, nvox, 65536 * lam);
+    k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, N, st, ctl, nbr, vox_lin, nvox, 65536 * lam);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     int64_t R = 0;
