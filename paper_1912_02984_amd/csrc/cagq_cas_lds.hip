@@ -91,8 +91,9 @@ __device__ __forceinline__ uint32_t uncovered(const uint4& v, uint32_t base, uin
 }
 
 // A winner's marks on entries base..base+7 of its list: rescoring for the
-// unpicked ones (the winner itself and earlier picks keep their pick key in
-// dty), coverage for the first n_r (those within distance r).
+// unpicked ones other than the winner itself (it and earlier picks keep
+// their pick key in dty), coverage for the first n_r (those within distance
+// r).
 __device__ __forceinline__ void mark(const uint4& v, uint32_t base, uint32_t n_r, uint32_t n2, uint32_t self,
                                      uint16_t cur, const uint16_t* rnd, uint16_t* dty, uint8_t* cov) {
     uint32_t sl[8];
@@ -108,8 +109,90 @@ __device__ __forceinline__ void mark(const uint4& v, uint32_t base, uint32_t n_r
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         if (base + j < n2) {
-            if (rr[j] == 0) dty[sl[j]] = cur;
+            if (rr[j] == 0 && sl[j] != self) dty[sl[j]] = cur;
             if (base + j < n_r) cov[sl[j]] = (uint8_t)(cc[j] + 1);
+        }
+    }
+}
+
+// The picking pass over the queued voxels, P lanes per voxel: lane `sub`
+// of a voxel's P takes the groups of 8 list entries sub, sub + P, ...,
+// kPre of them per load (the first kPre with the header, clamped to the
+// list's storage; later ones clamped to its last group). A voxel is beaten
+// when some entry within 2r holds a larger key; the lowest such position
+// over the P lanes is the same blocker a single lane's in-order scan finds.
+// A winner takes its pick round and key, and its lanes mark their groups:
+// rescoring within 2r, coverage within r. A round's winners are more than
+// 2r apart, so no other winner is on the list and their r-neighbourhoods are
+// disjoint: plain updates are exact.
+template <int P, int ST>
+__device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, const uint16_t* nb,
+                                            const uint16_t* que, const uint32_t* key, uint16_t* rnd,
+                                            uint16_t* blk, uint16_t* dty, uint8_t* cov) {
+    constexpr uint32_t kRoom = (ST - 8) / 8;  // groups a slot's storage holds after its header
+    constexpr int KB = (int)((kRoom + P - 1) / P) < kPre ? (int)((kRoom + P - 1) / P) : kPre;  // groups per load
+    const uint32_t sub = (uint32_t)tid & (P - 1);
+    for (uint32_t i = (uint32_t)tid / P; i < qb; i += kT / P) {
+        const uint32_t s = que[i];
+        const uint32_t my = key[s];
+        const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
+        uint4 pre[KB];
+        const uint4 h = e[0];
+#pragma unroll
+        for (int t = 0; t < KB; ++t) {
+            const uint32_t c = sub + (uint32_t)(P * t);
+            pre[t] = e[1 + (c < kRoom ? c : kRoom - 1)];
+        }
+        const uint32_t n_r = h.x & 0xFFFFu, n2 = h.x >> 16;
+        const uint32_t nch = (n2 + 7) / 8;  // groups of 8 entries (n2 >= 1: the voxel itself)
+        uint32_t hit = ~0u;                 // (position << 16) | slot of this lane's first larger key
+        for (uint32_t t0 = 0; sub + P * t0 < nch && hit == ~0u; t0 += KB) {
+            uint4 q[KB];
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                const uint32_t c = sub + P * (t0 + j);
+                q[j] = t0 == 0 ? pre[j] : e[1 + (c < nch ? c : nch - 1)];
+            }
+#pragma unroll
+            for (int jj = 0; jj < KB; ++jj) {
+                const uint32_t c = sub + P * (t0 + jj);
+                if (c >= nch || hit != ~0u) break;
+                uint32_t sl[8], kk[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(q[jj], j) : s;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (hit == ~0u && kk[j] > my) hit = ((c * 8 + (uint32_t)j) << 16) | sl[j];
+            }
+        }
+#pragma unroll
+        for (int d = 1; d < P; d <<= 1) {
+            const uint32_t o = (uint32_t)__shfl_xor((int)hit, d, kWave);
+            hit = o < hit ? o : hit;
+        }
+        if (hit != ~0u) {
+            if (sub == 0) blk[s] = (uint16_t)(hit & 0xFFFFu);
+            continue;
+        }
+        if (sub == 0) {
+            rnd[s] = cur;
+            blk[s] = (uint16_t)(my >> 16);
+            dty[s] = (uint16_t)(my & 0xFFFFu);
+        }
+        for (uint32_t t0 = 0; sub + P * t0 < nch; t0 += KB) {
+            uint4 q[KB];
+#pragma unroll
+            for (int j = 0; j < KB; ++j) {
+                const uint32_t c = sub + P * (t0 + j);
+                q[j] = t0 == 0 ? pre[j] : e[1 + (c < nch ? c : nch - 1)];
+            }
+#pragma unroll
+            for (int jj = 0; jj < KB; ++jj) {
+                const uint32_t c = sub + P * (t0 + jj);
+                if (c < nch) mark(q[jj], c * 8, n_r, n2, s, cur, rnd, dty, cov);
+            }
         }
     }
 }
@@ -129,7 +212,7 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     uint16_t* dty = blk + cap;   // unpicked: round that must rescore it; picked: pick key & 0xFFFF
     uint16_t* que = dty + cap;   // work queue of slots
     uint8_t* cov = reinterpret_cast<uint8_t*>(que + cap);       // centers covering the voxel
-    __shared__ uint32_t s_max, s_cnt, s_qn;
+    __shared__ uint32_t s_max, s_cnt, s_qa, s_qb;  // s_qa / s_qb: scoring / picking queue lengths
     __shared__ uint32_t s_hist[128];
     __shared__ uint32_t s_digit, s_below;
     __shared__ uint32_t s_wsum[kNW];
@@ -150,18 +233,24 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         dty[s] = 0;
         cov[s] = 0;
     }
+    if (tid == 0) {
+        s_max = 0;
+        s_qa = 0;
+    }
 
     bool done = false;
     const int32_t max_r = m + 2;
     for (int32_t R = 0; R < max_r; ++R) {
         const uint16_t cur = (uint16_t)(R + 1);
+        // Each counter is cleared at a point where every thread is past its
+        // last read and a barrier separates it from its next update:
+        // s_cnt and s_qb here, s_qa once G is read, s_max after the picking
+        // queue is complete.
         __syncthreads();
         if (tid == 0) {
-            s_max = 0;
             s_cnt = 0;
-            s_qn = 0;
+            s_qb = 0;
         }
-        __syncthreads();
         // -- scoring. Owned slots: last round's picks leave the competition,
         // clean unpicked keys count towards the maximum, the rest is queued.
         uint32_t lmax = 0, want = 0;
@@ -179,9 +268,9 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
                 want |= dirty ? 1u << k : 0u;
             }
         }
-        enqueue(want, que, &s_qn);
+        enqueue(want, que, &s_qa);
         __syncthreads();
-        const uint32_t qa = s_qn;
+        const uint32_t qa = s_qa;
         for (uint32_t i = tid; i < qa; i += kT) {
             const uint32_t s = que[i];
             const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
@@ -214,8 +303,7 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         if (lane == 0 && lmax) atomicMax(&s_max, lmax);
         __syncthreads();
         const uint32_t G = s_max;
-        if (tid == 0) s_qn = 0;
-        __syncthreads();
+        if (tid == 0) s_qa = 0;
         // -- picking. Owned slots: earlier picks above the best unpicked key
         // are counted; an unpicked voxel still beaten by its cached blocker
         // stays out; the rest is queued for a pass over its list.
@@ -237,73 +325,23 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         }
         above = wsum32(above);
         if (lane == 0 && above) atomicAdd(&s_cnt, above);
-        enqueue(want, que, &s_qn);
+        enqueue(want, que, &s_qb);
         __syncthreads();
+        if (tid == 0) s_max = 0;
         // the picks above the best unpicked key are the sequential greedy's
         // first ones; the voxels this round would pick all have keys <= G
         if (s_cnt >= (uint32_t)m) {
             done = true;
             break;
         }
-        const uint32_t qb = s_qn;
-        for (uint32_t i = tid; i < qb; i += kT) {
-            const uint32_t s = que[i];
-            const uint32_t my = key[s];
-            const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
-            uint4 pre[kPre];
-            const uint4 h = e[0];
-#pragma unroll
-            for (int c = 0; c < kPre; ++c) pre[c] = e[1 + c];
-            const uint32_t n_r = h.x & 0xFFFFu, n2 = h.x >> 16;
-            const uint32_t nch = (n2 + 7) / 8;  // groups of 8 entries (n2 >= 1: the voxel itself)
-            int32_t found = -1;
-            // kPre groups at a time: the first came with the header, each
-            // later batch is loaded in one go (clamped to the list's last
-            // group), so a long list costs one load latency per kPre groups
-            for (uint32_t c0 = 0; c0 < nch && found < 0; c0 += kPre) {
-                uint4 q[kPre];
-#pragma unroll
-                for (int j = 0; j < kPre; ++j) {
-                    const uint32_t cj = c0 + j < nch ? c0 + j : nch - 1;
-                    q[j] = c0 == 0 ? pre[j] : e[1 + cj];
-                }
-#pragma unroll
-                for (int jj = 0; jj < kPre; ++jj) {
-                    const uint32_t c = c0 + jj;
-                    if (c >= nch || found >= 0) break;
-                    uint32_t sl[8], kk[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) sl[j] = c * 8 + j < n2 ? entry(q[jj], j) : s;
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j)
-                        if (found < 0 && kk[j] > my) found = (int32_t)sl[j];
-                }
-            }
-            if (found >= 0) {
-                blk[s] = (uint16_t)found;
-                continue;
-            }
-            // a winner: rescoring within 2r, coverage within r. A round's
-            // winners are more than 2r apart, so no other winner is on the
-            // list and their r-neighbourhoods are disjoint: plain updates
-            // are exact.
-            rnd[s] = cur;
-            blk[s] = (uint16_t)(my >> 16);
-            dty[s] = (uint16_t)(my & 0xFFFFu);
-            for (uint32_t c0 = 0; c0 < nch; c0 += kPre) {
-                uint4 q[kPre];
-#pragma unroll
-                for (int j = 0; j < kPre; ++j) {
-                    const uint32_t cj = c0 + j < nch ? c0 + j : nch - 1;
-                    q[j] = c0 == 0 ? pre[j] : e[1 + cj];
-                }
-#pragma unroll
-                for (int jj = 0; jj < kPre; ++jj)
-                    if (c0 + jj < nch) mark(q[jj], (c0 + jj) * 8, n_r, n2, s, cur, rnd, dty, cov);
-            }
-        }
+        const uint32_t qb = s_qb;
+        // a short queue gets 16 lanes per voxel with r = 1, one group of
+        // list entries each, in at most two passes (2, 4 or 8 lanes per
+        // voxel spill registers here)
+        if (RAD == 1 && qb <= kT / 8)
+            drain_picks<16, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
+        else
+            drain_picks<1, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
     }
     if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
     __syncthreads();
