@@ -11,18 +11,27 @@
  *
  * Conventions for every entry point:
  *   - Pointers named "device" are HIP device pointers owned by the caller;
- *     the library never allocates, frees or retains memory. Host pointers
- *     are read before the call returns.
+ *     the library never allocates or frees device memory and keeps no
+ *     pointer to caller memory past a call (a cagq_grid record borrows the
+ *     caller's points and workspace; it is the caller's). Host pointers are
+ *     read before the call returns. One exception holds host memory: the
+ *     many-kernel CAS path (cagq_sample_centers) keeps one 64-byte pinned
+ *     host block per calling thread, allocated at its first use and kept
+ *     until the process ends, through which its round kernels report
+ *     progress to the waiting host thread.
  *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
  *     Work is enqueued asynchronously on it; results are valid once the
  *     stream has reached the enqueued work. cagq_sample_centers with the
- *     CAS mode may wait for its rounds (see there).
+ *     CAS mode may block the calling thread until its rounds finish (see
+ *     there); such a call cannot be captured into a HIP graph.
  *   - Argument errors are detected on the host before anything is
  *     enqueued and returned synchronously. Data-dependent errors
  *     (non-finite coordinates, center voxels that are not occupied) are
  *     recorded in the workspace and reported by cagq_get_device_status.
  *   - Calls on one workspace are ordered by the stream; distinct
- *     workspaces are independent (the library holds no global state).
+ *     workspaces are independent. The library's only state beyond the
+ *     caller's memory is the pinned block above (each call on it is told
+ *     apart by a per-call tag) and per-device kernel attributes it caches.
  *   - Array shapes are row-major; [B][N][3] means point n of cloud b has
  *     x, y, z at ((b*N)+n)*3 + {0,1,2}.
  */
@@ -64,7 +73,7 @@ extern "C" {
 #define CAGQ_POINTS_FPS 1   /* Farthest Point Sampling (comparison method, Sec. 4) */
 
 /* Library limits (checked on the host). */
-#define CAGQ_MAX_K 64       /* node points per group */
+#define CAGQ_MAX_K 128      /* node points per group */
 #define CAGQ_MAX_NV 64      /* points stored per voxel */
 #define CAGQ_MAX_RADIUS 3   /* neighbourhood half-width r */
 
@@ -117,6 +126,34 @@ typedef struct cagq_grid {
     size_t workspace_bytes;
 } cagq_grid;
 
+/*
+ * Grid descriptors from a bounding box (host only, pure: no device work, no
+ * state). Sec. 3.2 voxelizes the input space "by setting up a voxel size
+ * (v_x, v_y, v_z)"; these helpers fix the origin and extent it leaves open.
+ * lo, hi: host float[3], the box's corners (finite, lo_a <= hi_a).
+ *
+ * cagq_desc_from_voxel_size: origin = lo, voxel_size = vs (host float[3],
+ *   > 0 and finite), and per axis dims_a = floor(t_a) + 1 with t_a =
+ *   (hi_a - lo_a) / vs_a in fp32 (one rounded subtract, one correctly
+ *   rounded divide: the voxelize rule of cagq_grid_desc). The voxelize rule
+ *   then puts lo in voxel 0 and hi in voxel dims_a - 1 on every axis, so no
+ *   point of [lo, hi] is clamped; it is the smallest such grid at origin lo.
+ * cagq_desc_from_dims: origin = lo, dims = dims (host int32[3], >= 1), and
+ *   voxel_size_a = (hi_a - lo_a) / dims_a in fp32 (correctly rounded), or 1
+ *   when hi_a == lo_a. A point of [lo, hi] whose quotient rounds up to dims_a
+ *   is clamped onto the last voxel by the voxelize rule.
+ * Both copy n_v and radius into `out` (host) and validate the result as
+ * cagq_build_grid does. Return CAGQ_OK; CAGQ_ERR_INVALID_ARG for a null
+ * pointer, a non-finite or inverted box, a voxel size that is not positive
+ * and finite (given or computed), or n_v / radius out of range;
+ * CAGQ_ERR_GRID_TOO_LARGE when a dimension or the voxel count exceeds
+ * 2^31-1. `out` is written only on CAGQ_OK.
+ */
+CAGQ_API int cagq_desc_from_voxel_size(const float lo[3], const float hi[3], const float vs[3], int32_t n_v,
+                                       int32_t radius, cagq_grid_desc* out);
+CAGQ_API int cagq_desc_from_dims(const float lo[3], const float hi[3], const int32_t dims[3], int32_t n_v,
+                                 int32_t radius, cagq_grid_desc* out);
+
 /* Host only, no device work. Fills `out` for a batch of B clouds of N points
  * on `desc`. Returns CAGQ_OK, CAGQ_ERR_INVALID_ARG or CAGQ_ERR_GRID_TOO_LARGE. */
 CAGQ_API int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out);
@@ -153,9 +190,13 @@ CAGQ_API int cagq_build_grid(const float* points, int32_t B, int32_t N, const ca
  *     beta = beta_q16 / 2^16), ties to the lowest lin; the first m_valid
  *     picks are the centers. Requires (2^16 + beta_q16) * lambda^2 < 2^31.
  *     `seed` is unused. With beta_q16 = 0, r <= 2 and N <= 4096 (one
- *     workgroup per cloud holds the whole state) the call is asynchronous;
- *     otherwise its round count is data dependent and it waits on the host
- *     for the rounds to finish (without synchronising `stream` as a whole).
+ *     workgroup per cloud holds the whole state) the call is asynchronous.
+ *     Otherwise (r <= 2 only: r = 3 returns CAGQ_ERR_INVALID_ARG) its round
+ *     count is data dependent: the calling thread issues rounds and spins
+ *     until the kernels report every cloud done (without synchronising
+ *     `stream` as a whole); up to two rounds with nothing left to do may
+ *     still be queued when it returns. On an error return it first waits
+ *     for the rounds it queued.
  *   mode CAGQ_SAMPLE_CAS_SWAP: the paper's own procedure (Eqs. 2-3). The
  *     m_valid incumbents start as the RVS choice for `seed`, held in slots
  *     0..m_valid-1 in ascending lin; every other occupied voxel C, in

@@ -28,7 +28,7 @@ ERR_CENTER_NOT_OCCUPIED = -7
 
 SAMPLE = {"rvs": 0, "cas": 1, "cas_swap": 2}
 QUERY = {"cube": 0, "knn": 1, "knn_ring": 2}
-MAX_K = 64
+MAX_K = 128
 MAX_NV = 64
 MAX_RADIUS = 3
 
@@ -65,6 +65,11 @@ def lib() -> C.CDLL:
             raise RuntimeError(f"{LIB_PATH} is missing: build it with paper_1912_02984_amd.build")
         L = C.CDLL(LIB_PATH)
         P = C.c_void_p
+        F3, I3 = C.c_float * 3, C.c_int32 * 3
+        L.cagq_desc_from_voxel_size.argtypes = [C.POINTER(F3), C.POINTER(F3), C.POINTER(F3), C.c_int32,
+                                                C.c_int32, C.POINTER(GridDesc)]
+        L.cagq_desc_from_dims.argtypes = [C.POINTER(F3), C.POINTER(F3), C.POINTER(I3), C.c_int32, C.c_int32,
+                                          C.POINTER(GridDesc)]
         L.cagq_workspace_layout.argtypes = [C.c_int32, C.c_int32, C.POINTER(GridDesc), C.POINTER(LayoutC)]
         L.cagq_build_grid.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(GridDesc), P, C.c_size_t, P,
                                       C.POINTER(GridC)]
@@ -82,7 +87,7 @@ def lib() -> C.CDLL:
         L.cagq_get_device_status.argtypes = [C.POINTER(GridC), P]
         L.cagq_status_string.argtypes = [C.c_int]
         L.cagq_status_string.restype = C.c_char_p
-        for f in ("cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
+        for f in ("cagq_desc_from_voxel_size", "cagq_desc_from_dims", "cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
                   "cagq_query_context", "cagq_query_points", "cagq_context_offsets", "cagq_context_list",
                   "cagq_sample_points", "cagq_ball_query", "cagq_coverage", "cagq_get_device_status"):
             getattr(L, f).restype = C.c_int
@@ -108,6 +113,27 @@ def make_desc(origin: Sequence[float], voxel_size: Sequence[float], dims: Sequen
         d.dims[a] = int(dims[a])
     d.n_v = int(n_v)
     d.radius = int(radius)
+    return d
+
+
+def desc_from_voxel_size(lo: Sequence[float], hi: Sequence[float], voxel_size: Sequence[float], n_v: int,
+                         radius: int = 1) -> GridDesc:
+    """GridDesc of the smallest grid at origin ``lo`` with the given voxel
+    size whose voxels hold every point of the box [lo, hi] without clamping."""
+    F3 = C.c_float * 3
+    d = GridDesc()
+    _check(lib().cagq_desc_from_voxel_size(C.byref(F3(*lo)), C.byref(F3(*hi)), C.byref(F3(*voxel_size)),
+                                           int(n_v), int(radius), C.byref(d)), "cagq_desc_from_voxel_size")
+    return d
+
+
+def desc_from_dims(lo: Sequence[float], hi: Sequence[float], dims: Sequence[int], n_v: int,
+                   radius: int = 1) -> GridDesc:
+    """GridDesc at origin ``lo`` with ``dims`` voxels per axis spanning [lo, hi]."""
+    F3, I3 = C.c_float * 3, C.c_int32 * 3
+    d = GridDesc()
+    _check(lib().cagq_desc_from_dims(C.byref(F3(*lo)), C.byref(F3(*hi)), C.byref(I3(*dims)),
+                                     int(n_v), int(radius), C.byref(d)), "cagq_desc_from_dims")
     return d
 
 

@@ -93,6 +93,60 @@ using namespace cagq;
 
 extern "C" {
 
+// The box [lo, hi] must be finite and not inverted on any axis.
+static int check_box(const float* lo, const float* hi) {
+    if (!lo || !hi) return CAGQ_ERR_INVALID_ARG;
+    for (int a = 0; a < 3; ++a)
+        if (!isfinite(lo[a]) || !isfinite(hi[a]) || !(lo[a] <= hi[a])) return CAGQ_ERR_INVALID_ARG;
+    return CAGQ_OK;
+}
+
+int cagq_desc_from_voxel_size(const float lo[3], const float hi[3], const float vs[3], int32_t n_v, int32_t radius,
+                              cagq_grid_desc* out) {
+    int rc = check_box(lo, hi);
+    if (rc != CAGQ_OK) return rc;
+    if (!vs || !out) return CAGQ_ERR_INVALID_ARG;
+    cagq_grid_desc d;
+    for (int a = 0; a < 3; ++a) {
+        if (!(vs[a] > 0.0f) || !isfinite(vs[a])) return CAGQ_ERR_INVALID_ARG;
+        // the voxelize rule applied to hi: one rounded subtract, one
+        // correctly rounded divide (the host compiler keeps fp32 here)
+        const volatile float diff = hi[a] - lo[a];
+        const volatile float t = diff / vs[a];
+        const float f = floorf(t);
+        if (!isfinite(t) || f >= 2147483647.0f) return CAGQ_ERR_GRID_TOO_LARGE;
+        d.origin[a] = lo[a];
+        d.voxel_size[a] = vs[a];
+        d.dims[a] = (int32_t)f + 1;
+    }
+    d.n_v = n_v;
+    d.radius = radius;
+    rc = check_desc(&d);
+    if (rc == CAGQ_OK) *out = d;
+    return rc;
+}
+
+int cagq_desc_from_dims(const float lo[3], const float hi[3], const int32_t dims[3], int32_t n_v, int32_t radius,
+                        cagq_grid_desc* out) {
+    int rc = check_box(lo, hi);
+    if (rc != CAGQ_OK) return rc;
+    if (!dims || !out) return CAGQ_ERR_INVALID_ARG;
+    cagq_grid_desc d;
+    for (int a = 0; a < 3; ++a) {
+        if (dims[a] < 1) return CAGQ_ERR_INVALID_ARG;
+        const volatile float diff = hi[a] - lo[a];
+        const volatile float s = diff / (float)dims[a];
+        d.origin[a] = lo[a];
+        d.voxel_size[a] = diff == 0.0f ? 1.0f : s;
+        d.dims[a] = dims[a];
+    }
+    d.n_v = n_v;
+    d.radius = radius;
+    rc = check_desc(&d);
+    if (rc == CAGQ_OK) *out = d;
+    return rc;
+}
+
 int cagq_workspace_layout(int32_t B, int32_t N, const cagq_grid_desc* desc, cagq_layout* out) {
     if (!out) return CAGQ_ERR_INVALID_ARG;
     int rc = check_desc(desc);

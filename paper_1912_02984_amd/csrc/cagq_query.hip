@@ -1,7 +1,8 @@
 // Node points querying and group centers (Sec. 3.2 "Node points querying";
 // Appendix D, general procedure, step 3; Appendix E, Eqs. 7-8).
 //
-// One group of G lanes (G = 16, 32 or 64, G >= K) per center voxel v, 64/G
+// One group of G lanes (G = 16, 32 or 64, G >= K; a whole wave with two
+// result registers per lane for 64 < K <= 128) per center voxel v, 64/G
 // centers per wavefront:
 //   1. the group's lanes probe the (2r+1)^3 voxels of pi(v) in the occupancy
 //      bitmap and compact the occupied ones (slot start, running context
@@ -200,7 +201,32 @@ __device__ __forceinline__ void gmerge_low(uint64_t& bk, uint32_t& bp, uint64_t 
     for (int j = G >> 1; j > 0; j >>= 1) gcx(bk, bp, j, (lg & j) == 0);
 }
 
-template <int MODE, int G, int RAD, bool UP>
+// `bk` and `b1` sorted ascending across the group with every key of bk below
+// every key of b1 (ranks 0..G-1 and G..2G-1 of the keys seen so far), and a
+// chunk `ak` sorted ascending: bk and b1 receive ranks 0..2G-1 of the union.
+// The G smallest of b1 and the chunk hold every key of rank below 2G that
+// is not in bk; bk and those are then split by a bitonic merge.
+template <int G>
+__device__ __forceinline__ void gmerge_low2(uint64_t& bk, uint32_t& bp, uint64_t& b1k, uint32_t& b1p, uint64_t ak,
+                                            uint32_t ap, int lg) {
+    gmerge_low<G>(b1k, b1p, ak, ap, lg);
+    const uint64_t rk = gshfl64<G>(b1k, G - 1 - lg);
+    const uint32_t rp = (uint32_t)__shfl((int)b1p, G - 1 - lg, G);
+    const bool sw = rk < bk;
+    b1k = sw ? bk : rk;
+    b1p = sw ? bp : rp;
+    bk = sw ? rk : bk;
+    bp = sw ? rp : bp;
+#pragma unroll
+    for (int j = G >> 1; j > 0; j >>= 1) {
+        gcx(bk, bp, j, (lg & j) == 0);
+        gcx(b1k, b1p, j, (lg & j) == 0);
+    }
+}
+
+// NR result registers per lane: NR = 1 keeps ranks 0..G-1 (K <= G), NR = 2
+// (G = 64) also ranks 64..127 in a second register (64 < K <= 128).
+template <int MODE, int G, int RAD, bool UP, int NR>
 __global__ __launch_bounds__(kQueryThreads) void k_query(
     const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
     int64_t W, const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
@@ -351,8 +377,9 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
             if (l + 1 == ls) base = cum[l];
         part = cs > (uint32_t)K;
     }
-    uint64_t bk = ~0ull;
-    uint32_t bp = 0;
+    static_assert(NR == 1 || (NR == 2 && G == kWave), "two result registers need a whole wave");
+    uint64_t bk = ~0ull, b1k = ~0ull;
+    uint32_t bp = 0, b1p = 0;
     // the chunk loop runs the same number of times for every group of the wave
     uint32_t cmax = cs;
 #pragma unroll
@@ -407,49 +434,67 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         if (e0 == 0) {
             bk = key;
             bp = pos;
-        } else {
+        } else if (NR == 1) {
             gmerge_low<G>(bk, bp, key, pos, lg);
+        } else {
+            gmerge_low2<G>(bk, bp, b1k, b1p, key, pos, lg);
         }
     }
 
-    // 4. outputs (an empty context gives n = 0 and zeros)
+    // 4. outputs (an empty context gives n = 0 and zeros): node slot k is
+    // lane k of the first register or lane k - G of the second; slots k >= n
+    // repeat slot 0
     const uint32_t n = c < (uint32_t)K ? c : (uint32_t)K;
-    // slots k >= n repeat slot 0
-    const bool own = (uint32_t)lg < n;
     const uint64_t k0 = ((uint64_t)gbcast<G>((uint32_t)(bk >> 32), 0) << 32) | gbcast<G>((uint32_t)bk, 0);
-    const uint64_t mine = own ? bk : k0;
-    const uint32_t mpos = own ? bp : gbcast<G>(bp, 0);
-    // the node's point index is the key's low half, except in the level-wise
-    // mode, whose keys order by position: there it comes with the point
-    uint32_t idx = n ? (uint32_t)mine : 0u;
-    // a one-chunk context reads node point and weight from the lane holding
-    // them; a longer one reads them again
-    const int from = one ? (int)mpos : 0;
-    float x = __shfl(v0.x, from, G), y = __shfl(v0.y, from, G), z = __shfl(v0.z, from, G);
-    uint32_t w = (uint32_t)__shfl((int)w0, from, G);
-    if (MODE == kRing) idx = (uint32_t)__shfl((int)__float_as_uint(v0.w), from, G);
-    if (!one) {
-        const float4 pv = p4[mpos];
-        x = pv.x;
-        y = pv.y;
-        z = pv.z;
-        if (MODE == kRing) idx = __float_as_uint(pv.w);
-        w = Wt ? Wt[(size_t)b * N + idx] : 1u;
-    }
-    if (!n) {
-        x = y = z = 0.0f;
-        w = 1u;
-        idx = 0u;
-    }
-    if (UP) {
-        if (live && lg < K) {
-            node_idx[cK + lg] = n ? (int32_t)idx : -1;
+    const uint32_t p0 = gbcast<G>(bp, 0);
+    float tx = 0.f, ty = 0.f, tz = 0.f, ux = 0.f, uy = 0.f, uz = 0.f;
+    uint32_t wsum = 0;
+#pragma unroll
+    for (int h = 0; h < NR; ++h) {
+        const uint32_t k = (uint32_t)(h * G + lg);
+        const bool own = k < n;
+        const uint64_t mine = own ? (h ? b1k : bk) : k0;
+        const uint32_t mpos = own ? (h ? b1p : bp) : p0;
+        // the node's point index is the key's low half, except in the
+        // level-wise mode, whose keys order by position: there it comes with
+        // the point
+        uint32_t idx = n ? (uint32_t)mine : 0u;
+        // a one-chunk context reads node point and weight from the lane
+        // holding them; a longer one reads them again
+        const int from = one ? (int)mpos : 0;
+        float x = __shfl(v0.x, from, G), y = __shfl(v0.y, from, G), z = __shfl(v0.z, from, G);
+        uint32_t w = (uint32_t)__shfl((int)w0, from, G);
+        if (MODE == kRing) idx = (uint32_t)__shfl((int)__float_as_uint(v0.w), from, G);
+        if (!one) {
+            const float4 pv = p4[mpos];
+            x = pv.x;
+            y = pv.y;
+            z = pv.z;
+            if (MODE == kRing) idx = __float_as_uint(pv.w);
+            w = Wt ? Wt[(size_t)b * N + idx] : 1u;
+        }
+        if (!n) {
+            x = y = z = 0.0f;
+            w = 1u;
+            idx = 0u;
+        }
+        if (live && k < (uint32_t)K) {
+            node_idx[cK + k] = UP ? (n ? (int32_t)idx : -1) : (int32_t)idx;
             if (node_xyz) {
-                node_xyz[(cK + lg) * 3 + 0] = x;
-                node_xyz[(cK + lg) * 3 + 1] = y;
-                node_xyz[(cK + lg) * 3 + 2] = z;
+                node_xyz[(cK + k) * 3 + 0] = x;
+                node_xyz[(cK + k) * 3 + 1] = y;
+                node_xyz[(cK + k) * 3 + 2] = z;
             }
         }
+        const float wf = (float)w;
+        if (h == 0) {
+            tx = wf * x, ty = wf * y, tz = wf * z;
+        } else {
+            ux = wf * x, uy = wf * y, uz = wf * z;
+        }
+        wsum += own ? w : 0u;
+    }
+    if (UP) {
         if (live && lg == 0) {
             n_valid[cid] = (int32_t)n;
             if (ctx_count) ctx_count[cid] = (int32_t)c;
@@ -457,34 +502,38 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         }
         return;
     }
-    if (live && lg < K) {
-        node_idx[cK + lg] = (int32_t)idx;
-        if (node_xyz) {
-            node_xyz[(cK + lg) * 3 + 0] = x;
-            node_xyz[(cK + lg) * 3 + 1] = y;
-            node_xyz[(cK + lg) * 3 + 2] = z;
-        }
-    }
-    // n <= top: the levels at and above `top` add nothing
-    const bool valid = (uint32_t)lg < n;
-    uint32_t wc = valid ? w : 0u;
+    // n <= top, or n > G = top with two registers: the levels at and above
+    // `top` add nothing
+    uint32_t wc = wsum;
 #pragma unroll
     for (int d = 1; d < G; d <<= 1)
         if ((uint32_t)d < top) wc += xlane(wc, d);
-    const float wf = (float)w;
-    float tx = wf * x, ty = wf * y, tz = wf * z;
 #pragma unroll
     for (int h = 1; h < G; h <<= 1) {
         if ((uint32_t)h >= top) break;
         // the lanes that add (multiples of 2h) read lane + h = lane ^ h
+        const bool lead = (lg & (2 * h - 1)) == 0;
         const float ox = xlanef(tx, h);
         const float oy = xlanef(ty, h);
         const float oz = xlanef(tz, h);
-        if ((lg & (2 * h - 1)) == 0 && (uint32_t)(lg + h) < n) {
+        if (lead && (uint32_t)(lg + h) < n) {
             tx = tx + ox;
             ty = ty + oy;
             tz = tz + oz;
         }
+        if (NR == 2 && cmax > (uint32_t)G) {
+            const float px = xlanef(ux, h), py = xlanef(uy, h), pz = xlanef(uz, h);
+            if (lead && (uint32_t)(G + lg + h) < n) {
+                ux = ux + px;
+                uy = uy + py;
+                uz = uz + pz;
+            }
+        }
+    }
+    if (NR == 2 && n > (uint32_t)G) {  // stride G: node G into node 0 (lane 0)
+        tx = tx + ux;
+        ty = ty + uy;
+        tz = tz + uz;
     }
     // lanes 0, 1, 2 of the group each divide one of lane 0's sums
     const float sx = __uint_as_float((uint32_t)__builtin_amdgcn_mov_dpp((int)__float_as_uint(tx), 0x00, 0xF, 0xF, true));
@@ -861,7 +910,7 @@ struct QueryIO {
     int32_t* lin_out;
 };
 
-template <int MODE, int G, int RAD, bool UP>
+template <int MODE, int G, int RAD, bool UP, int NR>
 void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int32_t M, int32_t K, uint64_t seed,
               hipStream_t s) {
     constexpr int GPB = kQueryThreads / G;
@@ -869,21 +918,21 @@ void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int3
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
     constexpr int side = 2 * RAD + 1;
     const size_t lds = (size_t)GPB * (2 * side * side * side + 1) * sizeof(uint32_t);
-    k_query<MODE, G, RAD, UP><<<blocks, kQueryThreads, lds, s>>>(
+    k_query<MODE, G, RAD, UP, NR><<<blocks, kQueryThreads, lds, s>>>(
         io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
         io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status));
 }
 
-template <int MODE, int G, bool UP>
+template <int MODE, int G, bool UP, int NR = 1>
 void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const QueryIO& io, int32_t M, int32_t K,
               uint64_t seed, hipStream_t s) {
     if (rad == 1)
-        launch_g<MODE, G, 1, UP>(L, g, ws, io, M, K, seed, s);
+        launch_g<MODE, G, 1, UP, NR>(L, g, ws, io, M, K, seed, s);
     else if (rad == 2)
-        launch_g<MODE, G, 2, UP>(L, g, ws, io, M, K, seed, s);
+        launch_g<MODE, G, 2, UP, NR>(L, g, ws, io, M, K, seed, s);
     else
-        launch_g<MODE, G, 3, UP>(L, g, ws, io, M, K, seed, s);
+        launch_g<MODE, G, 3, UP, NR>(L, g, ws, io, M, K, seed, s);
 }
 
 template <int MODE, int RAD, bool UP>
@@ -915,8 +964,10 @@ void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const Q
         launch_r<MODE, 16, UP>(L, g, rad, ws, io, M, K, seed, s);
     else if (K <= 32)
         launch_r<MODE, 32, UP>(L, g, rad, ws, io, M, K, seed, s);
-    else
+    else if (K <= 64)
         launch_r<MODE, 64, UP>(L, g, rad, ws, io, M, K, seed, s);
+    else
+        launch_r<MODE, 64, UP, 2>(L, g, rad, ws, io, M, K, seed, s);
 }
 
 QGrid make_qgrid(const cagq_grid_desc& d, int32_t M) {

@@ -47,8 +47,10 @@ struct CasPtrs {
     uint32_t* done;   // [B]
     uint32_t* ndone;  // clouds done
     uint32_t* uhist;  // [B][kCasParts][kCasUBins] picks per uncovered count U (lists, beta = 0)
-    uint32_t* host;       // pinned host words (or null): [0] = 1 once every cloud is done,
-                          // [1] = the round being scored (all earlier rounds have finished)
+    uint64_t* host;       // pinned host words (or null), each tagged with the call's epoch in
+                          // the top half: [0] = (epoch, 1) once every cloud is done,
+                          // [1] = (epoch, the round being run: all earlier rounds have finished)
+    uint64_t epoch;       // this call's tag, shifted into the top half
 };
 
 CasPtrs cas_ptrs(const Layout& L, void* ws) {
@@ -61,6 +63,7 @@ CasPtrs cas_ptrs(const Layout& L, void* ws) {
     c.ndone = c.done + L.B;
     c.uhist = c.ndone + 1;
     c.host = nullptr;
+    c.epoch = 0;
     return c;
 }
 
@@ -483,7 +486,7 @@ __global__ __launch_bounds__(256) void k_cas_score(
     const uint32_t lin0 = in_range ? vox_lin[gid] : 0u;
     bool active = in_range && ctl.done[b] == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
-        __hip_atomic_store(ctl.host + 1, (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(ctl.host + 1, ctl.epoch | (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int32_t nv = nvox[b];
     const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) & 1) * B * kCasParts, b) : 0u;
     if (active && R > 0 && prev >= (uint32_t)(M < nv ? M : nv)) {
@@ -491,7 +494,7 @@ __global__ __launch_bounds__(256) void k_cas_score(
             ctl.done[b] = 1;
             // the last cloud to finish tells the host, without a copy on the stream
             if (atomicAdd(ctl.ndone, 1u) + 1 == (uint32_t)B && ctl.host)
-                __hip_atomic_store(ctl.host, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                __hip_atomic_store(ctl.host, ctl.epoch | 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
         active = false;
     }
@@ -739,7 +742,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const int32_t bl0 = in_range ? st.blocker[gid] : -1;
     bool active = in_range && ctl.done[b] == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
-        __hip_atomic_store(ctl.host + 1, (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        __hip_atomic_store(ctl.host + 1, ctl.epoch | (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
     const int32_t nv = nvox[b];
     const size_t part = (size_t)B * kCasParts;
     const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) % kCasBufs) * part, b) : 0u;
@@ -748,7 +751,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
             ctl.done[b] = 1;
             // the last cloud to finish tells the host, without a copy on the stream
             if (atomicAdd(ctl.ndone, 1u) + 1 == (uint32_t)B && ctl.host)
-                __hip_atomic_store(ctl.host, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                __hip_atomic_store(ctl.host, ctl.epoch | 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
         }
         active = false;
     }
@@ -959,17 +962,25 @@ __global__ void k_sel_cas_u(int64_t tiles_s, const int32_t* __restrict__ nvox, i
     }
 }
 
-// A small pinned host buffer per calling thread for polling the number of
-// clouds done without stalling the stream. Allocated on first use, kept for
-// the life of the process.
-uint32_t* poll_buffer() {
-    thread_local uint32_t* buf = nullptr;
-    if (!buf) {
+// A small pinned host buffer per calling thread for polling the progress of
+// the rounds without stalling the stream. Allocated on first use, kept for
+// the life of the process. Every call takes a new epoch, and its kernels
+// tag each word they write with it: a round still queued from an earlier
+// call of the thread (whose words it may overwrite) is told apart and
+// ignored.
+struct PollBuffer {
+    uint64_t* words;
+    uint32_t epoch;
+};
+
+PollBuffer* poll_buffer() {
+    thread_local PollBuffer pb{nullptr, 0u};
+    if (!pb.words) {
         void* p = nullptr;
         if (hipHostMalloc(&p, 64, hipHostMallocDefault) != hipSuccess) return nullptr;
-        buf = static_cast<uint32_t*>(p);
+        pb.words = static_cast<uint64_t*>(p);
     }
-    return buf;
+    return &pb;
 }
 
 }  // namespace
@@ -1083,7 +1094,7 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     // every cloud needs several rounds: the first batch is long, later ones
     // short so that few rounds run after the last cloud is done
     const int first_batch = 6, batch = 1;
-    uint32_t* poll = poll_buffer();
+    PollBuffer* poll = poll_buffer();
     if (!poll) {
         // synchronous polling, a few rounds per copy of the done count
         const int sync_batch = 4;
@@ -1099,34 +1110,45 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
         return hipSuccess;
     }
     const int ahead = 2;
-    // The scoring kernel publishes its round and, once every cloud is done,
-    // a done flag in pinned host memory. The host keeps at least `ahead`
-    // rounds queued until it sees the flag: no copies and no events on the
-    // stream, so the GPU does not idle between rounds.
+    // The round kernel publishes its round and, once every cloud is done, a
+    // done flag in pinned host memory, both tagged with this call's epoch.
+    // The host keeps at least `ahead` rounds queued until it sees the flag:
+    // no copies and no events on the stream, so the GPU does not idle
+    // between rounds. A word of another epoch is stale: it reads as no
+    // progress.
     void* dev_words = nullptr;
-    if ((e = hipHostGetDevicePointer(&dev_words, poll, 0)) != hipSuccess) return e;
-    volatile uint32_t* words = poll;
-    words[0] = 0;
-    words[1] = 0;
-    ctl.host = static_cast<uint32_t*>(dev_words);
-    if ((e = launch_batch(first_batch)) != hipSuccess) return e;
+    if ((e = hipHostGetDevicePointer(&dev_words, poll->words, 0)) != hipSuccess) return e;
+    if (++poll->epoch == 0) ++poll->epoch;  // 0 is never an epoch
+    const uint64_t tag = (uint64_t)poll->epoch << 32;
+    volatile uint64_t* words = poll->words;
+    ctl.host = static_cast<uint64_t*>(dev_words);
+    ctl.epoch = tag;
+    // an error return first lets the rounds already queued finish, so that
+    // none of them runs after the call
+    auto fail = [&](hipError_t err, int status) {
+        const hipError_t q = hipStreamSynchronize(s);
+        *status_out = status;
+        return err != hipSuccess ? err : q;
+    };
+    if ((e = launch_batch(first_batch)) != hipSuccess) return fail(e, CAGQ_OK);
+    auto progress = [&]() -> int64_t {  // the round being run, or -1 before this call's first
+        const uint64_t w = words[1];
+        return (w & 0xFFFFFFFF00000000ull) == tag ? (int64_t)(uint32_t)w : -1;
+    };
     uint32_t seen = ~0u;
     auto seen_at = std::chrono::steady_clock::now();
     for (uint64_t spins = 1;; ++spins) {
-        if (words[0] == 1u) return hipSuccess;
-        if ((int64_t)words[1] + ahead >= R) {  // fewer than `ahead` rounds still queued
-            if (R > max_rounds + 2 * batch) {
-                *status_out = CAGQ_ERR_CAPACITY;
-                return hipSuccess;
-            }
-            if ((e = launch_batch(batch)) != hipSuccess) return e;
+        if (words[0] == (tag | 1u)) return hipSuccess;
+        if (progress() + ahead >= R) {  // fewer than `ahead` rounds still queued
+            if (R > max_rounds + 2 * batch) return fail(hipSuccess, CAGQ_ERR_CAPACITY);
+            if ((e = launch_batch(batch)) != hipSuccess) return fail(e, CAGQ_OK);
             continue;
         }
         // A failed stream ends the wait. The stream is queried only once no
         // round has started for a millisecond: a query of a busy stream puts
         // a marker into its queue, which holds back the next round by ~5 us.
         if ((spins & 1023) == 0) {
-            const uint32_t w = words[1];
+            const uint32_t w = (uint32_t)progress();
             const auto now = std::chrono::steady_clock::now();
             if (w != seen) {
                 seen = w;

@@ -140,7 +140,7 @@ def test_query_rejects_bad_arguments():
     args = lambda K=16, mode=0, M=8, ni=p, nv=p, cx=p, cw=p, cl=p: L.cagq_query_context(
         C.byref(g), None, cl, M, K, mode, 1, ni, None, nv, cx, cw, None, None)
     assert args(K=0) == cagq.ERR_INVALID_ARG
-    assert args(K=65) == cagq.ERR_INVALID_ARG
+    assert args(K=129) == cagq.ERR_INVALID_ARG
     assert args(mode=3) == cagq.ERR_INVALID_ARG
     assert args(M=0) == cagq.ERR_INVALID_ARG
     assert args(ni=None) == cagq.ERR_INVALID_ARG
@@ -157,7 +157,7 @@ def test_query_points_rejects_bad_arguments():
     args = lambda K=16, mode=1, M=8, c=p, ni=p, nv=p: L.cagq_query_points(
         C.byref(g), c, M, K, mode, 1, ni, None, nv, None, None, None)
     assert args(K=0) == cagq.ERR_INVALID_ARG
-    assert args(K=65) == cagq.ERR_INVALID_ARG
+    assert args(K=129) == cagq.ERR_INVALID_ARG
     assert args(mode=3) == cagq.ERR_INVALID_ARG
     assert args(M=0) == cagq.ERR_INVALID_ARG
     assert args(c=None) == cagq.ERR_INVALID_ARG
@@ -207,3 +207,107 @@ def test_comparison_methods_reject_bad_arguments():
     assert L.cagq_coverage(C.byref(g), None, p, 8, 8, p, None) == cagq.ERR_INVALID_ARG
     assert L.cagq_coverage(C.byref(g), p, None, 8, 8, p, None) == cagq.ERR_INVALID_ARG
     assert L.cagq_coverage(C.byref(g), p, p, 8, 8, None, None) == cagq.ERR_INVALID_ARG
+
+
+# ---------------------------------------------------------------- grid descriptors from a box
+# Host-only helpers (no device work). Pinned against the oracle's voxelize,
+# which shares no code with the library: lo must land in voxel 0 and hi in
+# the last voxel on every axis.
+
+import numpy as np  # noqa: E402
+
+import oracle  # noqa: E402
+
+
+def _lin_of(P, d):
+    g = oracle.make_grid(list(d.origin), list(d.voxel_size), list(d.dims), d.n_v, d.radius)
+    return oracle.voxelize(np.asarray(P, np.float32).reshape(-1, 3), g)
+
+
+def _cell(lin, dims):
+    return (lin % dims[0], (lin // dims[0]) % dims[1], lin // (dims[0] * dims[1]))
+
+
+def test_desc_from_voxel_size_holds_the_box_without_clamping():
+    rng = np.random.default_rng(11)
+    cases = [((0, 0, 0), (1, 1, 1), (0.1, 0.1, 0.1)),
+             ((-0.2, -0.2, -0.2), (8.2, 8.2, 3.2), (0.05, 0.05, 0.05)),
+             ((-80.2, -80.2, -2.2), (80.2, 80.2, 4.4), (0.2, 0.2, 0.2)),
+             ((0.5, 0.5, 0.5), (0.5, 0.5, 0.5), (0.3, 0.3, 0.3))]
+    for _ in range(40):
+        lo = rng.normal(0, 5, 3).astype(np.float32)
+        hi = lo + rng.random(3, dtype=np.float32) * np.float32(20)
+        vs = (rng.random(3, dtype=np.float32) * np.float32(0.5) + np.float32(0.01))
+        cases.append((tuple(lo), tuple(hi), tuple(vs)))
+    for lo, hi, vs in cases:
+        d = cagq.desc_from_voxel_size(lo, hi, vs, 16, 1)
+        lo32, hi32, vs32 = (np.asarray(x, np.float32) for x in (lo, hi, vs))
+        t = (hi32 - lo32) / vs32  # float32 subtract and correctly rounded divide
+        assert list(d.dims) == [int(np.floor(v)) + 1 for v in t], (lo, hi, vs)
+        assert list(d.origin) == list(lo32) and list(d.voxel_size) == list(vs32)
+        D = list(d.dims)
+        l_lo, l_hi = _lin_of([lo32, hi32], d)
+        assert _cell(int(l_lo), D) == (0, 0, 0)
+        # hi falls in the last voxel by the division itself, not by the clamp
+        assert _cell(int(l_hi), D) == tuple(x - 1 for x in D)
+        assert all(np.floor(t) == np.asarray(D) - 1)
+
+
+def test_desc_from_voxel_size_worked_case():
+    # [0, 1] with 0.1f voxels: 1 / 0.1f rounds to 10, so the point 1.0 is in
+    # voxel 10 and the grid needs 11 voxels per axis
+    d = cagq.desc_from_voxel_size((0, 0, 0), (1, 1, 1), (0.1, 0.1, 0.1), 8, 2)
+    assert list(d.dims) == [11, 11, 11] and d.n_v == 8 and d.radius == 2
+
+
+def test_desc_from_dims_spans_the_box():
+    rng = np.random.default_rng(12)
+    for _ in range(40):
+        lo = rng.normal(0, 5, 3).astype(np.float32)
+        hi = lo + rng.random(3, dtype=np.float32) * np.float32(20)
+        dims = rng.integers(1, 300, 3)
+        d = cagq.desc_from_dims(tuple(lo), tuple(hi), tuple(int(x) for x in dims), 32, 1)
+        s = (hi - lo) / dims.astype(np.float32)
+        assert list(d.voxel_size) == list(s.astype(np.float32)) and list(d.dims) == list(dims)
+        l_lo, l_hi = _lin_of([lo, hi], d)
+        assert _cell(int(l_lo), list(dims)) == (0, 0, 0)
+        assert _cell(int(l_hi), list(dims)) == tuple(int(x) - 1 for x in dims)
+    flat = cagq.desc_from_dims((1, 2, 3), (1, 5, 3), (4, 4, 4), 8, 1)
+    assert list(flat.voxel_size) == [1.0, np.float32(0.75), 1.0]
+
+
+def test_desc_helpers_reject_bad_boxes():
+    bad = cagq.CagqError
+    ok_box = ((0, 0, 0), (1, 1, 1))
+    for lo, hi in (((0, 0, 0), (1, -1, 1)), ((0, float("nan"), 0), (1, 1, 1)),
+                   ((0, 0, 0), (1, 1, float("inf")))):
+        with pytest.raises(bad) as e:
+            cagq.desc_from_voxel_size(lo, hi, (0.1,) * 3, 8, 1)
+        assert e.value.code == cagq.ERR_INVALID_ARG
+        with pytest.raises(bad) as e:
+            cagq.desc_from_dims(lo, hi, (4, 4, 4), 8, 1)
+        assert e.value.code == cagq.ERR_INVALID_ARG
+    for vs in ((0, 0.1, 0.1), (-0.1, 0.1, 0.1), (float("nan"), 0.1, 0.1)):
+        with pytest.raises(bad) as e:
+            cagq.desc_from_voxel_size(*ok_box, vs, 8, 1)
+        assert e.value.code == cagq.ERR_INVALID_ARG
+    for n_v, r in ((0, 1), (65, 1), (8, 0), (8, 4)):
+        with pytest.raises(bad):
+            cagq.desc_from_voxel_size(*ok_box, (0.1,) * 3, n_v, r)
+        with pytest.raises(bad):
+            cagq.desc_from_dims(*ok_box, (4, 4, 4), n_v, r)
+    with pytest.raises(bad) as e:
+        cagq.desc_from_dims(*ok_box, (0, 4, 4), 8, 1)
+    assert e.value.code == cagq.ERR_INVALID_ARG
+    with pytest.raises(bad) as e:  # 2^31 voxels
+        cagq.desc_from_voxel_size((0, 0, 0), (2047.5, 2047.5, 511.5), (0.5, 0.5, 0.5), 8, 1)
+    assert e.value.code == cagq.ERR_GRID_TOO_LARGE
+    with pytest.raises(bad) as e:  # one axis beyond 2^31 - 1
+        cagq.desc_from_voxel_size((0, 0, 0), (1e30, 1, 1), (1e-9, 1, 1), 8, 1)
+    assert e.value.code == cagq.ERR_GRID_TOO_LARGE
+    # out is untouched on an error
+    d = cagq.make_desc((9, 9, 9), (1, 1, 1), (3, 3, 3), 5, 1)
+    F3, I3 = C.c_float * 3, C.c_int32 * 3
+    rc = cagq.lib().cagq_desc_from_dims(C.byref(F3(0, 0, 0)), C.byref(F3(1, 1, 1)), C.byref(I3(0, 1, 1)),
+                                        8, 1, C.byref(d))
+    assert rc == cagq.ERR_INVALID_ARG and list(d.dims) == [3, 3, 3] and d.n_v == 5
