@@ -177,18 +177,24 @@ def measure_cas_swap(P, P_np, B: int, N: int, L, with_oracle: bool, reps: int = 
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
+    status = cagq.get_device_status(g)
     row = {"workload": f"layer 1 of the bench batch: B={B} x {N} pts, M={L.M}, r={L.grid.radius}",
            "ms": round(ms, 3), "challenges": challenges,
-           "challenges_per_s": round(challenges / (ms / 1e3), 1), "bound": "latency (sequential challenges)"}
+           "challenges_per_s": round(challenges / (ms / 1e3), 1), "bound": "latency (sequential challenges)",
+           "device_status": status}
     if with_oracle:
         import oracle
         t0 = time.perf_counter()
         ot = oracle.Table(P_np[:1], oracle.grid_from_spec(L.grid))
-        ot.sample_cas_swap(L.M, L.seed)
+        ocl, omv, _, _ = ot.sample_cas_swap(L.M, L.seed)
         dt = time.perf_counter() - t0
         ch1 = int(ot.nvox[0]) - min(L.M, int(ot.nvox[0]))
         row["oracle"] = {"ms": round(dt * 1e3, 2), "challenges": ch1, "challenges_per_s": round(ch1 / dt, 1),
                          "cores": 1, "sample": "1 of the scenes, table build included"}
+        same = (status == 0 and np.array_equal(cl[:1].cpu().numpy(), ocl)
+                and np.array_equal(mv[:1].cpu().numpy(), omv))
+        row["parity"] = {"checked": "scene 0: center_lin and m_valid of the timed call vs the oracle, "
+                                    "and the device status", "bit_exact": bool(same)}
     return row
 
 
@@ -729,6 +735,11 @@ def main():
     wall = time.perf_counter() - wall0
     ms_step = t_ev0.elapsed_time(t_ev1) / args.steps
     points_per_s = B * N / (ms_step / 1e3)
+    # what the timed steps left in the outputs: scene 0 of every layer of both
+    # variants, checked against the oracle in the CPU leg below
+    timed_out = {w.name: [(cl[0].cpu().numpy(), mv[:1].cpu().numpy(),
+                           {k: v[0].cpu().numpy() for k, v in out.items() if v is not None})
+                          for (L, desc, ws, out, cl, mv) in layers] for w, layers in plans}
 
     # per-variant times, one variant at a time on the default stream
     variant_ms = {}
@@ -802,17 +813,28 @@ def main():
         configs["host"] = _host_info()
 
     cpu = None
+    parity = None
     if not args.no_cpu_baseline:
         import oracle
         pin = _OneCore()
         pin.__enter__()
         t0 = time.perf_counter()
         done = 0
+        mismatch = []
         while True:
             for w in wls:
                 pts, wts = P_np[:1], None
-                for L in w.layers:
-                    _, _, _, q = oracle.run_layer(pts, L, weights=wts)
+                for li, L in enumerate(w.layers):
+                    _, ocl, omv, q = oracle.run_layer(pts, L, weights=wts)
+                    if done == 0:  # the timed step's scene 0, element by element (floats as bits)
+                        gcl, gmv, gq = timed_out[w.name][li]
+                        same = np.array_equal(gcl, ocl[0]) and np.array_equal(gmv, omv)
+                        for k, v in gq.items():
+                            o = q[k][0]
+                            same = same and np.array_equal(np.ascontiguousarray(v).view(np.uint32),
+                                                           np.ascontiguousarray(o).view(np.uint32))
+                        if not same:
+                            mismatch.append(f"{w.name} layer {li + 1}")
                     pts, wts = q["center_xyz"], q["center_w"]
             done += 1
             if time.perf_counter() - t0 >= args.cpu_seconds or done >= 32:
@@ -824,6 +846,9 @@ def main():
                          f"{'both variants' if len(wls) == 2 else variants[0]}) over 1 of the {B} scenes, "
                          f"single-threaded C oracle pinned to {pin.where}, {dt:.1f} s",
                **_host_info()}
+        parity = {"checked": "the timed step's outputs for scene 0, every layer of "
+                             f"{' and '.join(w.name for w in wls)}, vs the oracle's timed pass",
+                  "bit_exact": not mismatch, "mismatch": mismatch}
 
     line = {
         "metric": METRIC,
@@ -846,10 +871,14 @@ def main():
         "wall_s": round(wall, 3),
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "parity": parity,
         "next_rows": next_rows,
         "configs": configs,
     }
     print(json.dumps(line), flush=True)
+    if parity is not None and not parity["bit_exact"]:
+        print(f"bench.py: the timed step differs from the oracle: {parity['mismatch']}", file=sys.stderr)
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -15,7 +15,9 @@ from typing import Dict, Optional
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libcagq_oracle.so")
+# CAGQ_ORACLE_LIB selects another build of the same source (the sanitizer
+# run in sanitize.sh); the default is the in-tree build
+LIB_PATH = os.environ.get("CAGQ_ORACLE_LIB") or os.path.join(_HERE, "libcagq_oracle.so")
 SRC_PATH = os.path.join(_HERE, "cagq_oracle.c")
 
 CFLAGS = ["-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fPIC", "-shared",

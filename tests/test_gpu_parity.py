@@ -159,7 +159,7 @@ def test_more_centers_than_occupied_voxels():
     run_both(P, spec, 20, 16, "cas", "cube", 7, where="M>nvox cas")
 
 
-@pytest.mark.parametrize("K", [1, 2, 16, 17, 24, 31, 32, 33, 64])
+@pytest.mark.parametrize("K", [1, 2, 16, 17, 24, 31, 32, 33, 64, 65, 96, 128])
 def test_node_counts(K):
     w = W.get_workload("room")
     L = w.layers[0]
@@ -220,6 +220,45 @@ def test_cas_swap_radius_and_penalty(r, beta_q16):
     run_both(P, spec, 100, 8, "cas_swap", "cube", 11, beta_q16=beta_q16, where=f"r={r} beta={beta_q16}")
 
 
+@pytest.mark.parametrize("beta_q16", [0, 65536 // 4])
+def test_cas_swap_at_bench_size(beta_q16):
+    """CAS-P where the bench times it: one full indoor scene of 81920 points,
+    M = 8192, r = 1 (about 125 KB of one workgroup's LDS), with and without
+    the over-coverage penalty."""
+    w = W.get_workload("bigroom/cas-knn")
+    L = w.layers[0]
+    print(f"[parity] cas_swap N=81920 M={L.M} beta={beta_q16}", flush=True)
+    run_both(w.points(B=1), L.grid, L.M, L.K, "cas_swap", "knn", L.seed, beta_q16=beta_q16,
+             where=f"cas_swap bench size beta={beta_q16}")
+
+
+def test_back_to_back_cas_calls():
+    """Two CAS calls in a row from one thread, each on its own stream and
+    workspace, without waiting in between: the first (81920 points, M = 8192)
+    returns while some of its rounds may still be queued, the second (M = 4)
+    must neither be paced by them nor stopped early. Both against the
+    oracle."""
+    w = W.get_workload("bigroom/cas-knn")
+    L = w.layers[0]
+    P = w.points(B=2)
+    ot = oracle.Table(P, oracle.grid_from_spec(L.grid))
+    Pt = torch.from_numpy(P).to(DEV)
+    desc = cagq.desc_from_spec(L.grid)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    for rep in range(3):
+        with torch.cuda.stream(s1):
+            g1 = cagq.build_grid(Pt, desc)
+            cl1, mv1 = cagq.sample_centers(g1, L.M, "cas", 0)
+        with torch.cuda.stream(s2):
+            g2 = cagq.build_grid(Pt, desc)
+            cl2, mv2 = cagq.sample_centers(g2, 4, "cas", 0)
+        assert cagq.get_device_status(g1, s1) == 0 and cagq.get_device_status(g2, s2) == 0
+        for M, cl, mv in ((L.M, cl1, mv1), (4, cl2, mv2)):
+            ocl, omv, _, _ = ot.sample_cas(M)
+            assert np.array_equal(_np(cl), ocl), (rep, M)
+            assert np.array_equal(_np(mv), omv), (rep, M)
+
+
 def test_cas_swap_more_centers_than_voxels_and_capacity():
     rng = np.random.default_rng(4)
     P = rng.random((2, 60, 3), dtype=np.float32) * np.float32(0.5)
@@ -255,27 +294,42 @@ def test_weighted_centers():
     run_both(P, L.grid, 512, 32, "rvs", "cube", 1, weights=wts, where="weights cube")
 
 
-def test_repeat_runs_are_identical():
-    """Atomic arrival order never reaches an output."""
-    w = W.get_workload("bigroom/rvs-cube")
-    L = w.layers[0]
-    Pt = torch.from_numpy(w.points(B=2)).to(DEV)
-    outs = []
-    for _ in range(3):
-        g = cagq.build_grid(Pt, cagq.desc_from_spec(L.grid))
-        cl, mv = cagq.sample_centers(g, L.M, "cas", 0)
-        q = cagq.query_context(g, cl, L.K, "knn", 0)
+def _workload_outputs(w, Pt):
+    """Every layer of a workload on the GPU, chained through centers and
+    weights: the valid part of each table and every sample / query output."""
+    res, pts, wts = [], Pt, None
+    for L in w.layers:
+        g = cagq.build_grid(pts, cagq.desc_from_spec(L.grid))
+        cl, mv = cagq.sample_centers(g, L.M, L.sample, L.seed)
+        q = cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts)
+        assert cagq.get_device_status(g) == 0
         tb = {k: _np(v) for k, v in g.table().items()}
-        valid = [tb["nvox"]]
-        for b in range(2):  # entries past nvox / the stored total are unspecified
+        res.append(tb["nvox"])
+        for b in range(pts.shape[0]):  # entries past nvox / the stored total are unspecified
             nv = int(tb["nvox"][b])
             S = int(tb["vox_off"][b, nv])
-            valid += [tb["vox_lin"][b, :nv], tb["vox_count"][b, :nv], tb["vox_off"][b, :nv + 1],
-                      tb["pt_list"][b, :S]]
-        outs.append(valid + [_np(cl)] + [_np(v) for v in q.values()])
-    for o in outs[1:]:
-        for a, b in zip(outs[0], o):
-            assert np.array_equal(a, b)
+            res += [tb["vox_lin"][b, :nv], tb["vox_count"][b, :nv], tb["vox_off"][b, :nv + 1],
+                    tb["pt_list"][b, :S]]
+        res += [_np(cl), _np(mv)] + [_np(v).copy() for v in q.values() if v is not None]
+        pts, wts = q["center_xyz"], q["center_w"]
+    return res
+
+
+@pytest.mark.parametrize("name", ["tiny", "object", "room", "bigroom/cas-knn", "bigroom/rvs-cube", "lidar"])
+def test_repeat_runs_are_identical(name):
+    """Atomic arrival order never reaches an output: every workload ten times
+    at two batch sizes (different grids of blocks, and for the indoor layers
+    both the one-workgroup and the many-block build and CAS), each run
+    bitwise equal to the first."""
+    w = W.get_workload(name)
+    for B in sorted({1, min(w.B, 3)}):
+        Pt = torch.from_numpy(w.points(B=B)).to(DEV)
+        print(f"[determinism] {name} B={B}", flush=True)
+        first = _workload_outputs(w, Pt)
+        for rep in range(1, 10):
+            again = _workload_outputs(w, Pt)
+            for i, (a, b) in enumerate(zip(first, again)):
+                assert np.array_equal(a, b), (name, B, rep, i)
 
 
 def test_nonfinite_input_is_reported():
@@ -346,7 +400,7 @@ def test_query_points_workloads(name):
 
 
 @pytest.mark.parametrize("r", [1, 2, 3])
-@pytest.mark.parametrize("K", [1, 16, 17, 32, 33, 64])
+@pytest.mark.parametrize("K", [1, 16, 17, 32, 33, 64, 65, 128])
 def test_query_points_radius_and_node_counts(r, K):
     """Centers of three kinds (cloud points, points in the box, points
     outside it, clamped): contexts from empty to a few hundred points."""
@@ -447,7 +501,7 @@ def test_knn_ring_workloads(name):
 
 
 @pytest.mark.parametrize("r", [1, 2, 3])
-@pytest.mark.parametrize("K", [1, 5, 32, 64])
+@pytest.mark.parametrize("K", [1, 5, 32, 64, 65, 96, 128])
 def test_knn_ring_radius_and_node_counts(r, K):
     """Levels cut at every position: clustered points with small and large
     voxel populations, n_v binding, weights."""
@@ -549,6 +603,38 @@ def test_sixteen_lane_query_with_large_contexts(r, K):
     assert qo["ctx_count"].max() > 64 and qo["ctx_count"].min() < 16
 
 
+@pytest.mark.parametrize("r", [1, 2, 3])
+@pytest.mark.parametrize("K", [65, 96, 128])
+def test_two_register_query_with_large_contexts(r, K):
+    """64 < K <= 128 (a whole wave per center, ranks 64..127 in a second
+    register): contexts from a handful of points to a few thousand, so that
+    some chunks are merged into both registers, others leave the second one
+    empty; weights; every mode."""
+    rng = np.random.default_rng(11 * r + K)
+    B, N = 2, 6000
+    P = (rng.random((B, N, 3), dtype=np.float32) ** 4).astype(np.float32)
+    spec = _spec((0, 0, 0), (0.04,) * 3, (25, 25, 25), 64, r)
+    wts = rng.integers(1, 50, (B, N)).astype(np.uint32)
+    for q in ("knn", "cube", "knn_ring"):
+        qo = run_both(P, spec, 333, K, "rvs", q, 3, weights=wts, where=f"r={r} K={K} {q}")
+        assert qo["ctx_count"].max() > 2 * K and qo["ctx_count"].min() < 64
+    assert (qo["n_valid"] == K).any() and (qo["n_valid"] < 64).any()
+
+
+def test_paper_latency_conditions_with_k128():
+    """The paper's latency tables sweep K up to 128 (Sec. 4; Appendix F):
+    N = 81920 and N = 8192 with M = 1024 and K = 128, both samplers and both
+    queries, on the synthetic indoor scene."""
+    w = W.get_workload("bigroom/rvs-cube")
+    L = w.layers[0]
+    P = w.points(B=1)
+    for (sample, query) in (("rvs", "cube"), ("cas", "knn"), ("rvs", "knn"), ("cas", "cube")):
+        print(f"[parity] K=128 N=81920 M=1024 {sample}+{query}", flush=True)
+        run_both(P, L.grid, 1024, 128, sample, query, L.seed, where=f"K=128 {sample}+{query}")
+    r = W.get_workload("room")
+    run_both(r.points(B=1), r.layers[0].grid, 1024, 128, "cas", "knn", 3, where="K=128 N=8192")
+
+
 # ---------------------------------------------------------------- HIP graph replay
 
 def _rvs_plan(w, B, dev):
@@ -624,6 +710,58 @@ def test_graph_replay_of_the_rvs_cube_path():
                 assert np.array_equal(_bits(a_out[k]), _bits(b_out[k])), (rep, li, k)
         _run_plan(P2, other)  # the program's own eager work between replays
         torch.cuda.synchronize()
+
+
+def test_two_stream_overlapped_step_matches_oracle():
+    """The bench's step: RVS+Cube replayed from a graph on one stream while
+    CAS+k-NN runs eagerly (its large layers paced from the host) on another;
+    every layer of both variants against the oracle, three steps in a row."""
+    B = 2
+    dev = torch.device(DEV)
+    w_cas, w_rvs = W.get_workload("bigroom/cas-knn"), W.get_workload("bigroom/rvs-cube")
+    P_np = w_cas.points(B=B)
+    P = torch.from_numpy(P_np).to(dev)
+    plan_cas, plan_rvs = _rvs_plan(w_cas, B, dev), _rvs_plan(w_rvs, B, dev)
+    s_cas, s_rvs = torch.cuda.Stream(), torch.cuda.Stream()
+    with torch.cuda.stream(s_rvs):
+        _run_plan(P, plan_rvs)
+    torch.cuda.synchronize()
+    gr = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gr, stream=s_rvs):
+        _run_plan(P, plan_rvs)
+    torch.cuda.synchronize()
+    expect = {}
+    for w in (w_cas, w_rvs):
+        pts, wts, layers = P_np, None, []
+        for L in w.layers:
+            _, ocl, omv, q = oracle.run_layer(pts, L, weights=wts)
+            layers.append((ocl, omv, q))
+            pts, wts = q["center_xyz"], q["center_w"]
+        expect[w.name] = layers
+    for step in range(3):
+        for plan in (plan_cas, plan_rvs):  # clobber the outputs of the previous step
+            for (L, desc, ws, out, cl, mv) in plan:
+                cl.fill_(-5)
+                for v in out.values():
+                    if v is not None:
+                        v.fill_(7)
+        torch.cuda.synchronize()
+        main = torch.cuda.current_stream()
+        s_cas.wait_stream(main)
+        s_rvs.wait_stream(main)
+        with torch.cuda.stream(s_rvs):
+            gr.replay()
+        with torch.cuda.stream(s_cas):
+            _run_plan(P, plan_cas)
+        torch.cuda.synchronize()
+        for w, plan in ((w_cas, plan_cas), (w_rvs, plan_rvs)):
+            for li, ((L, desc, ws, out, cl, mv), (ocl, omv, q)) in enumerate(zip(plan, expect[w.name])):
+                where = f"step {step} {w.name} layer {li + 1}"
+                assert np.array_equal(_np(cl), ocl), where
+                assert np.array_equal(_np(mv), omv), where
+                for k, v in out.items():
+                    if v is not None:
+                        assert np.array_equal(_bits(_np(v)), _bits(q[k])), (where, k)
 
 
 def test_graph_replay_of_the_single_workgroup_cas_layers():
