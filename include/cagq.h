@@ -175,6 +175,28 @@ CAGQ_API int cagq_build_grid(const float* points, int32_t B, int32_t N, const ca
                     void* workspace, size_t workspace_bytes, void* stream, cagq_grid* out);
 
 /*
+ * cagq_build_grid without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc). The same build, bit for bit, into a
+ * library-owned array of CAGQ_STATIC_WORKSPACE_BYTES per GPU, resident from
+ * the library's load until the process ends; the call itself allocates
+ * nothing. `out` borrows the array of the current device (its workspace is
+ * that array's device address). Every grid built this way on one GPU shares
+ * that array: a build overwrites the previous one (whose grid record is
+ * then stale), and calls that overlap on one GPU race. The build clears
+ * what must start at zero itself. Sampling and querying take the grid like
+ * any other; with RVS, or CAS on clouds of at most 4096 points, nothing on
+ * the path allocates.
+ * Returns CAGQ_ERR_WORKSPACE_TOO_SMALL when cagq_workspace_layout's
+ * total_bytes exceeds CAGQ_STATIC_WORKSPACE_BYTES (for example B = 1 with
+ * 81920 points on a 168x168x68 grid fits, B = 2 does not), otherwise the
+ * errors of cagq_build_grid.
+ */
+#define CAGQ_STATIC_WORKSPACE_BYTES (64u << 20)
+CAGQ_API int cagq_build_grid_static(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc,
+                                    void* stream, cagq_grid* out);
+
+/*
  * Choose M center voxels per cloud (Sec. 3.2, "center voxels sampling";
  * Appendix D step 2). m_valid[b] = min(M, nvox[b]) distinct voxels are chosen
  * and written as linear ids in ascending order to center_lin[b][0..m_valid);

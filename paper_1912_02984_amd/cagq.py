@@ -71,6 +71,7 @@ def lib() -> C.CDLL:
         L.cagq_desc_from_dims.argtypes = [C.POINTER(F3), C.POINTER(F3), C.POINTER(I3), C.c_int32, C.c_int32,
                                           C.POINTER(GridDesc)]
         L.cagq_workspace_layout.argtypes = [C.c_int32, C.c_int32, C.POINTER(GridDesc), C.POINTER(LayoutC)]
+        L.cagq_build_grid_static.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(GridDesc), P, C.POINTER(GridC)]
         L.cagq_build_grid.argtypes = [P, C.c_int32, C.c_int32, C.POINTER(GridDesc), P, C.c_size_t, P,
                                       C.POINTER(GridC)]
         L.cagq_sample_centers.argtypes = [C.POINTER(GridC), C.c_int32, C.c_int32, C.c_uint64, C.c_uint32,
@@ -87,7 +88,7 @@ def lib() -> C.CDLL:
         L.cagq_get_device_status.argtypes = [C.POINTER(GridC), P]
         L.cagq_status_string.argtypes = [C.c_int]
         L.cagq_status_string.restype = C.c_char_p
-        for f in ("cagq_desc_from_voxel_size", "cagq_desc_from_dims", "cagq_workspace_layout", "cagq_build_grid", "cagq_sample_centers",
+        for f in ("cagq_desc_from_voxel_size", "cagq_desc_from_dims", "cagq_workspace_layout", "cagq_build_grid", "cagq_build_grid_static", "cagq_sample_centers",
                   "cagq_query_context", "cagq_query_points", "cagq_context_offsets", "cagq_context_list",
                   "cagq_sample_points", "cagq_ball_query", "cagq_coverage", "cagq_get_device_status"):
             getattr(L, f).restype = C.c_int
@@ -163,12 +164,16 @@ def _need(t: torch.Tensor, dtype, shape, name: str):
                          f"got {t.dtype} {tuple(t.shape)} on {t.device}")
 
 
+STATIC_WORKSPACE_BYTES = 64 << 20  # CAGQ_STATIC_WORKSPACE_BYTES
+
+
 @dataclass
 class Grid:
-    """A built grid: the C record plus the tensors it borrows."""
+    """A built grid: the C record plus the tensors it borrows (workspace is
+    None for a grid in the library's own array, cagq_build_grid_static)."""
     rec: GridC
     points: torch.Tensor
-    workspace: torch.Tensor
+    workspace: Optional[torch.Tensor]
     layout: LayoutC
 
     @property
@@ -179,20 +184,47 @@ class Grid:
     def N(self) -> int:
         return self.rec.N
 
-    def _view(self, off: int, count: int, dtype) -> torch.Tensor:
+    def _view(self, off: int, count: int, dtype, ws: torch.Tensor) -> torch.Tensor:
         nbytes = count * torch.tensor([], dtype=dtype).element_size()
-        return self.workspace[off:off + nbytes].view(dtype)
+        return ws[off:off + nbytes].view(dtype)
+
+    def _exposed(self) -> torch.Tensor:
+        """The workspace bytes up to the end of the exposed arrays: the
+        tensor itself, or a copy out of the library's array."""
+        if self.workspace is not None:
+            return self.workspace
+        L = self.layout
+        n = L.pt_list + 4 * self.B * self.N
+        out = torch.empty(n, dtype=torch.uint8, device=self.points.device)
+        torch.cuda.current_stream().synchronize()
+        _check(0 if _hip().hipMemcpy(C.c_void_p(out.data_ptr()), C.c_void_p(self.rec.workspace), C.c_size_t(n),
+                                     3) == 0 else ERR_HIP, "hipMemcpy")  # 3: device to device
+        return out
 
     def table(self) -> Dict[str, torch.Tensor]:
         """Views of the occupied-voxel table inside the workspace (uint32 as int32)."""
         B, N, L = self.B, self.N, self.layout
+        ws = self._exposed()
         return dict(
-            nvox=self._view(L.nvox, B, torch.int32),
-            vox_lin=self._view(L.vox_lin, B * N, torch.int32).view(B, N),
-            vox_count=self._view(L.vox_count, B * N, torch.int32).view(B, N),
-            vox_off=self._view(L.vox_off, B * (N + 1), torch.int32).view(B, N + 1),
-            pt_list=self._view(L.pt_list, B * N, torch.int32).view(B, N),
+            nvox=self._view(L.nvox, B, torch.int32, ws),
+            vox_lin=self._view(L.vox_lin, B * N, torch.int32, ws).view(B, N),
+            vox_count=self._view(L.vox_count, B * N, torch.int32, ws).view(B, N),
+            vox_off=self._view(L.vox_off, B * (N + 1), torch.int32, ws).view(B, N + 1),
+            pt_list=self._view(L.pt_list, B * N, torch.int32, ws).view(B, N),
         )
+
+
+_hip_lib = None
+
+
+def _hip() -> C.CDLL:
+    """The HIP runtime torch has loaded (for copies out of the library's own array)."""
+    global _hip_lib
+    if _hip_lib is None:
+        _hip_lib = C.CDLL("libamdhip64.so")
+        _hip_lib.hipMemcpy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]
+        _hip_lib.hipMemcpy.restype = C.c_int
+    return _hip_lib
 
 
 def build_grid(points: torch.Tensor, desc: GridDesc, workspace: Optional[torch.Tensor] = None,
@@ -209,6 +241,21 @@ def build_grid(points: torch.Tensor, desc: GridDesc, workspace: Optional[torch.T
     _check(lib().cagq_build_grid(_ptr(points), B, N, C.byref(desc), _ptr(workspace), workspace.numel(),
                                  _stream_ptr(stream), C.byref(rec)), "cagq_build_grid")
     return Grid(rec, points, workspace, lay)
+
+
+def build_grid_static(points: torch.Tensor, desc: GridDesc, stream: Optional[torch.cuda.Stream] = None) -> Grid:
+    """cagq_build_grid into the library's own array (cagq_build_grid_static):
+    no workspace, no allocation by the call. A later static build on the same
+    GPU overwrites the grid."""
+    if points.dim() != 3 or points.shape[2] != 3:
+        raise ValueError("points must be [B, N, 3]")
+    B, N = int(points.shape[0]), int(points.shape[1])
+    _need(points, torch.float32, (B, N, 3), "points")
+    lay = workspace_layout(B, N, desc)
+    rec = GridC()
+    _check(lib().cagq_build_grid_static(_ptr(points), B, N, C.byref(desc), _stream_ptr(stream), C.byref(rec)),
+           "cagq_build_grid_static")
+    return Grid(rec, points, None, lay)
 
 
 def sample_centers(grid: Grid, M: int, mode: str, seed: int, beta_q16: int = 0,

@@ -4,9 +4,36 @@
 #include <math.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "cagq_internal.h"
 
 namespace cagq {
+
+// The workspace of cagq_build_grid_static: one array per GPU, resident from
+// the library's load until the process ends. Host code never uses the
+// array's name as an address (on the host it is only a stand-in for the
+// symbol): its device address comes from hipGetSymbolAddress, once per
+// device.
+constexpr size_t kStaticScratchBytes = CAGQ_STATIC_WORKSPACE_BYTES;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+// The device address of the current device's array, or null on failure.
+static void* static_scratch() {
+    static std::mutex mu;
+    static void* ptr[kMaxDevices] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[dev]) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return nullptr;
+        ptr[dev] = p;
+    }
+    return ptr[dev];
+}
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -178,6 +205,26 @@ int cagq_build_grid(const float* points, int32_t B, int32_t N, const cagq_grid_d
     out->workspace = workspace;
     out->workspace_bytes = workspace_bytes;
     hipError_t e = launch_build(points, L, *desc, workspace, (hipStream_t)stream);
+    return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
+}
+
+int cagq_build_grid_static(const float* points, int32_t B, int32_t N, const cagq_grid_desc* desc, void* stream,
+                           cagq_grid* out) {
+    if (!points || !out) return CAGQ_ERR_INVALID_ARG;
+    int rc = check_desc(desc);
+    if (rc != CAGQ_OK) return rc;
+    Layout L;
+    if (!make_layout(B, N, desc, &L)) return CAGQ_ERR_INVALID_ARG;
+    if (L.total > kStaticScratchBytes) return CAGQ_ERR_WORKSPACE_TOO_SMALL;
+    void* ws = static_scratch();
+    if (!ws) return CAGQ_ERR_HIP;
+    out->B = B;
+    out->N = N;
+    out->desc = *desc;
+    out->points = points;
+    out->workspace = ws;
+    out->workspace_bytes = kStaticScratchBytes;
+    hipError_t e = launch_build(points, L, *desc, ws, (hipStream_t)stream);
     return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
 }
 
