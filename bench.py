@@ -44,12 +44,27 @@ VARIANTS = ("bigroom/cas-knn", "bigroom/rvs-cube")
 METRIC = "CAGQ points/sec & ms/batch at 81920 pts; achieved HBM GB/s vs MI355X peak"
 
 
-def query_alg_bytes(M_total: int, K: int, ctx_total: int) -> int:
-    """Algorithmic bytes of one query launch: per center the center id (4 B)
-    and its outputs (node_idx 4K, node_xyz 12K, center_xyz 12, center_w 4,
-    n_valid 4, ctx_count 4); per context point its coordinates and index
-    (16 B)."""
+def query_alg_bytes(M_total: int, K: int, S_total: int) -> int:
+    """Algorithmic bytes of one query launch: the stored points' coordinates
+    read once (12 B each, S of them), per center its outputs (node_idx and
+    node_xyz, 16 B per node) and 28 B of center id, center_xyz, center_w and
+    n_valid."""
+    return 12 * S_total + M_total * (16 * K + 28)
+
+
+def query_reread_bytes(M_total: int, K: int, ctx_total: int) -> int:
+    """The same launch counting every context point of every center (16 B:
+    coordinates and index), so overlapping neighbourhoods are read again."""
     return M_total * (16 * K + 28) + 16 * ctx_total
+
+
+def layer_alg_bytes(N_total: int, S_total: int, nvox_total: int, M_total: int, K: int, weights: bool) -> int:
+    """Algorithmic bytes of a whole layer (voxelize, table, sampling, query):
+    points read (12 B, plus 4 B of weight), lists and voxel records written
+    and read (8 B per stored point, 24 B per occupied voxel), the stored
+    points' coordinates read by the query (12 B), the nodes (16 B) and the
+    centers (28 B)."""
+    return (12 + (4 if weights else 0)) * N_total + 20 * S_total + 24 * nvox_total + M_total * (16 * K + 28)
 
 
 def query_source_hash() -> str:
@@ -126,6 +141,88 @@ def summarize_counters(csv_path: str) -> str:
         n = len(disp[k])
         out.append(f"| {k} | {n} | " + " | ".join(f"{sums[k].get(c, 0.0) / n:.1f}" for c in names) + " |")
     return "\n".join(out) + "\n"
+
+
+LAYER_FILE = os.path.join(ROOT, "profiles", "cagq_layer1_bigroom_b4.md")
+LAYER_SOURCES = "paper_1912_02984_amd/csrc"
+
+
+def layer_source_hash() -> str:
+    """Hash of every HIP source and header of the library."""
+    h = hashlib.sha256()
+    d = os.path.join(ROOT, LAYER_SOURCES)
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def load_layer_profile() -> dict:
+    """Per variant: summed kernel time (us), HBM bytes and launches of one
+    layer-1 pass from the committed profile; empty unless it was taken on
+    the current library sources."""
+    try:
+        with open(LAYER_FILE) as f:
+            txt = f.read()
+    except OSError:
+        return {}
+    m = re.search(r"library source sha256\[:16\]: `([0-9a-f]+)`", txt)
+    if not m or m.group(1) != layer_source_hash():
+        return {}
+    out = {}
+    for v, us, by, n in re.findall(r"^layer1 (\S+): kernel_us=([0-9.]+) bytes=(\d+) launches=(\d+)$", txt, re.M):
+        out[v] = {"us": float(us), "bytes": int(by), "launches": int(n)}
+    return out
+
+
+def summarize_layer(variant: str, fetch_csv: str, write_csv: str, trace_csv: str, passes: int) -> str:
+    """One variant's layer-1 kernels from a --layer1-passes run: per kernel
+    the launches per pass, the average duration (kernel trace) and the HBM
+    bytes per launch (FETCH_SIZE and WRITE_SIZE, each scaled by what it reads
+    for the calibration copy); then their sums over one pass. The warm-up
+    pass (the first 1/(passes+1) of the dispatches) is left out."""
+    def cagq_rows(rows, key):
+        rows = sorted((r for r in rows if "cagq::" in r["Kernel_Name"]), key=lambda r: int(r[key]))
+        return rows[len(rows) // (passes + 1):]
+
+    def load(path, counter):
+        return [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+    fr, wr = load(fetch_csv, "FETCH_SIZE"), load(write_csv, "WRITE_SIZE")
+
+    def copy_kib(rows):  # the largest torch kernel of the run is the calibration copy
+        return max(float(r["Counter_Value"]) for r in rows if "at::native" in r["Kernel_Name"])
+    cf, cw = copy_kib(fr), copy_kib(wr)
+    sf, sw = COPY_PROBE_BYTES / (cf * 1024), COPY_PROBE_BYTES / (cw * 1024)
+    fr, wr = cagq_rows(fr, "Dispatch_Id"), cagq_rows(wr, "Dispatch_Id")
+    tr = cagq_rows(list(csv.DictReader(open(trace_csv))), "Start_Timestamp")
+    per = {}
+    for r in tr:
+        e = per.setdefault(_short(r["Kernel_Name"]), {"n": 0, "us": 0.0, "f": 0.0, "w": 0.0})
+        e["n"] += 1
+        e["us"] += (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+    for rows, k in ((fr, "f"), (wr, "w")):
+        for r in rows:
+            per.setdefault(_short(r["Kernel_Name"]), {"n": 0, "us": 0.0, "f": 0.0, "w": 0.0})[k] += \
+                float(r["Counter_Value"])
+    lines = [f"### {variant}", "",
+             f"Calibration: the {COPY_PROBE_BYTES >> 20} MiB copy reads FETCH_SIZE {cf:.0f} KiB (scale {sf:.4f}) and "
+             f"WRITE_SIZE {cw:.0f} KiB (scale {sw:.4f}).", "",
+             "| Kernel | Launches per pass | Avg (us) | FETCH_SIZE (KiB) per launch | WRITE_SIZE (KiB) per launch "
+             "| HBM bytes per pass |", "|---|---|---|---|---|---|"]
+    tot_us = tot_b = tot_n = 0.0
+    for k, e in sorted(per.items(), key=lambda kv: -kv[1]["us"]):
+        n = max(e["n"], 1)
+        b = (e["f"] * sf + e["w"] * sw) * 1024 / passes
+        tot_us += e["us"] / passes
+        tot_b += b
+        tot_n += e["n"] / passes
+        lines.append(f"| {k} | {e['n'] / passes:.1f} | {e['us'] / n:.2f} | {e['f'] / n:.1f} | {e['w'] / n:.1f} "
+                     f"| {int(round(b))} |")
+    lines.append(f"| **one layer-1 pass** | {tot_n:.1f} | {tot_us:.2f} (sum) | | | {int(round(tot_b))} |")
+    lines += ["", f"layer1 {variant}: kernel_us={tot_us:.2f} bytes={int(round(tot_b))} launches={int(round(tot_n))}", "",
+              f"library source sha256[:16]: `{layer_source_hash()}` ({LAYER_SOURCES}/*.hip, *.h)", ""]
+    return "\n".join(lines) + "\n"
 
 
 def summarize_traffic(fetch_csv: str, write_csv: str) -> str:
@@ -492,6 +589,10 @@ def measure_configs(dev, with_oracle: bool, reps: int = 50, reps_big: int = 20) 
             layers.append({"sample": L.sample, "query": L.query, "M": L.M, "K": L.K,
                            "build_ms": round(float(med[3 * li]), 4), "sample_ms": round(float(med[3 * li + 1]), 4),
                            "query_ms": round(float(med[3 * li + 2]), 4)})
+            if L.sample == "cas":  # greedy picks (one per step) over the sampling time
+                steps = int(mv.sum().item())
+                layers[-1]["cas_steps"] = steps
+                layers[-1]["cas_steps_per_s"] = round(steps / (float(med[3 * li + 1]) / 1e3), 1)
         t_med = float(np.median(tot))
         row = {"B": B, "N": N, "layers": layers, "ms_median": round(t_med, 4),
                "ms_iqr": [round(float(np.percentile(tot, 25)), 4), round(float(np.percentile(tot, 75)), 4)],
@@ -561,6 +662,12 @@ def main():
                     help="print a markdown table of a rocprofv3 kernel summary and exit")
     ap.add_argument("--summarize-counters", metavar="COUNTER_CSV",
                     help="print a markdown table of a rocprofv3 --pmc collection per kernel and exit")
+    ap.add_argument("--layer1-passes", type=int, default=0,
+                    help="profiling mode: run only layer 1 (build + sample + query) of the selected variants "
+                         "this many times after one warm-up pass, then exit (for the counter and trace runs "
+                         "behind the layer roofline)")
+    ap.add_argument("--summarize-layer", nargs=5, metavar=("VARIANT", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV", "PASSES"),
+                    help="per-kernel time and HBM bytes of a --layer1-passes run, and their sums per pass")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="print the query kernels' HBM bytes from two counter passes and exit")
     args = ap.parse_args()
@@ -572,6 +679,10 @@ def main():
         return
     if args.summarize_traffic:
         print(summarize_traffic(*args.summarize_traffic), end="")
+        return
+    if args.summarize_layer:
+        v, f, w_, t, n = args.summarize_layer
+        print(summarize_layer(v, f, w_, t, int(n)), end="")
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
@@ -613,6 +724,8 @@ def main():
     streams = [torch.cuda.Stream() for _ in plans]
     q_events = []  # (variant, start, end) around layer-1 query launches
 
+    grids_of = {}  # variant -> the grid records of its last pass, by layer
+
     def run_variant(plan, record=False, hook=None, hook_layer=-1, first=0, last=None):
         """Layers [first, last) of a variant; a later layer reads the
         previous layer's outputs, which stay at fixed addresses."""
@@ -625,6 +738,7 @@ def main():
         for li in range(first, len(layers) if last is None else last):
             L, desc, ws, out, cl, mv = layers[li]
             g = cagq.build_grid(pts, desc, ws)
+            grids_of.setdefault(w.name, {})[li] = g
             cagq.sample_centers(g, L.M, L.sample, L.seed, center_lin=cl, m_valid=mv)
             if li == hook_layer and hook is not None:
                 hook()
@@ -644,6 +758,27 @@ def main():
                 e1.record()
                 q_events.append((w.name, e0, e1))
             pts, wts = out["center_xyz"], out["center_w"]
+
+    if args.layer1_passes:
+        if args.copy_probe:
+            src = torch.ones(COPY_PROBE_BYTES // 4, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            torch.mul(src, 1.0, out=dst)
+            torch.cuda.synchronize()
+            del src, dst
+        sizes = {}
+        for plan in plans:
+            run_variant(plan, last=1)  # warm-up (not counted by the summaries, which take the last passes)
+            torch.cuda.synchronize()
+            for _ in range(args.layer1_passes):
+                run_variant(plan, last=1)
+            torch.cuda.synchronize()
+            tb = grids_of[plan[0].name][0].table()
+            nv = tb["nvox"].cpu().numpy().astype(np.int64)
+            sizes[plan[0].name] = {"nvox": int(nv.sum()),
+                                   "S": int(sum(int(tb["vox_off"][b, int(nv[b])]) for b in range(B)))}
+        print(json.dumps({"layer1_passes": args.layer1_passes, "sizes": sizes}), flush=True)
+        return
 
     def host_layers(w):
         """Leading layers whose sampling waits on the host: CAS outside the
@@ -762,17 +897,49 @@ def main():
             run_variant(plan, record=True)
     torch.cuda.synchronize()
 
-    # roofline of the layer-1 query kernel, per variant
-    roof = {}
+    # layer 1 of each variant as a whole (build + sample + query), between
+    # events after a GPU-side delay
+    l_events = []
+    for plan in plans:
+        for _ in range(ROOF_PASSES):
+            a, b_ = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda._sleep(SLEEP_CYCLES)
+            a.record()
+            run_variant(plan, last=1)
+            b_.record()
+            l_events.append((plan[0].name, a, b_))
+    torch.cuda.synchronize()
+
+    # roofline of the layer-1 query kernel and of the whole layer, per variant
+    roof, layer_roof = {}, {}
+    layer_prof = load_layer_profile()
     for w, layers in plans:
         L, desc, ws, out, cl, mv = layers[0]
+        tb = grids_of[w.name][0].table()
+        nv = tb["nvox"].cpu().numpy().astype(np.int64)
+        S_total = int(sum(int(tb["vox_off"][b, int(nv[b])]) for b in range(B)))
         durs = [a.elapsed_time(b) / QUERY_REPS for name, a, b in q_events if name == w.name]
         t_ms = float(np.mean(durs))
         ctx_total = int(out["ctx_count"].sum().item())
-        alg = query_alg_bytes(B * L.M, L.K, ctx_total)
+        alg = query_alg_bytes(B * L.M, L.K, S_total)
+        reread = query_reread_bytes(B * L.M, L.K, ctx_total)
         gbs = alg / (t_ms / 1e3) / 1e9
         roof[w.name] = dict(kernel=f"k_query<{L.query}>", us=t_ms * 1e3, alg_bytes=alg, achieved_gbs=gbs,
-                            ctx_total=ctx_total)
+                            S=S_total, ctx_total=ctx_total, reread_bytes=reread,
+                            reread_gbs=reread / (t_ms / 1e3) / 1e9)
+        l_ms = float(np.mean([a.elapsed_time(b) for name, a, b in l_events if name == w.name]))
+        l_alg = layer_alg_bytes(B * N, S_total, int(nv.sum()), B * L.M, L.K, weights=False)
+        ent = {"us": round(l_ms * 1e3, 2), "alg_bytes": l_alg,
+               "achieved_gbs": round(l_alg / (l_ms / 1e3) / 1e9, 1),
+               "frac": round(l_alg / (l_ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+               "nvox": int(nv.sum()), "S": S_total}
+        lp = layer_prof.get(w.name)
+        if lp:  # kernel time and counter bytes of the same layer from the committed profile
+            ent.update({"kernel_us_sum": lp["us"], "alg_gbs_over_kernel_sum": round(l_alg / lp["us"] / 1e3, 1),
+                        "frac_over_kernel_sum": round(l_alg / lp["us"] / 1e3 / HBM_PEAK_GBS, 4),
+                        "traffic": lp["bytes"], "traffic_gbs_over_kernel_sum": round(lp["bytes"] / lp["us"] / 1e3, 1),
+                        "launches": lp["launches"]})
+        layer_roof[w.name] = ent
     dom = max(roof.values(), key=lambda r: r["us"])
     traffic = load_traffic().get(dom["kernel"])
     # what a plain streaming copy reaches on this GPU, for context: a 1 GiB
@@ -796,7 +963,8 @@ def main():
                 "kernel": dom["kernel"], "launch_us": round(dom["us"], 2), "alg_bytes": dom["alg_bytes"],
                 "copy_gbs": round(copy_gbs, 1),
                 "per_variant": {k: {kk: (round(vv, 3) if isinstance(vv, float) else vv) for kk, vv in v.items()}
-                                for k, v in roof.items()}}
+                                for k, v in roof.items()},
+                "layer": layer_roof}
 
     # rows beyond the hot path, measured on the layer-1 grid of the same batch
     next_rows = None
