@@ -75,6 +75,9 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->vox_off = take(4 * (size_t)B * (N + 1));
     L->pt_list = take(4 * BN);
     L->status = take(4 * kStSlots);
+    L->sel_ghist = take(4 * (size_t)B * kSelBins);
+    L->sel_cnt = take(4 * (size_t)B);
+    L->clear_small = off;
     L->desc_w = take(8 * (size_t)B * L->tiles_w);
     L->desc_s = take(8 * (size_t)B * L->tiles_s);
     L->bytemap = take(64 * (size_t)B * L->W);
@@ -99,7 +102,11 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->cas_nbr = take(L->has_nbr16 ? 2 * BN * (size_t)nbr_stride(d->radius) : 0);
     L->cas_nbr32 = take(L->has_nbr32 ? 4 * BN * (size_t)kNbr32Stride : 0);
     L->sel_thr = take(8 * (size_t)B);
-    L->sel_hist = take(4 * (size_t)kSelPasses * B * kSelBins);
+    const size_t sel_chunks = ((size_t)N + kSelChunk - 1) / kSelChunk;
+    L->sel_keys = take(4 * (size_t)B * sel_chunks * kSelChunk);
+    L->sel_bins = take(4 * (size_t)B * sel_chunks * kSelBins);
+    L->sel_base = take(4 * (size_t)B * sel_chunks);
+    L->sel_take = take(4 * (size_t)B * sel_chunks);
     L->cov_mark = take((BN + 15) / 16 * 16);
     L->total = off;
     return true;

@@ -496,8 +496,10 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
     const GridArgs g = grid_args(d);
     int* status = at<int>(ws, L.status);
     if (N <= kSmallN && L.W <= kSmallW && (int64_t)small_lds_bytes(N, L.W) <= small_lds_avail()) {
-        // the status words only: the small build uses no scan descriptors or occupancy bytes
-        k_clear<<<1, 256, 0, s>>>(at<uint4>(ws, L.status), (4 * kStSlots + 15) / 16);
+        // the status words and the selection's histogram only: the small
+        // build uses no scan descriptors or occupancy bytes
+        k_clear<<<(unsigned)((L.clear_small - L.status + 4095) / 4096), 256, 0, s>>>(
+            at<uint4>(ws, L.status), (L.clear_small - L.status) / 16);
         const size_t bytes = small_lds_bytes(N, L.W);
         hipError_t e = hipFuncSetAttribute((const void*)k_build_small, hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)bytes);

@@ -24,14 +24,16 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
                                                          const int32_t* __restrict__ nvox,
                                                          const uint32_t* __restrict__ vox_lin,
                                                          const uint64_t* __restrict__ bitmap,
-                                                         const uint32_t* __restrict__ word_rank, E* __restrict__ nbr) {
+                                                         const uint32_t* __restrict__ word_rank, E* __restrict__ nbr,
+                                                         uint64_t* __restrict__ key, int64_t unit) {
     constexpr int H = 2 * RAD, S2 = 2 * H + 1;
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (gid >= B * N) return;
     const int32_t b = gid / N, s = gid - b * N;
     if (s >= nvox[b]) return;
     int32_t x, y, z;
-    decode_lin(vox_lin[gid], g, x, y, z);
+    const uint32_t lin = vox_lin[gid];
+    decode_lin(lin, g, x, y, z);
     const uint64_t* bm = bitmap + (size_t)b * W;
     const uint32_t* wr = word_rank + (size_t)b * W;
     E* out = nbr + (size_t)gid * ST;
@@ -64,6 +66,7 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
         }
         out[0] = (E)n_r;
         out[1] = (E)(n - HDR);
+        if (key) key[gid] = cas_key(unit * (int64_t)n_r, lin);
     } else {
         // one plane of rows at a time, the window within r first
         for (int dz = -RAD; dz <= RAD; ++dz) {
@@ -96,7 +99,8 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
 
 }  // namespace
 
-hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s) {
+hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s, uint64_t* key,
+                          int64_t unit) {
     GridDims g;
     for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
     const unsigned blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
@@ -106,13 +110,13 @@ hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hi
     const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
     if (L.has_nbr32 && d.radius == 1) {
         k_cas_nbr<1, uint32_t, kNbr32Stride, 4><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint32_t>(ws, L.cas_nbr32));
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint32_t>(ws, L.cas_nbr32), key, unit);
     } else if (L.has_nbr16 && d.radius == 1) {
         k_cas_nbr<1, uint16_t, nbr_stride(1), 8><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr));
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0);
     } else if (L.has_nbr16 && d.radius == 2) {
         k_cas_nbr<2, uint16_t, nbr_stride(2), 8><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr));
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0);
     } else {
         return hipErrorInvalidValue;
     }

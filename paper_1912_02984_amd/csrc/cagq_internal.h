@@ -18,8 +18,8 @@ constexpr int kScanThreads = 256;       // threads per scan tile
 constexpr int kScanItems = 4;           // items per thread in a scan tile
 constexpr int kScanTile = kScanThreads * kScanItems;
 constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
-constexpr int kSelPasses = 3;           // digits of a key's top 32 bits: 11, 11 and 10 bits
-constexpr int kSelBins = 2048;
+constexpr int kSelBins = 2048;          // bins of the 11-bit digits of the many-block select
+constexpr int kSelChunk = 4096;         // slots per chunk of the many-block select
 
 // Status word slots (int32 each) at the start of the workspace's control block.
 enum StatusSlot {
@@ -68,7 +68,13 @@ struct Layout {
     size_t cas_nbr32;     // u32 [B][N][kNbr32Stride] CAS neighbour lists of larger clouds, r = 1
     bool has_nbr16, has_nbr32;
     size_t sel_thr;       // u64 [B] selection threshold, see sel_pack
-    size_t sel_hist;      // u32 [kSelPasses][B][kSelBins] digit histograms of the many-block select
+    size_t sel_ghist;     // u32 [B][kSelBins] top-11-bit histogram of the many-block select (zero between selections)
+    size_t sel_cnt;       // u32 [B] block tickets of the many-block select (zero between selections)
+    size_t sel_keys;      // u32 [B][chunks][4096] top halves of the select keys, each chunk sorted by its top 11 bits
+    size_t sel_bins;      // u32 [B][chunks][kSelBins] end of each 11-bit bin in its sorted chunk
+    size_t sel_base;      // u32 [B][chunks] first output position of each chunk's chosen slots
+    size_t sel_take;      // u32 [B][chunks] ties at the bound each chunk takes
+    size_t clear_small;   // [status, clear_small) is zeroed by every build
     size_t cov_mark;      // u8  [B][N] coverage metric: 1 when the slot holds a node point
     size_t clear_end;     // [status, clear_end) is zeroed at the start of every build
 };
@@ -312,6 +318,12 @@ __device__ __forceinline__ uint32_t xcd_block(uint32_t bid, uint32_t nblocks) {
     return x < rem ? x * (q + 1) + i : rem * (q + 1) + (x - rem) * q + i;
 }
 
+// CAS key of a voxel of score `score` and linear id `lin`: (score, -lin) as
+// one unsigned 64-bit word, the score offset by 2^31.
+__device__ __forceinline__ uint64_t cas_key(int64_t score, uint32_t lin) {
+    return ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
+}
+
 // Slot of the occupied voxel `lin` of a cloud (the number of occupied voxels
 // with a smaller linear id), or -1 when it is empty.
 __device__ __forceinline__ int32_t slot_of(const uint64_t* bm, const uint32_t* wr, uint32_t lin) {
@@ -436,8 +448,10 @@ hipError_t launch_cas_swap(const Layout& L, const cagq_grid_desc& d, void* ws, i
                            uint32_t beta_q16, int32_t* center_lin, int32_t* m_valid, hipStream_t s);
 
 // Writes the CAS neighbour lists of the grid in whichever format the layout
-// holds (has_nbr16 or has_nbr32).
-hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s);
+// holds (has_nbr16 or has_nbr32). With u32 lists and `key` given, also sets
+// each occupied voxel's round-0 key, cas_key(unit * entries within r, lin).
+hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s,
+                          uint64_t* key = nullptr, int64_t unit = 0);
 
 // Greedy coverage-aware sampling (rounds of neighbourhood maxima).
 hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M,

@@ -39,7 +39,7 @@ namespace cagq {
 namespace {
 
 constexpr int kSelThreads = 1024;
-constexpr int32_t kSelManyBlockMin = 16384;  // clouds of this many points use the many-block select
+constexpr int32_t kSelManyBlockMin = 16384;  // clouds of this many points use the many-block select (measured: below it one workgroup per cloud is faster)
 
 struct CasPtrs {
     uint64_t* gpart;  // [kCasBufs][B][kCasParts] partial maxima of the unpicked keys, per round buffer
@@ -232,137 +232,323 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     }
 }
 
-// ---- many-block selection (large clouds): one histogram kernel per digit.
-// Digit q covers key bits [lo(q), hi(q)): bits 53..63, 42..52 and 32..41.
-__device__ __forceinline__ int sel_lo(int q) { return q == kSelPasses - 1 ? 32 : 64 - 11 * (q + 1); }
-__device__ __forceinline__ int sel_hi(int q) { return 64 - 11 * q; }
+// ---- many-block selection (large clouds): two launches.
+// k_sel_pick splits each cloud's slots into chunks of kPickSlots. Per chunk
+// it computes the select keys, counts the top 11 bits of their top halves
+// into the cloud's histogram and, in LDS, counting-sorts the top halves by
+// those 11 bits: the sorted chunk and the end of each bin go to memory. The
+// last block of each cloud to finish (by a ticket) reads the histogram,
+// finds the digit whose cumulative count reaches m,
+// gathers the keys of that digit from every chunk's bin and resolves them
+// exactly by a radix select over their next 11 and 10 bits (in LDS when
+// they fit, else reading them again per digit). It then writes each chunk's
+// first output position and share of the ties at the bound, and leaves the
+// histogram and the ticket at zero for the next selection (the build zeroes
+// them first).
+// k_sel_emit_chunks then writes every chunk's chosen slots in slot order.
+constexpr int kPickThreads = 1024;
+constexpr int kPickItems = 4;
+constexpr int kPickSlots = kPickThreads * kPickItems;  // slots per chunk (kSelChunk)
+constexpr int kPickBlocks = 1024;                       // at most this many blocks per cloud
+constexpr int kCandCap = 4096;                          // candidate keys held in LDS
+static_assert(kPickSlots == kSelChunk && kCandCap <= kPickSlots && 2 * kPickThreads == kSelBins, "select sizes");
 
-struct SelState {
-    uint64_t prefix, mask, bound;
-    uint32_t need;
-    bool done;  // bound and need are known
-};
+// Exclusive scan of one value per thread of a kPickThreads block.
+__device__ __forceinline__ uint32_t pick_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
+    const uint32_t incl = wave_incl_scan<uint32_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    __syncthreads();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kPickThreads / kWave; ++i) {
+        const uint32_t x = s_wave[i];
+        off += i < wv ? x : 0u;
+        tot += x;
+    }
+    __syncthreads();
+    *total = tot;
+    return off + incl - v;
+}
 
-// Re-derives, from the histograms of digits 0..passes-1 of cloud b, the digits
-// chosen so far (each the digit whose cumulative count first reaches the
-// remaining rank). Called by every thread of a kScanThreads block.
-__device__ SelState sel_derive(const uint32_t* __restrict__ hist, int32_t B, int32_t b, uint32_t m, int passes) {
-    __shared__ uint64_t s_wave[kScanThreads / kWave];
-    __shared__ uint32_t s_digit, s_below, s_cnt;
-    SelState st{0ull, 0ull, 0ull, m, false};
+// Over the histogram h of `bins` (1024 or 2048) bins in LDS: the bin where
+// the cumulative count first reaches `need`, the count before it and its
+// own count, returned to every thread (out[] keeps its previous content
+// when the total is below `need`). Every thread of the block calls it.
+__device__ __forceinline__ void pick_find(const uint32_t* h, int bins, uint32_t need, uint32_t* s_find,
+                                          uint32_t* s_wave, uint32_t (&out)[3]) {
+    const int per = bins / kPickThreads;
     const int tid = threadIdx.x;
-    for (int q = 0; q < passes && !st.done; ++q) {
-        const int lo = sel_lo(q), width = sel_hi(q) - lo;
-        const int bins = 1 << width;
-        const int per = bins / kScanThreads;  // 8, or 4 for the last digit
-        const uint32_t* h = hist + ((size_t)q * B + b) * kSelBins;
-        uint32_t v[8], sum = 0;
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            v[i] = i < per ? h[tid * per + i] : 0u;
-            sum += v[i];
-        }
-        uint64_t total;
-        uint32_t run = (uint32_t)block_excl_scan(sum, s_wave, &total);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            if (i < per && run < st.need && run + v[i] >= st.need) {
-                s_digit = (uint32_t)(tid * per + i);
-                s_below = run;
-                s_cnt = v[i];
-            }
-            run += v[i];
-        }
-        __syncthreads();
-        const uint32_t digit = s_digit, below = s_below, cnt = s_cnt;
-        __syncthreads();
-        st.prefix |= (uint64_t)digit << lo;
-        st.mask |= (uint64_t)(bins - 1) << lo;
-        st.need -= below;
-        if (cnt == st.need) {  // every key under this prefix is among the m smallest
-            st.bound = ((st.prefix | ~st.mask) >> 32) + 1;
-            st.need = 0;
-            st.done = true;
-        }
+    const uint32_t v0 = h[tid * per], v1 = per > 1 ? h[tid * per + 1] : 0u;
+    uint32_t tot;
+    uint32_t run = pick_excl_scan(v0 + v1, s_wave, &tot);
+    if (run < need && run + v0 >= need) {
+        s_find[0] = (uint32_t)(tid * per);
+        s_find[1] = run;
+        s_find[2] = v0;
     }
-    if (!st.done && passes == kSelPasses) {
-        st.bound = st.prefix >> 32;
-        st.done = true;
+    run += v0;
+    if (per > 1 && run < need && run + v1 >= need) {
+        s_find[0] = (uint32_t)(tid * per + 1);
+        s_find[1] = run;
+        s_find[2] = v1;
     }
-    return st;
+    __syncthreads();
+    if (tot >= need) {
+        out[0] = s_find[0];
+        out[1] = s_find[1];
+        out[2] = s_find[2];
+    }
+    __syncthreads();
 }
 
-__global__ void k_sel_mb_clear(int32_t B, int64_t tiles_s, uint32_t* __restrict__ hist,
-                               uint64_t* __restrict__ desc_s, int* __restrict__ status, int32_t M,
-                               const int32_t* __restrict__ nvox, int32_t* __restrict__ m_valid) {
-    const size_t n = (size_t)kSelPasses * B * kSelBins;
-    const size_t stride = (size_t)gridDim.x * blockDim.x;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) hist[i] = 0;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < (size_t)B * tiles_s; i += stride) desc_s[i] = 0;
-    const int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
-    if (gid == 0) status[kStTicketSel] = 0;
-    if (gid < B) m_valid[gid] = M < nvox[gid] ? M : nvox[gid];
-}
-
-// Digit q: blocks (j, b) count the keys of their share of cloud b's slots that
-// match the digits chosen so far.
-constexpr int kSelItems = 16;  // slots per thread of a histogram block
-
-__global__ __launch_bounds__(kScanThreads) void k_sel_mb_hist(
-    int q, int32_t B, int32_t N, const int32_t* __restrict__ nvox, int32_t M, int key_mode, uint64_t seed,
-    const uint64_t* __restrict__ cas_pick, uint32_t* __restrict__ hist) {
-    __shared__ uint32_t lh[kSelBins];
+__global__ __launch_bounds__(kPickThreads) void k_sel_pick(
+    int32_t N, const int32_t* __restrict__ nvox, int32_t M, int key_mode, uint64_t seed,
+    const uint64_t* __restrict__ cas_pick, uint32_t* __restrict__ sorted, uint32_t* __restrict__ bin_end,
+    uint32_t* __restrict__ ghist, uint32_t* __restrict__ gcnt, uint64_t* __restrict__ thr,
+    int32_t* __restrict__ m_valid, uint32_t* __restrict__ sel_base, uint32_t* __restrict__ sel_take) {
+    __shared__ uint32_t lh[kSelBins];     // histogram, then the bins' cursors
+    __shared__ uint32_t sk[kPickSlots];   // the chunk's sorted top halves; later the candidates
+    __shared__ uint32_t sp[kPickThreads]; // the last block: candidates before each chunk of a group
+    __shared__ uint32_t ss[kPickThreads]; //                 and where its bin starts
+    __shared__ uint32_t s_wave[kPickThreads / kWave];
+    __shared__ uint32_t s_find[3];
+    __shared__ uint32_t s_last;
     const int32_t b = blockIdx.y;
+    const int32_t nblk = gridDim.x;
+    const int tid = threadIdx.x;
     const int32_t nv = nvox[b];
     const uint32_t m = (uint32_t)(M < nv ? M : nv);
-    const SelState st = sel_derive(hist, B, b, m, q);
-    if (st.done) return;  // the whole block
-    const int lo = sel_lo(q), width = sel_hi(q) - lo;
-    const uint32_t dmask = (1u << width) - 1;
-    for (int i = threadIdx.x; i < kSelBins; i += kScanThreads) lh[i] = 0;
-    __syncthreads();
+    const int32_t nchunk = (N + kPickSlots - 1) / kPickSlots;
+    uint32_t* srt = sorted + (size_t)b * nchunk * kPickSlots;
+    uint32_t* be = bin_end + (size_t)b * nchunk * kSelBins;
+    // an unpicked CAS voxel (key ~0) is never chosen and is not counted: its
+    // top half 2^32-1 is no picked key's
+    auto counted = [&](uint32_t top) { return key_mode == 0 || top != 0xFFFFFFFFu; };
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
     const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
-    const int lane = lane_id();
-    const int32_t s0 = (int32_t)blockIdx.x * kScanThreads * kSelItems;
-    uint64_t k[kSelItems];
+    for (int32_t c = blockIdx.x; c < nchunk; c += nblk) {
+        for (int i = tid; i < kSelBins; i += kPickThreads) lh[i] = 0;
+        __syncthreads();
+        uint32_t top[kPickItems];
+        bool cnt_it[kPickItems];
 #pragma unroll
-    for (int u = 0; u < kSelItems; ++u) {
-        const int32_t s = s0 + u * kScanThreads + (int32_t)threadIdx.x;
-        k[u] = s < nv ? select_key(key_mode, hb, s, pick) : ~0ull;
-    }
-#pragma unroll
-    for (int u = 0; u < kSelItems; ++u) {
-        const int32_t s = s0 + u * kScanThreads + (int32_t)threadIdx.x;
-        // an unpicked CAS voxel (key ~0) is never chosen: it is not counted
-        const bool act = s < nv && (k[u] & st.mask) == st.prefix && (key_mode == 0 || k[u] != ~0ull);
-        const uint32_t d = (uint32_t)(k[u] >> lo) & dmask;
-        // one LDS atomic per distinct digit of the wave for the first few
-        // digits (pick keys share their leading digits), then one per lane
-        uint64_t am = __ballot(act);
-        for (int r = 0; r < 4 && am; ++r) {
-            const int leader = __ffsll((unsigned long long)am) - 1;
-            const uint32_t d0 = (uint32_t)__shfl((int)d, leader, kWave);
-            const uint64_t same = __ballot(act && d == d0) & am;
-            if (lane == leader) atomicAdd(&lh[d0], (uint32_t)__popcll(same));
-            am &= ~same;
+        for (int u = 0; u < kPickItems; ++u) {
+            const int32_t sl = c * kPickSlots + u * kPickThreads + tid;
+            top[u] = sl < nv ? (uint32_t)(select_key(key_mode, hb, sl, pick) >> 32) : 0u;
+            cnt_it[u] = sl < nv && counted(top[u]);
+            if (cnt_it[u]) atomicAdd(&lh[top[u] >> 21], 1u);
         }
-        if ((am >> lane) & 1ull) atomicAdd(&lh[d], 1u);
+        __syncthreads();
+        // the cloud's histogram, and this chunk's bins: ends in memory,
+        // starts as cursors in LDS
+        const uint32_t h0 = lh[2 * tid], h1 = lh[2 * tid + 1];
+        if (h0) atomicAdd(&ghist[(size_t)b * kSelBins + 2 * tid], h0);
+        if (h1) atomicAdd(&ghist[(size_t)b * kSelBins + 2 * tid + 1], h1);
+        uint32_t tot;
+        const uint32_t ex = pick_excl_scan(h0 + h1, s_wave, &tot);
+        be[(size_t)c * kSelBins + 2 * tid] = ex + h0;
+        be[(size_t)c * kSelBins + 2 * tid + 1] = ex + h0 + h1;
+        lh[2 * tid] = ex;
+        lh[2 * tid + 1] = ex + h0;
+        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kPickItems; ++u)
+            if (cnt_it[u]) sk[atomicAdd(&lh[top[u] >> 21], 1u)] = top[u];
+        __syncthreads();
+        for (uint32_t i = tid; i < tot; i += kPickThreads) srt[(size_t)c * kPickSlots + i] = sk[i];
+        __syncthreads();
+    }
+    // publish, then the last block of the cloud takes over. The barrier
+    // orders every wave's stores before thread 0's agent-scope fence (one
+    // L2 write-back per block, not per wave); the last block's fence, again
+    // by one thread before a barrier, makes the other blocks' stores visible
+    // to all its waves (they share the CU's caches)
+    __syncthreads();
+    if (tid == 0) {
+        __threadfence();
+        s_last = atomicAdd(&gcnt[b], 1u) == (uint32_t)(nblk - 1) ? 1u : 0u;
+        if (s_last) __threadfence();
     }
     __syncthreads();
-    uint32_t* gh = hist + ((size_t)q * B + b) * kSelBins;
-    for (int i = threadIdx.x; i < (int)(dmask + 1); i += kScanThreads)
-        if (lh[i]) atomicAdd(&gh[i], lh[i]);
+    if (!s_last) return;
+    for (int i = tid; i < kSelBins; i += kPickThreads)
+        lh[i] = __hip_atomic_load(&ghist[(size_t)b * kSelBins + i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    uint32_t f[3] = {kSelBins - 1, 0u, 0u};
+    pick_find(lh, kSelBins, m, s_find, s_wave, f);
+    const uint32_t dig = f[0];
+    uint32_t prefix = dig << 21, pmask = 0xFFE00000u;
+    uint32_t need = m - f[1];
+    const uint32_t cnt = f[2];
+    uint64_t bound = 0;
+    bool done = false;
+    if (cnt == need) {  // every key under this prefix is among the m smallest
+        bound = (uint64_t)(prefix | ~pmask) + 1;
+        need = 0;
+        done = true;
+    }
+    // Calls visit(i, key) for the keys of bin `dig` of every chunk, i
+    // counting them from 0: chunks 1024 at a time, their bins' counts
+    // scanned, each key found by a binary search over the scan.
+    auto gather = [&](auto visit) {
+        uint32_t base = 0;
+        for (int32_t c0 = 0; c0 < nchunk; c0 += kPickThreads) {
+            const int32_t c = c0 + tid;
+            uint32_t st = 0, n = 0;
+            if (c < nchunk) {
+                const uint32_t* e = be + (size_t)c * kSelBins;
+                st = dig ? e[dig - 1] : 0u;
+                n = e[dig] - st;
+            }
+            uint32_t tot;
+            const uint32_t pre = pick_excl_scan(n, s_wave, &tot);
+            sp[tid] = pre;
+            ss[tid] = (uint32_t)c * kPickSlots + st;
+            __syncthreads();
+            const int32_t nc = nchunk - c0 < kPickThreads ? nchunk - c0 : kPickThreads;
+            for (uint32_t i = tid; i < tot; i += kPickThreads) {
+                int32_t lo = 0, hi = nc - 1;
+                while (lo < hi) {
+                    const int32_t mid = (lo + hi + 1) >> 1;
+                    if (sp[mid] <= i) lo = mid; else hi = mid - 1;
+                }
+                visit(base + i, srt[ss[lo] + (i - sp[lo])]);
+            }
+            base += tot;
+            __syncthreads();
+        }
+    };
+    // the keys of the digit into LDS when they fit, in chunk order (with at
+    // most 1024 chunks the scan of the last group stays in LDS too)
+    const bool in_lds = cnt <= (uint32_t)kCandCap;
+    if (in_lds) {
+        gather([&](uint32_t i, uint32_t key) {
+            if (i < (uint32_t)kCandCap) sk[i] = key;  // exactly cnt of them
+        });
+        __syncthreads();
+    }
+    // digits of bits 10..20 and 0..9 among the keys under the prefix
+    for (int q = 0; q < 2 && !done; ++q) {
+        const int shift = q == 0 ? 10 : 0, width = q == 0 ? 11 : 10;
+        const uint32_t dmask = (1u << width) - 1;
+        for (int i = tid; i < kSelBins; i += kPickThreads) lh[i] = 0;
+        __syncthreads();
+        auto count = [&](uint32_t, uint32_t key) {
+            if ((key & pmask) == prefix) atomicAdd(&lh[(key >> shift) & dmask], 1u);
+        };
+        if (in_lds) {
+            for (uint32_t i = tid; i < cnt; i += kPickThreads) count(i, sk[i]);
+        } else {  // too many for LDS: read them again
+            gather(count);
+        }
+        __syncthreads();
+        f[0] = dmask;
+        f[1] = 0;
+        f[2] = 0;
+        pick_find(lh, 1 << width, need, s_find, s_wave, f);
+        prefix |= f[0] << shift;
+        pmask |= dmask << shift;
+        need -= f[1];
+        if (f[2] == need) {
+            bound = (uint64_t)(prefix | ~pmask) + 1;
+            need = 0;
+            done = true;
+        }
+    }
+    if (!done) bound = prefix;  // every bit fixed: ties at the bound go by slot
+    // Per chunk, in chunk order: the keys below the bound (its bins below
+    // `dig`, and those of bin `dig` below the bound) and the ties at it, of
+    // which the chunk takes what is left of `need`; the chunk's first output
+    // position is the number chosen in the chunks before it.
+    uint32_t run_eq = 0, run_base = 0;
+    for (int32_t c0 = 0; c0 < nchunk; c0 += kPickThreads) {
+        const int32_t c = c0 + tid;
+        uint32_t lt = 0, eq = 0;
+        if (in_lds && nchunk <= kPickThreads) {  // the chunk's start and keys from the gather, in LDS
+            if (c < nchunk) {
+                const uint32_t p0 = sp[c], p1 = c + 1 < nchunk ? sp[c + 1] : cnt;
+                lt = ss[c] - (uint32_t)c * kPickSlots;
+                for (uint32_t i = p0; i < p1; ++i) {
+                    const uint32_t top = sk[i];
+                    lt += (uint64_t)top < bound ? 1u : 0u;
+                    eq += (uint64_t)top == bound ? 1u : 0u;
+                }
+            }
+        } else if (c < nchunk) {
+            const uint32_t* e = be + (size_t)c * kSelBins;
+            const uint32_t st = dig ? e[dig - 1] : 0u, en = e[dig];
+            lt = st;
+            for (uint32_t i = st; i < en; ++i) {
+                const uint32_t top = srt[(size_t)c * kPickSlots + i];
+                lt += (uint64_t)top < bound ? 1u : 0u;
+                eq += (uint64_t)top == bound ? 1u : 0u;
+            }
+        }
+        uint32_t tot_eq, tot_ch;
+        const uint32_t eq_pre = run_eq + pick_excl_scan(eq, s_wave, &tot_eq);
+        const uint32_t take = need > eq_pre ? (need - eq_pre < eq ? need - eq_pre : eq) : 0u;
+        const uint32_t base = run_base + pick_excl_scan(lt + take, s_wave, &tot_ch);
+        if (c < nchunk) {
+            sel_base[(size_t)b * nchunk + c] = base;
+            sel_take[(size_t)b * nchunk + c] = take;
+        }
+        run_eq += tot_eq;
+        run_base += tot_ch;
+    }
+    if (tid == 0) {
+        thr[b] = sel_pack(bound, need);
+        m_valid[b] = (int32_t)m;
+        gcnt[b] = 0;
+    }
+    for (int i = tid; i < kSelBins; i += kPickThreads) ghist[(size_t)b * kSelBins + i] = 0;
 }
 
-// The bound and tie count of each cloud from its three histograms.
-__global__ __launch_bounds__(kScanThreads) void k_sel_mb_final(int32_t B, const int32_t* __restrict__ nvox,
-                                                               int32_t M, const uint32_t* __restrict__ hist,
-                                                               uint64_t* __restrict__ thr) {
-    const int32_t b = blockIdx.x;
+// The chosen slots of one chunk (block (c, b)), in slot order: a slot is
+// chosen when its key's top half is below the bound, or equal to it and
+// among the first `take` such slots of the chunk. Its output position is the
+// chunk's base plus the chosen slots before it in the chunk (one block scan
+// of the packed counts below / at the bound); it writes its linear id there
+// and at every m-th entry after it (the cyclic padding).
+__global__ __launch_bounds__(kPickThreads) void k_sel_emit_chunks(
+    int32_t N, const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin, int32_t M, int key_mode,
+    uint64_t seed, const uint64_t* __restrict__ cas_pick, const uint64_t* __restrict__ thr,
+    const uint32_t* __restrict__ sel_base, const uint32_t* __restrict__ sel_take, int32_t* __restrict__ center_lin) {
+    __shared__ uint32_t s_wave[kPickThreads / kWave];
+    const int32_t c = blockIdx.x, b = blockIdx.y, nchunk = gridDim.x;
     const int32_t nv = nvox[b];
-    const SelState st = sel_derive(hist, B, b, (uint32_t)(M < nv ? M : nv), kSelPasses);
-    if (threadIdx.x == 0) thr[b] = sel_pack(st.bound, st.need);
+    const int32_t m = M < nv ? M : nv;
+    const uint64_t bound = thr[b] & ((1ull << 33) - 1);
+    const uint32_t base = sel_base[(size_t)b * nchunk + c], take = sel_take[(size_t)b * nchunk + c];
+    const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
+    const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
+    const int32_t s0 = c * kPickSlots + (int32_t)threadIdx.x * kPickItems;
+    bool lt[kPickItems], eq[kPickItems];
+    uint32_t packed = 0;
+#pragma unroll
+    for (int u = 0; u < kPickItems; ++u) {
+        const int32_t sl = s0 + u;
+        const uint64_t top = sl < nv ? select_key(key_mode, hb, sl, pick) >> 32 : 0xFFFFFFFFull;
+        const bool counted = sl < nv && (key_mode == 0 || top != 0xFFFFFFFFull);
+        lt[u] = counted && top < bound;
+        eq[u] = counted && top == bound;
+        packed += lt[u] ? (1u << 16) : (eq[u] ? 1u : 0u);
+    }
+    uint32_t tot;
+    uint32_t run = pick_excl_scan(packed, s_wave, &tot);
+    int32_t* out = center_lin + (size_t)b * M;
+#pragma unroll
+    for (int u = 0; u < kPickItems; ++u) {
+        const uint32_t nlt = run >> 16, neq = run & 0xFFFFu;
+        if (lt[u] || (eq[u] && neq < take)) {
+            const uint32_t pos = base + nlt + (neq < take ? neq : take);
+            if (pos < (uint32_t)m) {
+                const int32_t l = (int32_t)vox_lin[(size_t)b * N + s0 + u];
+                for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
+            }
+        }
+        run += lt[u] ? (1u << 16) : (eq[u] ? 1u : 0u);
+    }
 }
 
 // Slot of bit j of a row, or `self` when bit j is clear (a harmless address).
@@ -435,17 +621,9 @@ struct CasState {
     uint32_t* dirty;    // round whose scoring must recompute the voxel's key (row-scan rounds)
 };
 
-// The key of a voxel of score `score` and linear id `lin`: (score, -lin) as
-// one unsigned 64-bit word, the score offset by 2^31.
-__device__ __forceinline__ uint64_t cas_key(int64_t score, uint32_t lin) {
-    return ((uint64_t)(score + 2147483648ll) << 32) | (uint64_t)(0xFFFFFFFFu - lin);
-}
-
-// Clears the state and the control block. With lists (nbr != null) also sets
-// every occupied voxel's key for round 0: nothing is covered yet, so every
-// voxel within r is uncovered and the score is 2^16 * lambda * n_r.
-__global__ void k_cas_init(int32_t BN, int32_t B, int32_t N, CasState st, CasPtrs ctl, const uint32_t* __restrict__ nbr,
-                           const uint32_t* __restrict__ vox_lin, const int32_t* __restrict__ nvox, int64_t unit) {
+// Clears the state and the control block. (With lists, the neighbour-list
+// kernel has set every occupied voxel's key for round 0.)
+__global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
     int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < BN) {
         st.cover[gid] = 0;
@@ -453,8 +631,6 @@ __global__ void k_cas_init(int32_t BN, int32_t B, int32_t N, CasState st, CasPtr
         st.round[gid] = 0;
         st.blocker[gid] = -1;
         st.dirty[gid] = 0;
-        if (nbr && gid - (gid / N) * N < nvox[gid / N])
-            st.key[gid] = cas_key(unit * (int64_t)nbr[(size_t)gid * kNbr32Stride], vox_lin[gid]);
     }
     if (gid < kCasBufs * B * kCasParts) {
         ctl.gpart[gid] = 0;
@@ -788,24 +964,28 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
             above = pk0 > G ? 1u : 0u;
         } else {
             k = my0;
-            // the list's header and first entries are loaded with the blocker's state
-            const uint4 h = el[0];
-            uint4 q[4];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) q[j] = el[1 + j];
             bool beaten = false;
             if (bl0 >= 0) {
                 const uint64_t kb = ky[bl0];
                 const uint32_t rb = rd[bl0];
                 beaten = kb > my0 && (rb == 0 || rb == cur);
             }
-            n2 = h.y;
-            n_r = h.x;
-            if (!beaten) found = beats(q, 0, n2, (uint32_t)s, my0, cur, ky, rd);
-            if (found == -1) {
-                uint4* se = reinterpret_cast<uint4*>(s_ent[threadIdx.x]);
+            // the list (which does not fit in the caches) is read only by a
+            // voxel its blocker no longer beats: after the first rounds most
+            // voxels stay blocked
+            if (!beaten) {
+                const uint4 h = el[0];
+                uint4 q[4];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) se[j] = q[j];
+                for (int j = 0; j < 4; ++j) q[j] = el[1 + j];
+                n2 = h.y;
+                n_r = h.x;
+                found = beats(q, 0, n2, (uint32_t)s, my0, cur, ky, rd);
+                if (found == -1) {
+                    uint4* se = reinterpret_cast<uint4*>(s_ent[threadIdx.x]);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) se[j] = q[j];
+                }
             }
         }
     }
@@ -993,15 +1173,17 @@ hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uin
     uint64_t* desc_s = at<uint64_t>(ws, L.desc_s);
     int* status = at<int>(ws, L.status);
     if (L.N >= kSelManyBlockMin) {
-        // large clouds: one histogram kernel per 11-bit digit over many blocks
-        uint32_t* hist = at<uint32_t>(ws, L.sel_hist);
-        const size_t nclear = (size_t)kSelPasses * L.B * kSelBins;
-        k_sel_mb_clear<<<(unsigned)((nclear + 255) / 256), 256, 0, s>>>(L.B, L.tiles_s, hist, desc_s, status, M, nvox,
-                                                                        m_valid);
-        const dim3 grid((unsigned)((L.N + kScanThreads * kSelItems - 1) / (kScanThreads * kSelItems)), (unsigned)L.B);
-        for (int q = 0; q < kSelPasses; ++q)
-            k_sel_mb_hist<<<grid, kScanThreads, 0, s>>>(q, L.B, L.N, nvox, M, key_mode, seed, pick, hist);
-        k_sel_mb_final<<<L.B, kScanThreads, 0, s>>>(L.B, nvox, M, hist, thr);
+        // large clouds: the keys and the bound over many blocks per cloud
+        const int64_t nchunk = (L.N + kPickSlots - 1) / kPickSlots;
+        const dim3 grid((unsigned)(nchunk < kPickBlocks ? nchunk : kPickBlocks), (unsigned)L.B);
+        uint32_t* base = at<uint32_t>(ws, L.sel_base);
+        uint32_t* take = at<uint32_t>(ws, L.sel_take);
+        k_sel_pick<<<grid, kPickThreads, 0, s>>>(L.N, nvox, M, key_mode, seed, pick, at<uint32_t>(ws, L.sel_keys),
+                                                 at<uint32_t>(ws, L.sel_bins), at<uint32_t>(ws, L.sel_ghist),
+                                                 at<uint32_t>(ws, L.sel_cnt), thr, m_valid, base, take);
+        k_sel_emit_chunks<<<dim3((unsigned)nchunk, (unsigned)L.B), kPickThreads, 0, s>>>(
+            L.N, nvox, at<uint32_t>(ws, L.vox_lin), M, key_mode, seed, pick, thr, base, take, center_lin);
+        return hipGetLastError();
     } else {
         k_sel_threshold<<<L.B, kSelThreads, 0, s>>>(L.N, L.tiles_s, nvox, M, key_mode, seed, pick, thr, m_valid,
                                                     desc_s, status);
@@ -1061,10 +1243,12 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     // neighbour lists replace the row scans where the layout holds them, and
     // then a round is one kernel that keeps the keys exact by itself
     const bool lists = L.has_nbr32 && rad == 1;
-    if (lists && (e = launch_cas_nbr(L, d, ws, s)) != hipSuccess) return e;
+    // with lists, the list kernel also sets the round-0 keys: nothing is
+    // covered yet, so the score is 2^16 * lambda * (occupied voxels within r)
+    if (lists && (e = launch_cas_nbr(L, d, ws, s, st.key, 65536 * lam)) != hipSuccess) return e;
     const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
     const int32_t init_n = std::max(BN, B * kCasParts * kCasUBins);
-    k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, N, st, ctl, nbr, vox_lin, nvox, 65536 * lam);
+    k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, st, ctl);
     if ((e = hipGetLastError()) != hipSuccess) return e;
 
     int64_t R = 0;

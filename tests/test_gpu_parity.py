@@ -232,6 +232,41 @@ def test_cas_swap_at_bench_size(beta_q16):
              where=f"cas_swap bench size beta={beta_q16}")
 
 
+@pytest.mark.parametrize("r,beta_q16,M", [(1, 65536 // 4, 2048), (2, 0, 2048), (2, 0, 20000),
+                                           (2, 3 * 65536 // 4, 2048)])
+def test_cas_on_large_clouds_with_penalty_or_radius_two(r, beta_q16, M):
+    """CAS on 81920-point scenes where neither the single workgroup nor the
+    list rounds apply (beta > 0, or r = 2): the row-scan rounds and the
+    many-block selection of the pick keys. With beta = 0 the pick keys take
+    few values, so the selection's threshold digit holds thousands of ties
+    (more than its LDS holds at M = 20000: the keys are read again)."""
+    w = W.get_workload("bigroom/cas-knn")
+    L = w.layers[0]
+    spec = _spec(L.grid.origin, L.grid.voxel_size, L.grid.dims, L.grid.n_v, r)
+    print(f"[parity] cas N=81920 r={r} beta={beta_q16} M={M}", flush=True)
+    run_both(w.points(B=2), spec, M, 16, "cas", "cube", 5, beta_q16=beta_q16, where=f"r={r} beta={beta_q16} M={M}")
+
+
+@pytest.mark.parametrize("M", [1, 2, 4095, 4096, 4097, 30000, 60000])
+def test_rvs_many_block_selection_bounds(M):
+    """The many-block RVS selection (clouds of 16384 points or more) at every
+    kind of bound: one center, the block size and its neighbours, most of
+    the occupied voxels, and more centers than occupied voxels."""
+    w = W.get_workload("bigroom/rvs-cube")
+    L = w.layers[0]
+    run_both(w.points(B=2), L.grid, M, 8, "rvs", "cube", 11 + M, where=f"M={M}")
+
+
+def test_rvs_many_block_selection_dense_cloud():
+    """A dense cloud (about 140K of 262K voxels occupied): M from one center
+    to beyond the occupied voxels."""
+    rng = np.random.default_rng(31)
+    P = rng.random((1, 200000, 3), dtype=np.float32)
+    spec = _spec((0, 0, 0), (1 / 64,) * 3, (64, 64, 64), 4)
+    for M in (1, 100000, 150000, 262143, 262144, 262145):
+        run_both(P, spec, M, 4, "rvs", "cube", M, where=f"dense M={M}")
+
+
 def test_back_to_back_cas_calls():
     """Two CAS calls in a row from one thread, each on its own stream and
     workspace, without waiting in between: the first (81920 points, M = 8192)
