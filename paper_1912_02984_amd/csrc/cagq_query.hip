@@ -226,7 +226,10 @@ __device__ __forceinline__ void gmerge_low2(uint64_t& bk, uint32_t& bp, uint64_t
 
 // NR result registers per lane: NR = 1 keeps ranks 0..G-1 (K <= G), NR = 2
 // (G = 64) also ranks 64..127 in a second register (64 < K <= 128).
-template <int MODE, int G, int RAD, bool UP, int NR>
+// DEFER: the second pass of a query whose 16-lane kernel left its largest
+// contexts (n_valid marked -1) to one wave each (G = 64); every other
+// center's wave returns at once. D: chunks whose points are loaded ahead.
+template <int MODE, int G, int RAD, bool UP, int NR, bool DEFER = false, int D = 1>
 __global__ __launch_bounds__(kQueryThreads) void k_query(
     const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
     int64_t W, const uint64_t* __restrict__ bitmap, const uint32_t* __restrict__ word_rank,
@@ -248,6 +251,10 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     // every group runs to the end (the group- and wave-wide steps need all
     // lanes); a group past the end works on center 0 and writes nothing
     const bool live = cid < total;
+    if constexpr (DEFER) {
+        static_assert(G == kWave, "one center per wave");
+        if (!live || n_valid[cid] != -1) return;  // the whole wave: no block-wide step follows
+    }
     const int32_t c_id = live ? cid : 0;
     const int32_t b = (int32_t)udiv((uint32_t)c_id, g.mm);
     const size_t cK = (size_t)c_id * K;
@@ -397,19 +404,45 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     while (top < cmax && top < (uint32_t)G) top <<= 1;
     float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f);
     uint32_t w0 = 1u;
+    // position in the copy of context entry e: the compacted voxel holding it
+    auto locate = [&](uint32_t e) {
+        uint32_t lo = 0, hi = nocc - 1;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi + 1) >> 1;
+            if (s_pre[mid] <= e) lo = mid; else hi = mid - 1;
+        }
+        return s_st[lo] + (e - s_pre[lo]);
+    };
+    // each chunk's points are loaded D chunks ahead, so that a long
+    // context's loads overlap the sort and merge of the chunks before
+    uint32_t pq[D];
+    float4 vq[D];
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+        const uint32_t e = (uint32_t)(d * G + lg);
+        pq[d] = 0;
+        vq[d] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (e < cs) {
+            pq[d] = locate(e);
+            vq[d] = p4[pq[d]];
+        }
+    }
+    uint64_t kth = ~0ull;
     for (uint32_t e0 = 0; e0 < cmax; e0 += G) {
         const uint32_t e = e0 + lg;
         uint64_t key = ~0ull;
-        uint32_t pos = 0;
+        uint32_t pos = pq[0];
+        const float4 v = vq[0];
+#pragma unroll
+        for (int d = 0; d + 1 < D; ++d) {
+            pq[d] = pq[d + 1];
+            vq[d] = vq[d + 1];
+        }
+        if (e + D * G < cs) {
+            pq[D - 1] = locate(e + D * G);
+            vq[D - 1] = p4[pq[D - 1]];
+        }
         if (e < cs) {
-            // the compacted voxel holding context entry e
-            uint32_t lo = 0, hi = nocc - 1;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi + 1) >> 1;
-                if (s_pre[mid] <= e) lo = mid; else hi = mid - 1;
-            }
-            pos = s_st[lo] + (e - s_pre[lo]);
-            const float4 v = p4[pos];
             const uint32_t i = __float_as_uint(v.w);
             if (one) {
                 v0 = v;
@@ -429,6 +462,15 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
                 else
                     key = ((uint64_t)__float_as_uint(d2) << 32) | i;
             }
+        } else {
+            pos = 0;
+        }
+        // a key above the K-th best so far can never be kept (keys are
+        // distinct); a chunk left without keys anywhere in the wave changes
+        // nothing and is not sorted
+        if (e0 != 0) {
+            key = key < kth ? key : ~0ull;
+            if (!__ballot(key != ~0ull)) continue;
         }
         gsort<G>(key, pos, lg, top);
         if (e0 == 0) {
@@ -439,6 +481,8 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         } else {
             gmerge_low2<G>(bk, bp, b1k, b1p, key, pos, lg);
         }
+        // the K-th best key so far (a filler, ~0, while fewer than K are held)
+        kth = NR == 1 ? gshfl64<G>(bk, K - 1) : gshfl64<G>(b1k, K - 1 - G);
     }
 
     // 4. outputs (an empty context gives n = 0 and zeros): node slot k is
@@ -600,7 +644,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
     const float* __restrict__ center_pts, uint64_t seed, int32_t* __restrict__ node_idx,
     float* __restrict__ node_xyz, int32_t* __restrict__ n_valid, float* __restrict__ center_xyz,
     uint32_t* __restrict__ center_w, int32_t* __restrict__ ctx_count, int32_t* __restrict__ lin_out,
-    int* __restrict__ status) {
+    int* __restrict__ status, uint32_t defer) {
     constexpr int G = 16, GPB = kQueryThreads / G;
     constexpr int S = 2 * RAD + 1, NR = S * S;
     __shared__ uint32_t s_st[GPB][NR];
@@ -608,6 +652,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
     __shared__ uint32_t s_c[GPB], s_lin[GPB], s_b[GPB];
     __shared__ float s_q[GPB][3];
     __shared__ uint32_t s_src[GPB];
+    __shared__ uint32_t s_def[GPB];
     const int lane = lane_id();
     const int lg = lane & (G - 1);
     const int gb = threadIdx.x / G;
@@ -685,9 +730,13 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
             if (live && !occupied && lg == 0) raise_error(status, CAGQ_ERR_CENTER_NOT_OCCUPIED);
             if (!occupied) c = 0;
         }
+        // a context above `defer` points is left to the one-wave-per-center
+        // pass: here it counts as empty, and its n_valid is marked -1
+        const bool def = live && c > defer;
         if (lg == 0) {
             s_pre[gb][NR] = c;
-            s_c[gb] = live ? c : 0u;
+            s_def[gb] = def ? 1u : 0u;
+            s_c[gb] = live && !def ? c : 0u;
             s_lin[gb] = lin;
             s_b[gb] = (uint32_t)b;
             s_q[gb][0] = qx, s_q[gb][1] = qy, s_q[gb][2] = qz;
@@ -709,7 +758,8 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
     __syncthreads();
     const int src = (int)s_src[gb];
     const int32_t cid = (int32_t)blk * GPB + src;
-    const bool live = cid < total;
+    if (s_def[src] && lg == 0) n_valid[cid] = -1;
+    const bool live = cid < total && !s_def[src];
     const uint32_t c = s_c[src];
     const uint32_t lin = s_lin[src];
     const int32_t b = (int32_t)s_b[src];
@@ -736,19 +786,35 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
     uint32_t b0p = 0, b1p = 0;
     float4 v0 = make_float4(0.f, 0.f, 0.f, 0.f);
     uint32_t w0 = 1u;
+    // position in the copy of context entry e: the last row range starting
+    // at or before it
+    auto locate = [&](uint32_t e) {
+        uint32_t lo = 0, hi = NR - 1;
+        while (lo < hi) {
+            const uint32_t mid = (lo + hi + 1) >> 1;
+            if (s_pr[mid] <= e) lo = mid; else hi = mid - 1;
+        }
+        return s_sr[lo] + (e - s_pr[lo]);
+    };
+    // each chunk's points are loaded one chunk ahead, so that a long
+    // context's loads overlap the previous chunk's sort and merge
+    uint32_t pos_n = 0;
+    float4 v_n = make_float4(0.f, 0.f, 0.f, 0.f);
+    uint64_t kth = ~0ull;
+    if ((uint32_t)lg < c) {
+        pos_n = locate((uint32_t)lg);
+        v_n = p4[pos_n];
+    }
     for (uint32_t e0 = 0; e0 < cmax; e0 += G) {
         const uint32_t e = e0 + lg;
         uint64_t key = ~0ull;
-        uint32_t pos = 0;
+        uint32_t pos = pos_n;
+        const float4 v = v_n;
+        if (e + G < c) {
+            pos_n = locate(e + G);
+            v_n = p4[pos_n];
+        }
         if (e < c) {
-            // the row holding entry e: the last range starting at or before it
-            uint32_t lo = 0, hi = NR - 1;
-            while (lo < hi) {
-                const uint32_t mid = (lo + hi + 1) >> 1;
-                if (s_pr[mid] <= e) lo = mid; else hi = mid - 1;
-            }
-            pos = s_sr[lo] + (e - s_pr[lo]);
-            const float4 v = p4[pos];
             const uint32_t i = __float_as_uint(v.w);
             if (one) {
                 v0 = v;
@@ -764,6 +830,15 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
                 const float d2 = sxy + zz;
                 key = ((uint64_t)__float_as_uint(d2) << 32) | i;
             }
+        } else {
+            pos = 0;
+        }
+        // a key above the K-th best so far can never be kept (keys are
+        // distinct); a chunk left without keys anywhere in the wave changes
+        // nothing and is not sorted
+        if (e0 != 0) {
+            key = key < kth ? key : ~0ull;
+            if (!__ballot(key != ~0ull)) continue;
         }
         gsort<G>(key, pos, lg, e0 == 0 ? top : (uint32_t)G);
         if (e0 == 0) {
@@ -789,6 +864,8 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
             clean16(b0k, b0p, lg);
             clean16(b1k, b1p, lg);
         }
+        // the K-th best key so far, rank K-1 in b1 (~0 while fewer than K are held)
+        kth = gshfl64<G>(b1k, K - 1 - G);
     }
 
     // 4. outputs (an empty context gives n = 0)
@@ -910,7 +987,7 @@ struct QueryIO {
     int32_t* lin_out;
 };
 
-template <int MODE, int G, int RAD, bool UP, int NR>
+template <int MODE, int G, int RAD, bool UP, int NR, bool DEFER = false, int D = 1>
 void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int32_t M, int32_t K, uint64_t seed,
               hipStream_t s) {
     constexpr int GPB = kQueryThreads / G;
@@ -918,7 +995,7 @@ void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int3
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
     constexpr int side = 2 * RAD + 1;
     const size_t lds = (size_t)GPB * (2 * side * side * side + 1) * sizeof(uint32_t);
-    k_query<MODE, G, RAD, UP, NR><<<blocks, kQueryThreads, lds, s>>>(
+    k_query<MODE, G, RAD, UP, NR, DEFER, D><<<blocks, kQueryThreads, lds, s>>>(
         io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
         io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status));
@@ -935,29 +1012,39 @@ void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const Quer
         launch_g<MODE, G, 3, UP, NR>(L, g, ws, io, M, K, seed, s);
 }
 
+// Contexts of more points than this go to one wave each when the grid can
+// hold contexts of more than kBigGrid points ((2r+1)^3 n_v): a 16-lane group
+// works through a long context chunk after chunk, one load latency each.
+constexpr uint32_t kDefer = 256;
+constexpr int64_t kBigGrid = 1024;
+
 template <int MODE, int RAD, bool UP>
 void launch_r2(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int32_t M, int32_t K, uint64_t seed,
-               hipStream_t s) {
+               int32_t n_v, hipStream_t s) {
     constexpr int GPB = kQueryThreads / 16;
     const int32_t total = L.B * M;
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
+    constexpr int64_t side = 2 * RAD + 1;
+    const bool big = side * side * side * (int64_t)n_v > kBigGrid;
     k_query_r2<MODE, RAD, UP><<<blocks, kQueryThreads, 0, s>>>(
         io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
-        io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status));
+        io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status),
+        big ? kDefer : 0xFFFFFFFFu);
+    if (big) launch_g<MODE, 64, RAD, UP, 1, true, 4>(L, g, ws, io, M, K, seed, s);
 }
 
 template <int MODE, bool UP>
-void launch_mode(const Layout& L, const QGrid& g, int32_t rad, void* ws, const QueryIO& io, int32_t M, int32_t K,
-                 uint64_t seed, hipStream_t s) {
+void launch_mode(const Layout& L, const QGrid& g, int32_t rad, int32_t n_v, void* ws, const QueryIO& io, int32_t M,
+                 int32_t K, uint64_t seed, hipStream_t s) {
     if (MODE != kRing && K > 16 && K <= 32) {
         // 16 lanes and two result registers per center
         if (rad == 1)
-            launch_r2<MODE, 1, UP>(L, g, ws, io, M, K, seed, s);
+            launch_r2<MODE, 1, UP>(L, g, ws, io, M, K, seed, n_v, s);
         else if (rad == 2)
-            launch_r2<MODE, 2, UP>(L, g, ws, io, M, K, seed, s);
+            launch_r2<MODE, 2, UP>(L, g, ws, io, M, K, seed, n_v, s);
         else
-            launch_r2<MODE, 3, UP>(L, g, ws, io, M, K, seed, s);
+            launch_r2<MODE, 3, UP>(L, g, ws, io, M, K, seed, n_v, s);
         return;
     }
     if (K <= 16)
@@ -995,11 +1082,11 @@ hipError_t launch_query(const Layout& L, const cagq_grid_desc& d, const float* p
     const QueryIO io{weights, center_lin, nullptr, node_idx, node_xyz, n_valid, center_xyz, center_w, ctx_count,
                      nullptr};
     if (mode == CAGQ_QUERY_CUBE)
-        launch_mode<CAGQ_QUERY_CUBE, false>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<CAGQ_QUERY_CUBE, false>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     else if (mode == CAGQ_QUERY_KNN)
-        launch_mode<CAGQ_QUERY_KNN, false>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<CAGQ_QUERY_KNN, false>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     else
-        launch_mode<kRing, false>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<kRing, false>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     return hipGetLastError();
 }
 
@@ -1010,11 +1097,11 @@ hipError_t launch_query_points(const Layout& L, const cagq_grid_desc& d, void* w
     const QueryIO io{nullptr, nullptr, centers, node_idx, node_xyz, n_valid, nullptr, nullptr, ctx_count,
                      center_lin};
     if (mode == CAGQ_QUERY_CUBE)
-        launch_mode<CAGQ_QUERY_CUBE, true>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<CAGQ_QUERY_CUBE, true>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     else if (mode == CAGQ_QUERY_KNN)
-        launch_mode<CAGQ_QUERY_KNN, true>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<CAGQ_QUERY_KNN, true>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     else
-        launch_mode<kRing, true>(L, g, d.radius, ws, io, M, K, seed, s);
+        launch_mode<kRing, true>(L, g, d.radius, d.n_v, ws, io, M, K, seed, s);
     return hipGetLastError();
 }
 
