@@ -59,7 +59,7 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->N = N;
     L->V = (int64_t)d->dims[0] * d->dims[1] * d->dims[2];
     L->W = (L->V + 63) / 64;
-    L->tiles_w = (L->W + kScanTile - 1) / kScanTile;
+    L->tiles_w = (L->W + kRankTile - 1) / kRankTile;
     L->tiles_s = ((int64_t)N + kScanTile - 1) / kScanTile;
     L->big_cap = (int64_t)B * N / (kBigVoxel + 1) + 1;
     const size_t BN = (size_t)B * N;

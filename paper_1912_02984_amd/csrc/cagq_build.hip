@@ -100,11 +100,11 @@ __global__ __launch_bounds__(kScanThreads) void k_rank(
     const int64_t tile = (int64_t)(t % tiles_w);
     const uint4* bytes = reinterpret_cast<const uint4*>(bytemap + (size_t)b * W * 64);
     uint64_t* bm = bitmap + (size_t)b * W;
-    const int64_t w0 = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
-    uint64_t words[kScanItems];
+    const int64_t w0 = tile * kRankTile + (int64_t)threadIdx.x * kRankItems;
+    uint64_t words[kRankItems];
     uint32_t cnt = 0;
 #pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
+    for (int i = 0; i < kRankItems; ++i) {
         int64_t w = w0 + i;
         words[i] = w < W ? pack_bytes(bytes + (size_t)w * 4) : 0ull;
         if (w < W) bm[w] = words[i];
@@ -118,7 +118,7 @@ __global__ __launch_bounds__(kScanThreads) void k_rank(
     uint32_t* vl = vox_lin + (size_t)b * N;
     uint32_t* vc = vox_count + (size_t)b * N;
 #pragma unroll
-    for (int i = 0; i < kScanItems; ++i) {
+    for (int i = 0; i < kRankItems; ++i) {
         int64_t w = w0 + i;
         if (w >= W) break;
         wr[w] = r;
@@ -140,14 +140,32 @@ __global__ __launch_bounds__(256) void k_count(int32_t BN, int32_t N, int64_t W,
                                                const uint32_t* __restrict__ word_rank,
                                                uint32_t* __restrict__ pt_slot, uint32_t* __restrict__ pt_pos,
                                                uint32_t* __restrict__ vox_count) {
-    int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
-    if (gid >= BN) return;
-    int32_t b = gid / N;
-    uint32_t lin = pt_slot[gid];
-    uint32_t slot = (uint32_t)slot_of(bitmap + (size_t)b * W, word_rank + (size_t)b * W, lin);
-    uint32_t pos = atomicAdd(&vox_count[(size_t)b * N + slot], 1u);
+    const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    const bool active = gid < BN;  // a prefix of the wave
+    const int32_t b = active ? gid / N : 0;
+    const uint32_t lin = active ? pt_slot[gid] : 0u;
+    const uint32_t slot = active ? (uint32_t)slot_of(bitmap + (size_t)b * W, word_rank + (size_t)b * W, lin) : 0u;
+    // Adjacent lanes with the same voxel (runs of one voxel's points, as in
+    // a scan-ordered cloud) take their arrival positions with one atomic per
+    // run: the positions within a voxel are a permutation either way.
+    const size_t gs = (size_t)b * N + slot;
+    const int lane = lane_id();
+    const uint64_t prev = shfl_up64((uint64_t)gs, 1);
+    const bool head = active && (lane == 0 || prev != (uint64_t)gs);
+    const uint64_t heads = __ballot(head);
+    const uint32_t n_act = (uint32_t)__popcll(__ballot(active));
+    const uint64_t upto = lane == kWave - 1 ? ~0ull : ((2ull << lane) - 1);  // lanes <= this one
+    const int h = active ? 63 - __clzll(heads & upto) : lane;  // the head of this lane's run
+    uint32_t pos0 = 0;
+    if (head) {
+        const uint64_t next = heads & ~upto;
+        const uint32_t end = next ? (uint32_t)(__ffsll((unsigned long long)next) - 1) : n_act;
+        pos0 = atomicAdd(&vox_count[gs], end - (uint32_t)lane);
+    }
+    pos0 = (uint32_t)__shfl((int)pos0, h, kWave);
+    if (!active) return;
     pt_slot[gid] = slot;
-    pt_pos[gid] = pos;
+    pt_pos[gid] = pos0 + (uint32_t)(lane - h);
 }
 
 // Offsets: vox_off = exclusive prefix of min(count, n_v), full_off = exclusive
@@ -258,11 +276,18 @@ __global__ __launch_bounds__(256) void k_finalize(
         uint32_t s = g - (uint32_t)b * N;
         uint32_t cnt = vox_count[g];
         const uint32_t* bk = bucket + (size_t)b * N + full_off[(size_t)b * (N + 1) + s];
-        uint64_t best = ~0ull;
+        uint64_t best = ~0ull, kth = ~0ull;
+        uint64_t k_n = (uint32_t)lane < cnt ? (uint64_t)bk[lane] : ~0ull;  // loaded a chunk ahead
         for (uint32_t c0 = 0; c0 < cnt; c0 += kWave) {
-            uint64_t k = (c0 + lane < cnt) ? (uint64_t)bk[c0 + lane] : ~0ull;
+            uint64_t k = k_n;
+            k_n = (c0 + kWave + lane < cnt) ? (uint64_t)bk[c0 + kWave + lane] : ~0ull;
+            // an index above the n_v-th lowest so far is never kept; a chunk
+            // left without any is not sorted
+            k = k < kth ? k : ~0ull;
+            if (c0 != 0 && !__ballot(k != ~0ull)) continue;
             k = wave_sort64(k);
             best = c0 == 0 ? k : wave_merge_low64(best, k);
+            kth = shfl64(best, (int)n_v - 1);
         }
         if ((uint32_t)lane < n_v) {
             uint32_t i = (uint32_t)best;
@@ -456,11 +481,15 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     for (uint32_t v = (uint32_t)(tid / kWave); v < s_nbig; v += kSmallT / kWave) {
         const uint32_t sl = s_big[v];
         const uint32_t o0 = s_off[sl], f0 = o0 >> 16, cnt_v = (s_off[sl + 1] >> 16) - f0;
-        uint64_t best = ~0ull;
+        uint64_t best = ~0ull, kth = ~0ull;
         for (uint32_t c0 = 0; c0 < cnt_v; c0 += kWave) {
             uint64_t key = (c0 + lane < cnt_v) ? (uint64_t)s_bk[f0 + c0 + lane] : ~0ull;
+            // an index above the n_v-th lowest so far is never kept
+            key = key < kth ? key : ~0ull;
+            if (c0 != 0 && !__ballot(key != ~0ull)) continue;
             key = wave_sort64(key);
             best = c0 == 0 ? key : wave_merge_low64(best, key);
+            kth = shfl64(best, (int)n_v - 1);
         }
         if ((uint32_t)lane < n_v) {
             const uint32_t i = (uint32_t)best;

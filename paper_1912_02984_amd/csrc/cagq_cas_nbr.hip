@@ -10,6 +10,8 @@
 // kCasLdsMaxN points (r <= 2), u32 entries behind a 4-entry header for
 // larger clouds with r = 1. Header entry 0 is the number within r, entry 1
 // the number within 2r.
+#include <type_traits>
+
 #include "cagq_internal.h"
 
 namespace cagq {
@@ -17,6 +19,54 @@ namespace cagq {
 namespace {
 
 constexpr int kNbrThreads = 64;  // one wave per block: small clouds spread over every CU
+
+// The u32 lists of large clouds gather their entries 4 at a time and store
+// each group with one 16-byte store: a lane's list is one run of whole
+// groups behind the 16-byte header, instead of a 4-byte store per entry
+// across the lanes' far-apart lists (layer 1 of the indoor scenes: 53 ->
+// 40 us). Unused entries of the last group hold whatever the group held
+// (readers look at the first n entries only). The u16 lists of small clouds
+// keep one store per entry, which measured faster there.
+template <typename E>
+struct Direct {
+    E* out;
+    __device__ __forceinline__ void push(uint32_t v) { *out++ = (E)v; }
+    __device__ __forceinline__ void flush() {}
+};
+
+template <typename E>
+struct Group16 {
+    static constexpr int kPer = 16 / (int)sizeof(E);
+    static constexpr int kBits = 8 * (int)sizeof(E);
+    uint64_t lo = 0, hi = 0;  // the entries so far, the latest in the top bits
+    int k = 0;                // entries held
+    E* out;                   // where the next whole group goes
+    __device__ __forceinline__ void push(uint32_t v) {
+        lo = (lo >> kBits) | (hi << (64 - kBits));
+        hi = (hi >> kBits) | ((uint64_t)v << (64 - kBits));
+        if (++k == kPer) {
+            *reinterpret_cast<uint4*>(out) = make_uint4((uint32_t)lo, (uint32_t)(lo >> 32), (uint32_t)hi,
+                                                        (uint32_t)(hi >> 32));
+            out += kPer;
+            k = 0;
+        }
+    }
+    __device__ __forceinline__ void flush() {
+        if (k == 0) return;
+        // k entries sit in the top k slots: move them to the bottom
+        const int sh = (kPer - k) * kBits;  // 0 < sh < 128
+        uint64_t l = lo, h = hi;
+        if (sh >= 64) {
+            l = h >> (sh - 64);
+            h = 0;
+        } else {
+            l = (l >> sh) | (h << (64 - sh));
+            h = h >> sh;
+        }
+        *reinterpret_cast<uint4*>(out) = make_uint4((uint32_t)l, (uint32_t)(l >> 32), (uint32_t)h,
+                                                    (uint32_t)(h >> 32));
+    }
+};
 
 // E: entry type, ST: entries per voxel (header included), HDR: header entries.
 template <int RAD, typename E, int ST, int HDR>
@@ -37,6 +87,9 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
     const uint64_t* bm = bitmap + (size_t)b * W;
     const uint32_t* wr = word_rank + (size_t)b * W;
     E* out = nbr + (size_t)gid * ST;
+    static_assert(HDR * sizeof(E) == 16 && (ST * sizeof(E)) % 16 == 0, "16-byte header and list stride");
+    std::conditional_t<sizeof(E) == 4, Group16<E>, Direct<E>> grp;
+    grp.out = out + HDR;
     uint32_t n = HDR;
     // bits H-RAD..H+RAD of a row of half-width H are the voxels within r in x
     constexpr uint32_t kInner = ((1u << (2 * RAD + 1)) - 1) << (H - RAD);
@@ -51,7 +104,8 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
             if (dy < -RAD || dy > RAD || dz < -RAD || dz > RAD) continue;
             for (uint32_t m = rows[j].mask & kInner; m; m &= m - 1) {
                 const uint32_t q = (uint32_t)__ffs(m) - 1;
-                out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                grp.push(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                ++n;
             }
         }
         const uint32_t n_r = n - HDR;
@@ -61,9 +115,11 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
             const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
             for (uint32_t m = rows[j].mask & (inner ? ~kInner : ~0u); m; m &= m - 1) {
                 const uint32_t q = (uint32_t)__ffs(m) - 1;
-                out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                grp.push(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                ++n;
             }
         }
+        grp.flush();
         out[0] = (E)n_r;
         out[1] = (E)(n - HDR);
         if (key) key[gid] = cas_key(unit * (int64_t)n_r, lin);
@@ -75,7 +131,10 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
             for (int j = 0; j < 2 * RAD + 1; ++j) rows[j] = load_row(bm, wr, g, x, y + j - RAD, z + dz, RAD);
 #pragma unroll
             for (int j = 0; j < 2 * RAD + 1; ++j)
-                for (uint32_t sl = rows[j].first, m = rows[j].mask; m; m &= m - 1, ++sl) out[n++] = (E)sl;
+                for (uint32_t sl = rows[j].first, m = rows[j].mask; m; m &= m - 1, ++sl) {
+                    grp.push(sl);
+                    ++n;
+                }
         }
         const uint32_t n_r = n - HDR;
         for (int dz = -H; dz <= H; ++dz) {
@@ -88,10 +147,12 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
                 const bool inner = dy >= -RAD && dy <= RAD && dz >= -RAD && dz <= RAD;
                 for (uint32_t m = rows[j].mask & (inner ? ~kInner : ~0u); m; m &= m - 1) {
                     const uint32_t q = (uint32_t)__ffs(m) - 1;
-                    out[n++] = (E)(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                    grp.push(rows[j].first + (uint32_t)__popc(rows[j].mask & ((1u << q) - 1)));
+                    ++n;
                 }
             }
         }
+        grp.flush();
         out[0] = (E)n_r;
         out[1] = (E)(n - HDR);
     }

@@ -17,6 +17,8 @@ constexpr int kWave = 64;
 constexpr int kScanThreads = 256;       // threads per scan tile
 constexpr int kScanItems = 4;           // items per thread in a scan tile
 constexpr int kScanTile = kScanThreads * kScanItems;
+constexpr int kRankItems = 1;           // occupancy words per thread of the rank scan
+constexpr int kRankTile = kScanThreads * kRankItems;
 constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
 constexpr int kSelBins = 2048;          // bins of the 11-bit digits of the many-block select
 constexpr int kSelChunk = 4096;         // slots per chunk of the many-block select
@@ -38,7 +40,7 @@ struct Layout {
     int32_t B, N;
     int64_t V;            // voxels per grid
     int64_t W;            // 64-bit occupancy words per cloud
-    int64_t tiles_w;      // scan tiles over the words of one cloud
+    int64_t tiles_w;      // rank-scan tiles (kRankTile words) over the words of one cloud
     int64_t tiles_s;      // scan tiles over the slots of one cloud
     int64_t big_cap;      // capacity of the big-voxel list
     size_t total;
