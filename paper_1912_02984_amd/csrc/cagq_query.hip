@@ -246,7 +246,9 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
     const int gb = threadIdx.x / G;  // group within the block
     uint32_t* s_pre = smem + (size_t)gb * (2 * nnb + 1);
     uint32_t* s_st = s_pre + nnb + 1;
-    const uint32_t blk = xcd_block(blockIdx.x, gridDim.x);
+    // the deferred pass spreads neighbouring (similarly long) contexts over
+    // the XCDs round-robin; the others keep neighbours on one XCD's L2
+    const uint32_t blk = DEFER ? blockIdx.x : xcd_block(blockIdx.x, gridDim.x);
     const int32_t cid = (int32_t)blk * GPB + gb;
     // every group runs to the end (the group- and wave-wide steps need all
     // lanes); a group past the end works on center 0 and writes nothing
@@ -413,6 +415,95 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         }
         return s_st[lo] + (e - s_pre[lo]);
     };
+    if constexpr (DEFER) {
+        // A long context, one wave: the keys below the K-th best so far are
+        // gathered in an LDS buffer of 64 and sorted and merged only when it
+        // is full (at the end, what is left). The chunk's positions come from
+        // a walk over the compacted voxels that the whole wave shares: the
+        // voxel holding the chunk's first entry, and the voxel starts inside
+        // the chunk as one 64-bit mask (every compacted voxel holds at least
+        // one point, so at most 64 of them start inside a chunk).
+        static_assert(G == kWave, "one center per wave");
+        uint64_t* cbk = reinterpret_cast<uint64_t*>(smem + ((GPB * (2 * nnb + 1) + 1) & ~1)) + gb * kWave;
+        uint32_t* cbp = reinterpret_cast<uint32_t*>(cbk + (GPB - gb) * kWave) + gb * kWave;
+        uint32_t wv = 0;  // the compacted voxel holding the walk's next chunk start
+        auto walk = [&](uint32_t c0) {
+            const uint32_t j = wv + 1 + (uint32_t)lg;
+            const uint32_t bj = j < nocc ? s_pre[j] - c0 : 65u;  // >= 1: voxel j starts after c0
+            uint64_t mk = bj < 64 ? (1ull << bj) : 0ull;
+#pragma unroll
+            for (int d = 1; d < kWave; d <<= 1) mk |= shfl_xor64(mk, d);
+            const uint32_t v = wv + (uint32_t)__popcll(mk & ((2ull << lg) - 1));
+            wv += (uint32_t)__popcll(mk) + (__ballot(bj == 64) ? 1u : 0u);
+            return s_st[v] + (c0 + (uint32_t)lg - s_pre[v]);
+        };
+        uint32_t pq[D];
+        float4 vq[D];
+#pragma unroll
+        for (int d = 0; d < D; ++d) {
+            pq[d] = walk((uint32_t)(d * G));
+            vq[d] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if ((uint32_t)(d * G + lg) < cs) vq[d] = p4[pq[d]];
+        }
+        uint64_t kth = ~0ull;
+        uint32_t fill = 0;
+        auto flush = [&]() {
+            uint64_t key = (uint32_t)lg < fill ? cbk[lg] : ~0ull;
+            uint32_t pos = (uint32_t)lg < fill ? cbp[lg] : 0u;
+            gsort<G>(key, pos, lg, (uint32_t)G);
+            if (NR == 1)
+                gmerge_low<G>(bk, bp, key, pos, lg);
+            else
+                gmerge_low2<G>(bk, bp, b1k, b1p, key, pos, lg);
+            kth = NR == 1 ? gshfl64<G>(bk, K - 1) : gshfl64<G>(b1k, K - 1 - G);
+            fill = 0;
+        };
+        for (uint32_t e0 = 0; e0 < cmax; e0 += G) {
+            const uint32_t e = e0 + lg;
+            const uint32_t pos = pq[0];
+            const float4 v = vq[0];
+#pragma unroll
+            for (int d = 0; d + 1 < D; ++d) {
+                pq[d] = pq[d + 1];
+                vq[d] = vq[d + 1];
+            }
+            if (e0 + D * G < cs) {  // the wave's next chunk to load
+                pq[D - 1] = walk(e0 + D * G);
+                if (e + D * G < cs) vq[D - 1] = p4[pq[D - 1]];
+            }
+            uint64_t key = ~0ull;
+            if (e < cs) {
+                const uint32_t i = __float_as_uint(v.w);
+                if (MODE == CAGQ_QUERY_CUBE) {
+                    key = (sm64(hc ^ (uint64_t)i) & 0xFFFFFFFF00000000ull) | i;
+                } else {
+                    const float dx = v.x - qx, dy = v.y - qy, dz = v.z - qz;
+                    const float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+                    const float sxy = xx + yy;
+                    const float d2 = sxy + zz;
+                    key = ((uint64_t)__float_as_uint(d2) << 32) | i;
+                }
+                key = key < kth ? key : ~0ull;
+            }
+            const uint64_t m = __ballot(key != ~0ull);
+            const uint32_t nc = (uint32_t)__popcll(m);
+            if (fill + nc > (uint32_t)kWave) {
+                flush();
+                wave_lds_sync();
+                // the new keys against the new K-th best
+                key = key < kth ? key : ~0ull;
+            }
+            const uint64_t m2 = __ballot(key != ~0ull);
+            if (key != ~0ull) {
+                const uint32_t at_ = fill + (uint32_t)__popcll(m2 & ((1ull << lg) - 1));
+                cbk[at_] = key;
+                cbp[at_] = pos;
+            }
+            fill += (uint32_t)__popcll(m2);
+            wave_lds_sync();
+        }
+        if (fill) flush();
+    } else {
     // each chunk's points are loaded D chunks ahead, so that a long
     // context's loads overlap the sort and merge of the chunks before
     uint32_t pq[D];
@@ -483,6 +574,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         }
         // the K-th best key so far (a filler, ~0, while fewer than K are held)
         kth = NR == 1 ? gshfl64<G>(bk, K - 1) : gshfl64<G>(b1k, K - 1 - G);
+    }
     }
 
     // 4. outputs (an empty context gives n = 0 and zeros): node slot k is
@@ -994,7 +1086,10 @@ void launch_g(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int3
     const int32_t total = L.B * M;
     const unsigned blocks = (unsigned)((total + GPB - 1) / GPB);
     constexpr int side = 2 * RAD + 1;
-    const size_t lds = (size_t)GPB * (2 * side * side * side + 1) * sizeof(uint32_t);
+    // the groups' compacted voxels; with DEFER also each group's candidate
+    // buffer (64 keys and positions), 8-byte aligned after them
+    const size_t lds = (((size_t)GPB * (2 * side * side * side + 1) + 1) & ~(size_t)1) * sizeof(uint32_t) +
+                       (DEFER ? (size_t)GPB * kWave * (sizeof(uint64_t) + sizeof(uint32_t)) : 0);
     k_query<MODE, G, RAD, UP, NR, DEFER, D><<<blocks, kQueryThreads, lds, s>>>(
         io.weights, L.N, M, K, total, g, L.W, at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
@@ -1015,7 +1110,7 @@ void launch_r(const Layout& L, const QGrid& g, int32_t rad, void* ws, const Quer
 // Contexts of more points than this go to one wave each when the grid can
 // hold contexts of more than kBigGrid points ((2r+1)^3 n_v): a 16-lane group
 // works through a long context chunk after chunk, one load latency each.
-constexpr uint32_t kDefer = 256;
+constexpr uint32_t kDefer = 128;
 constexpr int64_t kBigGrid = 1024;
 
 template <int MODE, int RAD, bool UP>
@@ -1031,7 +1126,7 @@ void launch_r2(const Layout& L, const QGrid& g, void* ws, const QueryIO& io, int
         at<uint32_t>(ws, L.vox_off), at<float4>(ws, L.pt4), io.center_lin, io.center_pts, seed, io.node_idx,
         io.node_xyz, io.n_valid, io.center_xyz, io.center_w, io.ctx_count, io.lin_out, at<int>(ws, L.status),
         big ? kDefer : 0xFFFFFFFFu);
-    if (big) launch_g<MODE, 64, RAD, UP, 1, true, 4>(L, g, ws, io, M, K, seed, s);
+    if (big) launch_g<MODE, 64, RAD, UP, 1, true, 6>(L, g, ws, io, M, K, seed, s);
 }
 
 template <int MODE, bool UP>
