@@ -126,6 +126,17 @@ __device__ __forceinline__ uint64_t xlane64(uint64_t v, int j) {
     return ((uint64_t)xlane((uint32_t)(v >> 32), j) << 32) | xlane((uint32_t)v, j);
 }
 
+// One 12-byte store of a node's coordinates (a single dwordx3 store: the
+// group's nodes land as one contiguous run).
+__device__ __forceinline__ void store_xyz(float* p, float x, float y, float z) {
+    typedef float f3 __attribute__((ext_vector_type(3)));
+    f3 v;
+    v.x = x;
+    v.y = y;
+    v.z = z;
+    __builtin_nontemporal_store(v, reinterpret_cast<f3*>(p));
+}
+
 // Value of lane `first` (0 or G-1) of this lane's group of G, by lane reads.
 template <int G>
 __device__ __forceinline__ uint32_t gbcast(uint32_t v, int first) {
@@ -617,9 +628,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query(
         if (live && k < (uint32_t)K) {
             node_idx[cK + k] = UP ? (n ? (int32_t)idx : -1) : (int32_t)idx;
             if (node_xyz) {
-                node_xyz[(cK + k) * 3 + 0] = x;
-                node_xyz[(cK + k) * 3 + 1] = y;
-                node_xyz[(cK + k) * 3 + 2] = z;
+                store_xyz(node_xyz + (cK + k) * 3, x, y, z);
             }
         }
         const float wf = (float)w;
@@ -998,9 +1007,7 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
         if (live && k < (uint32_t)K) {
             node_idx[cK + k] = UP ? (n ? (int32_t)idx : -1) : (int32_t)idx;
             if (node_xyz) {
-                node_xyz[(cK + k) * 3 + 0] = x;
-                node_xyz[(cK + k) * 3 + 1] = y;
-                node_xyz[(cK + k) * 3 + 2] = z;
+                store_xyz(node_xyz + (cK + k) * 3, x, y, z);
             }
         }
         if (!UP) {
