@@ -638,6 +638,43 @@ def measure_configs(dev, with_oracle: bool, reps: int = 50, reps_big: int = 20) 
     return out_all
 
 
+def profile_workload(name: str, passes: int, dev) -> None:
+    """Every layer of one workload config, chained as in the parity tests,
+    passes times after a warm-up pass (for kernel traces and counters of one
+    config alone)."""
+    import torch
+    from paper_1912_02984_amd import cagq
+    from paper_1912_02984_amd import workloads as W
+    w = W.get_workload(name)
+    P = torch.from_numpy(w.points()).to(dev)
+    B = P.shape[0]
+    plan, n = [], w.N
+    for L in w.layers:
+        desc = cagq.desc_from_spec(L.grid)
+        lay = cagq.workspace_layout(B, n, desc)
+        plan.append((L, desc, torch.empty(lay.total_bytes, dtype=torch.uint8, device=dev),
+                     cagq.alloc_query_outputs(B, L.M, L.K, dev)))
+        n = L.M
+
+    def run():
+        pts, wts = P, None
+        for (L, desc, ws, out) in plan:
+            g = cagq.build_grid(pts, desc, ws)
+            cl, _ = cagq.sample_centers(g, L.M, L.sample, L.seed)
+            cagq.query_context(g, cl, L.K, L.query, L.seed, weights=wts, out=out)
+            pts, wts = out["center_xyz"], out["center_w"]
+    run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(passes):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    print(json.dumps({"workload": name, "passes": passes, "ms_per_pass": round(e0.elapsed_time(e1) / passes, 4)}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -666,6 +703,10 @@ def main():
                     help="profiling mode: run only layer 1 (build + sample + query) of the selected variants "
                          "this many times after one warm-up pass, then exit (for the counter and trace runs "
                          "behind the layer roofline)")
+    ap.add_argument("--profile-workload", metavar="NAME",
+                    help="profiling mode: run every layer of one workload config (tiny, object, room, "
+                         "bigroom/cas-knn, bigroom/rvs-cube, lidar) --layer1-passes times (default 10) after "
+                         "one warm-up pass, then exit")
     ap.add_argument("--summarize-layer", nargs=5, metavar=("VARIANT", "FETCH_CSV", "WRITE_CSV", "TRACE_CSV", "PASSES"),
                     help="per-kernel time and HBM bytes of a --layer1-passes run, and their sums per pass")
     ap.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
@@ -696,6 +737,9 @@ def main():
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.profile_workload:
+        profile_workload(args.profile_workload, args.layer1_passes or 10, dev)
+        return
     variants = VARIANTS if args.variants == "both" else (f"bigroom/{args.variants}",)
     wls = [W.get_workload(v) for v in variants]
     B = args.batch
