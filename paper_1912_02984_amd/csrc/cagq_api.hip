@@ -63,6 +63,15 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->tiles_s = ((int64_t)N + kScanTile - 1) / kScanTile;
     L->big_cap = (int64_t)B * N / (kBigVoxel + 1) + 1;
     const size_t BN = (size_t)B * N;
+    L->Q = (int32_t)((L->W + kBrickW - 1) / kBrickW);
+    L->T = (int32_t)(((int64_t)B * N + kSortTile - 1) / kSortTile);
+    // the histogram matrix (B * Q by T entries) stays within 2^24 entries
+    L->bricks = (int64_t)B * L->Q <= kMaxBricks && (int64_t)B * L->Q * L->T <= (int64_t(1) << 24);
+    const size_t BQ = L->bricks ? (size_t)B * L->Q : 0;
+    const size_t hist_n = BQ * (size_t)L->T;
+    L->items_max = L->bricks ? (int64_t)BQ + ((int64_t)BN + kBrickCap - 1) / kBrickCap : 0;
+    L->heavy_max = L->bricks ? (int64_t)BN / (kBrickCap + 1) : 0;
+    const size_t H = (size_t)L->heavy_max;
     size_t off = 0;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -78,18 +87,36 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->sel_ghist = take(4 * (size_t)B * kSelBins);
     L->sel_cnt = take(4 * (size_t)B);
     L->clear_small = off;
-    L->desc_w = take(8 * (size_t)B * L->tiles_w);
+    L->desc_h = take(8 * ((BQ + 63) / 64));
+    L->hdone = take(4 * (L->bricks ? (size_t)BN / (kBrickCap + 1) : 0));
+    L->clear_brick = off;
+    // the occupancy bytes and rank descriptors serve the many-kernel build of
+    // grids too large for the bricks only
+    L->desc_w = take(L->bricks ? 0 : 8 * (size_t)B * L->tiles_w);
     L->desc_s = take(8 * (size_t)B * L->tiles_s);
-    L->bytemap = take(64 * (size_t)B * L->W);
+    L->bytemap = take(L->bricks ? 0 : 64 * (size_t)B * L->W);
     L->clear_end = off;
     L->bitmap = take(8 * (size_t)B * L->W);
     L->word_rank = take(4 * (size_t)B * L->W);
     L->pt_slot = take(4 * BN);
     L->pt_pos = take(4 * BN);
-    L->full_off = take(4 * (size_t)B * (N + 1));
+    L->hist = take(4 * hist_n);
+    L->bstart = take(4 * BQ);
+    L->brick_hb = take(4 * BQ);
+    L->item_extra = take(8 * ((size_t)L->items_max - BQ));
+    L->agg = take(8 * BQ);
+    L->hlist = take(4 * H);
+    L->hebase = take(4 * H);
+    L->pcnt = take(4 * ((size_t)L->items_max - BQ) * kBrickV);
+
+    L->hfo = take(4 * H * (kBrickV + 1));
+    L->hso = take(4 * H * kBrickV);
+    L->hpre = take(8 * H);
+    L->sorted = take(L->bricks ? 16 * BN : 0);
+    L->full_off = take(L->bricks ? 0 : 4 * (size_t)B * (N + 1));
     L->bucket = take(4 * BN);
     L->pt4 = take(16 * BN);
-    L->big = take(4 * (size_t)L->big_cap);
+    L->big = take(L->bricks ? 0 : 4 * (size_t)L->big_cap);
     L->cas_cover = take(4 * BN);
     L->cas_key = take(8 * BN);
     L->cas_pick = take(8 * BN);
@@ -350,7 +377,8 @@ int cagq_coverage(const cagq_grid* g, const int32_t* node_idx, const int32_t* n_
     if (rc != CAGQ_OK) return rc;
     if (!node_idx || !n_valid || !covered || M < 1 || K < 1) return CAGQ_ERR_INVALID_ARG;
     if ((int64_t)g->B * M * K > 2147483647LL) return CAGQ_ERR_INVALID_ARG;
-    hipError_t e = launch_coverage(L, g->workspace, node_idx, n_valid, M, K, covered, (hipStream_t)stream);
+    hipError_t e = launch_coverage(L, g->desc, g->points, g->workspace, node_idx, n_valid, M, K, covered,
+                                   (hipStream_t)stream);
     return e == hipSuccess ? CAGQ_OK : CAGQ_ERR_HIP;
 }
 

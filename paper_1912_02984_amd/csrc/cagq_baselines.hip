@@ -210,12 +210,20 @@ __global__ void k_cov_clear(uint4* __restrict__ p, size_t n16) {
         p[i] = make_uint4(0u, 0u, 0u, 0u);
 }
 
-// Every valid node point stores 1 into its slot's byte (the same value from
-// every writer: no atomic needed).
-__global__ __launch_bounds__(256) void k_cov_mark(int32_t N, int32_t M, int32_t K, int64_t total,
-                                                  const int32_t* __restrict__ node_idx,
+struct CovGrid {
+    float o[3], s[3];
+    int32_t D[3];
+    int64_t W;
+};
+
+// Every valid node point stores 1 into the byte of its voxel's slot (the same
+// value from every writer: no atomic needed). The slot comes from the point's
+// coordinates by the voxelization rule and the occupancy words.
+__global__ __launch_bounds__(256) void k_cov_mark(const float* __restrict__ P, int32_t N, int32_t M, int32_t K,
+                                                  int64_t total, CovGrid g, const int32_t* __restrict__ node_idx,
                                                   const int32_t* __restrict__ n_valid,
-                                                  const uint32_t* __restrict__ pt_slot, uint8_t* __restrict__ mark) {
+                                                  const uint64_t* __restrict__ bitmap,
+                                                  const uint32_t* __restrict__ word_rank, uint8_t* __restrict__ mark) {
     const int64_t t = (int64_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     if (t >= total) return;
     const int64_t cj = t / K;
@@ -224,7 +232,16 @@ __global__ __launch_bounds__(256) void k_cov_mark(int32_t N, int32_t M, int32_t 
     const int32_t i = node_idx[t];
     if (i < 0 || i >= N) return;
     const int32_t b = (int32_t)(cj / M);
-    mark[(size_t)b * N + pt_slot[(size_t)b * N + i]] = 1;
+    const float* p = P + ((size_t)b * N + i) * 3;
+    uint32_t gg[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        const float c = p[a];
+        gg[a] = isfinite(c) ? (uint32_t)axis_index(c, g.o[a], g.s[a], g.D[a]) : 0u;
+    }
+    const uint32_t lin = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
+    const int32_t slot = slot_of(bitmap + (size_t)b * g.W, word_rank + (size_t)b * g.W, lin);
+    if (slot >= 0) mark[(size_t)b * N + slot] = 1;
 }
 
 __global__ __launch_bounds__(1024) void k_cov_count(int32_t N, const int32_t* __restrict__ nvox,
@@ -274,16 +291,25 @@ hipError_t launch_ball_query(const float* points, int32_t B, int32_t N, const in
     return hipGetLastError();
 }
 
-hipError_t launch_coverage(const Layout& L, void* ws, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
-                           int32_t K, int32_t* covered, hipStream_t s) {
+hipError_t launch_coverage(const Layout& L, const cagq_grid_desc& d, const float* points, void* ws,
+                           const int32_t* node_idx, const int32_t* n_valid, int32_t M, int32_t K, int32_t* covered,
+                           hipStream_t s) {
     const size_t BN = (size_t)L.B * L.N;
     uint8_t* mark = at<uint8_t>(ws, L.cov_mark);
     const size_t n16 = (BN + 15) / 16;
     k_cov_clear<<<(unsigned)((n16 + 255) / 256 < 2048 ? (n16 + 255) / 256 : 2048), 256, 0, s>>>(
         reinterpret_cast<uint4*>(mark), n16);
     const int64_t total = (int64_t)L.B * M * K;
-    k_cov_mark<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(L.N, M, K, total, node_idx, n_valid,
-                                                               at<uint32_t>(ws, L.pt_slot), mark);
+    CovGrid g;
+    for (int a = 0; a < 3; ++a) {
+        g.o[a] = d.origin[a];
+        g.s[a] = d.voxel_size[a];
+        g.D[a] = d.dims[a];
+    }
+    g.W = L.W;
+    k_cov_mark<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(points, L.N, M, K, total, g, node_idx, n_valid,
+                                                               at<uint64_t>(ws, L.bitmap),
+                                                               at<uint32_t>(ws, L.word_rank), mark);
     k_cov_count<<<L.B, 1024, 0, s>>>(L.N, at<int32_t>(ws, L.nvox), mark, covered);
     return hipGetLastError();
 }

@@ -299,6 +299,700 @@ __global__ __launch_bounds__(256) void k_finalize(
     }
 }
 
+// ---- larger clouds: sort the points into bricks, then build each brick.
+// A brick is a run of kBrickV consecutive linear voxel ids (kBrickW occupancy
+// words) of one cloud; the batch holds B * Q of them. The points are grouped
+// by brick with a counting sort: a histogram per tile of points (one row per
+// tile), a scan of each brick's column and of the bricks' totals, a scatter
+// that carries each point's coordinates and index. Then one workgroup per
+// brick marks its occupancy words in LDS, ranks its occupied voxels by
+// popcount, counts their points, and places the n_v lowest point indices of
+// every voxel. The occupied and stored counts of the cloud's earlier bricks
+// come from a look-back. Every output is written once, the work is
+// proportional to the points and the occupied voxels, and no global atomic
+// is taken per point.
+constexpr int kSortT = 1024;                    // threads per sort tile
+constexpr int kSortIPT = kSortTile / kSortT;    // points per thread
+constexpr int kHGroup = 64;                     // bricks per block of the column scan
+constexpr int kBrickIPT = kBrickCap / kBrickT;  // points per thread, kept in registers
+constexpr int kBrickWaves = kBrickT / kWave;
+static_assert(2 * kBrickCap + 1 >= kBrickV, "a heavy part counts every voxel of its brick in LDS");
+static_assert(kBrickCap <= kBrickV, "a brick of one part has at most kBrickCap occupied voxels");
+static_assert(kBrickW <= kWave, "a brick's occupancy words are scanned by one wave");
+
+// Linear voxel id of a point; `bad` is set for a non-finite coordinate (its
+// axis index is then 0).
+__device__ __forceinline__ uint32_t voxel_lin(float x, float y, float z, const GridArgs& g, bool& bad) {
+    const float c[3] = {x, y, z};
+    uint32_t gg[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        if (!isfinite(c[a])) {
+            bad = true;
+            gg[a] = 0;
+        } else {
+            gg[a] = (uint32_t)axis_index(c[a], g.o[a], g.s[a], g.D[a]);
+        }
+    }
+    return gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
+}
+
+// Row t of the histogram: points of tile t in each brick of the batch. The
+// blocks also zero the control words [clr, clr + n16) (status, tickets,
+// descriptors) that the later kernels use.
+__global__ __launch_bounds__(kSortT) void k_bhist(const float* __restrict__ P, int32_t N, int32_t BN, GridArgs g,
+                                                  int32_t Q, int32_t BQ, int32_t T, uint32_t* __restrict__ hist,
+                                                  uint4* __restrict__ clr, int64_t n16) {
+    __shared__ uint32_t s_h[kMaxBricks];
+    const int tid = threadIdx.x;
+    const int32_t t = (int32_t)blockIdx.x;
+    for (int32_t i = tid; i < BQ; i += kSortT) s_h[i] = 0u;
+    for (int64_t i = (int64_t)t * kSortT + tid; i < n16; i += (int64_t)T * kSortT) clr[i] = make_uint4(0u, 0u, 0u, 0u);
+    lds_barrier();
+#pragma unroll
+    for (int k = 0; k < kSortIPT; ++k) {
+        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        if (gid >= BN) break;
+        const float* p = P + (size_t)gid * 3;
+        bool bad = false;
+        const uint32_t lin = voxel_lin(p[0], p[1], p[2], g, bad);
+        atomicAdd(&s_h[(gid / N) * Q + (int32_t)(lin / kBrickV)], 1u);
+    }
+    lds_barrier();
+    uint32_t* row = hist + (size_t)t * BQ;
+    for (int32_t i = tid; i < BQ; i += kSortT) row[i] = s_h[i];
+}
+
+// Sorted positions and work items: bstart[g] = points of the bricks before g
+// (bricks in cloud-major order), and entry (t, g) of the histogram becomes
+// the first position of tile t's points in brick g. Work item g < B * Q is
+// brick g (its first kBrickCap points); a brick of more than kBrickCap points
+// (heavy) has one more item per further kBrickCap points, listed in
+// item_extra as (part << 32 | g), and heavy bricks are numbered in hlist. A
+// block takes kHGroup bricks (one per lane) and splits the tiles over its
+// waves; the blocks' totals are chained by a look-back.
+__global__ __launch_bounds__(kScanThreads) void k_hscan(uint32_t* __restrict__ hist, int32_t BQ, int32_t T,
+                                                        uint32_t* __restrict__ bstart, int32_t* __restrict__ brick_hb,
+                                                        uint64_t* __restrict__ item_extra,
+                                                        uint32_t* __restrict__ hlist, uint32_t* __restrict__ hebase,
+                                                        uint64_t* __restrict__ desc,
+                                                        int* __restrict__ status) {
+    constexpr int kW = kScanThreads / kWave;
+    __shared__ uint32_t s_ticket;
+    __shared__ uint32_t s_part[kW][kHGroup];
+    __shared__ uint32_t s_bex[kHGroup];
+    __shared__ uint64_t s_prefix;
+    if (threadIdx.x == 0) s_ticket = atomicAdd((unsigned*)&status[kStTicketHist], 1u);
+    __syncthreads();
+    const int32_t grp = (int32_t)s_ticket;
+    const int lane = lane_id(), wv = threadIdx.x / kWave;
+    const int32_t g = grp * kHGroup + lane;
+    const bool valid = g < BQ;
+    const int32_t tc = (T + kW - 1) / kW;
+    const int32_t t0 = wv * tc, t1 = t0 + tc < T ? t0 + tc : T;
+    // the column's first kHKeep entries stay in registers for the rewrite
+    constexpr int kHKeep = 16;
+    uint32_t col[kHKeep];
+    uint32_t sum = 0;
+    if (valid) {
+#pragma unroll
+        for (int j = 0; j < kHKeep; ++j) {
+            col[j] = t0 + j < t1 ? hist[(size_t)(t0 + j) * BQ + g] : 0u;
+            sum += col[j];
+        }
+        for (int32_t t = t0 + kHKeep; t < t1; ++t) sum += hist[(size_t)t * BQ + g];
+    }
+    s_part[wv][lane] = sum;
+    __syncthreads();
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) {
+        const uint32_t x = s_part[w][lane];
+        pre += w < wv ? x : 0u;
+        tot += x;
+    }
+    // (extra parts << 32 | points), scanned over the bricks
+    const uint32_t parts = !valid ? 0u : (tot > (uint32_t)kBrickCap ? (tot + kBrickCap - 1) / kBrickCap : 1u);
+    uint64_t gtot = 0, ex = 0;
+    if (wv == 0) {
+        const uint64_t x = ((uint64_t)(parts ? parts - 1 : 0u) << 32) | tot;
+        const uint64_t incl = wave_incl_scan<uint64_t>(x);
+        ex = incl - x;
+        s_bex[lane] = (uint32_t)ex;
+        gtot = shfl64(incl, kWave - 1);
+    }
+    const uint64_t P0 = tile_lookback(desc, grp, gtot, &s_prefix);
+    if (!valid) return;
+    const uint32_t base = (uint32_t)P0 + s_bex[lane];
+    if (wv == 0) {
+        const uint32_t ebase = (uint32_t)((P0 + ex) >> 32);
+        bstart[g] = base;
+        for (uint32_t k = 1; k < parts; ++k) item_extra[ebase + k - 1] = ((uint64_t)k << 32) | (uint32_t)g;
+        int32_t hb = -1;
+        if (parts > 1) {
+            hb = (int32_t)atomicAdd((unsigned*)&status[kStHeavy], 1u);
+            hlist[hb] = (uint32_t)g;
+            hebase[hb] = ebase;
+        }
+        brick_hb[g] = hb;
+        if (g == BQ - 1) status[kStItems] = (int)(ebase + parts - 1);
+    }
+    uint32_t run = base + pre;
+#pragma unroll
+    for (int j = 0; j < kHKeep; ++j) {
+        if (t0 + j < t1) hist[(size_t)(t0 + j) * BQ + g] = run;
+        run += col[j];
+    }
+    for (int32_t t = t0 + kHKeep; t < t1; ++t) {
+        const size_t e = (size_t)t * BQ + g;
+        const uint32_t x = hist[e];
+        hist[e] = run;
+        run += x;
+    }
+}
+
+// One lane per point: (x, y, z, index) at the next free position of its
+// brick within the tile's range.
+__global__ __launch_bounds__(kSortT) void k_bscatter(const float* __restrict__ P, int32_t N, int32_t BN, GridArgs g,
+                                                     int32_t Q, int32_t BQ, int64_t W, const uint32_t* __restrict__ hist,
+                                                     float4* __restrict__ sorted, const uint32_t* __restrict__ hlist,
+                                                     uint64_t* __restrict__ bitmap, int* __restrict__ status) {
+    __shared__ uint32_t s_o[kMaxBricks];
+    const int tid = threadIdx.x;
+    const int32_t t = (int32_t)blockIdx.x;
+    // heavy bricks: their occupancy words start at zero (their parts OR into them)
+    const uint64_t nz = (uint64_t)(uint32_t)status[kStHeavy] * kBrickW;
+    for (uint64_t i = (uint64_t)t * kSortT + tid; i < nz; i += (uint64_t)gridDim.x * kSortT) {
+        const uint32_t hb = (uint32_t)(i / kBrickW), j = (uint32_t)(i % kBrickW);
+        const int32_t gg = (int32_t)hlist[hb];
+        const int32_t bb = gg / Q, qq = gg - bb * Q;
+        const int64_t w = (int64_t)qq * kBrickW + j;
+        if (w < W) bitmap[(size_t)bb * W + w] = 0ull;
+    }
+    const uint32_t* row = hist + (size_t)t * BQ;
+    for (int32_t i = tid; i < BQ; i += kSortT) s_o[i] = row[i];
+    lds_barrier();
+    bool bad = false;
+#pragma unroll
+    for (int k = 0; k < kSortIPT; ++k) {
+        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        if (gid >= BN) break;
+        const float* p = P + (size_t)gid * 3;
+        const float x = p[0], y = p[1], z = p[2];
+        const uint32_t lin = voxel_lin(x, y, z, g, bad);
+        const int32_t b = gid / N;
+        const uint32_t pos = atomicAdd(&s_o[b * Q + (int32_t)(lin / kBrickV)], 1u);
+        sorted[pos] = make_float4(x, y, z, __uint_as_float((uint32_t)(gid - b * N)));
+    }
+    if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+}
+
+struct BrickArgs {
+    const float* P;
+    int32_t N, BN, Q, BQ;
+    int64_t W;
+    uint32_t n_v;
+    GridArgs g;
+    const uint32_t* bstart;
+    const int32_t* brick_hb;
+    const uint64_t* item_extra;
+    const uint32_t* hlist;
+    const float4* sorted;
+    uint64_t* bitmap;
+    uint32_t* word_rank;
+    uint32_t* vox_lin;
+    uint32_t* vox_count;
+    int32_t* nvox;
+    uint32_t* vox_off;
+    uint32_t* pt_list;
+    float4* pt4;
+    uint64_t* agg;      // per brick: occupied voxels << 31 | stored points
+    uint32_t* bucket;   // point indices of heavy bricks, grouped by voxel
+    const uint32_t* hebase; // per heavy brick: its first item in item_extra
+    uint32_t* pcnt;     // per further part of a heavy brick and voxel: the brick's points in the parts before it
+    uint32_t* hfo;      // per heavy brick and voxel: exclusive prefix of the points (kBrickV + 1)
+    uint32_t* hso;      // per heavy brick and voxel: exclusive prefix of min(points, n_v)
+    uint64_t* hpre;     // per heavy brick: the aggregate of the cloud's bricks before it
+    uint32_t* hdone;    // per heavy brick: its parts that have grouped their points
+    int* status;
+};
+
+// Occupancy words of a brick and their exclusive ranks.
+struct WordLds {
+    uint64_t word[kBrickW];
+    uint32_t wocc[kBrickW];
+    uint32_t nocc;
+};
+
+__device__ __forceinline__ uint32_t brick_rank(const WordLds& s, uint32_t v) {
+    return s.wocc[v >> 6] + (uint32_t)__popcll(s.word[v >> 6] & ((1ull << (v & 63)) - 1));
+}
+
+// Exclusive ranks of the occupancy words (one wave): sets s.wocc and s.nocc.
+__device__ __forceinline__ void brick_word_scan(WordLds& s) {
+    const int tid = threadIdx.x;
+    if (tid < kWave) {
+        const uint32_t o = tid < kBrickW ? (uint32_t)__popcll(s.word[tid]) : 0u;
+        const uint32_t oi = wave_incl_scan<uint32_t>(o);
+        if (tid < kBrickW) s.wocc[tid] = oi - o;
+        if (tid == kWave - 1) s.nocc = oi;
+    }
+}
+
+// Sum and exclusive scan of one value per thread over a brick block; the
+// waves meet at an LDS-only barrier (their global stores are not waited for).
+__device__ __forceinline__ uint64_t block_sum64(uint64_t v, uint64_t* s_wave) {
+    v = wave_sum<uint64_t>(v);
+    if (lane_id() == 0) s_wave[threadIdx.x / kWave] = v;
+    lds_barrier();
+    uint64_t t = 0;
+#pragma unroll
+    for (int i = 0; i < kBrickWaves; ++i) t += s_wave[i];
+    return t;
+}
+
+__device__ __forceinline__ uint64_t brick_excl_scan(uint64_t v, uint64_t* s_wave, uint64_t* total) {
+    const uint64_t incl = wave_incl_scan<uint64_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    lds_barrier();
+    uint64_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kBrickWaves; ++i) {
+        const uint64_t x = s_wave[i];
+        off += i < wv ? x : 0ull;
+        tot += x;
+    }
+    *total = tot;
+    return off + incl - v;
+}
+
+// The work item of a block: brick g = blockIdx.x (its first kBrickCap
+// points), or a further part of a heavy brick.
+struct BrickItem {
+    int32_t g, b, q;
+    uint32_t start, cnt;  // the brick's sorted range
+    uint32_t p0, n;       // the part's sorted range
+    uint32_t part, parts;
+    bool heavy;
+};
+
+__device__ __forceinline__ bool brick_id(const BrickArgs& a, BrickItem& it) {
+    const uint32_t u = blockIdx.x;
+    it.part = 0;
+    if (u < (uint32_t)a.BQ) {
+        it.g = (int32_t)u;
+    } else {
+        if (u - (uint32_t)a.BQ >= (uint32_t)a.status[kStItems]) return false;
+        const uint64_t x = a.item_extra[u - a.BQ];
+        it.g = (int32_t)(uint32_t)x;
+        it.part = (uint32_t)(x >> 32);
+    }
+    it.b = it.g / a.Q;
+    it.q = it.g - it.b * a.Q;
+    return true;
+}
+
+__device__ __forceinline__ void brick_range(const BrickArgs& a, BrickItem& it) {
+    it.start = a.bstart[it.g];
+    const uint32_t end = it.g + 1 < a.BQ ? a.bstart[it.g + 1] : (uint32_t)a.BN;
+    it.cnt = end - it.start;
+    it.heavy = it.cnt > (uint32_t)kBrickCap;
+    it.parts = it.heavy ? (it.cnt + kBrickCap - 1) / kBrickCap : 1u;
+    it.p0 = it.start + it.part * (uint32_t)kBrickCap;
+    it.n = end - it.p0 < (uint32_t)kBrickCap ? end - it.p0 : (uint32_t)kBrickCap;
+}
+
+__device__ __forceinline__ bool brick_item(const BrickArgs& a, BrickItem& it) {
+    if (!brick_id(a, it)) return false;
+    brick_range(a, it);
+    return true;
+}
+
+// Voxel (within the brick) of each of the part's points; with MARK, also its
+// occupancy bit in s.word (zeroed and published by the caller's barrier).
+template <bool MARK>
+__device__ __forceinline__ void brick_voxels(const BrickArgs& a, WordLds& s, const BrickItem& it,
+                                             uint32_t (&v)[kBrickIPT], uint32_t (&idx)[kBrickIPT]) {
+    const uint32_t vbase = (uint32_t)it.q * kBrickV;
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k) {
+        const uint32_t i = threadIdx.x + k * kBrickT;
+        v[k] = 0u;
+        idx[k] = 0u;
+        if (i < it.n) {
+            const float4 e = a.sorted[it.p0 + i];
+            bool bad = false;
+            v[k] = voxel_lin(e.x, e.y, e.z, a.g, bad) - vbase;
+            idx[k] = __float_as_uint(e.w);
+            if (MARK) atomicOr(reinterpret_cast<unsigned long long*>(&s.word[v[k] >> 6]), 1ull << (v[k] & 63));
+        }
+    }
+}
+
+struct CountLds {
+    WordLds w;
+    uint32_t cnt[kBrickV];  // per occupied voxel (by rank), or per voxel for a heavy brick
+    uint64_t wave[kScanThreads / kWave];
+};
+
+// Pass 1 over the bricks: per brick its occupancy words (final) and its
+// aggregate (occupied voxels, stored points). A heavy brick is counted by the
+// block of its first part, which streams the parts in turn and writes, per
+// part and voxel, the brick's points in the parts before it (the second pass
+// places each part's points after them), then the per-voxel prefixes and the
+// voxels of more than kBigVoxel points. The blocks of further parts have
+// nothing to do here.
+__global__ __launch_bounds__(kBrickT) void k_brick_count(BrickArgs a) {
+    __shared__ CountLds s;
+    BrickItem it;
+    if (!brick_item(a, it) || it.part != 0) return;
+    const int tid = threadIdx.x;
+    const size_t wbase = (size_t)it.b * a.W + (size_t)it.q * kBrickW;
+    const int64_t wlim = a.W - (int64_t)it.q * kBrickW;  // words of this brick inside the grid
+    if (it.cnt == 0) {
+        if (tid < kBrickW && tid < wlim) a.bitmap[wbase + tid] = 0ull;
+        if (tid == 0) a.agg[it.g] = 0ull;
+        return;
+    }
+    if (tid < kBrickW) s.w.word[tid] = 0ull;
+    if (it.heavy)
+        for (int j = tid; j < kBrickV; j += kBrickT) s.cnt[j] = 0u;
+    lds_barrier();
+    uint32_t v[kBrickIPT], idx[kBrickIPT];
+    if (!it.heavy) {
+        brick_voxels<true>(a, s.w, it, v, idx);
+        lds_barrier();
+        brick_word_scan(s.w);
+        lds_barrier();
+        const uint32_t n_occ = s.w.nocc;
+        for (uint32_t j = tid; j < n_occ; j += kBrickT) s.cnt[j] = 0u;
+        lds_barrier();
+#pragma unroll
+        for (int k = 0; k < kBrickIPT; ++k)
+            if (threadIdx.x + k * kBrickT < it.n) atomicAdd(&s.cnt[brick_rank(s.w, v[k])], 1u);
+        lds_barrier();
+        uint64_t st = 0;
+        for (uint32_t j = tid; j < n_occ; j += kBrickT) st += s.cnt[j] < a.n_v ? s.cnt[j] : a.n_v;
+        st = block_sum64(st, s.wave);
+        if (tid < kBrickW && tid < wlim) a.bitmap[wbase + tid] = s.w.word[tid];
+        if (tid == 0) a.agg[it.g] = ((uint64_t)n_occ << 31) | st;
+        return;
+    }
+    // a heavy brick: its parts in turn; before each, the counts so far are that part's row
+    const int32_t hb = a.brick_hb[it.g];
+    const uint32_t eb = a.hebase[hb];
+    for (uint32_t p = 0; p < it.parts; ++p) {
+        BrickItem pt = it;
+        pt.part = p;
+        pt.p0 = it.start + p * (uint32_t)kBrickCap;
+        pt.n = it.start + it.cnt - pt.p0 < (uint32_t)kBrickCap ? it.start + it.cnt - pt.p0 : (uint32_t)kBrickCap;
+        brick_voxels<true>(a, s.w, pt, v, idx);
+        if (p != 0) {
+            uint32_t* row = a.pcnt + (size_t)(eb + p - 1) * kBrickV;
+            for (int j = tid; j < kBrickV; j += kBrickT) row[j] = s.cnt[j];
+        }
+        lds_barrier();
+#pragma unroll
+        for (int k = 0; k < kBrickIPT; ++k)
+            if (threadIdx.x + k * kBrickT < pt.n) atomicAdd(&s.cnt[v[k]], 1u);
+        lds_barrier();
+    }
+    brick_word_scan(s.w);
+    if (tid < kBrickW && tid < wlim) a.bitmap[wbase + tid] = s.w.word[tid];
+    constexpr int kPer = kBrickV / kBrickT;
+    uint32_t c[kPer];
+    uint64_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        c[j] = s.cnt[tid * kPer + j];
+        sum += ((uint64_t)c[j] << 32) | (c[j] < a.n_v ? c[j] : a.n_v);
+    }
+    uint64_t total;
+    uint64_t pos = brick_excl_scan(sum, s.wave, &total);
+    uint32_t* fo = a.hfo + (size_t)hb * (kBrickV + 1);
+    uint32_t* so = a.hso + (size_t)hb * kBrickV;
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+        const uint32_t vv = tid * kPer + j;
+        fo[vv] = (uint32_t)(pos >> 32);
+        so[vv] = (uint32_t)pos;
+        pos += ((uint64_t)c[j] << 32) | (c[j] < a.n_v ? c[j] : a.n_v);
+    }
+    if (tid == 0) {
+        fo[kBrickV] = it.cnt;
+        a.agg[it.g] = ((uint64_t)s.w.nocc << 31) | (uint32_t)total;
+    }
+}
+
+// The n_v smallest of the cnt indices at p (in memory), sorted ascending over
+// the wave's lanes: 64-key chunks, four loaded at a time, each sorted by a
+// bitonic network and merged into the best so far; a chunk without an index
+// below the n_v-th best is skipped.
+__device__ __forceinline__ uint64_t wave_select_lowest(const uint32_t* p, uint32_t cnt, uint32_t n_v) {
+    const int lane = lane_id();
+    uint64_t best = ~0ull, kth = ~0ull;
+    for (uint32_t c0 = 0; c0 < cnt; c0 += 4 * kWave) {
+        uint64_t key[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint32_t i = c0 + j * kWave + lane;
+            key[j] = i < cnt ? (uint64_t)p[i] : ~0ull;
+        }
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (c0 + j * kWave >= cnt) break;
+            uint64_t k = key[j] < kth ? key[j] : ~0ull;
+            const bool first = c0 == 0 && j == 0;
+            if (!first && !__ballot(k != ~0ull)) continue;
+            k = wave_sort64(k);
+            best = first ? k : wave_merge_low64(best, k);
+            kth = shfl64(best, (int)n_v - 1);
+        }
+    }
+    return best;
+}
+
+struct BuildLds {
+    WordLds w;
+    uint64_t bigm[kBrickW];         // bit r: occupied voxel r holds more than kBigVoxel points
+    union {
+        struct {
+            uint32_t va[kBrickCap + 1]; // per occupied voxel: count, then (stored prefix << 16 | point prefix)
+            uint32_t idx[kBrickCap];    // point indices grouped by voxel (arrival order)
+        } one;                          // a brick of one part
+        uint32_t arr[kBrickV];          // a part of a heavy brick: its arrivals per voxel
+    } u;
+    uint64_t wave[kScanThreads / kWave];
+    uint32_t ticket;
+};
+
+// Pass 2 over the bricks: slots, offsets and stored lists. The aggregates of
+// the cloud's earlier bricks are summed directly (every one is final). A
+// brick of one part does everything in LDS; a part of a heavy brick groups
+// its points by voxel in `bucket`, and the last of its parts to finish then
+// selects the brick's lists from there.
+__global__ __launch_bounds__(kBrickT) void k_brick(BrickArgs a) {
+    __shared__ BuildLds s;
+    BrickItem it;
+    if (!brick_id(a, it)) return;
+    const int tid = threadIdx.x;
+    const int lane = lane_id();
+    const int wv = tid / kWave;
+    // the cloud's bricks before this one (loads issued with the range's)
+    uint64_t pre = 0;
+    const uint64_t* ag = a.agg + (size_t)it.b * a.Q;
+    for (int32_t j = tid; j < it.q; j += kBrickT) pre += ag[j];
+    const uint64_t my = ag[it.q];
+    brick_range(a, it);
+    const uint32_t vbase = (uint32_t)it.q * kBrickV;
+    const size_t pb = (size_t)it.b * a.N;
+    const size_t wbase = (size_t)it.b * a.W + (size_t)it.q * kBrickW;
+    const int64_t wlim = a.W - (int64_t)it.q * kBrickW;
+    uint32_t* vo = a.vox_off + (size_t)it.b * (a.N + 1);
+    if (tid < kBrickW) {
+        s.w.word[tid] = it.heavy ? (tid < wlim ? a.bitmap[wbase + tid] : 0ull) : 0ull;
+        s.bigm[tid] = 0ull;
+    }
+    pre = block_sum64(pre, s.wave);  // its barrier also publishes the words
+    const uint32_t p_occ = (uint32_t)(pre >> 31), p_st = (uint32_t)(pre & 0x7FFFFFFFu);
+    if (it.cnt == 0) {
+        if (tid < kBrickW && tid < wlim) a.word_rank[wbase + tid] = p_occ;
+        if (it.q == a.Q - 1 && tid == 0) {
+            a.nvox[it.b] = (int32_t)p_occ;
+            vo[p_occ] = p_st;
+        }
+        return;
+    }
+    uint32_t v[kBrickIPT], idx[kBrickIPT];
+    if (it.heavy) brick_voxels<false>(a, s.w, it, v, idx);
+    else brick_voxels<true>(a, s.w, it, v, idx);
+    lds_barrier();
+    brick_word_scan(s.w);
+    lds_barrier();
+    const uint32_t n_occ = (uint32_t)(my >> 31);
+    if (it.part == 0) {
+        if (tid < kBrickW && tid < wlim) a.word_rank[wbase + tid] = p_occ + s.w.wocc[tid];
+        if (it.q == a.Q - 1 && tid == 0) {
+            a.nvox[it.b] = (int32_t)(p_occ + n_occ);
+            vo[p_occ + n_occ] = p_st + (uint32_t)(my & 0x7FFFFFFFu);
+        }
+        if (it.heavy && tid == 0) a.hpre[a.brick_hb[it.g]] = pre;
+    }
+    if (it.heavy) {
+        // a point's position within its voxel: the voxel's points in the
+        // parts before this one, then its arrival in this part
+        const int32_t hb = a.brick_hb[it.g];
+        const uint32_t* before = it.part == 0 ? nullptr : a.pcnt + (size_t)(a.hebase[hb] + it.part - 1) * kBrickV;
+        const uint32_t* fo = a.hfo + (size_t)hb * (kBrickV + 1);
+        const uint32_t* so = a.hso + (size_t)hb * kBrickV;
+        for (int j = tid; j < kBrickV; j += kBrickT) s.u.arr[j] = 0u;
+        lds_barrier();
+        // every point's loads first, then the stores
+        uint32_t bf[kBrickIPT], f0s[kBrickIPT], f1s[kBrickIPT], sos[kBrickIPT];
+#pragma unroll
+        for (int k = 0; k < kBrickIPT; ++k) {
+            const bool in = threadIdx.x + k * kBrickT < it.n;
+            bf[k] = in && before ? before[v[k]] : 0u;
+            f0s[k] = in ? fo[v[k]] : 0u;
+            f1s[k] = in ? fo[v[k] + 1] : 0u;
+            sos[k] = in ? so[v[k]] : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kBrickIPT; ++k) {
+            if (threadIdx.x + k * kBrickT >= it.n) break;
+            const uint32_t ps = bf[k] + atomicAdd(&s.u.arr[v[k]], 1u);
+            const uint32_t f0 = f0s[k];
+            a.bucket[it.start + f0 + ps] = idx[k];
+            if (ps == 0) {
+                const uint32_t slot = p_occ + brick_rank(s.w, v[k]);
+                a.vox_lin[pb + slot] = vbase + v[k];
+                a.vox_count[pb + slot] = f1s[k] - f0;
+                vo[slot] = p_st + sos[k];
+            }
+        }
+        // the last part to finish selects the brick's stored lists: a point
+        // of a voxel of at most kBigVoxel points by its rank (one lane per
+        // point), a larger voxel by one wave's bitonic selection
+        __threadfence();
+        __syncthreads();
+        if (tid == 0) s.ticket = atomicAdd(&a.hdone[hb], 1u);
+        __syncthreads();
+        if (s.ticket != it.parts - 1) return;
+        __threadfence();
+        const uint32_t* bk = a.bucket + it.start;
+        for (uint32_t i = tid; i < it.cnt; i += kBrickT) {
+            const float4 e = a.sorted[it.start + i];
+            bool bad = false;
+            const uint32_t vv = voxel_lin(e.x, e.y, e.z, a.g, bad) - vbase;
+            const uint32_t f0 = fo[vv], c = fo[vv + 1] - f0;
+            if (c > kBigVoxel) continue;
+            const uint32_t id = __float_as_uint(e.w);
+            uint32_t rank = 0;
+            for (uint32_t j = 0; j < c; ++j) rank += bk[f0 + j] < id ? 1u : 0u;
+            if (rank < a.n_v) {
+                const size_t dst = pb + p_st + so[vv] + rank;
+                a.pt_list[dst] = id;
+                a.pt4[dst] = e;
+            }
+        }
+        for (uint32_t ch = tid / kWave; ch < (uint32_t)kBrickV / kWave; ch += kBrickWaves) {
+            const uint32_t f0v = fo[ch * kWave + lane], cv = fo[ch * kWave + lane + 1] - f0v;
+            const uint32_t sov = so[ch * kWave + lane];
+            for (uint64_t m = __ballot(cv > kBigVoxel); m; m &= m - 1) {
+                const int l = __ffsll((unsigned long long)m) - 1;
+                const uint32_t f0 = (uint32_t)__shfl((int)f0v, l, kWave);
+                const uint32_t cnt = (uint32_t)__shfl((int)cv, l, kWave);
+                const uint32_t sl = (uint32_t)__shfl((int)sov, l, kWave);
+                const uint64_t best = wave_select_lowest(bk + f0, cnt, a.n_v);
+                if ((uint32_t)lane < a.n_v) {
+                    const uint32_t i = (uint32_t)best;
+                    const size_t dst = pb + p_st + sl + lane;
+                    const float* p = a.P + (pb + i) * 3;
+                    a.pt_list[dst] = i;
+                    a.pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+                }
+            }
+        }
+        return;
+    }
+    // a brick of one part: counts per occupied voxel, arrival positions
+    uint32_t* va = s.u.one.va;  // n_occ + 1 entries
+    for (uint32_t j = tid; j <= n_occ; j += kBrickT) va[j] = 0u;
+    lds_barrier();
+    uint32_t r[kBrickIPT], pos[kBrickIPT];
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k) {
+        r[k] = 0u;
+        pos[k] = 0u;
+        if (threadIdx.x + k * kBrickT < it.n) {
+            r[k] = brick_rank(s.w, v[k]);
+            pos[k] = atomicAdd(&va[r[k]], 1u);
+        }
+    }
+    lds_barrier();
+    // the points' coordinates, loaded again for the stored lists (issued here
+    // so that the scan and grouping below hide their latency)
+    float4 e[kBrickIPT];
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k)
+        if (threadIdx.x + k * kBrickT < it.n) e[k] = a.sorted[it.p0 + threadIdx.x + k * kBrickT];
+    // exclusive prefixes of (count, stored) over the occupied voxels, packed
+    // as stored << 16 | count (both at most kBrickCap)
+    const uint32_t per = (n_occ + kBrickT - 1) / kBrickT;
+    const uint32_t r0 = (uint32_t)tid * per;
+    uint32_t sum = 0;
+    for (uint32_t j = 0; j < per; ++j) {
+        if (r0 + j >= n_occ) break;
+        const uint32_t c = va[r0 + j];
+        sum += ((c < a.n_v ? c : a.n_v) << 16) | c;
+    }
+    uint64_t total;
+    uint32_t run = (uint32_t)brick_excl_scan(sum, s.wave, &total);
+    for (uint32_t j = 0; j < per; ++j) {
+        const uint32_t rr = r0 + j;
+        if (rr >= n_occ) break;
+        const uint32_t c = va[rr];
+        va[rr] = run;
+        if (c > kBigVoxel) atomicOr(reinterpret_cast<unsigned long long*>(&s.bigm[rr >> 6]), 1ull << (rr & 63));
+        run += ((c < a.n_v ? c : a.n_v) << 16) | c;
+    }
+    if (tid == 0) va[n_occ] = it.cnt;
+    lds_barrier();
+    // the points grouped by voxel; the first arrival in a voxel writes its slot
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k) {
+        if (threadIdx.x + k * kBrickT >= it.n) break;
+        const uint32_t o = va[r[k]], f0 = o & 0xFFFFu;
+        s.u.one.idx[f0 + pos[k]] = idx[k];
+        if (pos[k] == 0) {
+            const uint32_t slot = p_occ + r[k];
+            a.vox_lin[pb + slot] = vbase + v[k];
+            a.vox_count[pb + slot] = (va[r[k] + 1] & 0xFFFFu) - f0;
+            vo[slot] = p_st + (o >> 16);
+        }
+    }
+    lds_barrier();
+    // stored lists: a point of a voxel of at most kBigVoxel points by its rank
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k) {
+        if (threadIdx.x + k * kBrickT >= it.n) break;
+        const uint32_t o = va[r[k]], f0 = o & 0xFFFFu, c = (va[r[k] + 1] & 0xFFFFu) - f0;
+        if (c > kBigVoxel) continue;
+        uint32_t rank = 0;
+        for (uint32_t j = 0; j < c; ++j) rank += s.u.one.idx[f0 + j] < idx[k] ? 1u : 0u;
+        if (rank < a.n_v) {
+            const size_t dst = pb + p_st + (o >> 16) + rank;
+            a.pt_list[dst] = idx[k];
+            a.pt4[dst] = e[k];
+        }
+    }
+    // larger voxels: one wave each, the n_v smallest indices by bitonic selection
+    for (int j = wv; j < kBrickW; j += kBrickWaves) {
+        for (uint64_t m = s.bigm[j]; m; m &= m - 1) {
+            const uint32_t rr = (uint32_t)j * kWave + (uint32_t)(__ffsll((unsigned long long)m) - 1);
+            const uint32_t o = va[rr], f0 = o & 0xFFFFu, c = (va[rr + 1] & 0xFFFFu) - f0;
+            uint64_t best = ~0ull, kth = ~0ull;
+            for (uint32_t c0 = 0; c0 < c; c0 += kWave) {
+                uint64_t key = (c0 + lane < c) ? (uint64_t)s.u.one.idx[f0 + c0 + lane] : ~0ull;
+                // an index above the n_v-th lowest so far is never kept
+                key = key < kth ? key : ~0ull;
+                if (c0 != 0 && !__ballot(key != ~0ull)) continue;
+                key = wave_sort64(key);
+                best = c0 == 0 ? key : wave_merge_low64(best, key);
+                kth = shfl64(best, (int)a.n_v - 1);
+            }
+            if ((uint32_t)lane < a.n_v) {
+                const uint32_t i = (uint32_t)best;
+                const size_t dst = pb + p_st + (o >> 16) + lane;
+                const float* p = a.P + (pb + i) * 3;
+                a.pt_list[dst] = i;
+                a.pt4[dst] = make_float4(p[0], p[1], p[2], __uint_as_float(i));
+            }
+        }
+    }
+}
+
 // ---- small clouds: the whole build in one workgroup per cloud.
 // For clouds of at most kSmallN points whose grid has at most kSmallW
 // occupancy words, every step above runs in one 1024-thread workgroup with
@@ -538,6 +1232,52 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
                                                 at<uint32_t>(ws, L.vox_lin), at<uint32_t>(ws, L.vox_count),
                                                 at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_off),
                                                 at<uint32_t>(ws, L.pt_list), at<float4>(ws, L.pt4), status);
+        return hipGetLastError();
+    }
+    if (L.bricks) {
+        const int32_t BQ = B * L.Q;
+        uint32_t* hist = at<uint32_t>(ws, L.hist);
+        int* status_w = at<int>(ws, L.status);
+        k_bhist<<<(unsigned)L.T, kSortT, 0, s>>>(points, N, BN, g, L.Q, BQ, L.T, hist, at<uint4>(ws, L.status),
+                                                 (int64_t)(L.clear_brick - L.status) / 16);
+        k_hscan<<<(unsigned)((BQ + kHGroup - 1) / kHGroup), kScanThreads, 0, s>>>(
+            hist, BQ, L.T, at<uint32_t>(ws, L.bstart), at<int32_t>(ws, L.brick_hb), at<uint64_t>(ws, L.item_extra),
+            at<uint32_t>(ws, L.hlist), at<uint32_t>(ws, L.hebase), at<uint64_t>(ws, L.desc_h), status_w);
+        k_bscatter<<<(unsigned)L.T, kSortT, 0, s>>>(points, N, BN, g, L.Q, BQ, L.W, hist, at<float4>(ws, L.sorted),
+                                                    at<uint32_t>(ws, L.hlist), at<uint64_t>(ws, L.bitmap), status_w);
+        BrickArgs a;
+        a.P = points;
+        a.N = N;
+        a.BN = BN;
+        a.Q = L.Q;
+        a.BQ = BQ;
+        a.W = L.W;
+        a.n_v = (uint32_t)d.n_v;
+        a.g = g;
+        a.bstart = at<uint32_t>(ws, L.bstart);
+        a.brick_hb = at<int32_t>(ws, L.brick_hb);
+        a.item_extra = at<uint64_t>(ws, L.item_extra);
+        a.hlist = at<uint32_t>(ws, L.hlist);
+        a.sorted = at<float4>(ws, L.sorted);
+        a.bitmap = at<uint64_t>(ws, L.bitmap);
+        a.word_rank = at<uint32_t>(ws, L.word_rank);
+        a.vox_lin = at<uint32_t>(ws, L.vox_lin);
+        a.vox_count = at<uint32_t>(ws, L.vox_count);
+        a.nvox = at<int32_t>(ws, L.nvox);
+        a.vox_off = at<uint32_t>(ws, L.vox_off);
+        a.pt_list = at<uint32_t>(ws, L.pt_list);
+        a.pt4 = at<float4>(ws, L.pt4);
+        a.agg = at<uint64_t>(ws, L.agg);
+        a.bucket = at<uint32_t>(ws, L.bucket);
+        a.hebase = at<uint32_t>(ws, L.hebase);
+        a.pcnt = at<uint32_t>(ws, L.pcnt);
+        a.hdone = at<uint32_t>(ws, L.hdone);
+        a.hfo = at<uint32_t>(ws, L.hfo);
+        a.hso = at<uint32_t>(ws, L.hso);
+        a.hpre = at<uint64_t>(ws, L.hpre);
+        a.status = status_w;
+        k_brick_count<<<(unsigned)L.items_max, kBrickT, 0, s>>>(a);
+        k_brick<<<(unsigned)L.items_max, kBrickT, 0, s>>>(a);
         return hipGetLastError();
     }
     size_t n16 = (L.clear_end - L.status) / 16;

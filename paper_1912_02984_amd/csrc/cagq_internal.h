@@ -22,6 +22,12 @@ constexpr int kRankTile = kScanThreads * kRankItems;
 constexpr uint32_t kBigVoxel = 64;      // voxels holding more points use the wave selector
 constexpr int kSelBins = 2048;          // bins of the 11-bit digits of the many-block select
 constexpr int kSelChunk = 4096;         // slots per chunk of the many-block select
+constexpr int kBrickW = 32;             // occupancy words per brick of the brick build
+constexpr int kBrickV = kBrickW * 64;   // voxels per brick (a run of consecutive linear ids)
+constexpr int32_t kMaxBricks = 8192;    // bricks over the batch the brick build's histograms hold
+constexpr int kSortTile = 4096;         // points per tile of the brick histogram and scatter
+constexpr int kBrickT = 256;            // threads per brick work item
+constexpr int kBrickCap = 2048;         // points per brick work item (heavier bricks are split)
 
 // Status word slots (int32 each) at the start of the workspace's control block.
 enum StatusSlot {
@@ -31,6 +37,9 @@ enum StatusSlot {
     kStBigCount = 3,   // number of voxels with more than kBigVoxel points
     kStTicketSel = 4,  // tile tickets of the center compaction scan
     kStTicketCtx = 5,  // tile tickets of the context-offsets scan
+    kStTicketHist = 6, // tile tickets of the brick-histogram scan
+    kStItems = 7,      // brick build: work items (bricks and parts of heavy bricks)
+    kStHeavy = 8,      // brick build: bricks of more than kBrickCap points
     kStSlots = 16
 };
 
@@ -43,11 +52,20 @@ struct Layout {
     int64_t tiles_w;      // rank-scan tiles (kRankTile words) over the words of one cloud
     int64_t tiles_s;      // scan tiles over the slots of one cloud
     int64_t big_cap;      // capacity of the big-voxel list
+    int32_t Q;            // bricks per cloud (kBrickW words each)
+    int32_t T;            // point tiles (kSortTile points) over the batch
+    bool bricks;          // the brick build's arrays are present (B * Q <= kMaxBricks)
+    int64_t items_max;    // brick build: bound on the work items, B * Q + ceil(B * N / kBrickCap)
+                          // (the bricks, then the further parts of heavy bricks)
+    int64_t heavy_max;    // brick build: bound on the heavy bricks, B * N / (kBrickCap + 1)
     size_t total;
     // exposed
     size_t nvox, vox_lin, vox_count, vox_off, pt_list;
     // internal
     size_t status;        // int32[kStSlots]
+    size_t desc_h;        // u64 [blocks of the column scan] scan descriptors (brick totals)
+    size_t clear_brick;   // [status, clear_brick) is zeroed by the brick build (status, tickets,
+                          // descriptors, hdone)
     size_t desc_w;        // u64 [B][tiles_w] scan descriptors (occupancy ranks)
     size_t desc_s;        // u64 [B][tiles_s] scan descriptors (offsets)
     size_t bytemap;       // u8  [B][64 W] one byte per voxel, 1 when a point lies in it
@@ -55,8 +73,23 @@ struct Layout {
     size_t word_rank;     // u32 [B][W] occupied voxels before word w (the slot of its first bit)
     size_t pt_slot;       // u32 [B][N] per point: linear id, then slot
     size_t pt_pos;        // u32 [B][N] per point: arrival position inside its voxel
+    size_t hist;          // u32 [T][B*Q] points of tile t in brick g, then the first sorted position of them
+    size_t bstart;        // u32 [B*Q] first sorted position of each brick
+    size_t brick_hb;      // i32 [B*Q] index of a heavy brick in hlist, else -1
+    size_t item_extra;    // u64 [items_max - B*Q] further parts of heavy bricks: part << 32 | brick
+    size_t agg;           // u64 [B*Q] occupied voxels << 31 | stored points of each brick
+    size_t hlist;         // u32 [heavy_max] the heavy bricks
+    size_t hebase;        // u32 [heavy_max] first item_extra entry of each heavy brick
+    size_t pcnt;          // u32 [items_max - B*Q][kBrickV] per further part of a heavy brick and voxel:
+                          // the brick's points in the parts before it
+    size_t hdone;         // u32 [heavy_max] parts of each heavy brick that have grouped their points
+    size_t hfo;           // u32 [heavy_max][kBrickV + 1] their exclusive prefix
+    size_t hso;           // u32 [heavy_max][kBrickV] exclusive prefix of min(points, n_v)
+    size_t hpre;          // u64 [heavy_max] aggregate of the bricks before each heavy brick
+    size_t sorted;        // float4 [B*N] x, y, z, bits(index) grouped by brick
     size_t full_off;      // u32 [B][N+1] exclusive prefix of the full counts
-    size_t bucket;        // u32 [B][N] every point index grouped by slot (arrival order)
+    size_t bucket;        // u32 [B][N] every point index grouped by slot (arrival order); in the
+                          // brick build, those of bricks too large for LDS, at their sorted position
     size_t pt4;           // float4 [B][N] stored points grouped by slot: x, y, z, bits(index)
     size_t big;           // u32 [big_cap] global slot ids (b*N + s) of big voxels
     size_t cas_cover;     // u32 [B][N] CAS: centers whose neighbourhood holds the voxel
@@ -478,8 +511,9 @@ hipError_t launch_sample_points(const float* points, int32_t B, int32_t N, int32
                                 int32_t* center_idx, hipStream_t s);
 hipError_t launch_ball_query(const float* points, int32_t B, int32_t N, const int32_t* center_idx, int32_t M,
                              int32_t K, float radius2, int32_t* node_idx, int32_t* n_valid, hipStream_t s);
-hipError_t launch_coverage(const Layout& L, void* ws, const int32_t* node_idx, const int32_t* n_valid, int32_t M,
-                           int32_t K, int32_t* covered, hipStream_t s);
+hipError_t launch_coverage(const Layout& L, const cagq_grid_desc& d, const float* points, void* ws,
+                           const int32_t* node_idx, const int32_t* n_valid, int32_t M, int32_t K, int32_t* covered,
+                           hipStream_t s);
 constexpr int32_t kFpsMaxN = 80 * 1024;  // points per cloud Farthest Point Sampling keeps in registers
 
 // Upsampling query around given center points [B][M][3] (Sec. 3.1).

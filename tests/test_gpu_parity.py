@@ -105,7 +105,9 @@ def _spec(origin, size, dims, n_v, r=1):
 def test_capped_and_big_voxels(N):
     """Voxels holding up to a few hundred points: the cap keeps the lowest
     indices, through both the per-point ranking and the wave selection, in
-    the one-workgroup build (5000 points) and the seven-kernel build (12000)."""
+    the one-workgroup build (5000 points) and the brick build (12000: one
+    brick of 12000 points per cloud, built by six parts that meet in
+    memory)."""
     rng = np.random.default_rng(5)
     B = 3
     P = rng.random((B, N, 3), dtype=np.float32)
@@ -117,6 +119,41 @@ def test_capped_and_big_voxels(N):
         s = _spec((0, 0, 0), (0.125,) * 3, (8, 8, 8), n_v)
         run_both(P, s, 40, 32, "rvs", "knn", 3, where=f"n_v={n_v}")
     run_both(P, spec, 12, 64, "cas", "cube", 9, where="cas")
+
+
+@pytest.mark.parametrize("case", ["brick-capacity", "ragged-bricks", "grid-too-large-for-bricks"])
+def test_brick_build_edges(case):
+    """The brick build of larger clouds: bricks of 2048 consecutive voxels
+    holding exactly the 2048 points one work item takes and one more (then
+    split into two parts that meet in memory), voxels of more than 64 points
+    in both, a last brick cut short by the grid; and a grid with more bricks
+    than the build holds, which takes the seven-kernel build."""
+    rng = np.random.default_rng(11)
+    if case == "brick-capacity":
+        # 64 x 32 voxels per z-slice: brick q is slice z = q
+        B, N, dims, n_v = 2, 10000, (64, 32, 64), 16
+        P = rng.random((B, N, 3), dtype=np.float32) * np.float32([6.4, 3.2, 6.4])
+        P[:, 4197:, 2] = np.float32(0.3) + rng.random((B, N - 4197), dtype=np.float32) * np.float32(6.0)
+        P[:, :1948, 2] = np.float32(0.05)                 # brick 0: 1948 spread points
+        P[:, 1948:2048] = np.float32([0.33, 0.47, 0.05])  # and 100 in one voxel: 2048
+        P[:, 2048:3997, 2] = np.float32(0.15)             # brick 1: 1949 spread points
+        P[:, 3997:4097] = np.float32([0.33, 0.47, 0.15])  # and 100 in one voxel: 2049
+        P[:, 4097:4197] = np.float32([0.33, 0.47, 0.25])  # 100 in one voxel of brick 2
+        P = P[:, rng.permutation(N)]
+        spec = _spec((0, 0, 0), (0.1,) * 3, dims, n_v)
+    elif case == "ragged-bricks":
+        B, N, dims, n_v = 3, 9000, (70, 33, 50), 8
+        P = rng.random((B, N, 3), dtype=np.float32) * np.float32([7.0, 3.3, 5.0])
+        P[:, :300] = np.float32([6.95, 3.25, 4.95])      # the grid's last voxel
+        spec = _spec((0, 0, 0), (0.1,) * 3, dims, n_v)
+    else:
+        B, N, dims, n_v = 2, 9000, (512, 512, 128), 4
+        P = rng.random((B, N, 3), dtype=np.float32) * np.float32([5.12, 5.12, 1.28])
+        P[:, :500] = np.float32([0.001, 0.001, 0.001])
+        spec = _spec((0, 0, 0), (0.01,) * 3, dims, n_v)
+    print(f"[parity] brick build {case}: B={B} N={N} dims={dims} n_v={n_v}", flush=True)
+    run_both(P, spec, 300, 32, "rvs", "knn", 4, where=case)
+    run_both(P, spec, 300, 16, "rvs", "cube", 5, where=case + " cube")
 
 
 def test_all_points_in_one_voxel():
