@@ -1079,7 +1079,7 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     }
     lds_barrier();
 
-    // ranks of the words; the linear id of every occupied voxel at its slot
+    // ranks of the words
     uint64_t wd[kSmallWd];
     uint32_t cnt = 0;
 #pragma unroll
@@ -1098,12 +1098,13 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         s_wr[w] = r;
         bitmap[(size_t)b * W + w] = wd[j];
         word_rank[(size_t)b * W + w] = r;
-        for (uint64_t m = wd[j]; m; m &= m - 1) vox_lin[pb + r++] = (uint32_t)(w * 64 + __ffsll((unsigned long long)m) - 1);
+        r += (uint32_t)__popcll(wd[j]);
     }
     if (tid == 0) nvox[b] = (int32_t)nv;
     lds_barrier();
 
-    // slot and arrival position of every point, packed as slot << 16 | position
+    // slot and arrival position of every point, packed as slot << 16 | position;
+    // the first arrival in a voxel writes its linear id at its slot
     uint32_t sp[kSmallPts];
 #pragma unroll
     for (int k = 0; k < kSmallPts; ++k) {
@@ -1112,8 +1113,10 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         if (i >= N) continue;
         const uint32_t w = lin[k] >> 6;
         const uint32_t sl = s_wr[w] + (uint32_t)__popcll(s_bm[w] & ((1ull << (lin[k] & 63)) - 1));
-        sp[k] = (sl << 16) | atomicAdd(&s_off[sl], 1u);
+        const uint32_t pos = atomicAdd(&s_off[sl], 1u);
+        sp[k] = (sl << 16) | pos;
         pt_slot[pb + i] = sl;
+        if (pos == 0) vox_lin[pb + sl] = lin[k];
     }
     lds_barrier();
 
