@@ -1060,14 +1060,18 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
             cv[u] = c + 1u;
             const int64_t d = (c == 0 ? unit : 0) + (int64_t)beta_q16;
             if (d != 0) {
-                const uint64_t dec = (uint64_t)(-d) << 32;  // the score field falls by d
+                // the score field (the key's upper word) falls by d: a 32-bit
+                // add to that word changes the key exactly as the 64-bit add
+                // of -d << 32 would, and 64-bit loads of the key still see it
+                // whole (the lower word never changes)
+                const uint32_t dec = (uint32_t)(-d);
+                uint32_t* kw = reinterpret_cast<uint32_t*>(st.key + ob) + 1;
                 const uint32_t o_s = (uint32_t)((size_t)o_gid - ob);
                 const uint32_t n_ru = lq[0].x;
 #pragma unroll
                 for (int i = 0; i < 16; ++i) {
                     const uint32_t v = u4(lq[1 + i / 4], i % 4);
-                    if ((uint32_t)i < n_ru && v != o_s)
-                        atomicAdd((unsigned long long*)&st.key[ob + v], (unsigned long long)dec);
+                    if ((uint32_t)i < n_ru && v != o_s) atomicAdd(kw + 2 * (size_t)v, dec);
                 }
                 if (n_ru > 16) {
 #pragma unroll
@@ -1075,8 +1079,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
 #pragma unroll
                     for (int i = 16; i < 28; ++i) {
                         const uint32_t v = u4(lq[1 + (i - 16) / 4], i % 4);
-                        if ((uint32_t)i < n_ru && v != o_s)
-                            atomicAdd((unsigned long long*)&st.key[ob + v], (unsigned long long)dec);
+                        if ((uint32_t)i < n_ru && v != o_s) atomicAdd(kw + 2 * (size_t)v, dec);
                     }
                 }
             }
