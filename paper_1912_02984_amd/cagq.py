@@ -149,9 +149,18 @@ def workspace_layout(B: int, N: int, desc: GridDesc) -> LayoutC:
     return out
 
 
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+_cur_device = getattr(torch._C, "_cuda_getDevice", None)
+
+
 def _stream_ptr(stream: Optional[torch.cuda.Stream] = None):
-    s = stream if stream is not None else torch.cuda.current_stream()
-    return C.c_void_p(s.cuda_stream)
+    """The HIP stream to launch on: ``stream``, else torch's current stream
+    (read as a raw handle: building a Stream object per call costs ~3 us)."""
+    if stream is not None:
+        return C.c_void_p(stream.cuda_stream)
+    if _raw_stream is not None and _cur_device is not None:
+        return C.c_void_p(_raw_stream(_cur_device()))
+    return C.c_void_p(torch.cuda.current_stream().cuda_stream)
 
 
 def _ptr(t: Optional[torch.Tensor]):
