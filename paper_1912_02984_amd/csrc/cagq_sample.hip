@@ -904,6 +904,7 @@ __device__ __forceinline__ int32_t beats(const uint4 (&q)[4], uint32_t c, uint32
 // round R-1's bound and round R+1 retires the cloud: the stopping rule of the
 // two-kernel rounds, one round later.
 constexpr int kRoundThreads = 64;  // one wave per block: the blocks spread over every CU
+constexpr int kRoundEnt = 28;      // list entries a possible winner keeps in LDS
 __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5))) void k_cas_round(int32_t R, int32_t B, int32_t N, int64_t unit, uint32_t beta_q16,
                                                    int32_t M, const int32_t* __restrict__ nvox,
                                                    const uint32_t* __restrict__ nbr, CasState st, CasPtrs ctl) {
@@ -956,9 +957,9 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const uint4* el = reinterpret_cast<const uint4*>(nbr + (size_t)(in_range ? gid : 0) * kNbr32Stride);
     int32_t found = -2;  // -2: not competing, -1: no entry beats it so far
     uint32_t n2 = 0, n_r = 0;
-    // a possible winner's first 16 list entries (its voxels within r come
-    // first), kept for the wave's coverage pass below
-    __shared__ uint32_t s_ent[kRoundThreads][16];
+    // a possible winner's list entries that can be within r (those come
+    // first: at most 27), kept for the wave's coverage pass below
+    __shared__ uint32_t s_ent[kRoundThreads][kRoundEnt];
     if (active && s < nv) {
         if (rnd0 != 0) {
             above = pk0 > G ? 1u : 0u;
@@ -1012,6 +1013,11 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
                 uint4 q[4];
 #pragma unroll
                 for (int j = 0; j < 4; ++j) q[j] = e[1 + 4 * c + j];
+                if (c == 1) {  // entries 16..27, which can be within r
+                    uint4* se = reinterpret_cast<uint4*>(s_ent[wbase + owner] + 16);
+#pragma unroll
+                    for (int j = 0; j < 3; ++j) se[j] = q[j];
+                }
                 const int32_t f = beats(q, c, o_n2, (uint32_t)((size_t)o_gid - ob), o_my, cur, st.key + ob,
                                         st.round + ob);
                 if (f >= 0) s_found[wbase + owner] = f;  // any beating entry will do
@@ -1050,12 +1056,12 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
         if (p < total) {
             const uint32_t j = p - (o_incl - o_nr);
             const size_t ob = (size_t)o_b * N;
-            const uint32_t u = j < 16 ? s_ent[wb + owner][j] : nbr[(size_t)o_gid * kNbr32Stride + 4 + j];
+            const uint32_t u = s_ent[wb + owner][j];
             uint32_t* cv = st.cover + ob;
             const uint4* lu = reinterpret_cast<const uint4*>(nbr + (ob + u) * kNbr32Stride);
-            uint4 lq[5];  // header and entries 0..15 (a list within r holds at most 27)
+            uint4 lq[8];  // header and entries 0..27 (a list within r holds at most 27)
 #pragma unroll
-            for (int i = 0; i < 5; ++i) lq[i] = lu[i];
+            for (int i = 0; i < 8; ++i) lq[i] = lu[i];
             const uint32_t c = cv[u];
             cv[u] = c + 1u;
             const int64_t d = (c == 0 ? unit : 0) + (int64_t)beta_q16;
@@ -1069,18 +1075,9 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
                 const uint32_t o_s = (uint32_t)((size_t)o_gid - ob);
                 const uint32_t n_ru = lq[0].x;
 #pragma unroll
-                for (int i = 0; i < 16; ++i) {
+                for (int i = 0; i < 28; ++i) {
                     const uint32_t v = u4(lq[1 + i / 4], i % 4);
                     if ((uint32_t)i < n_ru && v != o_s) atomicAdd(kw + 2 * (size_t)v, dec);
-                }
-                if (n_ru > 16) {
-#pragma unroll
-                    for (int i = 0; i < 3; ++i) lq[1 + i] = lu[5 + i];
-#pragma unroll
-                    for (int i = 16; i < 28; ++i) {
-                        const uint32_t v = u4(lq[1 + (i - 16) / 4], i % 4);
-                        if ((uint32_t)i < n_ru && v != o_s) atomicAdd(kw + 2 * (size_t)v, dec);
-                    }
                 }
             }
         }
