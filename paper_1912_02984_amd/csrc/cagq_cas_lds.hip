@@ -197,6 +197,110 @@ __device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, 
     }
 }
 
+// The picking pass over a long queue (r = 1): one lane per voxel checks the
+// kPre groups of entries loaded with its list's header. A voxel that none of
+// them beats and whose list is longer (an open voxel) goes on to a second
+// stage in which 16 lanes of its wave take it, four voxels at a time: each
+// lane loads one group, lanes 0..11 the groups after the first kPre (they
+// check them for a larger key), lanes 12..15 the first kPre again, so that
+// a winner's 16 lanes then mark its whole list one group each, without
+// another load. Every lane of the wave must call it.
+template <int ST>
+__device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, const uint16_t* nb,
+                                            const uint16_t* que, const uint32_t* key, uint16_t* rnd,
+                                            uint16_t* blk, uint16_t* dty, uint8_t* cov) {
+    constexpr int kRoom = (ST - 8) / 8;  // groups a slot's storage holds after its header
+    static_assert(kRoom == 16 && kPre == 4, "16 lanes take the 16 groups of an r = 1 list");
+    const int lane = lane_id();
+    const int sub = lane & 15, quad = lane >> 4;
+    // the group lane `sub` of a voxel's 16 loads in the second stage
+    const uint32_t gq = sub < kRoom - kPre ? (uint32_t)(kPre + sub) : (uint32_t)(sub - (kRoom - kPre));
+    for (uint32_t i0 = (uint32_t)(tid - lane); i0 < qb; i0 += kT) {
+        const uint32_t i = i0 + (uint32_t)lane;
+        uint32_t s = 0, my = 0, n_r = 0, n2 = 0;
+        bool open = false;
+        if (i < qb) {
+            s = que[i];
+            my = key[s];
+            const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
+            const uint4 h = e[0];
+            uint4 pre[kPre];
+#pragma unroll
+            for (int t = 0; t < kPre; ++t) pre[t] = e[1 + t];
+            n_r = h.x & 0xFFFFu;
+            n2 = h.x >> 16;
+            const uint32_t nch = (n2 + 7) / 8;  // n2 >= 1: the voxel itself
+            uint32_t hit = ~0u;
+#pragma unroll
+            for (int t = 0; t < kPre; ++t) {
+                if ((uint32_t)t >= nch || hit != ~0u) break;
+                uint32_t sl[8], kk[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sl[j] = (uint32_t)(t * 8 + j) < n2 ? entry(pre[t], j) : s;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (hit == ~0u && kk[j] > my) hit = ((uint32_t)(t * 8 + j) << 16) | sl[j];
+            }
+            if (hit != ~0u) {
+                blk[s] = (uint16_t)(hit & 0xFFFFu);
+            } else if (nch > (uint32_t)kPre) {
+                open = true;
+            } else {  // a short list, all checked: a winner, marked from the groups at hand
+                rnd[s] = cur;
+                blk[s] = (uint16_t)(my >> 16);
+                dty[s] = (uint16_t)(my & 0xFFFFu);
+#pragma unroll
+                for (int t = 0; t < kPre; ++t)
+                    if ((uint32_t)t < nch) mark(pre[t], (uint32_t)t * 8, n_r, n2, s, cur, rnd, dty, cov);
+            }
+        }
+        for (uint64_t om = __ballot(open); om;) {
+            // the quad-th open lane of the next four
+            uint64_t m = om;
+            for (int k = 0; k < quad && m; ++k) m &= m - 1;
+            const bool act = m != 0;
+            const int src = act ? __ffsll((unsigned long long)m) - 1 : 0;
+            for (int k = 0; k < 4 && om; ++k) om &= om - 1;
+            const uint32_t vs = (uint32_t)__shfl((int)s, src, kWave);
+            const uint32_t vmy = (uint32_t)__shfl((int)my, src, kWave);
+            const uint32_t vnr = (uint32_t)__shfl((int)n_r, src, kWave);
+            const uint32_t vn2 = (uint32_t)__shfl((int)n2, src, kWave);
+            const uint32_t vnch = (vn2 + 7) / 8;
+            const bool mine = act && gq < vnch;  // this lane's group holds entries of the list
+            uint4 q = make_uint4(0u, 0u, 0u, 0u);
+            if (mine) q = reinterpret_cast<const uint4*>(nb + (size_t)vs * ST)[1 + gq];
+            uint32_t hit = ~0u;
+            if (mine && gq >= (uint32_t)kPre) {
+                uint32_t sl[8], kk[8];
+#pragma unroll
+                for (int j = 0; j < 8; ++j) sl[j] = gq * 8 + (uint32_t)j < vn2 ? entry(q, j) : vs;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) kk[j] = key[sl[j]];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if (hit == ~0u && kk[j] > vmy) hit = ((gq * 8 + (uint32_t)j) << 16) | sl[j];
+            }
+#pragma unroll
+            for (int d = 1; d < 16; d <<= 1) {
+                const uint32_t o = (uint32_t)__shfl_xor((int)hit, d, kWave);
+                hit = o < hit ? o : hit;
+            }
+            if (act && hit != ~0u) {
+                if (sub == 0) blk[vs] = (uint16_t)(hit & 0xFFFFu);
+            } else if (act) {
+                if (sub == 0) {
+                    rnd[vs] = cur;
+                    blk[vs] = (uint16_t)(vmy >> 16);
+                    dty[vs] = (uint16_t)(vmy & 0xFFFFu);
+                }
+                if (mine) mark(q, gq * 8, vnr, vn2, vs, cur, rnd, dty, cov);
+            }
+        }
+    }
+}
+
 template <int RAD>
 __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t cap,
                                                 const int32_t* __restrict__ nvox,
@@ -335,13 +439,18 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
             break;
         }
         const uint32_t qb = s_qb;
-        // a short queue gets 16 lanes per voxel with r = 1, one group of
+        // with r = 1 a short queue gets 16 lanes per voxel, one group of
         // list entries each, in at most two passes (2, 4 or 8 lanes per
-        // voxel spill registers here)
-        if (RAD == 1 && qb <= kT / 8)
-            drain_picks<16, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
-        else
+        // voxel spill registers here); a longer one gets 16 lanes only for
+        // the voxels that the first groups of their lists do not decide
+        if constexpr (RAD == 1) {
+            if (qb <= kT / 8)
+                drain_picks<16, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
+            else
+                drain_mixed<ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
+        } else {
             drain_picks<1, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
+        }
     }
     if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
     __syncthreads();
