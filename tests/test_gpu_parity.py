@@ -294,6 +294,21 @@ def test_rvs_many_block_selection_bounds(M):
     run_both(w.points(B=2), L.grid, M, 8, "rvs", "cube", 11 + M, where=f"M={M}")
 
 
+@pytest.mark.parametrize("B,N,dims,M", [(1, 600000, (128, 128, 64), 250000),
+                                        (2, 300000, (100, 100, 50), 90000),
+                                        (3, 40000, (64, 64, 32), 20000)])
+def test_rvs_many_block_selection_large_clouds(B, N, dims, M):
+    """The many-block RVS select on larger and more clouds than the indoor
+    scenes: m = 250K of ~457K occupied voxels (a bound digit holding many
+    keys), 90K of ~226K in each of two clouds, 20K of ~34K in each of
+    three."""
+    rng = np.random.default_rng(N + M)
+    P = rng.random((B, N, 3), dtype=np.float32) * np.float32(0.999)
+    spec = _spec((0, 0, 0), tuple(1.0 / d for d in dims), dims, 4)
+    print(f"[parity] rvs many-block B={B} N={N} M={M}", flush=True)
+    run_both(P, spec, M, 4, "rvs", "cube", 17, where=f"B={B} N={N} M={M}")
+
+
 def test_rvs_many_block_selection_dense_cloud():
     """A dense cloud (about 140K of 262K voxels occupied): M from one center
     to beyond the occupied voxels."""
