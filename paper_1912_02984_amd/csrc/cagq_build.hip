@@ -1053,30 +1053,37 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     if (tid == 0) s_nbig = 0;
     lds_barrier();
 
-    // voxelize: linear id, occupancy bit
+    // voxelize: linear id, occupancy bit (every point's coordinates are
+    // loaded first, so that their loads are in flight together)
+    float pc[kSmallPts][3];
+#pragma unroll
+    for (int k = 0; k < kSmallPts; ++k) {
+        const int32_t i = tid + k * kSmallT;
+        const float* p = P + (pb + (i < N ? i : 0)) * 3;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) pc[k][a] = p[a];
+    }
     uint32_t lin[kSmallPts];
+    bool bad = false;
 #pragma unroll
     for (int k = 0; k < kSmallPts; ++k) {
         const int32_t i = tid + k * kSmallT;
         lin[k] = 0;
         if (i >= N) continue;
-        const float* p = P + (pb + i) * 3;
-        const float c[3] = {p[0], p[1], p[2]};
         uint32_t gg[3];
-        bool bad = false;
 #pragma unroll
         for (int a = 0; a < 3; ++a) {
-            if (!isfinite(c[a])) {
+            if (!isfinite(pc[k][a])) {
                 bad = true;
                 gg[a] = 0;
             } else {
-                gg[a] = (uint32_t)axis_index(c[a], g.o[a], g.s[a], g.D[a]);
+                gg[a] = (uint32_t)axis_index(pc[k][a], g.o[a], g.s[a], g.D[a]);
             }
         }
         lin[k] = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
         atomicOr(reinterpret_cast<unsigned long long*>(&s_bm[lin[k] >> 6]), 1ull << (lin[k] & 63));
-        if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
     }
+    if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
     lds_barrier();
 
     // ranks of the words
@@ -1104,7 +1111,8 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     lds_barrier();
 
     // slot and arrival position of every point, packed as slot << 16 | position;
-    // the first arrival in a voxel writes its linear id at its slot
+    // the first arrival in a voxel puts its linear id at its slot of s_bk
+    // (free until the buckets), for the coalesced writes after the offsets
     uint32_t sp[kSmallPts];
 #pragma unroll
     for (int k = 0; k < kSmallPts; ++k) {
@@ -1116,7 +1124,7 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         const uint32_t pos = atomicAdd(&s_off[sl], 1u);
         sp[k] = (sl << 16) | pos;
         pt_slot[pb + i] = sl;
-        if (pos == 0) vox_lin[pb + sl] = lin[k];
+        if (pos == 0) s_bk[sl] = lin[k];
     }
     lds_barrier();
 
@@ -1136,8 +1144,6 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         const uint32_t sl = (uint32_t)tid * kSmallPts + j;
         if (sl >= nv) break;
         const uint32_t full = (uint32_t)(run >> 31), stored = (uint32_t)(run & 0x7FFFFFFFu);
-        vo[sl] = stored;
-        vox_count[pb + sl] = c8[j];
         s_off[sl] = (full << 16) | stored;
         if (c8[j] > kBigVoxel) s_big[atomicAdd(&s_nbig, 1u)] = sl;
         run += ((uint64_t)c8[j] << 31) | (c8[j] < n_v ? c8[j] : n_v);
@@ -1147,6 +1153,15 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         s_off[nv] = ((uint32_t)(total >> 31) << 16) | (uint32_t)(total & 0x7FFFFFFFu);
     }
     lds_barrier();
+    // offsets, counts and linear ids, each slot's from LDS: consecutive
+    // threads store consecutive slots
+    for (uint32_t sl = (uint32_t)tid; sl < nv; sl += kSmallT) {
+        const uint32_t o0 = s_off[sl], o1 = s_off[sl + 1];
+        vo[sl] = o0 & 0xFFFFu;
+        vox_count[pb + sl] = (o1 >> 16) - (o0 >> 16);
+        vox_lin[pb + sl] = s_bk[sl];
+    }
+    lds_barrier();  // s_bk is read above and filled below
 
     // buckets
 #pragma unroll
