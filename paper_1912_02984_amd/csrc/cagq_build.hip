@@ -348,14 +348,23 @@ __global__ __launch_bounds__(kSortT) void k_bhist(const float* __restrict__ P, i
     const int32_t t = (int32_t)blockIdx.x;
     for (int32_t i = tid; i < BQ; i += kSortT) s_h[i] = 0u;
     for (int64_t i = (int64_t)t * kSortT + tid; i < n16; i += (int64_t)T * kSortT) clr[i] = make_uint4(0u, 0u, 0u, 0u);
+    // the points' coordinates first, all loads in flight together (a load
+    // under the bounds test would be waited for before the next is issued)
+    float c[kSortIPT][3];
+#pragma unroll
+    for (int k = 0; k < kSortIPT; ++k) {
+        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        const float* p = P + (size_t)(gid < BN ? gid : 0) * 3;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) c[k][a] = p[a];
+    }
     lds_barrier();
 #pragma unroll
     for (int k = 0; k < kSortIPT; ++k) {
         const int32_t gid = t * kSortTile + k * kSortT + tid;
         if (gid >= BN) break;
-        const float* p = P + (size_t)gid * 3;
         bool bad = false;
-        const uint32_t lin = voxel_lin(p[0], p[1], p[2], g, bad);
+        const uint32_t lin = voxel_lin(c[k][0], c[k][1], c[k][2], g, bad);
         atomicAdd(&s_h[(gid / N) * Q + (int32_t)(lin / kBrickV)], 1u);
     }
     lds_barrier();
@@ -471,14 +480,22 @@ __global__ __launch_bounds__(kSortT) void k_bscatter(const float* __restrict__ P
     }
     const uint32_t* row = hist + (size_t)t * BQ;
     for (int32_t i = tid; i < BQ; i += kSortT) s_o[i] = row[i];
+    // the points' coordinates first, all loads in flight together
+    float c[kSortIPT][3];
+#pragma unroll
+    for (int k = 0; k < kSortIPT; ++k) {
+        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        const float* p = P + (size_t)(gid < BN ? gid : 0) * 3;
+#pragma unroll
+        for (int a = 0; a < 3; ++a) c[k][a] = p[a];
+    }
     lds_barrier();
     bool bad = false;
 #pragma unroll
     for (int k = 0; k < kSortIPT; ++k) {
         const int32_t gid = t * kSortTile + k * kSortT + tid;
         if (gid >= BN) break;
-        const float* p = P + (size_t)gid * 3;
-        const float x = p[0], y = p[1], z = p[2];
+        const float x = c[k][0], y = c[k][1], z = c[k][2];
         const uint32_t lin = voxel_lin(x, y, z, g, bad);
         const int32_t b = gid / N;
         const uint32_t pos = atomicAdd(&s_o[b * Q + (int32_t)(lin / kBrickV)], 1u);
@@ -615,13 +632,21 @@ template <bool MARK>
 __device__ __forceinline__ void brick_voxels(const BrickArgs& a, WordLds& s, const BrickItem& it,
                                              uint32_t (&v)[kBrickIPT], uint32_t (&idx)[kBrickIPT]) {
     const uint32_t vbase = (uint32_t)it.q * kBrickV;
+    // every point's load first, so that they are in flight together (a load
+    // used under its bounds test would be waited for before the next)
+    float4 ee[kBrickIPT];
+#pragma unroll
+    for (int k = 0; k < kBrickIPT; ++k) {
+        const uint32_t i = threadIdx.x + k * kBrickT;
+        if (i < it.n) ee[k] = a.sorted[it.p0 + i];
+    }
 #pragma unroll
     for (int k = 0; k < kBrickIPT; ++k) {
         const uint32_t i = threadIdx.x + k * kBrickT;
         v[k] = 0u;
         idx[k] = 0u;
         if (i < it.n) {
-            const float4 e = a.sorted[it.p0 + i];
+            const float4 e = ee[k];
             bool bad = false;
             v[k] = voxel_lin(e.x, e.y, e.z, a.g, bad) - vbase;
             idx[k] = __float_as_uint(e.w);
@@ -779,10 +804,19 @@ __global__ __launch_bounds__(kBrickT) void k_brick(BrickArgs a) {
     const int tid = threadIdx.x;
     const int lane = lane_id();
     const int wv = tid / kWave;
-    // the cloud's bricks before this one (loads issued with the range's)
+    // the cloud's bricks before this one (loads issued with the range's,
+    // four per thread at a time)
     uint64_t pre = 0;
     const uint64_t* ag = a.agg + (size_t)it.b * a.Q;
-    for (int32_t j = tid; j < it.q; j += kBrickT) pre += ag[j];
+    for (int32_t j0 = 0; j0 < it.q; j0 += 4 * kBrickT) {
+        uint64_t x[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int32_t j = j0 + u * kBrickT + tid;
+            x[u] = j < it.q ? ag[j] : 0ull;
+        }
+        pre += (x[0] + x[1]) + (x[2] + x[3]);
+    }
     const uint64_t my = ag[it.q];
     brick_range(a, it);
     const uint32_t vbase = (uint32_t)it.q * kBrickV;
