@@ -94,10 +94,21 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
     // bits H-RAD..H+RAD of a row of half-width H are the voxels within r in x
     constexpr uint32_t kInner = ((1u << (2 * RAD + 1)) - 1) << (H - RAD);
     if constexpr (RAD == 1) {
-        // all 25 rows of the window at once
+        // the 25 rows of the window, a plane of 5 at a time
         GridRow rows[S2 * S2];
 #pragma unroll
-        for (int j = 0; j < S2 * S2; ++j) rows[j] = load_row(bm, wr, g, x, y + j % S2 - H, z + j / S2 - H, H);
+        for (int pl = 0; pl < S2; ++pl) {
+            int32_t yy[S2], zz[S2];
+            GridRow rp[S2];
+#pragma unroll
+            for (int i = 0; i < S2; ++i) {
+                yy[i] = y + i - H;
+                zz[i] = z + pl - H;
+            }
+            load_rows<S2>(bm, wr, g, x, yy, zz, H, rp);
+#pragma unroll
+            for (int i = 0; i < S2; ++i) rows[pl * S2 + i] = rp[i];
+        }
 #pragma unroll
         for (int j = 0; j < S2 * S2; ++j) {
             const int dy = j % S2 - H, dz = j / S2 - H;

@@ -408,14 +408,49 @@ __device__ __forceinline__ GridRow load_row(const uint64_t* __restrict__ bm, con
     const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
     const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
     const uint32_t w0 = lo >> 6, o = lo & 63;
+    // the word's rank is loaded with the words (its address does not depend
+    // on them), so that the row costs one load latency
+    const uint32_t rk = wr[w0];
     const uint64_t a = bm[w0];
     const uint64_t c = bm[hi >> 6];
     // when both ends share a word, the bits shifted in from c lie above the segment
     const uint64_t bits = (a >> o) | (o ? c << (64 - o) : 0ull);
     GridRow r;
     r.mask = inside ? (uint32_t)(bits & ((1ull << (hi_x - lo_x + 1)) - 1)) << (lo_x - xs) : 0u;
-    r.first = wr[w0] + (uint32_t)__popcll(a & ((1ull << o) - 1));
+    r.first = rk + (uint32_t)__popcll(a & ((1ull << o) - 1));
     return r;
+}
+
+// NR rows (yy[i], zz[i]) around the same x at once, as load_row each: all
+// their loads are issued before any is used, so that the rows cost one load
+// latency together instead of one each.
+template <int NR>
+__device__ __forceinline__ void load_rows(const uint64_t* __restrict__ bm, const uint32_t* __restrict__ wr,
+                                          const GridDims& g, int32_t x, const int32_t (&yy)[NR],
+                                          const int32_t (&zz)[NR], int32_t h, GridRow (&out)[NR]) {
+    const int32_t xs = x - h;
+    const int32_t lo_x = xs < 0 ? 0 : xs;
+    const int32_t hi_x = x + h > g.D[0] - 1 ? g.D[0] - 1 : x + h;
+    uint32_t rk[NR], o[NR];
+    uint64_t a[NR], c[NR];
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+        const int32_t yc = yy[i] < 0 ? 0 : (yy[i] >= g.D[1] ? g.D[1] - 1 : yy[i]);
+        const int32_t zc = zz[i] < 0 ? 0 : (zz[i] >= g.D[2] ? g.D[2] - 1 : zz[i]);
+        const uint32_t base = (uint32_t)g.D[0] * ((uint32_t)yc + (uint32_t)g.D[1] * (uint32_t)zc);
+        const uint32_t lo = base + (uint32_t)lo_x, hi = base + (uint32_t)hi_x;
+        o[i] = lo & 63;
+        rk[i] = wr[lo >> 6];
+        a[i] = bm[lo >> 6];
+        c[i] = bm[hi >> 6];
+    }
+#pragma unroll
+    for (int i = 0; i < NR; ++i) {
+        const bool inside = yy[i] >= 0 && yy[i] < g.D[1] && zz[i] >= 0 && zz[i] < g.D[2];
+        const uint64_t bits = (a[i] >> o[i]) | (o[i] ? c[i] << (64 - o[i]) : 0ull);
+        out[i].mask = inside ? (uint32_t)(bits & ((1ull << (hi_x - lo_x + 1)) - 1)) << (lo_x - xs) : 0u;
+        out[i].first = rk[i] + (uint32_t)__popcll(a[i] & ((1ull << o[i]) - 1));
+    }
 }
 
 __device__ __forceinline__ void decode_lin(uint32_t lin, const GridDims& g, int32_t& x, int32_t& y, int32_t& z) {
