@@ -655,11 +655,15 @@ __global__ __launch_bounds__(256) void k_cas_score(
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
     // the voxel's own state is loaded up front, together with the cloud's,
-    // so that the chain of dependent loads stays short
-    const uint32_t rnd0 = in_range ? st.round[gid] : 0u;
-    const uint32_t dty0 = in_range ? st.dirty[gid] : 0u;
-    const uint64_t key0 = in_range ? st.key[gid] : 0ull;
-    const uint32_t lin0 = in_range ? vox_lin[gid] : 0u;
+    // so that the chain of dependent loads stays short (from a valid index
+    // for every lane: a load under the range test would be waited for alone)
+    const size_t gc = in_range ? (size_t)gid : 0;
+    const uint32_t rnd0_ = st.round[gc], dty0_ = st.dirty[gc], lin0_ = vox_lin[gc];
+    const uint64_t key0_ = st.key[gc];
+    const uint32_t rnd0 = in_range ? rnd0_ : 0u;
+    const uint32_t dty0 = in_range ? dty0_ : 0u;
+    const uint64_t key0 = in_range ? key0_ : 0ull;
+    const uint32_t lin0 = in_range ? lin0_ : 0u;
     bool active = in_range && ctl.done[b] == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
         __hip_atomic_store(ctl.host + 1, ctl.epoch | (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
@@ -913,10 +917,16 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
     // the voxel's own state is loaded up front, together with the cloud's
-    const uint32_t rnd0 = in_range ? st.round[gid] : 0u;
-    const uint64_t pk0 = in_range ? st.pick[gid] : 0ull;
-    const uint64_t my0 = in_range ? st.key[gid] : 0ull;
-    const int32_t bl0 = in_range ? st.blocker[gid] : -1;
+    // (from a valid index for every lane: a load under the range test would
+    // be waited for alone)
+    const size_t gc = in_range ? (size_t)gid : 0;
+    const uint32_t rnd0_ = st.round[gc];
+    const uint64_t pk0_ = st.pick[gc], my0_ = st.key[gc];
+    const int32_t bl0_ = st.blocker[gc];
+    const uint32_t rnd0 = in_range ? rnd0_ : 0u;
+    const uint64_t pk0 = in_range ? pk0_ : 0ull;
+    const uint64_t my0 = in_range ? my0_ : 0ull;
+    const int32_t bl0 = in_range ? bl0_ : -1;
     bool active = in_range && ctl.done[b] == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
         __hip_atomic_store(ctl.host + 1, ctl.epoch | (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
