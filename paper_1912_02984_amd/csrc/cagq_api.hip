@@ -67,6 +67,8 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->T = (int32_t)(((int64_t)B * N + kSortTile - 1) / kSortTile);
     // the histogram matrix (B * Q by T entries) stays within 2^24 entries
     L->bricks = (int64_t)B * L->Q <= kMaxBricks && (int64_t)B * L->Q * L->T <= (int64_t(1) << 24);
+    // a cloud's points span at most ceil(N / kSortTile) + 1 tiles
+    L->tile_scan = L->bricks && ((int64_t)(N + kSortTile - 1) / kSortTile + 1) * L->Q <= kTileScanCap;
     const size_t BQ = L->bricks ? (size_t)B * L->Q : 0;
     const size_t hist_n = BQ * (size_t)L->T;
     L->items_max = L->bricks ? (int64_t)BQ + ((int64_t)BN + kBrickCap - 1) / kBrickCap : 0;

@@ -337,23 +337,27 @@ __device__ __forceinline__ uint32_t voxel_lin(float x, float y, float z, const G
     return gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
 }
 
-// Row t of the histogram: points of tile t in each brick of the batch. The
-// blocks also zero the control words [clr, clr + n16) (status, tickets,
-// descriptors) that the later kernels use.
+// Row t of the histogram: points of tile t in each brick of the batch (with
+// `own`, only the entries of the bricks of the clouds the tile holds points
+// of, which are the only ones read then). The blocks also zero the control
+// words [clr, clr + n16) (status, tickets, descriptors) that the later
+// kernels use.
 __global__ __launch_bounds__(kSortT) void k_bhist(const float* __restrict__ P, int32_t N, int32_t BN, GridArgs g,
-                                                  int32_t Q, int32_t BQ, int32_t T, uint32_t* __restrict__ hist,
-                                                  uint4* __restrict__ clr, int64_t n16) {
+                                                  int32_t Q, int32_t BQ, int32_t T, bool own,
+                                                  uint32_t* __restrict__ hist, uint4* __restrict__ clr, int64_t n16) {
     __shared__ uint32_t s_h[kMaxBricks];
     const int tid = threadIdx.x;
     const int32_t t = (int32_t)blockIdx.x;
-    for (int32_t i = tid; i < BQ; i += kSortT) s_h[i] = 0u;
+    const int32_t p0 = t * kSortTile, p1 = p0 + kSortTile < BN ? p0 + kSortTile : BN;
+    const int32_t e0 = own ? (p0 / N) * Q : 0, e1 = own ? ((p1 - 1) / N + 1) * Q : BQ;
+    for (int32_t i = e0 + tid; i < e1; i += kSortT) s_h[i] = 0u;
     for (int64_t i = (int64_t)t * kSortT + tid; i < n16; i += (int64_t)T * kSortT) clr[i] = make_uint4(0u, 0u, 0u, 0u);
     // the points' coordinates first, all loads in flight together (a load
     // under the bounds test would be waited for before the next is issued)
     float c[kSortIPT][3];
 #pragma unroll
     for (int k = 0; k < kSortIPT; ++k) {
-        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        const int32_t gid = p0 + k * kSortT + tid;
         const float* p = P + (size_t)(gid < BN ? gid : 0) * 3;
 #pragma unroll
         for (int a = 0; a < 3; ++a) c[k][a] = p[a];
@@ -361,7 +365,7 @@ __global__ __launch_bounds__(kSortT) void k_bhist(const float* __restrict__ P, i
     lds_barrier();
 #pragma unroll
     for (int k = 0; k < kSortIPT; ++k) {
-        const int32_t gid = t * kSortTile + k * kSortT + tid;
+        const int32_t gid = p0 + k * kSortT + tid;
         if (gid >= BN) break;
         bool bad = false;
         const uint32_t lin = voxel_lin(c[k][0], c[k][1], c[k][2], g, bad);
@@ -369,7 +373,7 @@ __global__ __launch_bounds__(kSortT) void k_bhist(const float* __restrict__ P, i
     }
     lds_barrier();
     uint32_t* row = hist + (size_t)t * BQ;
-    for (int32_t i = tid; i < BQ; i += kSortT) row[i] = s_h[i];
+    for (int32_t i = e0 + tid; i < e1; i += kSortT) row[i] = s_h[i];
 }
 
 // Sorted positions and work items: bstart[g] = points of the bricks before g
@@ -460,26 +464,99 @@ __global__ __launch_bounds__(kScanThreads) void k_hscan(uint32_t* __restrict__ h
     }
 }
 
+// Exclusive scan of one value per thread of a kSortT block; *total receives
+// the block sum. Every thread of the block calls it.
+__device__ __forceinline__ uint32_t sort_excl_scan(uint32_t v, uint32_t* s_wave, uint32_t* total) {
+    const uint32_t incl = wave_incl_scan<uint32_t>(v);
+    const int wv = threadIdx.x / kWave;
+    if (lane_id() == kWave - 1) s_wave[wv] = incl;
+    lds_barrier();
+    uint32_t off = 0, tot = 0;
+#pragma unroll
+    for (int i = 0; i < kSortT / kWave; ++i) {
+        const uint32_t x = s_wave[i];
+        off += i < wv ? x : 0u;
+        tot += x;
+    }
+    lds_barrier();
+    *total = tot;
+    return off + incl - v;
+}
+
+// The first sorted position of tile t's points in each brick of the clouds
+// it holds points of, into s_o (indexed by brick): per brick, the column of
+// the histogram over the cloud's tiles gives the points of the tiles before
+// t and the brick's total, and an exclusive scan of the totals over the
+// cloud's bricks (clouds hold N sorted positions each) gives the brick's
+// first position. The cloud's first tile also writes those (bstart) and
+// lists the bricks of more than kBrickCap points (heavy): one more work item
+// per further kBrickCap points in item_extra as (part << 32 | brick),
+// numbered in hlist and counted in the status words.
+__device__ __forceinline__ void tile_columns(int32_t t, int32_t N, int32_t BN, int32_t Q, int32_t BQ,
+                                             const uint32_t* __restrict__ hist, uint32_t* s_o, uint32_t* s_wave,
+                                             uint32_t* __restrict__ bstart, int32_t* __restrict__ brick_hb,
+                                             uint64_t* __restrict__ item_extra, uint32_t* __restrict__ hlist,
+                                             uint32_t* __restrict__ hebase, int* __restrict__ status) {
+    constexpr int kU = 32;  // column loads in flight per thread (a cloud of up to 126976 points: all of them)
+    const int tid = threadIdx.x;
+    const int32_t p0 = t * kSortTile, p1 = p0 + kSortTile < BN ? p0 + kSortTile : BN;
+    for (int32_t b = p0 / N; b <= (p1 - 1) / N; ++b) {
+        const int32_t tf = (int32_t)((int64_t)b * N / kSortTile);
+        const int32_t tl = (int32_t)((((int64_t)b + 1) * N - 1) / kSortTile);
+        uint32_t carry = (uint32_t)b * (uint32_t)N;
+        for (int32_t q0 = 0; q0 < Q; q0 += kSortT) {
+            const int32_t q = q0 + tid;
+            const size_t col = (size_t)b * Q + (q < Q ? q : 0);
+            uint32_t pre = 0, tot = 0;
+            for (int32_t t0 = tf; t0 <= tl; t0 += kU) {
+                uint32_t x[kU];
+#pragma unroll
+                for (int u = 0; u < kU; ++u) x[u] = hist[(size_t)(t0 + u <= tl ? t0 + u : tl) * BQ + col];
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const uint32_t v = t0 + u <= tl ? x[u] : 0u;
+                    tot += v;
+                    pre += t0 + u < t ? v : 0u;
+                }
+            }
+            if (q >= Q) tot = 0;
+            uint32_t sum;
+            const uint32_t start = carry + sort_excl_scan(tot, s_wave, &sum);
+            carry += sum;
+            if (q >= Q) continue;
+            const int32_t gg = b * Q + q;
+            s_o[gg] = start + pre;
+            if (t != tf) continue;
+            bstart[gg] = start;
+            int32_t hb = -1;
+            if (tot > (uint32_t)kBrickCap) {
+                const uint32_t parts = (tot + kBrickCap - 1) / kBrickCap;
+                hb = atomicAdd(&status[kStHeavy], 1);
+                const uint32_t eb = (uint32_t)atomicAdd(&status[kStItems], (int)(parts - 1));
+                hlist[hb] = (uint32_t)gg;
+                hebase[hb] = eb;
+                for (uint32_t k = 1; k < parts; ++k) item_extra[eb + k - 1] = ((uint64_t)k << 32) | (uint32_t)gg;
+            }
+            brick_hb[gg] = hb;
+        }
+    }
+}
+
 // One lane per point: (x, y, z, index) at the next free position of its
-// brick within the tile's range.
+// brick within the tile's range. With SCAN the tile finds its ranges from
+// the histogram columns itself (tile_columns); otherwise k_hscan has
+// rewritten row t of the histogram into them.
+template <bool SCAN>
 __global__ __launch_bounds__(kSortT) void k_bscatter(const float* __restrict__ P, int32_t N, int32_t BN, GridArgs g,
-                                                     int32_t Q, int32_t BQ, int64_t W, const uint32_t* __restrict__ hist,
-                                                     float4* __restrict__ sorted, const uint32_t* __restrict__ hlist,
-                                                     uint64_t* __restrict__ bitmap, int* __restrict__ status) {
+                                                     int32_t Q, int32_t BQ, const uint32_t* __restrict__ hist,
+                                                     float4* __restrict__ sorted, uint32_t* __restrict__ bstart,
+                                                     int32_t* __restrict__ brick_hb, uint64_t* __restrict__ item_extra,
+                                                     uint32_t* __restrict__ hlist, uint32_t* __restrict__ hebase,
+                                                     int* __restrict__ status) {
     __shared__ uint32_t s_o[kMaxBricks];
+    __shared__ uint32_t s_wave[kSortT / kWave];
     const int tid = threadIdx.x;
     const int32_t t = (int32_t)blockIdx.x;
-    // heavy bricks: their occupancy words start at zero (their parts OR into them)
-    const uint64_t nz = (uint64_t)(uint32_t)status[kStHeavy] * kBrickW;
-    for (uint64_t i = (uint64_t)t * kSortT + tid; i < nz; i += (uint64_t)gridDim.x * kSortT) {
-        const uint32_t hb = (uint32_t)(i / kBrickW), j = (uint32_t)(i % kBrickW);
-        const int32_t gg = (int32_t)hlist[hb];
-        const int32_t bb = gg / Q, qq = gg - bb * Q;
-        const int64_t w = (int64_t)qq * kBrickW + j;
-        if (w < W) bitmap[(size_t)bb * W + w] = 0ull;
-    }
-    const uint32_t* row = hist + (size_t)t * BQ;
-    for (int32_t i = tid; i < BQ; i += kSortT) s_o[i] = row[i];
     // the points' coordinates first, all loads in flight together
     float c[kSortIPT][3];
 #pragma unroll
@@ -488,6 +565,12 @@ __global__ __launch_bounds__(kSortT) void k_bscatter(const float* __restrict__ P
         const float* p = P + (size_t)(gid < BN ? gid : 0) * 3;
 #pragma unroll
         for (int a = 0; a < 3; ++a) c[k][a] = p[a];
+    }
+    if constexpr (SCAN) {
+        tile_columns(t, N, BN, Q, BQ, hist, s_o, s_wave, bstart, brick_hb, item_extra, hlist, hebase, status);
+    } else {
+        const uint32_t* row = hist + (size_t)t * BQ;
+        for (int32_t i = tid; i < BQ; i += kSortT) s_o[i] = row[i];
     }
     lds_barrier();
     bool bad = false;
@@ -1290,13 +1373,16 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
         const int32_t BQ = B * L.Q;
         uint32_t* hist = at<uint32_t>(ws, L.hist);
         int* status_w = at<int>(ws, L.status);
-        k_bhist<<<(unsigned)L.T, kSortT, 0, s>>>(points, N, BN, g, L.Q, BQ, L.T, hist, at<uint4>(ws, L.status),
-                                                 (int64_t)(L.clear_brick - L.status) / 16);
-        k_hscan<<<(unsigned)((BQ + kHGroup - 1) / kHGroup), kScanThreads, 0, s>>>(
-            hist, BQ, L.T, at<uint32_t>(ws, L.bstart), at<int32_t>(ws, L.brick_hb), at<uint64_t>(ws, L.item_extra),
-            at<uint32_t>(ws, L.hlist), at<uint32_t>(ws, L.hebase), at<uint64_t>(ws, L.desc_h), status_w);
-        k_bscatter<<<(unsigned)L.T, kSortT, 0, s>>>(points, N, BN, g, L.Q, BQ, L.W, hist, at<float4>(ws, L.sorted),
-                                                    at<uint32_t>(ws, L.hlist), at<uint64_t>(ws, L.bitmap), status_w);
+        k_bhist<<<(unsigned)L.T, kSortT, 0, s>>>(points, N, BN, g, L.Q, BQ, L.T, L.tile_scan, hist,
+                                                 at<uint4>(ws, L.status), (int64_t)(L.clear_brick - L.status) / 16);
+        if (!L.tile_scan)
+            k_hscan<<<(unsigned)((BQ + kHGroup - 1) / kHGroup), kScanThreads, 0, s>>>(
+                hist, BQ, L.T, at<uint32_t>(ws, L.bstart), at<int32_t>(ws, L.brick_hb), at<uint64_t>(ws, L.item_extra),
+                at<uint32_t>(ws, L.hlist), at<uint32_t>(ws, L.hebase), at<uint64_t>(ws, L.desc_h), status_w);
+        (L.tile_scan ? k_bscatter<true> : k_bscatter<false>)<<<(unsigned)L.T, kSortT, 0, s>>>(
+            points, N, BN, g, L.Q, BQ, hist, at<float4>(ws, L.sorted), at<uint32_t>(ws, L.bstart),
+            at<int32_t>(ws, L.brick_hb), at<uint64_t>(ws, L.item_extra), at<uint32_t>(ws, L.hlist),
+            at<uint32_t>(ws, L.hebase), status_w);
         BrickArgs a;
         a.P = points;
         a.N = N;

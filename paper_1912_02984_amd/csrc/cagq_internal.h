@@ -28,6 +28,7 @@ constexpr int32_t kMaxBricks = 8192;    // bricks over the batch the brick build
 constexpr int kSortTile = 4096;         // points per tile of the brick histogram and scatter
 constexpr int kBrickT = 256;            // threads per brick work item
 constexpr int kBrickCap = 2048;         // points per brick work item (heavier bricks are split)
+constexpr int64_t kTileScanCap = 1 << 16;  // histogram entries a scatter tile may sum (tiles of a cloud x Q)
 
 // Status word slots (int32 each) at the start of the workspace's control block.
 enum StatusSlot {
@@ -55,6 +56,8 @@ struct Layout {
     int32_t Q;            // bricks per cloud (kBrickW words each)
     int32_t T;            // point tiles (kSortTile points) over the batch
     bool bricks;          // the brick build's arrays are present (B * Q <= kMaxBricks)
+    bool tile_scan;       // brick build: each scatter tile sums its clouds' histogram columns itself
+                          // (at most kTileScanCap entries per tile); otherwise a scan launch does
     int64_t items_max;    // brick build: bound on the work items, B * Q + ceil(B * N / kBrickCap)
                           // (the bricks, then the further parts of heavy bricks)
     int64_t heavy_max;    // brick build: bound on the heavy bricks, B * N / (kBrickCap + 1)

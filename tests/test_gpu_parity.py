@@ -121,13 +121,18 @@ def test_capped_and_big_voxels(N):
     run_both(P, spec, 12, 64, "cas", "cube", 9, where="cas")
 
 
-@pytest.mark.parametrize("case", ["brick-capacity", "ragged-bricks", "grid-too-large-for-bricks"])
+@pytest.mark.parametrize("case", ["brick-capacity", "ragged-bricks", "wide-bricks", "scan-launch",
+                                  "grid-too-large-for-bricks"])
 def test_brick_build_edges(case):
     """The brick build of larger clouds: bricks of 2048 consecutive voxels
     holding exactly the 2048 points one work item takes and one more (then
     split into two parts that meet in memory), voxels of more than 64 points
-    in both, a last brick cut short by the grid; and a grid with more bricks
-    than the build holds, which takes the seven-kernel build."""
+    in both, a last brick cut short by the grid; 1280 bricks per cloud (the
+    scatter tiles scan the bricks' totals in two passes); clouds whose tiles
+    times bricks exceed 2^16 (the histogram columns are scanned by a launch
+    of their own), with a brick of 3000 points and tiles holding points of
+    two clouds; and a grid with more bricks than the build holds, which
+    takes the seven-kernel build."""
     rng = np.random.default_rng(11)
     if case == "brick-capacity":
         # 64 x 32 voxels per z-slice: brick q is slice z = q
@@ -146,6 +151,18 @@ def test_brick_build_edges(case):
         P = rng.random((B, N, 3), dtype=np.float32) * np.float32([7.0, 3.3, 5.0])
         P[:, :300] = np.float32([6.95, 3.25, 4.95])      # the grid's last voxel
         spec = _spec((0, 0, 0), (0.1,) * 3, dims, n_v)
+    elif case == "wide-bricks":
+        B, N, dims, n_v = 1, 20000, (256, 256, 40), 8
+        P = rng.random((B, N, 3), dtype=np.float32) * np.float32([2.56, 2.56, 0.4])
+        spec = _spec((0, 0, 0), (0.01,) * 3, dims, n_v)
+    elif case == "scan-launch":
+        # (ceil(N / 4096) + 1) * Q = 26 * 2560 > 2^16
+        B, N, dims, n_v = 2, 100000, (256, 256, 80), 8
+        P = rng.random((B, N, 3), dtype=np.float32) * np.float32([2.56, 2.56, 0.8])
+        # brick 0 (x < 2.56, y < 0.08, z < 0.01): 3000 points, two work items
+        P[:, :3000] = rng.random((B, 3000, 3), dtype=np.float32) * np.float32([2.55, 0.079, 0.0099])
+        P = P[:, rng.permutation(N)]
+        spec = _spec((0, 0, 0), (0.01,) * 3, dims, n_v)
     else:
         B, N, dims, n_v = 2, 9000, (512, 512, 128), 4
         P = rng.random((B, N, 3), dtype=np.float32) * np.float32([5.12, 5.12, 1.28])
