@@ -36,19 +36,62 @@ constexpr uint32_t kSlotMask = (1u << kKeyShift) - 1;
 constexpr uint16_t kNone = 0xFFFF;
 constexpr int kPre = 4;                    // entry groups of 8 loaded with a list's header
 
-__device__ __forceinline__ uint32_t wmax32(uint32_t v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        const uint32_t o = (uint32_t)__shfl_xor((int)v, d, kWave);
-        v = o > v ? o : v;
+// Lane i of a 16-lane row reads lane i - N of the row (0 beyond its start).
+template <int N>
+__device__ __forceinline__ uint32_t row_shr(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + N, 0xF, 0xF, false);
+}
+
+// Value of lane `lane ^ J` within the 16-lane row (J = 1, 2, 4, 8).
+template <int J>
+__device__ __forceinline__ uint32_t row_xor(uint32_t v) {
+    if constexpr (J == 1) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true);  // quad_perm 1,0,3,2
+    if constexpr (J == 2) return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true);  // quad_perm 2,3,0,1
+    if constexpr (J == 4) {
+        const uint32_t up = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x104, 0xF, 0xF, true);  // row_shl:4
+        const uint32_t dn = (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x114, 0xF, 0xF, true);  // row_shr:4
+        return (threadIdx.x & 4) ? dn : up;
     }
-    return v;
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x128, 0xF, 0xF, true);  // row_ror:8
+}
+
+// Minimum over the 16 lanes of a row, in every lane of it.
+__device__ __forceinline__ uint32_t row_min16(uint32_t v) {
+    uint32_t o = row_xor<1>(v);
+    v = o < v ? o : v;
+    o = row_xor<2>(v);
+    v = o < v ? o : v;
+    o = row_xor<4>(v);
+    v = o < v ? o : v;
+    o = row_xor<8>(v);
+    return o < v ? o : v;
+}
+
+// Maximum and sum over the wave, as a value uniform across it: an inclusive
+// scan within each 16-lane row by row shifts, then the rows' last lanes read
+// as scalars. Every lane of the wave must call them.
+__device__ __forceinline__ uint32_t wmax32(uint32_t v) {
+    uint32_t o = row_shr<1>(v);
+    v = o > v ? o : v;
+    o = row_shr<2>(v);
+    v = o > v ? o : v;
+    o = row_shr<4>(v);
+    v = o > v ? o : v;
+    o = row_shr<8>(v);
+    v = o > v ? o : v;
+    const uint32_t a = (uint32_t)__builtin_amdgcn_readlane((int)v, 15), b = (uint32_t)__builtin_amdgcn_readlane((int)v, 31);
+    const uint32_t c = (uint32_t)__builtin_amdgcn_readlane((int)v, 47), d = (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+    const uint32_t ab = a > b ? a : b, cd = c > d ? c : d;
+    return ab > cd ? ab : cd;
 }
 
 __device__ __forceinline__ uint32_t wsum32(uint32_t v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
-    return v;
+    v += row_shr<1>(v);
+    v += row_shr<2>(v);
+    v += row_shr<4>(v);
+    v += row_shr<8>(v);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 15) + (uint32_t)__builtin_amdgcn_readlane((int)v, 31) +
+           (uint32_t)__builtin_amdgcn_readlane((int)v, 47) + (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 // Appends the slots s = tid + k*kT with bit k of `want` set to the queue.
@@ -65,7 +108,7 @@ __device__ __forceinline__ void enqueue(uint32_t want, uint16_t* q, uint32_t* s_
     }
     uint32_t base = 0;
     if (lane == 0 && tot) base = atomicAdd(s_qn, tot);
-    base = (uint32_t)__shfl((int)base, 0, kWave);
+    base = (uint32_t)__builtin_amdgcn_readfirstlane((int)base);
 #pragma unroll
     for (int k = 0; k < kKS; ++k) {
         if ((want >> k) & 1u) q[base + (uint32_t)__popcll(bal[k] & below)] = (uint16_t)(threadIdx.x + k * kT);
@@ -121,14 +164,17 @@ __device__ __forceinline__ void mark(const uint4& v, uint32_t base, uint32_t n_r
 // list's storage; later ones clamped to its last group). A voxel is beaten
 // when some entry within 2r holds a larger key; the lowest such position
 // over the P lanes is the same blocker a single lane's in-order scan finds.
-// A winner takes its pick round and key, and its lanes mark their groups:
-// rescoring within 2r, coverage within r. A round's winners are more than
-// 2r apart, so no other winner is on the list and their r-neighbourhoods are
-// disjoint: plain updates are exact.
-template <int P, int ST>
+// A winner takes its pick round and key. With LOWER it joins the round's
+// winner table (the lowering pass that follows updates coverage and keys);
+// otherwise its lanes mark their groups: rescoring within 2r, coverage
+// within r. A round's winners are more than 2r apart, so no other winner is
+// on the list and their r-neighbourhoods are disjoint: plain updates are
+// exact.
+template <int P, int ST, bool LOWER>
 __device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, const uint16_t* nb,
                                             const uint16_t* que, const uint32_t* key, uint16_t* rnd,
-                                            uint16_t* blk, uint16_t* dty, uint8_t* cov) {
+                                            uint16_t* blk, uint16_t* dty, uint8_t* cov, uint16_t* wtab,
+                                            uint32_t* s_nw, uint16_t* ptab, uint32_t* s_np) {
     constexpr uint32_t kRoom = (ST - 8) / 8;  // groups a slot's storage holds after its header
     constexpr int KB = (int)((kRoom + P - 1) / P) < kPre ? (int)((kRoom + P - 1) / P) : kPre;  // groups per load
     const uint32_t sub = (uint32_t)tid & (P - 1);
@@ -167,11 +213,8 @@ __device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, 
                     if (hit == ~0u && kk[j] > my) hit = ((c * 8 + (uint32_t)j) << 16) | sl[j];
             }
         }
-#pragma unroll
-        for (int d = 1; d < P; d <<= 1) {
-            const uint32_t o = (uint32_t)__shfl_xor((int)hit, d, kWave);
-            hit = o < hit ? o : hit;
-        }
+        static_assert(P == 1 || P == 16, "lanes per voxel");
+        if constexpr (P == 16) hit = row_min16(hit);
         if (hit != ~0u) {
             if (sub == 0) blk[s] = (uint16_t)(hit & 0xFFFFu);
             continue;
@@ -180,6 +223,20 @@ __device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, 
             rnd[s] = cur;
             blk[s] = (uint16_t)(my >> 16);
             dty[s] = (uint16_t)(my & 0xFFFFu);
+            if (LOWER) wtab[atomicAdd(s_nw, 1u)] = (uint16_t)s;
+        }
+        if constexpr (LOWER) {
+            // the entries within r (the first n_r, in groups 0..kPre-1 held
+            // by lanes 0..kPre-1) go to the round's pair table
+            static_assert(P == 16 && KB == 1, "lane `sub` holds group `sub`");
+            const uint32_t cnt = n_r > sub * 8 ? (n_r - sub * 8 < 8 ? n_r - sub * 8 : 8u) : 0u;
+            if (sub < (uint32_t)kPre && cnt) {
+                const uint32_t base = atomicAdd(s_np, cnt);
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if ((uint32_t)j < cnt) ptab[base + j] = (uint16_t)entry(pre[0], j);
+            }
+            continue;
         }
         for (uint32_t t0 = 0; sub + P * t0 < nch; t0 += KB) {
             uint4 q[KB];
@@ -200,31 +257,37 @@ __device__ __forceinline__ void drain_picks(uint32_t qb, int tid, uint16_t cur, 
 // The picking pass over a long queue (r = 1): one lane per voxel checks the
 // kPre groups of entries loaded with its list's header. A voxel that none of
 // them beats and whose list is longer (an open voxel) goes on to a second
-// stage in which 16 lanes of its wave take it, four voxels at a time: each
-// lane loads one group, lanes 0..11 the groups after the first kPre (they
-// check them for a larger key), lanes 12..15 the first kPre again, so that
-// a winner's 16 lanes then mark its whole list one group each, without
-// another load. Every lane of the wave must call it.
+// stage in which 16 lanes of its wave take it, four voxels at a time: lanes
+// 0..11 load and check one group each of those after the first kPre. A
+// winner joins the round's winner table. Every lane of the wave must call it.
 template <int ST>
 __device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, const uint16_t* nb,
                                             const uint16_t* que, const uint32_t* key, uint16_t* rnd,
-                                            uint16_t* blk, uint16_t* dty, uint8_t* cov) {
+                                            uint16_t* blk, uint16_t* dty, uint16_t* wtab, uint32_t* s_nw,
+                                            uint16_t* ptab, uint32_t* s_np) {
     constexpr int kRoom = (ST - 8) / 8;  // groups a slot's storage holds after its header
     static_assert(kRoom == 16 && kPre == 4, "16 lanes take the 16 groups of an r = 1 list");
     const int lane = lane_id();
     const int sub = lane & 15, quad = lane >> 4;
-    // the group lane `sub` of a voxel's 16 loads in the second stage
-    const uint32_t gq = sub < kRoom - kPre ? (uint32_t)(kPre + sub) : (uint32_t)(sub - (kRoom - kPre));
+    // the group lane `sub` of a voxel's 16 checks in the second stage
+    const uint32_t gq = (uint32_t)(kPre + sub);
     for (uint32_t i0 = (uint32_t)(tid - lane); i0 < qb; i0 += kT) {
         const uint32_t i = i0 + (uint32_t)lane;
         uint32_t s = 0, my = 0, n_r = 0, n2 = 0;
         bool open = false;
+        uint4 pre[kPre];
+        // a winner's entries within r (the first n_r) to the round's pair table
+        auto pairs = [&]() {
+            const uint32_t base = atomicAdd(s_np, n_r);
+#pragma unroll
+            for (int j = 0; j < kPre * 8; ++j)
+                if ((uint32_t)j < n_r) ptab[base + j] = (uint16_t)entry(pre[j / 8], j % 8);
+        };
         if (i < qb) {
             s = que[i];
             my = key[s];
             const uint4* e = reinterpret_cast<const uint4*>(nb + (size_t)s * ST);
             const uint4 h = e[0];
-            uint4 pre[kPre];
 #pragma unroll
             for (int t = 0; t < kPre; ++t) pre[t] = e[1 + t];
             n_r = h.x & 0xFFFFu;
@@ -247,13 +310,12 @@ __device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, 
                 blk[s] = (uint16_t)(hit & 0xFFFFu);
             } else if (nch > (uint32_t)kPre) {
                 open = true;
-            } else {  // a short list, all checked: a winner, marked from the groups at hand
+            } else {  // a short list, all checked: a winner
                 rnd[s] = cur;
                 blk[s] = (uint16_t)(my >> 16);
                 dty[s] = (uint16_t)(my & 0xFFFFu);
-#pragma unroll
-                for (int t = 0; t < kPre; ++t)
-                    if ((uint32_t)t < nch) mark(pre[t], (uint32_t)t * 8, n_r, n2, s, cur, rnd, dty, cov);
+                wtab[atomicAdd(s_nw, 1u)] = (uint16_t)s;
+                pairs();
             }
         }
         for (uint64_t om = __ballot(open); om;) {
@@ -265,14 +327,13 @@ __device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, 
             for (int k = 0; k < 4 && om; ++k) om &= om - 1;
             const uint32_t vs = (uint32_t)__shfl((int)s, src, kWave);
             const uint32_t vmy = (uint32_t)__shfl((int)my, src, kWave);
-            const uint32_t vnr = (uint32_t)__shfl((int)n_r, src, kWave);
             const uint32_t vn2 = (uint32_t)__shfl((int)n2, src, kWave);
             const uint32_t vnch = (vn2 + 7) / 8;
             const bool mine = act && gq < vnch;  // this lane's group holds entries of the list
             uint4 q = make_uint4(0u, 0u, 0u, 0u);
             if (mine) q = reinterpret_cast<const uint4*>(nb + (size_t)vs * ST)[1 + gq];
             uint32_t hit = ~0u;
-            if (mine && gq >= (uint32_t)kPre) {
+            if (mine) {
                 uint32_t sl[8], kk[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) sl[j] = gq * 8 + (uint32_t)j < vn2 ? entry(q, j) : vs;
@@ -282,23 +343,132 @@ __device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, 
                 for (int j = 0; j < 8; ++j)
                     if (hit == ~0u && kk[j] > vmy) hit = ((gq * 8 + (uint32_t)j) << 16) | sl[j];
             }
-#pragma unroll
-            for (int d = 1; d < 16; d <<= 1) {
-                const uint32_t o = (uint32_t)__shfl_xor((int)hit, d, kWave);
-                hit = o < hit ? o : hit;
-            }
-            if (act && hit != ~0u) {
-                if (sub == 0) blk[vs] = (uint16_t)(hit & 0xFFFFu);
-            } else if (act) {
-                if (sub == 0) {
+            hit = row_min16(hit);
+            if (act && sub == 0) {
+                if (hit != ~0u) {
+                    blk[vs] = (uint16_t)(hit & 0xFFFFu);
+                } else {
                     rnd[vs] = cur;
                     blk[vs] = (uint16_t)(vmy >> 16);
                     dty[vs] = (uint16_t)(vmy & 0xFFFFu);
+                    wtab[atomicAdd(s_nw, 1u)] = (uint16_t)vs;
                 }
-                if (mine) mark(q, gq * 8, vnr, vn2, vs, cur, rnd, dty, cov);
             }
         }
+        // an open voxel that won (its pick round was written above, by this
+        // wave) gives its pairs from the groups it holds
+        if (open && rnd[s] == cur) pairs();
     }
+}
+
+// The rounds with r = 1, keys kept exact by lowering (the scheme of the
+// many-kernel rounds on lists, in LDS). Keys start at U = n_r, the occupied
+// voxels within r (nothing is covered). Per round, three phases between
+// barriers:
+// * owned slots: the picks above the previous round's best unpicked key G
+//   are counted (when they reach m they are the sequential greedy's first m,
+//   and the rounds stop: one round after the round-by-round bound would
+//   allow); the best unpicked key is taken; an unpicked voxel still beaten
+//   by its cached blocker stays out, the rest is queued;
+// * the picking drain over the queue against the round-start keys: a voxel
+//   is beaten by the first larger key on its 2r-list, else it wins and
+//   joins the winner table;
+// * the lowering: the winners put the voxels u within r of them into a pair
+//   table (winners are more than 2r apart, so their r-neighbourhoods are
+//   disjoint: at most one entry per voxel, and no coverage count is raised
+//   twice in a round); one lane per u raises u's coverage count and, when u
+//   was uncovered, lowers by one U the key of every unpicked voxel within r
+//   of u (LDS atomics: such a voxel can lie within r of several newly
+//   covered voxels). The winners' keys become 0: they compete no more.
+// Returns whether the rounds reached m picks.
+template <int ST>
+__device__ __forceinline__ bool rounds_lowering(int32_t nv, int32_t m, int tid, int lane, const uint16_t* nb,
+                                                uint32_t* key, uint16_t* rnd, uint16_t* blk, uint16_t* dty,
+                                                uint16_t* que, uint16_t* wtab, uint16_t* ptab, uint8_t* cov,
+                                                uint32_t* s_max, uint32_t* s_cnt, uint32_t* s_qb, uint32_t* s_nw,
+                                                uint32_t* s_np) {
+    for (int32_t s = tid; s < nv; s += kT) {
+        const uint32_t n_r = reinterpret_cast<const uint4*>(nb + (size_t)s * ST)[0].x & 0xFFFFu;
+        key[s] = (n_r << kKeyShift) | (kSlotMask - (uint32_t)s);
+    }
+    if (tid == 0) {
+        *s_max = 0;
+        *s_cnt = 0;
+        *s_qb = 0;
+    }
+    uint32_t G = ~0u;  // the previous round's best unpicked key (none before the first round)
+    const int32_t max_r = m + 3;
+    for (int32_t R = 0; R < max_r; ++R) {
+        const uint16_t cur = (uint16_t)(R + 1);
+        __syncthreads();
+        if (tid == 0) {
+            *s_nw = 0;
+            *s_np = 0;
+        }
+        uint32_t lmax = 0, above = 0, want = 0;
+#pragma unroll
+        for (int k = 0; k < kKS; ++k) {
+            const int32_t s = tid + k * kT;
+            if (s < nv) {
+                const uint16_t r = rnd[s], bl = blk[s];
+                if (r != 0) {
+                    const uint32_t pk = ((uint32_t)bl << 16) | dty[s];
+                    above += pk > G ? 1u : 0u;
+                } else {
+                    const uint32_t kv = key[s];
+                    lmax = kv > lmax ? kv : lmax;
+                    const bool beaten = bl != kNone && key[bl] > kv;
+                    want |= beaten ? 0u : 1u << k;
+                }
+            }
+        }
+        lmax = wmax32(lmax);
+        above = wsum32(above);
+        if (lane == 0 && lmax) atomicMax(s_max, lmax);
+        if (lane == 0 && above) atomicAdd(s_cnt, above);
+        enqueue(want, que, s_qb);
+        __syncthreads();
+        if (*s_cnt >= (uint32_t)m) return true;
+        G = *s_max;
+        const uint32_t qb = *s_qb;
+        if (qb <= kT / 8)
+            drain_picks<16, ST, true>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov, wtab, s_nw, ptab, s_np);
+        else
+            drain_mixed<ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, wtab, s_nw, ptab, s_np);
+        __syncthreads();
+        if (tid == 0) {
+            *s_max = 0;
+            *s_cnt = 0;
+            *s_qb = 0;
+        }
+        // the winners leave the competition; each voxel u within r of one
+        // is covered once more and, if it was uncovered, lowers the keys
+        // within r of it
+        const uint32_t nw = *s_nw, np = *s_np;
+        for (uint32_t p = (uint32_t)tid; p < nw; p += kT) key[wtab[p]] = 0;
+        for (uint32_t p = (uint32_t)tid; p < np; p += kT) {
+            const uint32_t u = ptab[p];
+            const uint8_t c = cov[u];
+            cov[u] = (uint8_t)(c + 1);
+            if (c != 0) continue;
+            const uint4* eu = reinterpret_cast<const uint4*>(nb + (size_t)u * ST);
+            const uint4 hu = eu[0];
+            uint4 gu[kPre];  // the first kPre groups hold every entry within r
+#pragma unroll
+            for (int t = 0; t < kPre; ++t) gu[t] = eu[1 + t];
+            const uint32_t nru = hu.x & 0xFFFFu;
+            uint32_t v[kPre * 8];
+            uint16_t rv[kPre * 8];
+#pragma unroll
+            for (int i = 0; i < kPre * 8; ++i) v[i] = (uint32_t)i < nru ? entry(gu[i / 8], i % 8) : u;
+#pragma unroll
+            for (int i = 0; i < kPre * 8; ++i) rv[i] = rnd[v[i]];
+#pragma unroll
+            for (int i = 0; i < kPre * 8; ++i)
+                if ((uint32_t)i < nru && rv[i] == 0) atomicSub(&key[v[i]], 1u << kKeyShift);
+        }
+    }
+    return false;
 }
 
 template <int RAD>
@@ -315,8 +485,11 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     uint16_t* blk = rnd + cap;   // unpicked: a neighbour that beat it; picked: pick key >> 16
     uint16_t* dty = blk + cap;   // unpicked: round that must rescore it; picked: pick key & 0xFFFF
     uint16_t* que = dty + cap;   // work queue of slots
-    uint8_t* cov = reinterpret_cast<uint8_t*>(que + cap);       // centers covering the voxel
+    uint16_t* wtab = que + cap;  // r = 1: the round's winners
+    uint16_t* ptab = wtab + cap; // r = 1: the voxels within r of the round's winners
+    uint8_t* cov = reinterpret_cast<uint8_t*>(ptab + cap);      // centers covering the voxel
     __shared__ uint32_t s_max, s_cnt, s_qa, s_qb;  // s_qa / s_qb: scoring / picking queue lengths
+    __shared__ uint32_t s_nw, s_np;                // r = 1: winners and pairs of the round
     __shared__ uint32_t s_hist[128];
     __shared__ uint32_t s_digit, s_below;
     __shared__ uint32_t s_wsum[kNW];
@@ -343,6 +516,10 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     }
 
     bool done = false;
+    if constexpr (RAD == 1) {
+        done = rounds_lowering<ST>(nv, m, tid, lane, nb, key, rnd, blk, dty, que, wtab, ptab, cov, &s_max, &s_cnt,
+                                   &s_qb, &s_nw, &s_np);
+    } else {
     const int32_t max_r = m + 2;
     for (int32_t R = 0; R < max_r; ++R) {
         const uint16_t cur = (uint16_t)(R + 1);
@@ -443,14 +620,8 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         // list entries each, in at most two passes (2, 4 or 8 lanes per
         // voxel spill registers here); a longer one gets 16 lanes only for
         // the voxels that the first groups of their lists do not decide
-        if constexpr (RAD == 1) {
-            if (qb <= kT / 8)
-                drain_picks<16, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
-            else
-                drain_mixed<ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
-        } else {
-            drain_picks<1, ST>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov);
-        }
+        drain_picks<1, ST, false>(qb, tid, cur, nb, que, key, rnd, blk, dty, cov, wtab, &s_nw, ptab, &s_np);
+    }
     }
     if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
     __syncthreads();
@@ -532,7 +703,7 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
 }
 
 int32_t lds_cap(int32_t N) { return (N + 3) & ~3; }
-size_t lds_bytes(int32_t cap) { return (size_t)13 * cap + 16; }
+size_t lds_bytes(int32_t cap) { return (size_t)17 * cap + 16; }
 
 }  // namespace
 
