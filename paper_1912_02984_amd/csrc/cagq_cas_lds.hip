@@ -33,6 +33,7 @@ constexpr int kNW = kT / kWave;            // waves of the workgroup
 constexpr int kKS = kCasLdsMaxN / kT;      // owned slots per thread
 constexpr int kKeyShift = 25;              // key = (U << 25) | (2^25 - 1 - slot)
 constexpr uint32_t kSlotMask = (1u << kKeyShift) - 1;
+constexpr uint32_t kUnpicked = 1u << 31;      // r = 1: offset of an unpicked voxel's key
 constexpr uint16_t kNone = 0xFFFF;
 constexpr int kPre = 4;                    // entry groups of 8 loaded with a list's header
 
@@ -380,6 +381,10 @@ __device__ __forceinline__ void drain_mixed(uint32_t qb, int tid, uint16_t cur, 
 //   was uncovered, lowers by one U the key of every unpicked voxel within r
 //   of u (LDS atomics: such a voxel can lie within r of several newly
 //   covered voxels). The winners' keys become 0: they compete no more.
+// Keys carry 2^31 while the voxel is unpicked; a winner's key drops to 2^30.
+// A picked voxel's key is then lowered by at most 27 * 2^25 < 2^30 more, so
+// it stays positive and below every unpicked key: the lowering needs no
+// test of who is picked. The pick keys (with the offset) order as before.
 // Returns whether the rounds reached m picks.
 template <int ST>
 __device__ __forceinline__ bool rounds_lowering(int32_t nv, int32_t m, int tid, int lane, const uint16_t* nb,
@@ -389,7 +394,7 @@ __device__ __forceinline__ bool rounds_lowering(int32_t nv, int32_t m, int tid, 
                                                 uint32_t* s_np) {
     for (int32_t s = tid; s < nv; s += kT) {
         const uint32_t n_r = reinterpret_cast<const uint4*>(nb + (size_t)s * ST)[0].x & 0xFFFFu;
-        key[s] = (n_r << kKeyShift) | (kSlotMask - (uint32_t)s);
+        key[s] = kUnpicked | (n_r << kKeyShift) | (kSlotMask - (uint32_t)s);
     }
     if (tid == 0) {
         *s_max = 0;
@@ -445,27 +450,29 @@ __device__ __forceinline__ bool rounds_lowering(int32_t nv, int32_t m, int tid, 
         // is covered once more and, if it was uncovered, lowers the keys
         // within r of it
         const uint32_t nw = *s_nw, np = *s_np;
-        for (uint32_t p = (uint32_t)tid; p < nw; p += kT) key[wtab[p]] = 0;
-        for (uint32_t p = (uint32_t)tid; p < np; p += kT) {
-            const uint32_t u = ptab[p];
-            const uint8_t c = cov[u];
-            cov[u] = (uint8_t)(c + 1);
-            if (c != 0) continue;
-            const uint4* eu = reinterpret_cast<const uint4*>(nb + (size_t)u * ST);
-            const uint4 hu = eu[0];
+        for (uint32_t p = (uint32_t)tid; p < nw; p += kT) key[wtab[p]] = kUnpicked >> 1;
+        for (uint32_t p0 = 0; p0 < np; p0 += kT) {
+            const uint32_t p = p0 + (uint32_t)tid;
+            uint32_t nru = 0;
             uint4 gu[kPre];  // the first kPre groups hold every entry within r
+            if (p < np) {
+                const uint32_t u = ptab[p];
+                const uint8_t c = cov[u];
+                cov[u] = (uint8_t)(c + 1);
+                if (c == 0) {
+                    const uint4* eu = reinterpret_cast<const uint4*>(nb + (size_t)u * ST);
+                    const uint4 hu = eu[0];
 #pragma unroll
-            for (int t = 0; t < kPre; ++t) gu[t] = eu[1 + t];
-            const uint32_t nru = hu.x & 0xFFFFu;
-            uint32_t v[kPre * 8];
-            uint16_t rv[kPre * 8];
+                    for (int t = 0; t < kPre; ++t) gu[t] = eu[1 + t];
+                    nru = hu.x & 0xFFFFu;
+                }
+            }
+            const uint32_t nmax = wmax32(nru);
 #pragma unroll
-            for (int i = 0; i < kPre * 8; ++i) v[i] = (uint32_t)i < nru ? entry(gu[i / 8], i % 8) : u;
-#pragma unroll
-            for (int i = 0; i < kPre * 8; ++i) rv[i] = rnd[v[i]];
-#pragma unroll
-            for (int i = 0; i < kPre * 8; ++i)
-                if ((uint32_t)i < nru && rv[i] == 0) atomicSub(&key[v[i]], 1u << kKeyShift);
+            for (int i = 0; i < kPre * 8; ++i) {
+                if ((uint32_t)i >= nmax) break;
+                if ((uint32_t)i < nru) atomicSub(&key[entry(gu[i / 8], i % 8)], 1u << kKeyShift);
+            }
         }
     }
     return false;
@@ -626,7 +633,8 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     if (!done && tid == 0) raise_error(status, CAGQ_ERR_CAPACITY);
     __syncthreads();
 
-    // The m largest pick keys. A pick key is (U << 25) | (2^25 - 1 - slot):
+    // The m largest pick keys. A pick key is (U << 25) | (2^25 - 1 - slot)
+    // (with r = 1 plus 2^31, which adds 64 to every U below):
     // with U* the largest U for which at least m picks have U >= U*, the
     // chosen picks are those with U > U* and, of those with U = U*, the
     // `need` lowest slots.
