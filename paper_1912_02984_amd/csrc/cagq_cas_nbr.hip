@@ -75,9 +75,26 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
                                                          const uint32_t* __restrict__ vox_lin,
                                                          const uint64_t* __restrict__ bitmap,
                                                          const uint32_t* __restrict__ word_rank, E* __restrict__ nbr,
-                                                         uint64_t* __restrict__ key, int64_t unit) {
+                                                         uint64_t* __restrict__ key, int64_t unit, CasClear clr,
+                                                         bool clear) {
     constexpr int H = 2 * RAD, S2 = 2 * H + 1;
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
+    if (clear) {  // the rounds' starting state (the grid covers the control block too)
+        if (gid < B * N) {
+            clr.cover[gid] = 0;
+            clr.pick[gid] = 0;
+            clr.round[gid] = 0;
+            clr.blocker[gid] = -1;
+            clr.dirty[gid] = 0;
+        }
+        if (gid < clr.nparts) {
+            clr.gpart[gid] = 0;
+            clr.cpart[gid] = 0;
+        }
+        if (gid < B) clr.done[gid] = 0;
+        if (gid < clr.nhist) clr.uhist[gid] = 0;
+        if (gid == 0) *clr.ndone = 0;
+    }
     if (gid >= B * N) return;
     const int32_t b = gid / N, s = gid - b * N;
     if (s >= nvox[b]) return;
@@ -172,23 +189,28 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
 }  // namespace
 
 hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s, uint64_t* key,
-                          int64_t unit) {
+                          int64_t unit, const CasClear* clr) {
     GridDims g;
     for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
-    const unsigned blocks = (unsigned)(((int64_t)L.B * L.N + kNbrThreads - 1) / kNbrThreads);
+    int64_t lanes = (int64_t)L.B * L.N;
+    if (clr) lanes = std::max<int64_t>(lanes, std::max<int64_t>(clr->nparts, clr->nhist));
+    const unsigned blocks = (unsigned)((lanes + kNbrThreads - 1) / kNbrThreads);
+    const CasClear none{};
+    const CasClear c = clr ? *clr : none;
     const int32_t* nvox = at<int32_t>(ws, L.nvox);
     const uint32_t* vox_lin = at<uint32_t>(ws, L.vox_lin);
     const uint64_t* bitmap = at<uint64_t>(ws, L.bitmap);
     const uint32_t* word_rank = at<uint32_t>(ws, L.word_rank);
     if (L.has_nbr32 && d.radius == 1) {
         k_cas_nbr<1, uint32_t, kNbr32Stride, 4><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint32_t>(ws, L.cas_nbr32), key, unit);
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint32_t>(ws, L.cas_nbr32), key, unit, c,
+            clr != nullptr);
     } else if (L.has_nbr16 && d.radius == 1) {
         k_cas_nbr<1, uint16_t, nbr_stride(1), 8><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0);
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0, c, false);
     } else if (L.has_nbr16 && d.radius == 2) {
         k_cas_nbr<2, uint16_t, nbr_stride(2), 8><<<blocks, kNbrThreads, 0, s>>>(
-            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0);
+            L.B, L.N, L.W, g, nvox, vox_lin, bitmap, word_rank, at<uint16_t>(ws, L.cas_nbr), nullptr, 0, c, false);
     } else {
         return hipErrorInvalidValue;
     }

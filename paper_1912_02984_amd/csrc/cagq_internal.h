@@ -520,11 +520,30 @@ bool cas_swap_fits(const Layout& L, const cagq_grid_desc& d, int32_t M);
 hipError_t launch_cas_swap(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M, uint64_t seed,
                            uint32_t beta_q16, int32_t* center_lin, int32_t* m_valid, hipStream_t s);
 
+// The words the CAS rounds on lists start from: per slot zero coverage,
+// pick, pick round and rescoring round and no blocker; the control block's
+// partial slots, done flags and U histogram at zero.
+struct CasClear {
+    uint32_t* cover;
+    uint64_t* pick;
+    uint32_t* round;
+    int32_t* blocker;
+    uint32_t* dirty;
+    uint64_t* gpart;
+    uint32_t* cpart;
+    uint32_t* done;
+    uint32_t* ndone;
+    uint32_t* uhist;
+    int32_t nparts;  // entries of gpart and of cpart
+    int32_t nhist;   // entries of uhist
+};
+
 // Writes the CAS neighbour lists of the grid in whichever format the layout
 // holds (has_nbr16 or has_nbr32). With u32 lists and `key` given, also sets
-// each occupied voxel's round-0 key, cas_key(unit * entries within r, lin).
+// each occupied voxel's round-0 key, cas_key(unit * entries within r, lin),
+// and with `clr` given clears the rounds' state (a launch of its own before).
 hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hipStream_t s,
-                          uint64_t* key = nullptr, int64_t unit = 0);
+                          uint64_t* key = nullptr, int64_t unit = 0, const CasClear* clr = nullptr);
 
 // Greedy coverage-aware sampling (rounds of neighbourhood maxima).
 hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M,

@@ -1255,11 +1255,17 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     const bool lists = L.has_nbr32 && rad == 1;
     // with lists, the list kernel also sets the round-0 keys: nothing is
     // covered yet, so the score is 2^16 * lambda * (occupied voxels within r)
-    if (lists && (e = launch_cas_nbr(L, d, ws, s, st.key, 65536 * lam)) != hipSuccess) return e;
-    const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
+    // (and clears the rounds' state, which takes a launch of its own otherwise)
     const int32_t init_n = std::max(BN, B * kCasParts * kCasUBins);
-    k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, st, ctl);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
+    if (lists) {
+        const CasClear clr{st.cover, st.pick, st.round, st.blocker, st.dirty, ctl.gpart, ctl.cpart, ctl.done,
+                           ctl.ndone, ctl.uhist, kCasBufs * B * kCasParts, B * kCasParts * kCasUBins};
+        if ((e = launch_cas_nbr(L, d, ws, s, st.key, 65536 * lam, &clr)) != hipSuccess) return e;
+    } else {
+        k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, st, ctl);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    const uint32_t* nbr = lists ? at<uint32_t>(ws, L.cas_nbr32) : nullptr;
 
     int64_t R = 0;
     auto launch_batch = [&](int rounds) {
