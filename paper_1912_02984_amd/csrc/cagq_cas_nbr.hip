@@ -10,6 +10,7 @@
 // kCasLdsMaxN points (r <= 2), u32 entries behind a 4-entry header for
 // larger clouds with r = 1. Header entry 0 is the number within r, entry 1
 // the number within 2r.
+#include <algorithm>
 #include <type_traits>
 
 #include "cagq_internal.h"
@@ -93,7 +94,11 @@ __global__ __launch_bounds__(kNbrThreads) void k_cas_nbr(int32_t B, int32_t N, i
         }
         if (gid < B) clr.done[gid] = 0;
         if (gid < clr.nhist) clr.uhist[gid] = 0;
-        if (gid == 0) *clr.ndone = 0;
+        if (gid < clr.ndesc) clr.desc[gid] = 0;
+        if (gid == 0) {
+            *clr.ndone = 0;
+            *clr.ticket = 0;
+        }
     }
     if (gid >= B * N) return;
     const int32_t b = gid / N, s = gid - b * N;
@@ -193,7 +198,7 @@ hipError_t launch_cas_nbr(const Layout& L, const cagq_grid_desc& d, void* ws, hi
     GridDims g;
     for (int a = 0; a < 3; ++a) g.D[a] = d.dims[a];
     int64_t lanes = (int64_t)L.B * L.N;
-    if (clr) lanes = std::max<int64_t>(lanes, std::max<int64_t>(clr->nparts, clr->nhist));
+    if (clr) lanes = std::max<int64_t>({lanes, clr->nparts, clr->nhist, clr->ndesc});
     const unsigned blocks = (unsigned)((lanes + kNbrThreads - 1) / kNbrThreads);
     const CasClear none{};
     const CasClear c = clr ? *clr : none;

@@ -522,7 +522,8 @@ hipError_t launch_cas_swap(const Layout& L, const cagq_grid_desc& d, void* ws, i
 
 // The words the CAS rounds on lists start from: per slot zero coverage,
 // pick, pick round and rescoring round and no blocker; the control block's
-// partial slots, done flags and U histogram at zero.
+// partial slots, done flags and U histogram at zero; and the scan state of
+// the selection's compaction after the rounds.
 struct CasClear {
     uint32_t* cover;
     uint64_t* pick;
@@ -536,6 +537,9 @@ struct CasClear {
     uint32_t* uhist;
     int32_t nparts;  // entries of gpart and of cpart
     int32_t nhist;   // entries of uhist
+    uint64_t* desc;  // the compaction's tile descriptors
+    int32_t ndesc;
+    int* ticket;     // the compaction's tile ticket
 };
 
 // Writes the CAS neighbour lists of the grid in whichever format the layout

@@ -175,27 +175,88 @@ __global__ __launch_bounds__(kSelThreads) void k_sel_threshold(
     }
 }
 
+// Bound and tie count of the m largest CAS pick keys from the picks' U
+// (beta = 0: a pick key is (unit * U + 2^31, ~lin), so the m largest are the
+// picks with U > U* and, of those with U = U*, the lowest slots, U* being the
+// largest U with at least m picks at or above it), as the select key's
+// packed bound (the select key is the pick key's complement). Cloud b's
+// kCasParts partial histograms are summed by 8 threads per bin, 16 partials
+// each, loaded together; the result goes to *out. Every thread of a
+// kScanThreads block calls it.
+__device__ __forceinline__ void cas_u_bound(const uint32_t* __restrict__ uhist, int32_t b, uint32_t m, int64_t unit,
+                                            uint32_t* s_h, uint64_t* out) {
+    constexpr int kPer = kCasParts / 8;
+    static_assert(8 * kCasUBins <= kScanThreads && kCasParts % 8 == 0, "8 threads per bin");
+    const int tid = threadIdx.x;
+    if (tid < kCasUBins) s_h[tid] = 0;
+    __syncthreads();
+    if (tid < 8 * kCasUBins) {
+        const int bin = tid % kCasUBins, g = tid / kCasUBins;
+        const uint32_t* h0 = uhist + ((size_t)b * kCasParts + (size_t)g * kPer) * kCasUBins + bin;
+        uint32_t x[kPer], h = 0;
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) x[i] = h0[(size_t)i * kCasUBins];
+#pragma unroll
+        for (int i = 0; i < kPer; ++i) h += x[i];
+        if (h) atomicAdd(&s_h[bin], h);
+    }
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t run = 0, need = 0;
+        uint64_t bound = 0;
+        for (int u = kCasUBins - 1; u >= 0 && m > 0; --u) {
+            const uint32_t hu = s_h[u];
+            if (run + hu >= m) {
+                bound = 0xFFFFFFFFull - (uint64_t)(unit * u + 2147483648ll);
+                need = m - run;
+                break;
+            }
+            run += hu;
+        }
+        *out = sel_pack(bound, need);
+    }
+}
+
 // Ordered compaction of the chosen slots: tile of kScanTile slots per block,
 // look-back scan over the packed pair (keys below the bound << 31 | keys at
 // the bound). Slot s chosen at position p < m writes its linear id to every
-// j = p, p + m, p + 2m, ... < M (the cyclic padding).
+// j = p, p + m, p + 2m, ... < M (the cyclic padding). The bound comes from
+// thr, or with `uhist` (CAS on lists, beta = 0) from the picks' U histogram,
+// when the first tile of each cloud also writes thr and m_valid.
 __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     int32_t N, int64_t tiles_s, const int32_t* __restrict__ nvox, const uint32_t* __restrict__ vox_lin,
     int32_t M, int key_mode, uint64_t seed, const uint64_t* __restrict__ cas_pick,
-    const uint64_t* __restrict__ thr, int32_t* __restrict__ center_lin, uint64_t* __restrict__ desc_s,
-    int* __restrict__ status) {
+    uint64_t* __restrict__ thr, int32_t* __restrict__ center_lin, uint64_t* __restrict__ desc_s,
+    int* __restrict__ status, const uint32_t* __restrict__ uhist, int64_t unit, int32_t* __restrict__ m_valid) {
     __shared__ uint32_t s_ticket;
     __shared__ uint64_t s_wave[kScanThreads / kWave];
     __shared__ uint64_t s_prefix;
+    __shared__ uint32_t s_h[kCasUBins];
+    __shared__ uint64_t s_thr;
     if (threadIdx.x == 0) s_ticket = atomicAdd((unsigned*)&status[kStTicketSel], 1u);
     __syncthreads();
     const uint32_t t = s_ticket;
     const int32_t b = (int32_t)(t / tiles_s);
     const int64_t tile = (int64_t)(t % tiles_s);
     const int32_t nv = nvox[b];
-    if (tile * kScanTile >= nv) return;  // later tiles never wait on this one
     const int32_t m = M < nv ? M : nv;
-    const uint64_t packed = thr[b];
+    if (uhist && tile == 0 && threadIdx.x == 0 && m <= 0) {
+        thr[b] = sel_pack(0, 0);
+        m_valid[b] = 0;
+    }
+    if (tile * kScanTile >= nv) return;  // later tiles never wait on this one
+    uint64_t packed;
+    if (uhist) {
+        cas_u_bound(uhist, b, (uint32_t)m, unit, s_h, &s_thr);
+        __syncthreads();
+        packed = s_thr;
+        if (tile == 0 && threadIdx.x == 0) {
+            thr[b] = packed;
+            m_valid[b] = m;
+        }
+    } else {
+        packed = thr[b];
+    }
     const uint64_t bound = packed & ((1ull << 33) - 1);
     const uint32_t need = (uint32_t)(packed >> 33);
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
@@ -1107,50 +1168,6 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     }
 }
 
-// Bound and tie count of the m largest pick keys from the histogram of the
-// picks' U (beta = 0: a pick key is (unit * U + 2^31, ~lin), so the m
-// largest are the picks with U > U* and, of those with U = U*, the lowest
-// slots, U* being the largest U with at least m picks at or above it). Also
-// clears the scan state of the compaction that follows.
-__global__ void k_sel_cas_u(int64_t tiles_s, const int32_t* __restrict__ nvox, int32_t M,
-                            const uint32_t* __restrict__ uhist, int64_t unit, uint64_t* __restrict__ thr,
-                            int32_t* __restrict__ m_valid, uint64_t* __restrict__ desc_s, int* __restrict__ status) {
-    const int32_t b = blockIdx.x;
-    for (int64_t t = threadIdx.x; t < tiles_s; t += blockDim.x) desc_s[(size_t)b * tiles_s + t] = 0;
-    if (b == 0 && threadIdx.x == 0) status[kStTicketSel] = 0;
-    // bin totals over the partial histograms: lane l sums bin l % 32 over
-    // half of the partials, the two halves then add up
-    __shared__ uint32_t s_h[kCasUBins];
-    static_assert(2 * kCasUBins == kWave, "two lanes per bin");
-    {
-        const int bin = threadIdx.x % kCasUBins, half = threadIdx.x / kCasUBins;
-        const uint32_t* h0 = uhist + ((size_t)b * kCasParts + (size_t)half * (kCasParts / 2)) * kCasUBins + bin;
-        uint32_t h = 0;
-#pragma unroll 16
-        for (int i = 0; i < kCasParts / 2; ++i) h += h0[(size_t)i * kCasUBins];
-        h += (uint32_t)__shfl_down((int)h, kCasUBins, kWave);
-        if (threadIdx.x < kCasUBins) s_h[threadIdx.x] = h;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        const int32_t nv = nvox[b];
-        const uint32_t m = (uint32_t)(M < nv ? M : nv);
-        uint32_t run = 0, need = 0;
-        uint64_t bound = 0;
-        for (int u = kCasUBins - 1; u >= 0 && m > 0; --u) {
-            const uint32_t h = s_h[u];
-            if (run + h >= m) {
-                // the select key is the complement of the pick key: its top half
-                bound = 0xFFFFFFFFull - (uint64_t)(unit * u + 2147483648ll);
-                need = m - run;
-                break;
-            }
-            run += h;
-        }
-        thr[b] = sel_pack(bound, need);
-        m_valid[b] = (int32_t)m;
-    }
-}
 
 // A small pinned host buffer per calling thread for polling the progress of
 // the rounds without stalling the stream. Allocated on first use, kept for
@@ -1200,7 +1217,8 @@ hipError_t launch_select(const Layout& L, void* ws, int32_t M, int key_mode, uin
     }
     k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(L.N, L.tiles_s, nvox,
                                                                    at<uint32_t>(ws, L.vox_lin), M, key_mode, seed,
-                                                                   pick, thr, center_lin, desc_s, status);
+                                                                   pick, thr, center_lin, desc_s, status, nullptr, 0,
+                                                                   nullptr);
     return hipGetLastError();
 }
 
@@ -1214,12 +1232,12 @@ hipError_t launch_select_cas(const Layout& L, const cagq_grid_desc& d, void* ws,
     uint64_t* desc_s = at<uint64_t>(ws, L.desc_s);
     int* status = at<int>(ws, L.status);
     const int32_t* nvox = at<int32_t>(ws, L.nvox);
-    k_sel_cas_u<<<L.B, kWave, 0, s>>>(L.tiles_s, nvox, M, ctl.uhist, 65536 * side * side * side, thr, m_valid,
-                                      desc_s, status);
+    // the neighbour-list kernel has cleared the compaction's scan state
     k_sel_emit<<<(unsigned)(L.B * L.tiles_s), kScanThreads, 0, s>>>(L.N, L.tiles_s, nvox,
                                                                    at<uint32_t>(ws, L.vox_lin), M, 1, 0,
                                                                    at<uint64_t>(ws, L.cas_pick), thr, center_lin,
-                                                                   desc_s, status);
+                                                                   desc_s, status, ctl.uhist, 65536 * side * side * side,
+                                                                   m_valid);
     return hipGetLastError();
 }
 
@@ -1259,7 +1277,8 @@ hipError_t run_cas(const Layout& L, const cagq_grid_desc& d, void* ws, int32_t M
     const int32_t init_n = std::max(BN, B * kCasParts * kCasUBins);
     if (lists) {
         const CasClear clr{st.cover, st.pick, st.round, st.blocker, st.dirty, ctl.gpart, ctl.cpart, ctl.done,
-                           ctl.ndone, ctl.uhist, kCasBufs * B * kCasParts, B * kCasParts * kCasUBins};
+                           ctl.ndone, ctl.uhist, kCasBufs * B * kCasParts, B * kCasParts * kCasUBins,
+                           at<uint64_t>(ws, L.desc_s), (int32_t)(B * L.tiles_s), at<int>(ws, L.status) + kStTicketSel};
         if ((e = launch_cas_nbr(L, d, ws, s, st.key, 65536 * lam, &clr)) != hipSuccess) return e;
     } else {
         k_cas_init<<<(init_n + 63) / 64, 64, 0, s>>>(BN, B, st, ctl);
