@@ -737,6 +737,8 @@ __device__ __forceinline__ void clean16(uint64_t& k, uint32_t& p, int lg) {
 //   4. Node slot k is b0 lane k or b1 lane k - 16; slots k >= n repeat slot 0.
 //      The center's pairwise sum runs strides 1..8 inside each half, then
 //      node 16 into node 0 -- the order of the single-register tree.
+constexpr int32_t kRankMin = 8192;  // centers of a launch above which k_query_r2 ranks a block's centers
+
 template <int MODE, int RAD, bool UP>
 __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
     const uint32_t* __restrict__ Wt, int32_t N, int32_t M, int32_t K, int32_t total, QGrid g,
@@ -843,21 +845,31 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
             s_q[gb][0] = qx, s_q[gb][1] = qy, s_q[gb][2] = qz;
         }
     }
-    __syncthreads();
-    // 2. the block's centers by context size (ties by group): group g takes
-    // the center of rank g
-    if (lg == 0) {
-        const uint32_t mine = s_c[gb];
-        uint32_t r = 0;
+    // 2. in a launch of more than kRankMin centers, the block's centers by
+    // context size (ties by group): group g takes the center of rank g, so
+    // that a wave's four centers are alike. A smaller launch skips the
+    // block's two barriers: each group goes on with its own center, whose
+    // rows its own wave has put in LDS.
+    int src = gb;
+    if (total > kRankMin) {
+        __syncthreads();
+        if (lg == 0) {
+            const uint32_t mine = s_c[gb];
+            uint32_t r = 0;
 #pragma unroll
-        for (int h = 0; h < GPB; ++h) {
-            const uint32_t o = s_c[h];
-            r += (o < mine || (o == mine && h < gb)) ? 1u : 0u;
+            for (int h = 0; h < GPB; ++h) {
+                const uint32_t o = s_c[h];
+                r += (o < mine || (o == mine && h < gb)) ? 1u : 0u;
+            }
+            s_src[r] = (uint32_t)gb;
         }
-        s_src[r] = (uint32_t)gb;
+        __syncthreads();
+        src = (int)s_src[gb];
+    } else {
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
-    __syncthreads();
-    const int src = (int)s_src[gb];
     const int32_t cid = (int32_t)blk * GPB + src;
     if (s_def[src] && lg == 0) n_valid[cid] = -1;
     const bool live = cid < total && !s_def[src];
