@@ -218,6 +218,48 @@ __device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
     return v;
 }
 
+// Lane i of a 16-lane row reads lane i - N of the row; lanes below N read 0.
+template <int N>
+__device__ __forceinline__ uint32_t dpp_row_shr(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x110 + N, 0xF, 0xF, false);
+}
+
+// Sum and maximum over the wave, the same in every lane: an inclusive scan
+// within each 16-lane row by DPP row shifts, then the four rows' last lanes
+// read as scalars (no LDS permutes). Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+    v += dpp_row_shr<1>(v);
+    v += dpp_row_shr<2>(v);
+    v += dpp_row_shr<4>(v);
+    v += dpp_row_shr<8>(v);
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 15) + (uint32_t)__builtin_amdgcn_readlane((int)v, 31) +
+           (uint32_t)__builtin_amdgcn_readlane((int)v, 47) + (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+template <int N>
+__device__ __forceinline__ uint64_t dpp_row_shr64(uint64_t v) {
+    return ((uint64_t)dpp_row_shr<N>((uint32_t)(v >> 32)) << 32) | dpp_row_shr<N>((uint32_t)v);
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+    uint64_t o = dpp_row_shr64<1>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr64<2>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr64<4>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr64<8>(v);
+    v = o > v ? o : v;
+    uint64_t m = 0;
+#pragma unroll
+    for (int r = 15; r < kWave; r += 16) {
+        const uint64_t x = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), r) << 32) |
+                           (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, r);
+        m = x > m ? x : m;
+    }
+    return m;
+}
+
 // Ascending bitonic sort of one 64-bit key per lane over the whole wave.
 __device__ __forceinline__ uint64_t wave_sort64(uint64_t v) {
     const int lane = lane_id();

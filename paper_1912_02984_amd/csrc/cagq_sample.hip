@@ -638,12 +638,7 @@ __device__ __forceinline__ uint64_t parts_max(const uint64_t* __restrict__ part,
             const uint64_t o = part[(size_t)b0 * kCasParts + i * kWave + lane_id()];
             v = o > v ? o : v;
         }
-#pragma unroll
-        for (int d = 1; d < kWave; d <<= 1) {
-            uint64_t o = shfl_xor64(v, d);
-            v = o > v ? o : v;
-        }
-        return v;
+        return wave_max_u64(v);
     }
     uint64_t v = 0;
     for (int i = 0; i < kCasParts; ++i) {
@@ -659,9 +654,7 @@ __device__ __forceinline__ uint32_t parts_sum(const uint32_t* __restrict__ part,
         uint32_t v = 0;
 #pragma unroll
         for (int i = 0; i < kCasParts / kWave; ++i) v += part[(size_t)b0 * kCasParts + i * kWave + lane_id()];
-#pragma unroll
-        for (int d = 1; d < kWave; d <<= 1) v += (uint32_t)__shfl_xor((int)v, d, kWave);
-        return v;
+        return wave_sum_u32(v);
     }
     uint32_t v = 0;
     for (int i = 0; i < kCasParts; ++i) v += part[(size_t)b * kCasParts + i];
@@ -1158,8 +1151,8 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const size_t mine = (size_t)(R % kCasBufs) * part;
     const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
     if (b0 == b1) {
-        const uint64_t mx = wave_max64(k);
-        const uint32_t tot = wave_sum<uint32_t>(above);
+        const uint64_t mx = wave_max_u64(k);
+        const uint32_t tot = wave_sum_u32(above);
         if (lane_id() == 0 && mx) atomicMax((unsigned long long*)&ctl.gpart[mine + (size_t)b * kCasParts + part_slot()], mx);
         if (lane_id() == 0 && tot) atomicAdd(&ctl.cpart[mine + (size_t)b * kCasParts + part_slot()], tot);
     } else {
