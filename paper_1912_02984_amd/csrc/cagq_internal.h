@@ -236,6 +236,20 @@ __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
            (uint32_t)__builtin_amdgcn_readlane((int)v, 47) + (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
+// Inclusive prefix sum over the wave by DPP alone: within each 16-lane row
+// by row shifts, then row 0's total into rows 1 and 3 (row_bcast:15, lane
+// 15 of each even row into the next row) and rows 0-1's into rows 2 and 3
+// (row_bcast:31). Every lane of the wave must be active.
+__device__ __forceinline__ uint32_t wave_incl_sum_u32(uint32_t v) {
+    v += dpp_row_shr<1>(v);
+    v += dpp_row_shr<2>(v);
+    v += dpp_row_shr<4>(v);
+    v += dpp_row_shr<8>(v);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    return v;
+}
+
 template <int N>
 __device__ __forceinline__ uint64_t dpp_row_shr64(uint64_t v) {
     return ((uint64_t)dpp_row_shr<N>((uint32_t)(v >> 32)) << 32) | dpp_row_shr<N>((uint32_t)v);

@@ -1055,8 +1055,8 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
         }
     }
     const uint32_t nrest = found == -1 && n2 > 16 ? (n2 - 1) / 16 : 0u;  // chunks 1.. still to scan
-    const uint32_t sincl = wave_incl_scan<uint32_t>(nrest);
-    const uint32_t stot = (uint32_t)__shfl((int)sincl, kWave - 1, kWave);
+    const uint32_t sincl = wave_incl_sum_u32(nrest);
+    const uint32_t stot = (uint32_t)__builtin_amdgcn_readlane((int)sincl, kWave - 1);
     if (stot) {
         __shared__ int32_t s_found[kRoundThreads];
         const int wbase = threadIdx.x & ~(kWave - 1);
@@ -1107,8 +1107,8 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     // A lane loads u's count and u's list within r together, and when u was
     // uncovered (or beta > 0) lowers the keys on that list.
     const uint32_t nrw = winner ? n_r : 0u;
-    const uint32_t incl = wave_incl_scan<uint32_t>(nrw);
-    const uint32_t total = (uint32_t)__shfl((int)incl, kWave - 1, kWave);
+    const uint32_t incl = wave_incl_sum_u32(nrw);
+    const uint32_t total = (uint32_t)__builtin_amdgcn_readlane((int)incl, kWave - 1);
     const int wb = threadIdx.x & ~(kWave - 1);
     for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
         const uint32_t p = p0 + (uint32_t)lane_id();
