@@ -185,39 +185,6 @@ __device__ __forceinline__ uint64_t shfl_up64(uint64_t v, int d) {
     return ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo;
 }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
-template <typename T>
-__device__ __forceinline__ T wave_incl_scan(T v) {
-    const int lane = lane_id();
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        T o;
-        if constexpr (sizeof(T) == 8) o = (T)shfl_up64((uint64_t)v, d);
-        else o = (T)__shfl_up((int)v, d, kWave);
-        if (lane >= d) v += o;
-    }
-    return v;
-}
-
-template <typename T>
-__device__ __forceinline__ T wave_sum(T v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        if constexpr (sizeof(T) == 8) v += (T)shfl_xor64((uint64_t)v, d);
-        else v += (T)__shfl_xor((int)v, d, kWave);
-    }
-    return v;
-}
-
-__device__ __forceinline__ uint64_t wave_max64(uint64_t v) {
-#pragma unroll
-    for (int d = 1; d < kWave; d <<= 1) {
-        uint64_t o = shfl_xor64(v, d);
-        v = o > v ? o : v;
-    }
-    return v;
-}
-
 // Lane i of a 16-lane row reads lane i - N of the row; lanes below N read 0.
 template <int N>
 __device__ __forceinline__ uint32_t dpp_row_shr(uint32_t v) {
@@ -273,6 +240,47 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     }
     return m;
 }
+
+template <int C, int RM>
+__device__ __forceinline__ uint64_t dpp64(uint64_t v) {
+    return ((uint64_t)(uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), C, RM, 0xF, false) << 32) |
+           (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, C, RM, 0xF, false);
+}
+
+// Inclusive prefix sum across the 64 lanes of a wave, by DPP as
+// wave_incl_sum_u32 (64-bit values move as two halves). Every lane of the
+// wave must be active.
+template <typename T>
+__device__ __forceinline__ T wave_incl_scan(T v) {
+    static_assert(sizeof(T) == 4 || sizeof(T) == 8, "32- or 64-bit values");
+    if constexpr (sizeof(T) == 4) {
+        return (T)wave_incl_sum_u32((uint32_t)v);
+    } else {
+        uint64_t x = (uint64_t)v;
+        x += dpp64<0x111, 0xF>(x);
+        x += dpp64<0x112, 0xF>(x);
+        x += dpp64<0x114, 0xF>(x);
+        x += dpp64<0x118, 0xF>(x);
+        x += dpp64<0x142, 0xA>(x);  // row_bcast:15 into rows 1 and 3
+        x += dpp64<0x143, 0xC>(x);  // row_bcast:31 into rows 2 and 3
+        return (T)x;
+    }
+}
+
+// Sum over the wave, in every lane (the inclusive sum's last lane).
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+    const T incl = wave_incl_scan<T>(v);
+    if constexpr (sizeof(T) == 4) {
+        return (T)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)incl, kWave - 1);
+    } else {
+        return (T)(((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)incl >> 32), kWave - 1)
+                    << 32) |
+                   (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(uint64_t)incl, kWave - 1));
+    }
+}
+
+__device__ __forceinline__ uint64_t wave_max64(uint64_t v) { return wave_max_u64(v); }
 
 // Ascending bitonic sort of one 64-bit key per lane over the whole wave.
 __device__ __forceinline__ uint64_t wave_sort64(uint64_t v) {
