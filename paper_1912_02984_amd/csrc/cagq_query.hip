@@ -705,6 +705,12 @@ __device__ __forceinline__ uint64_t mirror64(uint64_t v) {
     return ((uint64_t)mirror((uint32_t)(v >> 32)) << 32) | mirror((uint32_t)v);
 }
 
+// Value of lane L of this lane's 16-lane row (DPP row_share).
+template <int L>
+__device__ __forceinline__ uint32_t row_lane(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x150 + L, 0xF, 0xF, true);
+}
+
 // Value of lane 0 of this lane's 16-lane row.
 __device__ __forceinline__ uint32_t row0(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x150, 0xF, 0xF, true);  // row_share:0
@@ -812,20 +818,19 @@ __global__ __launch_bounds__(kQueryThreads) void k_query_r2(
                 st = vo[r.first];
                 len = mask ? vo[r.first + (uint32_t)__popc(mask)] - st : 0u;
             }
-            if (NR / 2 >= q0 && NR / 2 < q0 + G)
-                occupied = (__shfl((int)mask, NR / 2 - q0, G) >> RAD) & 1;
+            static_assert(G == 16, "a group is a 16-lane row");
+            if (NR / 2 >= q0 && NR / 2 < q0 + G) occupied = (row_lane<(NR / 2) % G>(mask) >> RAD) & 1;
             // inclusive scan of the lengths across the row of 16 lanes
             uint32_t incl = len;
-#pragma unroll
-            for (int d = 1; d < G; d <<= 1) {
-                const uint32_t o = (uint32_t)__shfl_up((int)incl, d, G);
-                if (lg >= d) incl += o;
-            }
+            incl += dpp_row_shr<1>(incl);
+            incl += dpp_row_shr<2>(incl);
+            incl += dpp_row_shr<4>(incl);
+            incl += dpp_row_shr<8>(incl);
             if (q < NR) {
                 s_st[gb][q] = st;
                 s_pre[gb][q] = c + incl - len;
             }
-            c += (uint32_t)__shfl((int)incl, G - 1, G);
+            c += row_lane<G - 1>(incl);
         }
         // a sampled center that is not occupied has an empty context and
         // gets zeros (an upsampling center's voxel may be empty)
