@@ -6,6 +6,8 @@
 
 #include <mutex>
 
+#include <vector>
+
 #include "cagq_internal.h"
 
 namespace cagq {
@@ -86,6 +88,7 @@ bool make_layout(int32_t B, int32_t N, const cagq_grid_desc* d, Layout* L) {
     L->vox_off = take(4 * (size_t)B * (N + 1));
     L->pt_list = take(4 * BN);
     L->status = take(4 * kStSlots);
+    L->berr = take(4 * (size_t)B);
     L->sel_ghist = take(4 * (size_t)B * kSelBins);
     L->sel_cnt = take(4 * (size_t)B);
     L->clear_small = off;
@@ -389,6 +392,14 @@ int cagq_get_device_status(const cagq_grid* g, void* stream) {
     int rc = grid_layout(g, &L);
     if (rc != CAGQ_OK) return rc;
     if (hipStreamSynchronize((hipStream_t)stream) != hipSuccess) return CAGQ_ERR_HIP;
+    // the build's per-cloud codes come first in the pipeline (only the
+    // one-workgroup build writes them; every build leaves them at zero otherwise)
+    std::vector<int> berr((size_t)L.B);
+    if (hipMemcpy(berr.data(), at<int>(g->workspace, L.berr), sizeof(int) * (size_t)L.B, hipMemcpyDeviceToHost) !=
+        hipSuccess)
+        return CAGQ_ERR_HIP;
+    for (int e : berr)
+        if (e != 0) return e;
     int st = 0;
     if (hipMemcpy(&st, at<int>(g->workspace, L.status), sizeof(int), hipMemcpyDeviceToHost) != hipSuccess)
         return CAGQ_ERR_HIP;

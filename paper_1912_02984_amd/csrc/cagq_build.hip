@@ -1152,7 +1152,7 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     const float* __restrict__ P, int32_t N, GridArgs g, int64_t W, uint32_t n_v, uint32_t* __restrict__ pt_slot,
     uint64_t* __restrict__ bitmap, uint32_t* __restrict__ word_rank, uint32_t* __restrict__ vox_lin,
     uint32_t* __restrict__ vox_count, int32_t* __restrict__ nvox, uint32_t* __restrict__ vox_off,
-    uint32_t* __restrict__ pt_list, float4* __restrict__ pt4, int* __restrict__ status) {
+    uint32_t* __restrict__ pt_list, float4* __restrict__ pt4, int* __restrict__ status, int* __restrict__ berr) {
     extern __shared__ __align__(16) unsigned char lds[];
     uint64_t* s_bm = reinterpret_cast<uint64_t*>(lds);   // [W] occupancy words
     uint32_t* s_wr = reinterpret_cast<uint32_t*>(s_bm + W);  // [W] ranks
@@ -1160,14 +1160,20 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
     uint32_t* s_bk = s_off + N + 1;  // [N] point indices grouped by slot (arrival order)
     __shared__ uint64_t s_wave[kSmallT / kWave];
     __shared__ uint32_t s_big[kSmallBig];
-    __shared__ uint32_t s_nbig;
+    __shared__ uint32_t s_nbig, s_bad;
     const int32_t b = blockIdx.x;
     const int tid = threadIdx.x;
     const size_t pb = (size_t)b * N;
 
+    // the status words start at zero for the kernels after this one (this
+    // kernel writes none: its errors go to the cloud's own word)
+    if (b == 0 && tid < kStSlots) status[tid] = 0;
     for (int64_t w = tid; w < W; w += kSmallT) s_bm[w] = 0ull;
     for (int32_t i = tid; i <= N; i += kSmallT) s_off[i] = 0u;
-    if (tid == 0) s_nbig = 0;
+    if (tid == 0) {
+        s_nbig = 0;
+        s_bad = 0;
+    }
     lds_barrier();
 
     // voxelize: linear id, occupancy bit (every point's coordinates are
@@ -1200,8 +1206,9 @@ __global__ __launch_bounds__(kSmallT) void k_build_small(
         lin[k] = gg[0] + (uint32_t)g.D[0] * (gg[1] + (uint32_t)g.D[1] * gg[2]);
         atomicOr(reinterpret_cast<unsigned long long*>(&s_bm[lin[k] >> 6]), 1ull << (lin[k] & 63));
     }
-    if (bad) raise_error(status, CAGQ_ERR_NONFINITE_INPUT);
+    if (bad) s_bad = 1;
     lds_barrier();
+    if (tid == 0) berr[b] = s_bad ? CAGQ_ERR_NONFINITE_INPUT : 0;
 
     // ranks of the words
     uint64_t wd[kSmallWd];
@@ -1354,10 +1361,10 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
     const GridArgs g = grid_args(d);
     int* status = at<int>(ws, L.status);
     if (N <= kSmallN && L.W <= kSmallW && (int64_t)small_lds_bytes(N, L.W) <= small_lds_avail()) {
-        // the status words and the selection's histogram only: the small
-        // build uses no scan descriptors or occupancy bytes
-        k_clear<<<(unsigned)((L.clear_small - L.status + 4095) / 4096), 256, 0, s>>>(
-            at<uint4>(ws, L.status), (L.clear_small - L.status) / 16);
+        // no clearing launch: the build zeroes the status words itself and
+        // writes each cloud's error code (the selection's histogram serves
+        // clouds of at least 16384 points only, the scan descriptors and
+        // occupancy bytes other builds)
         const size_t bytes = small_lds_bytes(N, L.W);
         hipError_t e = hipFuncSetAttribute((const void*)k_build_small, hipFuncAttributeMaxDynamicSharedMemorySize,
                                            (int)bytes);
@@ -1366,7 +1373,8 @@ hipError_t launch_build(const float* points, const Layout& L, const cagq_grid_de
                                                 at<uint64_t>(ws, L.bitmap), at<uint32_t>(ws, L.word_rank),
                                                 at<uint32_t>(ws, L.vox_lin), at<uint32_t>(ws, L.vox_count),
                                                 at<int32_t>(ws, L.nvox), at<uint32_t>(ws, L.vox_off),
-                                                at<uint32_t>(ws, L.pt_list), at<float4>(ws, L.pt4), status);
+                                                at<uint32_t>(ws, L.pt_list), at<float4>(ws, L.pt4), status,
+                                                at<int>(ws, L.berr));
         return hipGetLastError();
     }
     if (L.bricks) {

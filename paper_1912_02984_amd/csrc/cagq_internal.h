@@ -66,6 +66,7 @@ struct Layout {
     size_t nvox, vox_lin, vox_count, vox_off, pt_list;
     // internal
     size_t status;        // int32[kStSlots]
+    size_t berr;          // int32[B] per cloud: the one-workgroup build's error code (0 = none)
     size_t desc_h;        // u64 [blocks of the column scan] scan descriptors (brick totals)
     size_t clear_brick;   // [status, clear_brick) is zeroed by the brick build (status, tickets,
                           // descriptors, hdone)

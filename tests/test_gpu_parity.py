@@ -446,6 +446,25 @@ def test_nonfinite_input_is_reported():
         oracle.Table(P, oracle.make_grid((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
 
 
+@pytest.mark.parametrize("N", [100, 12000])
+def test_build_error_of_a_later_cloud_and_its_clearing(N):
+    """A non-finite coordinate in cloud 2 of 3 is reported whichever build
+    runs (100 points: the one-workgroup build, which keeps each cloud's code
+    in a word of its own; 12000: the brick build), and a build of finite
+    points into the same workspace reports none."""
+    rng = np.random.default_rng(N)
+    P = rng.random((3, N, 3), dtype=np.float32)
+    P[2, N // 2, 0] = np.float32(np.inf)
+    desc = cagq.make_desc((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1)
+    g = cagq.build_grid(torch.from_numpy(P).to(DEV), desc)
+    assert cagq.get_device_status(g) == cagq.ERR_NONFINITE_INPUT
+    P[2, N // 2, 0] = np.float32(0.5)
+    g2 = cagq.build_grid(torch.from_numpy(P).to(DEV), desc, workspace=g.workspace)
+    assert cagq.get_device_status(g2) == 0
+    cl, mv = cagq.sample_centers(g2, 8, "rvs", 1)
+    assert cagq.get_device_status(g2) == 0
+
+
 def test_unoccupied_center_is_reported():
     P = np.random.default_rng(0).random((1, 20, 3), dtype=np.float32) * np.float32(0.2)
     g = cagq.build_grid(torch.from_numpy(P).to(DEV), cagq.make_desc((0, 0, 0), (0.25,) * 3, (4, 4, 4), 8, 1))
