@@ -303,8 +303,9 @@ __global__ __launch_bounds__(256) void k_finalize(
 // A brick is a run of kBrickV consecutive linear voxel ids (kBrickW occupancy
 // words) of one cloud; the batch holds B * Q of them. The points are grouped
 // by brick with a counting sort: a histogram per tile of points (one row per
-// tile), a scan of each brick's column and of the bricks' totals, a scatter
-// that carries each point's coordinates and index. Then one workgroup per
+// tile), a scan of each brick's column and of the bricks' totals (by each
+// scatter tile itself, or by a launch of its own when a tile would read too
+// many entries), a scatter that carries each point's coordinates and index. Then one workgroup per
 // brick marks its occupancy words in LDS, ranks its occupied voxels by
 // popcount, counts their points, and places the n_v lowest point indices of
 // every voxel. The occupied and stored counts of the cloud's earlier bricks

@@ -15,13 +15,18 @@
 // no geometry at all.
 //
 // Per round, each thread first looks at the slots it owns (slot tid + k*1024)
-// and puts those that need real work into an LDS queue: voxels to rescore,
-// then voxels that their cached blocker no longer beats. The workgroup then
-// drains the queue, one voxel per thread, packed into as few waves as
-// possible. A voxel picked in round R keeps its key as a competitor for the
-// rest of round R; from round R+1 on its key is 0 (it competes no more) and
-// its pick key is kept in the two 16-bit words that an unpicked voxel uses
-// for its blocker and its rescoring round.
+// and puts those that need real work into an LDS queue; the workgroup then
+// drains the queue, one voxel per lane (or 16 lanes per voxel for a short
+// queue with r = 1), packed into as few waves as possible. With r = 1 the
+// keys stay exact by lowering (rounds_lowering): the queue holds the voxels
+// that their cached blocker no longer beats, and after the picks one lane per
+// voxel within r of a winner lowers the keys around it. With r = 2 a round
+// first rescores the voxels near the last picks, then queues the voxels
+// for picking. A voxel picked in round R keeps its key as a competitor for
+// the rest of round R; after that its key drops below every unpicked key (to
+// 0 with r = 2; to 2^30 with r = 1, where unpicked keys carry 2^31) and its
+// pick key is kept in the two 16-bit words that an unpicked voxel uses for
+// its blocker and its rescoring round.
 #include "cagq_internal.h"
 
 namespace cagq {

@@ -675,8 +675,8 @@ struct CasState {
     uint32_t* dirty;    // round whose scoring must recompute the voxel's key (row-scan rounds)
 };
 
-// Clears the state and the control block. (With lists, the neighbour-list
-// kernel has set every occupied voxel's key for round 0.)
+// Clears the state and the control block for the row-scan rounds (with
+// lists, the neighbour-list kernel clears them and sets the round-0 keys).
 __global__ void k_cas_init(int32_t BN, int32_t B, CasState st, CasPtrs ctl) {
     int32_t gid = blockIdx.x * blockDim.x + threadIdx.x;
     if (gid < BN) {
