@@ -238,6 +238,17 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     const uint32_t t = s_ticket;
     const int32_t b = (int32_t)(t / tiles_s);
     const int64_t tile = (int64_t)(t % tiles_s);
+    const int32_t s0 = (int32_t)(tile * kScanTile) + (int32_t)threadIdx.x * kScanItems;
+    // the slots' picks and linear ids are loaded at once, beside the bound's
+    // inputs (from indices clamped into the cloud's row; used below nv only)
+    uint64_t pk[kScanItems];
+    uint32_t ln[kScanItems];
+#pragma unroll
+    for (int i = 0; i < kScanItems; ++i) {
+        const size_t at = (size_t)b * N + (size_t)(s0 + i < N ? s0 + i : N - 1);
+        pk[i] = cas_pick ? cas_pick[at] : 0ull;
+        ln[i] = vox_lin[at];
+    }
     const int32_t nv = nvox[b];
     const int32_t m = M < nv ? M : nv;
     if (uhist && tile == 0 && threadIdx.x == 0 && m <= 0) {
@@ -260,14 +271,12 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     const uint64_t bound = packed & ((1ull << 33) - 1);
     const uint32_t need = (uint32_t)(packed >> 33);
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
-    const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
-    const int32_t s0 = (int32_t)(tile * kScanTile) + (int32_t)threadIdx.x * kScanItems;
     bool lt[kScanItems], eq[kScanItems];
     uint64_t cnt = 0;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         const int32_t s = s0 + i;
-        const uint64_t k = s < nv ? select_key(key_mode, hb, s, pick) : ~0ull;
+        const uint64_t k = s < nv ? (key_mode == 0 ? select_key(0, hb, s, nullptr) : ~pk[i]) : ~0ull;
         const uint64_t top = k >> 32;
         const bool counted = s < nv && (key_mode == 0 || k != ~0ull);
         lt[i] = counted && top < bound;
@@ -278,14 +287,13 @@ __global__ __launch_bounds__(kScanThreads) void k_sel_emit(
     const uint64_t excl = block_excl_scan(cnt, s_wave, &total);
     uint64_t before = tile_lookback(desc_s + (size_t)b * tiles_s, tile, total, &s_prefix) + excl;
     int32_t* out = center_lin + (size_t)b * M;
-    const uint32_t* vl = vox_lin + (size_t)b * N;
 #pragma unroll
     for (int i = 0; i < kScanItems; ++i) {
         const uint32_t nlt = (uint32_t)(before >> 31), neq = (uint32_t)(before & 0x7FFFFFFFull);
         if (lt[i] || (eq[i] && neq < need)) {
             const uint32_t pos = nlt + (neq < need ? neq : need);
             if (pos < (uint32_t)m) {
-                const int32_t l = (int32_t)vl[s0 + i];
+                const int32_t l = (int32_t)ln[i];
                 for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
             }
         }
@@ -577,19 +585,28 @@ __global__ __launch_bounds__(kPickThreads) void k_sel_emit_chunks(
     const uint32_t* __restrict__ sel_base, const uint32_t* __restrict__ sel_take, int32_t* __restrict__ center_lin) {
     __shared__ uint32_t s_wave[kPickThreads / kWave];
     const int32_t c = blockIdx.x, b = blockIdx.y, nchunk = gridDim.x;
+    const int32_t s0 = c * kPickSlots + (int32_t)threadIdx.x * kPickItems;
+    // the slots' picks and linear ids are loaded at once, beside the bound
+    // (from indices clamped into the cloud's row; used below nv only)
+    uint64_t pk[kPickItems];
+    uint32_t ln[kPickItems];
+#pragma unroll
+    for (int u = 0; u < kPickItems; ++u) {
+        const size_t at = (size_t)b * N + (size_t)(s0 + u < N ? s0 + u : N - 1);
+        pk[u] = cas_pick ? cas_pick[at] : 0ull;
+        ln[u] = vox_lin[at];
+    }
     const int32_t nv = nvox[b];
     const int32_t m = M < nv ? M : nv;
     const uint64_t bound = thr[b] & ((1ull << 33) - 1);
     const uint32_t base = sel_base[(size_t)b * nchunk + c], take = sel_take[(size_t)b * nchunk + c];
     const uint64_t hb = sm64(sm64(seed ^ 1ull) ^ (uint64_t)b);
-    const uint64_t* pick = cas_pick ? cas_pick + (size_t)b * N : nullptr;
-    const int32_t s0 = c * kPickSlots + (int32_t)threadIdx.x * kPickItems;
     bool lt[kPickItems], eq[kPickItems];
     uint32_t packed = 0;
 #pragma unroll
     for (int u = 0; u < kPickItems; ++u) {
         const int32_t sl = s0 + u;
-        const uint64_t top = sl < nv ? select_key(key_mode, hb, sl, pick) >> 32 : 0xFFFFFFFFull;
+        const uint64_t top = sl < nv ? (key_mode == 0 ? select_key(0, hb, sl, nullptr) : ~pk[u]) >> 32 : 0xFFFFFFFFull;
         const bool counted = sl < nv && (key_mode == 0 || top != 0xFFFFFFFFull);
         lt[u] = counted && top < bound;
         eq[u] = counted && top == bound;
@@ -604,7 +621,7 @@ __global__ __launch_bounds__(kPickThreads) void k_sel_emit_chunks(
         if (lt[u] || (eq[u] && neq < take)) {
             const uint32_t pos = base + nlt + (neq < take ? neq : take);
             if (pos < (uint32_t)m) {
-                const int32_t l = (int32_t)vox_lin[(size_t)b * N + s0 + u];
+                const int32_t l = (int32_t)ln[u];
                 for (int64_t j = (int64_t)pos; j < M; j += m) out[j] = l;
             }
         }
