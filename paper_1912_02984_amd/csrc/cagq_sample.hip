@@ -944,10 +944,14 @@ __device__ __forceinline__ int32_t beats(const uint4 (&q)[4], uint32_t c, uint32
         kk[j] = ky[sl[j]];
         rr[j] = rd[sl[j]];
     }
+    // every entry is tested, without short cuts (which the compiler turns
+    // into loads issued one at a time), the first from the end to the front
     int32_t found = -1;
 #pragma unroll
-    for (int j = 0; j < 16; ++j)
-        if (found < 0 && kk[j] > my && (rr[j] == 0 || rr[j] == cur)) found = (int32_t)sl[j];
+    for (int j = 15; j >= 0; --j) {
+        const bool bt = (kk[j] > my) & ((rr[j] == 0u) | (rr[j] == cur));
+        found = bt ? (int32_t)sl[j] : found;
+    }
     return found;
 }
 
@@ -987,23 +991,44 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const int32_t gid = (int32_t)xcd_block(blockIdx.x, gridDim.x) * blockDim.x + threadIdx.x;
     const bool in_range = gid < B * N;
     const int32_t b = in_range ? gid / N : B - 1, s = in_range ? gid - b * N : N;
-    // the voxel's own state is loaded up front, together with the cloud's
-    // (from a valid index for every lane: a load under the range test would
-    // be waited for alone)
+    // Everything the round's first decisions need is loaded at once: the
+    // voxel's own state, the cloud's done flag and size, and the previous
+    // round's partials (no kernel of this round writes them), from valid
+    // indices for every lane (a load under a test would be waited for
+    // alone); then the blocker's key and pick round, together.
     const size_t gc = in_range ? (size_t)gid : 0;
     const uint32_t rnd0_ = st.round[gc];
     const uint64_t pk0_ = st.pick[gc], my0_ = st.key[gc];
     const int32_t bl0_ = st.blocker[gc];
+    const uint32_t done0 = ctl.done[b];
+    const int32_t nv = nvox[b];
+    const size_t part = (size_t)B * kCasParts;
+    const int32_t b0 = __builtin_amdgcn_readlane(b, 0), b1 = __builtin_amdgcn_readlane(b, kWave - 1);
+    const bool one_cloud = b0 == b1;  // the wave's lanes all in one cloud: each lane reduces two partials
+    static_assert(kCasParts == 2 * kWave, "two partials per lane");
+    uint32_t cp0 = 0, cp1 = 0;
+    uint64_t gp0 = 0, gp1 = 0;
+    if (R > 0 && one_cloud) {
+        const size_t pp = (size_t)((R - 1) % kCasBufs) * part + (size_t)b0 * kCasParts + lane_id();
+        cp0 = ctl.cpart[pp];
+        cp1 = ctl.cpart[pp + kWave];
+        gp0 = ctl.gpart[pp];
+        gp1 = ctl.gpart[pp + kWave];
+    }
+    const size_t cb = (size_t)b * N;
+    const int32_t blc = bl0_ >= 0 && bl0_ < N ? bl0_ : 0;
+    const uint64_t kb_ = st.key[cb + blc];
+    const uint32_t rb_ = st.round[cb + blc];
     const uint32_t rnd0 = in_range ? rnd0_ : 0u;
     const uint64_t pk0 = in_range ? pk0_ : 0ull;
     const uint64_t my0 = in_range ? my0_ : 0ull;
     const int32_t bl0 = in_range ? bl0_ : -1;
-    bool active = in_range && ctl.done[b] == 0;
+    bool active = in_range && done0 == 0;
     if (ctl.host && blockIdx.x == 0 && threadIdx.x == 0)  // progress for the host's round issue
         __hip_atomic_store(ctl.host + 1, ctl.epoch | (uint32_t)R, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-    const int32_t nv = nvox[b];
-    const size_t part = (size_t)B * kCasParts;
-    const uint32_t prev = R > 0 ? parts_sum(ctl.cpart + (size_t)((R - 1) % kCasBufs) * part, b) : 0u;
+    const uint32_t prev = R == 0 ? 0u
+                          : one_cloud ? wave_sum_u32(cp0 + cp1)
+                                      : parts_sum(ctl.cpart + (size_t)((R - 1) % kCasBufs) * part, b);
     if (active && prev >= (uint32_t)(M < nv ? M : nv)) {
         if (s == 0) {
             ctl.done[b] = 1;
@@ -1019,9 +1044,10 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
             ctl.gpart[o] = 0;
             ctl.cpart[o] = 0;
         }
-    const uint64_t G = R > 0 ? parts_max(ctl.gpart + (size_t)((R - 1) % kCasBufs) * part, b) : ~0ull;
+    const uint64_t G = R == 0 ? ~0ull
+                       : one_cloud ? wave_max_u64(gp0 > gp1 ? gp0 : gp1)
+                                   : parts_max(ctl.gpart + (size_t)((R - 1) % kCasBufs) * part, b);
     const uint32_t cur = (uint32_t)R + 1;
-    const size_t cb = (size_t)b * N;
     uint64_t k = 0;
     uint32_t above = 0;
     bool winner = false;
@@ -1047,11 +1073,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
         } else {
             k = my0;
             bool beaten = false;
-            if (bl0 >= 0) {
-                const uint64_t kb = ky[bl0];
-                const uint32_t rb = rd[bl0];
-                beaten = kb > my0 && (rb == 0 || rb == cur);
-            }
+            if (bl0 >= 0) beaten = kb_ > my0 && (rb_ == 0 || rb_ == cur);
             // the list (which does not fit in the caches) is read only by a
             // voxel its blocker no longer beats: after the first rounds most
             // voxels stay blocked
@@ -1166,8 +1188,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     // per-cloud maximum of the unpicked keys and count of picks above the
     // previous round's maximum, into this round's partial slots
     const size_t mine = (size_t)(R % kCasBufs) * part;
-    const int32_t b0 = __shfl(b, 0, kWave), b1 = __shfl(b, kWave - 1, kWave);
-    if (b0 == b1) {
+    if (one_cloud) {
         const uint64_t mx = wave_max_u64(k);
         const uint32_t tot = wave_sum_u32(above);
         if (lane_id() == 0 && mx) atomicMax((unsigned long long*)&ctl.gpart[mine + (size_t)b * kCasParts + part_slot()], mx);
