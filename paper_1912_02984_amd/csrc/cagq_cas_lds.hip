@@ -643,6 +643,15 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     // with U* the largest U for which at least m picks have U >= U*, the
     // chosen picks are those with U > U* and, of those with U = U*, the
     // `need` lowest slots.
+    // the owned slots' linear ids for the emit below, loaded now (from
+    // indices clamped into the cloud's row) so that the histogram's phases
+    // cover their latency
+    uint32_t lv[kKS];
+#pragma unroll
+    for (int k = 0; k < kKS; ++k) {
+        const int32_t s = k * kT + tid;
+        lv[k] = vl[s < N ? s : N - 1];
+    }
     uint32_t pk[kKS];
     for (int32_t i = tid; i < 128; i += kT) s_hist[i] = 0;
     __syncthreads();
@@ -689,7 +698,6 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
     uint32_t base_h = 0, base_t = 0;
 #pragma unroll
     for (int k = 0; k < kKS; ++k) {
-        const int32_t s = k * kT + tid;
         const uint32_t u = pk[k] >> kKeyShift;
         const bool hi = pk[k] != 0 && u > ustar, tie = pk[k] != 0 && u == ustar;
         const uint64_t bh = __ballot(hi), bt = __ballot(tie);
@@ -705,7 +713,7 @@ __global__ __launch_bounds__(kT) void k_cas_lds(int32_t N, int32_t M, int32_t ca
         const uint32_t tb = base_t + (off >> 16) + (uint32_t)__popcll(bt & below);
         if (hi || (tie && tb < need)) {
             const uint32_t pos = hb + (tb < need ? tb : need);
-            const int32_t lin = (int32_t)vl[s];
+            const int32_t lin = (int32_t)lv[k];
             for (int32_t j = (int32_t)pos; j < M; j += m) out[j] = lin;
         }
         base_h += tot & 0xFFFFu;
