@@ -929,6 +929,45 @@ __device__ __forceinline__ int pair_owner(uint32_t incl, uint32_t p) {
     return lo < kWave ? lo : kWave - 1;
 }
 
+// The lane of the wave that owns pair p0 + lane_id(), lane L owning the pairs
+// [incl - n, incl) of its own incl and n (lanes in order, ranges possibly
+// empty): a range that starts inside the window marks its start with L + 1
+// in the wave's LDS row, an unsigned max-scan across the lanes (DPP) carries
+// each mark forward, and the window's first pair goes to the first lane whose
+// range ends past it (one ballot). One LDS round trip and six DPP steps, where
+// a binary search over the lanes takes six dependent permutes. Every lane of
+// the wave must call it; pairs at or past the wave's total get the last range.
+__device__ __forceinline__ int window_owner(uint32_t incl, uint32_t n, uint32_t p0, uint32_t* s_mark) {
+    const int lane = lane_id();
+    s_mark[lane] = 0u;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    const uint32_t st = incl - n;
+    if (n != 0 && st >= p0 && st - p0 < (uint32_t)kWave) s_mark[st - p0] = (uint32_t)lane + 1u;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    uint32_t v = s_mark[lane];
+    const uint64_t past = __ballot(incl > p0);
+    const uint32_t first = past ? (uint32_t)__ffsll((unsigned long long)past) : (uint32_t)kWave;  // lane + 1
+    if (lane == 0) v = v > first ? v : first;
+    uint32_t o;
+    o = dpp_row_shr<1>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr<2>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr<4>(v);
+    v = o > v ? o : v;
+    o = dpp_row_shr<8>(v);
+    v = o > v ? o : v;
+    o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);  // row_bcast:15
+    v = o > v ? o : v;
+    o = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);  // row_bcast:31
+    v = o > v ? o : v;
+    return (int)v - 1;
+}
+
 // The first of entries 16c..16c+15 of a list of n2 entries (held in q) that
 // is a competitor and whose key beats `my`, or -1. Positions past the list's
 // end read the voxel's own slot `self`, whose key never beats its own.
@@ -1096,13 +1135,14 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const uint32_t nrest = found == -1 && n2 > 16 ? (n2 - 1) / 16 : 0u;  // chunks 1.. still to scan
     const uint32_t sincl = wave_incl_sum_u32(nrest);
     const uint32_t stot = (uint32_t)__builtin_amdgcn_readlane((int)sincl, kWave - 1);
+    __shared__ uint32_t s_mark[kRoundThreads];  // window_owner's row (the block is one wave)
     if (stot) {
         __shared__ int32_t s_found[kRoundThreads];
         const int wbase = threadIdx.x & ~(kWave - 1);
         s_found[threadIdx.x] = -1;
         for (uint32_t p0 = 0; p0 < stot; p0 += kWave) {
             const uint32_t p = p0 + (uint32_t)lane_id();
-            const int owner = pair_owner(sincl, p);
+            const int owner = window_owner(sincl, nrest, p0, s_mark);
             const uint32_t o_incl = (uint32_t)__shfl((int)sincl, owner, kWave);
             const uint32_t o_n = (uint32_t)__shfl((int)nrest, owner, kWave);
             const uint32_t o_n2 = (uint32_t)__shfl((int)n2, owner, kWave);
@@ -1151,7 +1191,7 @@ __global__ __launch_bounds__(kRoundThreads) __attribute__((amdgpu_waves_per_eu(5
     const int wb = threadIdx.x & ~(kWave - 1);
     for (uint32_t p0 = 0; p0 < total; p0 += kWave) {
         const uint32_t p = p0 + (uint32_t)lane_id();
-        const int owner = pair_owner(incl, p);
+        const int owner = window_owner(incl, nrw, p0, s_mark);
         const uint32_t o_incl = (uint32_t)__shfl((int)incl, owner, kWave);
         const uint32_t o_nr = (uint32_t)__shfl((int)nrw, owner, kWave);
         const int32_t o_gid = __shfl(gid, owner, kWave);
