@@ -918,17 +918,6 @@ __global__ __launch_bounds__(256) void k_cas_pick(
     }
 }
 
-// The lane of the wave whose inclusive count is the first to exceed p.
-__device__ __forceinline__ int pair_owner(uint32_t incl, uint32_t p) {
-    int lo = 0;
-#pragma unroll
-    for (int step = kWave / 2; step > 0; step >>= 1) {
-        const uint32_t v = (uint32_t)__shfl((int)incl, lo + step - 1, kWave);
-        if (v <= p) lo += step;
-    }
-    return lo < kWave ? lo : kWave - 1;
-}
-
 // The lane of the wave that owns pair p0 + lane_id(), lane L owning the pairs
 // [incl - n, incl) of its own incl and n (lanes in order, ranges possibly
 // empty): a range that starts inside the window marks its start with L + 1
