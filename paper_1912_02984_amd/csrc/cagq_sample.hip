@@ -201,19 +201,21 @@ __device__ __forceinline__ void cas_u_bound(const uint32_t* __restrict__ uhist, 
         if (h) atomicAdd(&s_h[bin], h);
     }
     __syncthreads();
-    if (tid == 0) {
-        uint32_t run = 0, need = 0;
-        uint64_t bound = 0;
-        for (int u = kCasUBins - 1; u >= 0 && m > 0; --u) {
-            const uint32_t hu = s_h[u];
-            if (run + hu >= m) {
-                bound = 0xFFFFFFFFull - (uint64_t)(unit * u + 2147483648ll);
-                need = m - run;
-                break;
-            }
-            run += hu;
+    // the first wave: lane l holds U = kCasUBins - 1 - l (from the top), an
+    // inclusive scan of the counts, and the first lane whose running count
+    // reaches m gives U* and the ties taken there (no picks at all: 0, 0)
+    static_assert(kCasUBins <= kWave, "one bin per lane");
+    if (tid < kWave) {
+        const int u = kCasUBins - 1 - tid;
+        const uint32_t hu = tid < kCasUBins ? s_h[u] : 0u;
+        const uint32_t incl = wave_incl_sum_u32(hu);
+        const uint64_t hit = __ballot(m > 0 && tid < kCasUBins && incl >= m);
+        if (!hit) {
+            if (tid == 0) *out = sel_pack(0, 0);
+        } else if (tid == __ffsll((unsigned long long)hit) - 1) {
+            const uint64_t bound = 0xFFFFFFFFull - (uint64_t)(unit * u + 2147483648ll);
+            *out = sel_pack(bound, m - (incl - hu));
         }
-        *out = sel_pack(bound, need);
     }
 }
 
